@@ -1,0 +1,81 @@
+"""Scalar-loop brute force of the PCED decode step for tiny inputs.
+
+TEST INFRASTRUCTURE ONLY (see ``pced_oracle``). Pure Python floats and loops,
+no NumPy linear algebra: an independent second reading of the same definitions
+(Section 3, Eq. 2 and Eq. 3), used to cross-check the NumPy oracle. Inputs are
+nested lists of Python floats that already hold the stored values.
+"""
+from __future__ import annotations
+
+import math
+
+
+def attention(q, K, V):
+    """q[h][d]; K[t][g][d]; V[t][g][d] -> o[h][d]."""
+    Hq, D, T, Hkv = len(q), len(q[0]), len(K), len(K[0])
+    group = Hq // Hkv
+    out = []
+    for h in range(Hq):
+        g = h // group
+        z = []
+        for t in range(T):
+            acc = 0.0
+            for d in range(D):
+                acc += q[h][d] * K[t][g][d]
+            z.append(acc / math.sqrt(D))
+        zmax = max(z)
+        w = [math.exp(x - zmax) for x in z]
+        tot = sum(w)
+        out.append([sum(w[t] * V[t][g][d] for t in range(T)) / tot for d in range(D)])
+    return out
+
+
+def logits(x, W, rms: bool):
+    """x[j] (one sequence); W[v][j] -> s[v]."""
+    n = len(x)
+    rho = 1.0 / math.sqrt(sum(v * v for v in x) / n + 1e-5) if rms else 1.0
+    return [rho * sum(x[j] * W[v][j] for j in range(n)) for v in range(len(W))]
+
+
+def jsd_bits(sk, s0):
+    def probs(s):
+        m = max(s)
+        e = [math.exp(x - m) for x in s]
+        z = sum(e)
+        return [x / z for x in e]
+    p, q = probs(sk), probs(s0)
+    tot = 0.0
+    for a, b in zip(p, q):
+        m = 0.5 * (a + b)
+        if a > 0:
+            tot += 0.5 * a * math.log2(a / m)
+        if b > 0:
+            tot += 0.5 * b * math.log2(b / m)
+    return tot
+
+
+def pick(rows, relevance, gamma, beta):
+    """rows[0] = amateur logits, rows[1..N] = experts; returns (token, winner, top1, top2).
+
+    Enumerates every (token, expert) pair."""
+    N, V = len(rows) - 1, len(rows[0])
+    best_v = []
+    best_k = []
+    for v in range(V):
+        bv, bk = -math.inf, 0
+        for k in range(1, N + 1):
+            r = min(max(relevance[k - 1], 1e-8), 1 - 1e-8)
+            val = (1 + beta[k - 1]) * rows[k][v] - beta[k - 1] * rows[0][v] + gamma * math.log(r)
+            if val > bv:
+                bv, bk = val, k
+        best_v.append(bv)
+        best_k.append(bk)
+    tok = 0
+    for v in range(1, V):
+        if best_v[v] > best_v[tok]:
+            tok = v
+    top2 = -math.inf
+    for v in range(V):
+        if v != tok and best_v[v] > top2:
+            top2 = best_v[v]
+    return tok, best_k[tok], best_v[tok], top2
