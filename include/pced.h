@@ -1,0 +1,248 @@
+/*
+ * pced.h - C ABI of libpced, the per-token decode step of Parallel
+ * Context-of-Experts Decoding (PCED; Corallo and Papotti, arXiv 2601.08670)
+ * on one AMD Instinct MI355X (gfx950).
+ *
+ * The method (paper, Section 3): a query q has N retrieved documents with
+ * relevance scores r_1..r_N. Each document k owns a precomputed KV cache K_k; an
+ * "amateur" sequence (k = 0) holds no document. The N+1 sequences ("experts")
+ * decode in one batched forward pass. At each step every expert yields full
+ * vocabulary logits s_k, which are fused by the retrieval-aware contrastive rule
+ *     Eq. 2:  s_hat_k = (1 + beta_k) s_k - beta_k s_0 + gamma log r_k,   k = 1..N
+ *     Eq. 3:  y_t = argmax_v max_{k=1..N} s_hat_k(v)
+ * and y_t is appended to the shared generation history of every expert.
+ *
+ * What one decode step runs here, all on the device:
+ *   1. the new token's K/V row (one per sequence and layer) is written into the
+ *      paged KV pool (shared-history append);
+ *   2. per layer, every sequence attends with its own query over its own ragged
+ *      cache (grouped-query attention, scale 1/sqrt(head_dim));
+ *   3. the last layer's attention output, concatenated over heads and rounded to
+ *      the storage type, is each sequence's hidden state x; logits are
+ *      rho * x W^T with rho = 1/sqrt(mean(x^2) + 1e-5) (norm = RMS) or 1;
+ *   4. at the first step with dynamic beta: beta_k = JSD(softmax s_k || softmax s_0)
+ *      in bits, frozen for the following steps;
+ *   5. Eq. 2 and Eq. 3 per query; ties go to the lowest token id, and the
+ *      reported expert is the lowest k reaching the maximum.
+ *
+ * Conventions (every function):
+ *   - Device memory is owned by the caller: KV pools, workspace, weights, inputs
+ *     and outputs. The library never allocates or frees device memory. It owns
+ *     only the host-side context.
+ *   - Work is enqueued on the caller's stream and never synchronised; outputs
+ *     are valid once the caller synchronises that stream. A NULL stream is the
+ *     default stream.
+ *   - Every argument and capacity check runs on the host before anything is
+ *     enqueued. On any non-OK status nothing was enqueued and the context is
+ *     unchanged; pced_last_error() returns a description (thread-local).
+ *   - A context is not thread-safe; separate contexts are independent. Calls on
+ *     one context must be issued on streams that order them (normally one).
+ */
+#ifndef PCED_H
+#define PCED_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum pced_status {
+  PCED_OK = 0,
+  PCED_ERR_INVALID_ARG = 1,  /* NULL pointer, bad shape, value out of range      */
+  PCED_ERR_CAPACITY = 2,     /* would exceed a configured maximum or a page set  */
+  PCED_ERR_HIP = 3,          /* a HIP call or kernel launch failed               */
+  PCED_ERR_UNSUPPORTED = 4,  /* valid but not implemented for this configuration */
+  PCED_ERR_STATE = 5         /* call out of order (e.g. step before load)        */
+} pced_status;
+
+typedef enum pced_dtype {
+  PCED_F32 = 0,   /* float32 storage of q, K/V, lm_head and x */
+  PCED_BF16 = 1   /* bfloat16 storage (raw 16-bit patterns)   */
+} pced_dtype;
+
+typedef enum pced_norm {
+  PCED_NORM_NONE = 0,  /* logits = x W^T                               */
+  PCED_NORM_RMS = 1    /* logits = x W^T / sqrt(mean(x^2) + 1e-5) per row */
+} pced_norm;
+
+/* Static shape and capacity of a context. */
+typedef struct pced_config {
+  int32_t n_layers;          /* L  >= 1                                          */
+  int32_t n_q_heads;         /* Hq, a multiple of n_kv_heads                     */
+  int32_t n_kv_heads;        /* Hkv; Hq / Hkv <= 16                              */
+  int32_t head_dim;          /* D: 64 or 128                                     */
+  int32_t hidden;            /* must equal Hq * D (the hidden state is the
+                                concatenated per-head attention output)         */
+  int32_t vocab;             /* V >= 2                                           */
+  int32_t dtype;             /* pced_dtype                                       */
+  int32_t page_size;         /* tokens per KV page; must be 16                   */
+  int32_t max_queries;       /* B, queries per batch                             */
+  int32_t max_seqs;          /* S = sum over queries of (N_b + 1)                */
+  int32_t max_pages;         /* pool capacity in pages (per layer)               */
+  int32_t max_pages_per_seq; /* page-table row length                            */
+  int32_t norm;              /* pced_norm                                        */
+} pced_config;
+
+typedef struct pced_ctx pced_ctx;
+
+/* Bytes of one KV pool (K or V) for cfg: n_layers * max_pages * n_kv_heads *
+ * page_size * head_dim * sizeof(storage). Layout (opaque to callers):
+ * [layer][page][kv_head][16 x head_dim tile]; inside a bf16 tile the elements are
+ * ordered so that each matrix-core operand is one contiguous 16-byte load per
+ * lane. Returns 0 for an invalid cfg. */
+size_t pced_pool_bytes(const pced_config* cfg);
+
+/* Bytes of device workspace a context needs (0 for an invalid cfg). */
+size_t pced_workspace_bytes(const pced_config* cfg);
+
+/* Create a context over caller-owned device workspace (>= pced_workspace_bytes,
+ * 256-byte aligned). Host-only: enqueues nothing. */
+pced_status pced_create(const pced_config* cfg, void* d_workspace, size_t ws_bytes, pced_ctx** out);
+
+/* Destroy a context (NULL is ignored). The caller must have synchronised any
+ * stream the context used. */
+void pced_destroy(pced_ctx* ctx);
+
+/* Description of the calling thread's last non-OK status ("" if none). */
+const char* pced_last_error(void);
+
+/*
+ * Load one batch: the N_b + 1 precomputed caches of each query (paper, Section 3,
+ * Eq. 1 datastore: one cache per retrieved document; the amateur's cache holds
+ * only the query) and the per-document relevance scores r_k.
+ *
+ *   n_queries       B, 1 .. max_queries
+ *   n_experts       host [B]: N_b >= 1 documents of query b
+ *   cache_len       host [S]: preloaded tokens of each sequence (>= 1), in order
+ *                   query 0: amateur, expert 1..N_0; query 1: amateur, ...
+ *   src_k, src_v    host arrays [S] of DEVICE pointers, each to a contiguous
+ *                   [L][cache_len[s]][Hkv][D] tensor of the storage type; they must
+ *                   stay valid until the stream has executed this call
+ *   k_pool, v_pool  device, pced_pool_bytes(cfg) each, caller-owned; this call
+ *                   writes the caches into them and later steps append to them
+ *   page_table      host [S][max_pages_per_seq] physical page ids (>= 0,
+ *                   < max_pages, distinct across the batch; -1 marks pages not
+ *                   given). Page p of sequence s holds tokens 16p .. 16p+15. NULL
+ *                   assigns pages in order, giving every sequence
+ *                   ceil((cache_len + reserve_tokens) / 16) pages.
+ *   reserve_tokens  tokens each sequence must be able to append (NULL page table
+ *                   only; checked against max_pages and max_pages_per_seq)
+ *   relevance       host [sum N_b] r_k; clipped to [1e-8, 1 - 1e-8] before the log
+ *                   (paper, Appendix B: scores mapped into [0,1) and clipped away
+ *                   from 0, eps = 1e-8)
+ *   gamma           weight of the retrieval prior (paper default 2.5)
+ *   beta            host [sum N_b] fixed contrastive strengths (paper, Appendix
+ *                   C.1), or NULL for dynamic beta: JSD in bits between each
+ *                   expert's and the amateur's next-token distributions at the first
+ *                   step, kept fixed afterwards (paper, Section 3)
+ * Resets the step counter. Errors: INVALID_ARG, CAPACITY (pages), HIP.
+ */
+pced_status pced_load_caches(pced_ctx* ctx, int32_t n_queries, const int32_t* n_experts,
+                             const int32_t* cache_len, const void* const* src_k,
+                             const void* const* src_v, void* k_pool, void* v_pool,
+                             const int32_t* page_table, int32_t reserve_tokens,
+                             const float* relevance, float gamma, const float* beta,
+                             hipStream_t stream);
+
+/* Optional device outputs of a step; any NULL member is skipped. */
+typedef struct pced_step_out {
+  float* attn_out;        /* [S][L][Hq][D] fp32 attention output of every layer     */
+  float* logits;          /* [S][V] fp32 logits s_k (Section 3, per-expert logits)  */
+  int32_t* winner;        /* [B] expert k* (1..N_b) whose score chose the token     */
+  float* top1;            /* [B] fused score of the chosen token                   */
+  float* top2;            /* [B] best fused score over all other tokens            */
+  float* beta_used;       /* [sum N_b] beta_k used by this step                    */
+  float* hidden;          /* [S][hidden] fp32 copy of the stored hidden state x    */
+} pced_step_out;
+
+/*
+ * One decode step for every sequence of every loaded query (paper, Section 3:
+ * batched forward pass, Eq. 2, Eq. 3, shared history).
+ *   q          device [S][L][Hq][D]    this step's query vectors
+ *   k_new      device [S][L][Hkv][D]   this step's K row (the shared token's)
+ *   v_new      device [S][L][Hkv][D]   this step's V row
+ *   lm_head    device [V][hidden]      row-major output projection
+ *   tokens_out device [B]              chosen token y_t per query
+ *   extra      optional outputs, may be NULL
+ * All in the storage type except the fp32 outputs. Errors: STATE (nothing
+ * loaded), CAPACITY (a sequence has no page for the new token), INVALID_ARG, HIP.
+ */
+pced_status pced_step(pced_ctx* ctx, const void* q, const void* k_new, const void* v_new,
+                      const void* lm_head, int32_t* tokens_out, const pced_step_out* extra,
+                      hipStream_t stream);
+
+/* Deterministic stand-in for the model's projections in multi-step generation:
+ * the step-t query and K/V rows of sequence s, layer l are SplitMix64 streams
+ * keyed by (seed, tag, t, s, l, y_{t-1}) where y_{t-1} is the query's previous
+ * token (first_token at t = 0); values are Irwin-Hall(4) sums of 16-bit fields
+ * scaled to unit variance. The exact definition is in pced_generate's source. */
+typedef struct pced_synth {
+  uint64_t seed;
+  int32_t first_token;
+} pced_synth;
+
+/*
+ * n_steps decode steps (paper, Section 3: greedy generation with the shared
+ * history). Step t's q / k_new / v_new are produced on the device from the
+ * previous chosen token (pced_synth), so the only host interaction is the
+ * caller's final synchronisation.
+ *   tokens_out  device [B][n_steps]
+ *   last_extra  optional outputs of the last step
+ */
+pced_status pced_generate(pced_ctx* ctx, int32_t n_steps, const pced_synth* synth,
+                          const void* lm_head, int32_t* tokens_out,
+                          const pced_step_out* last_extra, hipStream_t stream);
+
+/*
+ * Stage entry: full-vocabulary logits for given hidden states (paper, Section 3:
+ * per-expert logits s_k). x: device [n_rows][hidden] storage type; lm_head:
+ * device [V][hidden]; logits: device [n_rows][V] fp32; n_rows <= max_seqs.
+ */
+pced_status pced_lmhead(pced_ctx* ctx, const void* x, int32_t n_rows, const void* lm_head,
+                        float* logits, hipStream_t stream);
+
+/*
+ * Stage entry: Eq. 2 and Eq. 3 on given logits for the loaded batch.
+ *   logits        device [S][V] fp32, rows in load order
+ *   refresh_beta  with dynamic beta: nonzero recomputes beta from these logits
+ *                 and freezes it (what the first step does); zero uses the frozen
+ *                 value (STATE if none yet). Ignored with fixed beta.
+ *   tokens_out    device [B]
+ */
+pced_status pced_fuse(pced_ctx* ctx, const float* logits, int32_t refresh_beta,
+                      int32_t* tokens_out, const pced_step_out* extra, hipStream_t stream);
+
+/* Host mirror of the current cache length of every sequence: out [S]. */
+pced_status pced_get_lengths(const pced_ctx* ctx, int32_t* out, int32_t capacity);
+
+/* Kernel timing with HIP events recorded around each launch on the launch
+ * stream. Classes: */
+enum {
+  PCED_PROF_APPEND = 0,  /* shared-history append and work planning */
+  PCED_PROF_ATTN = 1,    /* decode attention, one launch per layer */
+  PCED_PROF_LMHEAD = 2,  /* LM head                                */
+  PCED_PROF_BETA = 3,    /* dynamic beta (first step only)         */
+  PCED_PROF_FUSE = 4,    /* Eq. 2 + Eq. 3                          */
+  PCED_PROF_SYNTH = 5,   /* pced_generate's input synthesis        */
+  PCED_PROF_NCLASS = 6
+};
+typedef struct pced_profile {
+  int64_t launches[PCED_PROF_NCLASS];
+  double total_ms[PCED_PROF_NCLASS];
+  double bytes[PCED_PROF_NCLASS];   /* algorithmic bytes of the timed launches */
+  double flops[PCED_PROF_NCLASS];   /* algorithmic flops of the timed launches */
+} pced_profile;
+
+/* Start (nonzero) or stop (zero) recording; starting clears the totals. */
+pced_status pced_profile_enable(pced_ctx* ctx, int32_t on);
+/* Totals of the launches recorded so far; the caller must have synchronised the
+ * stream. */
+pced_status pced_profile_read(pced_ctx* ctx, pced_profile* out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PCED_H */

@@ -1,0 +1,666 @@
+// Host side of libpced: argument validation, workspace carving, the host mirror
+// of sequence lengths and page tables, and the launch sequence of a PCED decode
+// step (arXiv 2601.08670, Section 3). See include/pced.h for the contract.
+#include "pced.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "pced_internal.h"
+
+using namespace pced;
+
+namespace {
+
+thread_local std::string g_err;
+
+pced_status fail(pced_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define HIP_OK(expr)                                                               \
+  do {                                                                             \
+    hipError_t e_ = (expr);                                                        \
+    if (e_ != hipSuccess) return fail(PCED_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+size_t esize_of(const pced_config& c) { return c.dtype == PCED_BF16 ? 2 : 4; }
+int ceil_div(long a, long b) { return (int)((a + b - 1) / b); }
+
+bool cfg_valid(const pced_config* c, std::string* why) {
+  auto bad = [&](const char* m) { if (why) *why = m; return false; };
+  if (!c) return bad("cfg is NULL");
+  if (c->n_layers < 1) return bad("n_layers < 1");
+  if (c->n_kv_heads < 1 || c->n_q_heads < 1 || c->n_q_heads % c->n_kv_heads) return bad("n_q_heads must be a positive multiple of n_kv_heads");
+  if (c->n_q_heads / c->n_kv_heads > kMaxGroup) return bad("n_q_heads / n_kv_heads > 16");
+  if (c->dtype != PCED_BF16 && c->dtype != PCED_F32) return bad("unknown dtype");
+  if (c->dtype == PCED_BF16 && c->head_dim != 64 && c->head_dim != 128) return bad("bf16 needs head_dim 64 or 128");
+  if (c->dtype == PCED_F32 && (c->head_dim < 4 || c->head_dim > 128 || c->head_dim % 4)) return bad("f32 needs head_dim in [4,128], a multiple of 4");
+  if (c->hidden != c->n_q_heads * c->head_dim) return bad("hidden must equal n_q_heads * head_dim");
+  if (c->dtype == PCED_BF16 && c->hidden % 64) return bad("bf16 hidden must be a multiple of 64");
+  if (c->vocab < 2) return bad("vocab < 2");
+  if (c->page_size != kPage) return bad("page_size must be 16");
+  if (c->max_queries < 1) return bad("max_queries < 1");
+  if (c->max_seqs < 2) return bad("max_seqs < 2");
+  if (c->max_pages < 1 || c->max_pages_per_seq < 1) return bad("max_pages and max_pages_per_seq must be >= 1");
+  if (c->norm != PCED_NORM_NONE && c->norm != PCED_NORM_RMS) return bad("unknown norm");
+  // 32-bit index guards used by the kernels
+  if ((double)c->max_seqs * c->vocab > 2147483647.0) return bad("max_seqs * vocab exceeds 2^31");
+  return true;
+}
+
+struct Layout {
+  size_t len0, page_table, seq_query, query_seq0, query_exp0, exp_seq, exp_query, prior, beta_fixed,
+      load_items, src_k, src_v, meta_end;
+  size_t work_off, tick_attn, tick_fuse, tick_beta, prev_tok, beta, part_acc, part_ml, x, logits,
+      fuse_part, lse_part, jsd_part, syn_q, syn_k, syn_v, total;
+  int rows_pad, nblk_fuse, nchunk, max_work;
+};
+
+Layout make_layout(const pced_config& c) {
+  Layout L{};
+  const size_t S = c.max_seqs, B = c.max_queries, es = esize_of(c);
+  const int G = c.n_q_heads / c.n_kv_heads;
+  L.rows_pad = ceil_div(c.max_seqs, kLmRowsPad) * kLmRowsPad;
+  L.nblk_fuse = ceil_div(c.vocab, kFuseBlock);
+  L.nchunk = ceil_div(c.vocab, kBetaChunk);
+  L.max_work = c.max_pages;  // every split covers at least one page of its sequence
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes); return r; };
+  // metadata block, uploaded by one copy at load
+  L.len0 = take(S * 4);
+  L.page_table = take(S * c.max_pages_per_seq * 4);
+  L.seq_query = take(S * 4);
+  L.query_seq0 = take((B + 1) * 4);
+  L.query_exp0 = take((B + 1) * 4);
+  L.exp_seq = take(S * 4);
+  L.exp_query = take(S * 4);
+  L.prior = take(S * 4);
+  L.beta_fixed = take(S * 4);
+  L.load_items = take((size_t)c.max_pages * 2 * 4);
+  L.src_k = take(S * 8);
+  L.src_v = take(S * 8);
+  L.meta_end = o;
+  L.work_off = take((S + 1) * 4);
+  L.tick_attn = take(S * c.n_kv_heads * 4);
+  L.tick_fuse = take(B * 4);
+  L.tick_beta = take(S * 4);
+  L.prev_tok = take(B * 4);
+  L.beta = take(S * 4);
+  L.part_acc = take((size_t)L.max_work * c.n_kv_heads * G * c.head_dim * 4);
+  L.part_ml = take((size_t)L.max_work * c.n_kv_heads * G * 2 * 4);
+  L.x = take((size_t)L.rows_pad * c.hidden * es);
+  L.logits = take(S * c.vocab * 4);
+  L.fuse_part = take(B * L.nblk_fuse * 5 * 4);
+  L.lse_part = take(S * L.nchunk * 2 * 4);
+  L.jsd_part = take(S * L.nchunk * 4);
+  L.syn_q = take(S * c.n_layers * c.n_q_heads * c.head_dim * es);
+  L.syn_k = take(S * c.n_layers * c.n_kv_heads * c.head_dim * es);
+  L.syn_v = take(S * c.n_layers * c.n_kv_heads * c.head_dim * es);
+  L.total = o;
+  return L;
+}
+
+struct ProfRec {
+  int cls;
+  hipEvent_t a, b;
+  double bytes, flops;
+};
+
+}  // namespace
+
+struct pced_ctx {
+  pced_config cfg;
+  Layout lay;
+  char* ws;
+  bool bf16;
+  int G;
+  // host mirror of the loaded batch
+  bool loaded = false;
+  int B = 0, S = 0, NE = 0;
+  std::vector<int32_t> n_experts, seq_off, exp_off, len, page_table;
+  bool dynamic_beta = false, beta_frozen = false;
+  int t = 0;
+  void* kpool = nullptr;
+  void* vpool = nullptr;
+  std::vector<char> staging;
+  int num_cus = 0;
+  // profiling
+  bool prof = false;
+  std::vector<ProfRec> recs;
+  std::vector<hipEvent_t> ev_free;
+  pced_profile totals{};
+
+  template <class T> T* at(size_t off) { return reinterpret_cast<T*>(ws + off); }
+};
+
+namespace {
+
+// Event pair around one launch when profiling is on.
+struct ProfScope {
+  pced_ctx* c;
+  ProfRec rec;
+  hipStream_t st;
+  bool on;
+  ProfScope(pced_ctx* ctx, int cls, hipStream_t s, double bytes, double flops)
+      : c(ctx), st(s), on(ctx->prof) {
+    if (!on) return;
+    rec.cls = cls;
+    rec.bytes = bytes;
+    rec.flops = flops;
+    rec.a = take();
+    rec.b = take();
+    hipEventRecord(rec.a, st);
+  }
+  hipEvent_t take() {
+    if (!c->ev_free.empty()) { hipEvent_t e = c->ev_free.back(); c->ev_free.pop_back(); return e; }
+    hipEvent_t e = nullptr;
+    hipEventCreate(&e);
+    return e;
+  }
+  ~ProfScope() {
+    if (!on) return;
+    hipEventRecord(rec.b, st);
+    c->recs.push_back(rec);
+  }
+};
+
+int device_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 256;
+  return n;
+}
+
+// Tokens per attention split: enough work items to fill the chip several times
+// over (the ragged tail of the last wave of work items is what limits a launch),
+// while keeping each split long enough to amortise its partial-state write.
+int choose_split_tokens(const pced_ctx* c) {
+  long page_heads = 0;
+  for (int s = 0; s < c->S; ++s) page_heads += ceil_div(c->len[s] + 1, kPage);
+  page_heads *= c->cfg.n_kv_heads;
+  const long target = (long)c->num_cus * 8;
+  int sp = (int)std::max<long>(1, (page_heads + target - 1) / target);
+  sp = std::min(sp, 64);
+  return sp * kPage;
+}
+
+int count_work(const pced_ctx* c, int split_tokens) {
+  long n = 0;
+  for (int s = 0; s < c->S; ++s) n += ceil_div(c->len[s] + 1, split_tokens);
+  return (int)n;
+}
+
+pced_status check_ctx(const pced_ctx* c, bool need_loaded) {
+  if (!c) return fail(PCED_ERR_INVALID_ARG, "ctx is NULL");
+  if (need_loaded && !c->loaded) return fail(PCED_ERR_STATE, "no batch loaded (call pced_load_caches first)");
+  return PCED_OK;
+}
+
+// Launch the beta (first step) and fuse kernels over `logits`.
+pced_status run_fuse(pced_ctx* c, const float* logits, bool refresh_beta, int32_t* tokens_out,
+                     int tok_stride, const pced_step_out* extra, hipStream_t st) {
+  const pced_config& cfg = c->cfg;
+  if (c->dynamic_beta && refresh_beta) {
+    BetaArgs b{};
+    b.logits = logits;
+    b.query_seq0 = c->at<int32_t>(c->lay.query_seq0);
+    b.exp_seq = c->at<int32_t>(c->lay.exp_seq);
+    b.exp_query = c->at<int32_t>(c->lay.exp_query);
+    b.lse_part = c->at<float>(c->lay.lse_part);
+    b.jsd_part = c->at<float>(c->lay.jsd_part);
+    b.tickets = c->at<int32_t>(c->lay.tick_beta);
+    b.beta = c->at<float>(c->lay.beta);
+    b.V = cfg.vocab;
+    b.nchunk = c->lay.nchunk;
+    ProfScope ps(c, PCED_PROF_BETA, st, (double)(c->S + 2.0 * c->NE) * cfg.vocab * 4, 0);
+    HIP_OK(launch_beta(b, c->S, c->NE, st));
+    c->beta_frozen = true;
+  }
+  FuseArgs f{};
+  f.logits = logits;
+  f.query_seq0 = c->at<int32_t>(c->lay.query_seq0);
+  f.query_exp0 = c->at<int32_t>(c->lay.query_exp0);
+  f.beta = c->at<float>(c->lay.beta);
+  f.prior = c->at<float>(c->lay.prior);
+  f.part = c->at<float>(c->lay.fuse_part);
+  f.tickets = c->at<int32_t>(c->lay.tick_fuse);
+  f.tokens_out = tokens_out;
+  f.prev_tok = c->at<int32_t>(c->lay.prev_tok);
+  f.winner = extra ? extra->winner : nullptr;
+  f.top1 = extra ? extra->top1 : nullptr;
+  f.top2 = extra ? extra->top2 : nullptr;
+  f.V = cfg.vocab;
+  f.nblk = c->lay.nblk_fuse;
+  f.tok_stride = tok_stride;
+  {
+    ProfScope ps(c, PCED_PROF_FUSE, st, (double)c->S * cfg.vocab * 4, 0);
+    HIP_OK(launch_fuse(f, c->B, st));
+  }
+  if (extra && extra->beta_used)
+    HIP_OK(hipMemcpyAsync(extra->beta_used, c->at<float>(c->lay.beta), (size_t)c->NE * 4,
+                          hipMemcpyDeviceToDevice, st));
+  return PCED_OK;
+}
+
+pced_status run_lmhead(pced_ctx* c, const void* x, int M, const void* w, float* logits, hipStream_t st) {
+  const pced_config& cfg = c->cfg;
+  LmArgs a{};
+  a.x = x;
+  a.w = w;
+  a.logits = logits;
+  a.M = M;
+  a.V = cfg.vocab;
+  a.K = cfg.hidden;
+  a.rms = cfg.norm == PCED_NORM_RMS;
+  const double es = (double)esize_of(cfg);
+  ProfScope ps(c, PCED_PROF_LMHEAD, st,
+               (double)cfg.vocab * cfg.hidden * es + (double)M * cfg.hidden * es + (double)M * cfg.vocab * 4,
+               2.0 * M * cfg.vocab * cfg.hidden);
+  HIP_OK(launch_lmhead(a, c->bf16, st));
+  return PCED_OK;
+}
+
+// The step body shared by pced_step and pced_generate.
+pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* v_new, const void* w,
+                     int32_t* tokens_out, int tok_stride, const pced_step_out* extra, hipStream_t st) {
+  const pced_config& cfg = c->cfg;
+  const int P = cfg.max_pages_per_seq;
+  for (int s = 0; s < c->S; ++s) {
+    const int pidx = c->len[s] / kPage;
+    if (pidx >= P || c->page_table[(size_t)s * P + pidx] < 0)
+      return fail(PCED_ERR_CAPACITY, "sequence %d has no page for token %d", s, c->len[s]);
+  }
+  const int split = choose_split_tokens(c);
+  const int n_work = count_work(c, split);
+  if (n_work > c->lay.max_work) return fail(PCED_ERR_CAPACITY, "attention work list exceeds workspace");
+  const double es = (double)esize_of(cfg);
+
+  AppendArgs ap{};
+  ap.k_new = k_new;
+  ap.v_new = v_new;
+  ap.kpool = c->kpool;
+  ap.vpool = c->vpool;
+  ap.len0 = c->at<int32_t>(c->lay.len0);
+  ap.page_table = c->at<int32_t>(c->lay.page_table);
+  ap.work_off = c->at<int32_t>(c->lay.work_off);
+  ap.n_seqs = c->S;
+  ap.n_layers = cfg.n_layers;
+  ap.n_kv_heads = cfg.n_kv_heads;
+  ap.head_dim = cfg.head_dim;
+  ap.max_pages = cfg.max_pages;
+  ap.maxpps = P;
+  ap.t = c->t;
+  ap.split_tokens = split;
+  {
+    ProfScope ps(c, PCED_PROF_APPEND, st,
+                 4.0 * c->S * cfg.n_layers * cfg.n_kv_heads * cfg.head_dim * es, 0);
+    HIP_OK(launch_append(ap, c->bf16, st));
+  }
+
+  AttnArgs at{};
+  at.q = q;
+  at.kpool = c->kpool;
+  at.vpool = c->vpool;
+  at.len0 = ap.len0;
+  at.page_table = ap.page_table;
+  at.work_off = ap.work_off;
+  at.part_acc = c->at<float>(c->lay.part_acc);
+  at.part_ml = c->at<float>(c->lay.part_ml);
+  at.tickets = c->at<int32_t>(c->lay.tick_attn);
+  at.x_out = c->at<void>(c->lay.x);
+  at.attn_out = extra ? extra->attn_out : nullptr;
+  at.hidden_out = extra ? extra->hidden : nullptr;
+  at.n_seqs = c->S;
+  at.n_layers = cfg.n_layers;
+  at.n_q_heads = cfg.n_q_heads;
+  at.n_kv_heads = cfg.n_kv_heads;
+  at.group = c->G;
+  at.max_pages = cfg.max_pages;
+  at.maxpps = P;
+  at.t = c->t;
+  at.split_tokens = split;
+  at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)cfg.head_dim));
+  double kv_tokens = 0;
+  for (int s = 0; s < c->S; ++s) kv_tokens += c->len[s] + 1;
+  const double attn_bytes = kv_tokens * 2.0 * cfg.n_kv_heads * cfg.head_dim * es +
+                            2.0 * c->S * cfg.n_q_heads * cfg.head_dim * es;
+  const double attn_flops = kv_tokens * 4.0 * cfg.n_q_heads * cfg.head_dim;
+  for (int l = 0; l < cfg.n_layers; ++l) {
+    at.layer = l;
+    at.is_last_layer = l == cfg.n_layers - 1;
+    ProfScope ps(c, PCED_PROF_ATTN, st, attn_bytes, attn_flops);
+    HIP_OK(launch_attn(at, n_work * cfg.n_kv_heads, cfg.head_dim, c->bf16, st));
+  }
+
+  float* logits = (extra && extra->logits) ? extra->logits : c->at<float>(c->lay.logits);
+  pced_status r = run_lmhead(c, at.x_out, c->S, w, logits, st);
+  if (r != PCED_OK) return r;
+  r = run_fuse(c, logits, c->dynamic_beta && !c->beta_frozen, tokens_out, tok_stride, extra, st);
+  if (r != PCED_OK) return r;
+  for (int s = 0; s < c->S; ++s) c->len[s] += 1;
+  c->t += 1;
+  return PCED_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t pced_pool_bytes(const pced_config* cfg) {
+  if (!cfg_valid(cfg, nullptr)) return 0;
+  return (size_t)cfg->n_layers * cfg->max_pages * cfg->n_kv_heads * kPage * cfg->head_dim * esize_of(*cfg);
+}
+
+size_t pced_workspace_bytes(const pced_config* cfg) {
+  if (!cfg_valid(cfg, nullptr)) return 0;
+  return make_layout(*cfg).total;
+}
+
+const char* pced_last_error(void) { return g_err.c_str(); }
+
+pced_status pced_create(const pced_config* cfg, void* d_workspace, size_t ws_bytes, pced_ctx** out) {
+  std::string why;
+  if (!out) return fail(PCED_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!cfg_valid(cfg, &why)) return fail(PCED_ERR_INVALID_ARG, "invalid config: %s", why.c_str());
+  if (!d_workspace) return fail(PCED_ERR_INVALID_ARG, "workspace is NULL");
+  if ((uintptr_t)d_workspace % kAlign) return fail(PCED_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  const Layout lay = make_layout(*cfg);
+  if (ws_bytes < lay.total)
+    return fail(PCED_ERR_CAPACITY, "workspace too small: %zu < %zu bytes", ws_bytes, lay.total);
+  pced_ctx* c = new pced_ctx();
+  c->cfg = *cfg;
+  c->lay = lay;
+  c->ws = (char*)d_workspace;
+  c->bf16 = cfg->dtype == PCED_BF16;
+  c->G = cfg->n_q_heads / cfg->n_kv_heads;
+  *out = c;
+  return PCED_OK;
+}
+
+void pced_destroy(pced_ctx* ctx) {
+  if (!ctx) return;
+  for (auto& r : ctx->recs) { hipEventDestroy(r.a); hipEventDestroy(r.b); }
+  for (auto e : ctx->ev_free) hipEventDestroy(e);
+  delete ctx;
+}
+
+pced_status pced_load_caches(pced_ctx* c, int32_t n_queries, const int32_t* n_experts,
+                             const int32_t* cache_len, const void* const* src_k,
+                             const void* const* src_v, void* k_pool, void* v_pool,
+                             const int32_t* page_table, int32_t reserve_tokens,
+                             const float* relevance, float gamma, const float* beta,
+                             hipStream_t st) {
+  pced_status r = check_ctx(c, false);
+  if (r != PCED_OK) return r;
+  const pced_config& cfg = c->cfg;
+  if (n_queries < 1 || n_queries > cfg.max_queries)
+    return fail(PCED_ERR_INVALID_ARG, "n_queries %d not in [1, %d]", n_queries, cfg.max_queries);
+  if (!n_experts || !cache_len || !src_k || !src_v || !k_pool || !v_pool || !relevance)
+    return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  if (!std::isfinite(gamma)) return fail(PCED_ERR_INVALID_ARG, "gamma is not finite");
+  if (reserve_tokens < 0) return fail(PCED_ERR_INVALID_ARG, "reserve_tokens < 0");
+  long S = 0, NE = 0;
+  for (int b = 0; b < n_queries; ++b) {
+    if (n_experts[b] < 1) return fail(PCED_ERR_INVALID_ARG, "query %d has %d experts", b, n_experts[b]);
+    S += n_experts[b] + 1;
+    NE += n_experts[b];
+  }
+  if (S > cfg.max_seqs) return fail(PCED_ERR_CAPACITY, "%ld sequences > max_seqs %d", S, cfg.max_seqs);
+  for (long s = 0; s < S; ++s) {
+    if (cache_len[s] < 1) return fail(PCED_ERR_INVALID_ARG, "cache_len[%ld] = %d < 1", s, cache_len[s]);
+    if (!src_k[s] || !src_v[s]) return fail(PCED_ERR_INVALID_ARG, "source pointer of sequence %ld is NULL", s);
+  }
+  for (long e = 0; e < NE; ++e) {
+    if (!std::isfinite(relevance[e])) return fail(PCED_ERR_INVALID_ARG, "relevance[%ld] is not finite", e);
+    if (beta && !std::isfinite(beta[e])) return fail(PCED_ERR_INVALID_ARG, "beta[%ld] is not finite", e);
+  }
+  const int P = cfg.max_pages_per_seq;
+  std::vector<int32_t> pt((size_t)S * P, -1);
+  if (page_table) {
+    std::vector<char> used(cfg.max_pages, 0);
+    for (long s = 0; s < S; ++s) {
+      const int need = ceil_div(cache_len[s], kPage);
+      if (need > P) return fail(PCED_ERR_CAPACITY, "sequence %ld needs %d pages > max_pages_per_seq", s, need);
+      for (int p = 0; p < P; ++p) {
+        const int32_t id = page_table[s * P + p];
+        if (id < 0) {
+          if (p < need) return fail(PCED_ERR_INVALID_ARG, "sequence %ld: page %d of its cache not given", s, p);
+          continue;
+        }
+        if (id >= cfg.max_pages) return fail(PCED_ERR_INVALID_ARG, "page id %d >= max_pages", id);
+        if (used[id]) return fail(PCED_ERR_INVALID_ARG, "page id %d used twice", id);
+        used[id] = 1;
+        pt[s * P + p] = id;
+      }
+    }
+  } else {
+    long next = 0;
+    for (long s = 0; s < S; ++s) {
+      const int need = ceil_div((long)cache_len[s] + reserve_tokens, kPage);
+      if (need > P) return fail(PCED_ERR_CAPACITY, "sequence %ld needs %d pages > max_pages_per_seq %d", s, need, P);
+      if (next + need > cfg.max_pages) return fail(PCED_ERR_CAPACITY, "pool of %d pages exhausted", cfg.max_pages);
+      for (int p = 0; p < need; ++p) pt[s * P + p] = (int32_t)(next + p);
+      next += need;
+    }
+  }
+  if (c->num_cus == 0) c->num_cus = device_cus();
+
+  // host mirror
+  c->B = n_queries;
+  c->S = (int)S;
+  c->NE = (int)NE;
+  c->n_experts.assign(n_experts, n_experts + n_queries);
+  c->seq_off.assign(n_queries + 1, 0);
+  c->exp_off.assign(n_queries + 1, 0);
+  for (int b = 0; b < n_queries; ++b) {
+    c->seq_off[b + 1] = c->seq_off[b] + n_experts[b] + 1;
+    c->exp_off[b + 1] = c->exp_off[b] + n_experts[b];
+  }
+  c->len.assign(cache_len, cache_len + S);
+  c->page_table = pt;
+
+  // metadata image, uploaded with one copy
+  const Layout& L = c->lay;
+  c->staging.assign(L.meta_end, 0);
+  auto put = [&](size_t off, const void* src, size_t n) { std::memcpy(c->staging.data() + off, src, n); };
+  put(L.len0, cache_len, S * 4);
+  put(L.page_table, pt.data(), pt.size() * 4);
+  std::vector<int32_t> seq_query(S), exp_seq(NE), exp_query(NE);
+  std::vector<float> prior(NE), bfix(NE, 0.f);
+  std::vector<int32_t> items;
+  for (int b = 0; b < n_queries; ++b) {
+    for (int k = 0; k <= n_experts[b]; ++k) seq_query[c->seq_off[b] + k] = b;
+    for (int k = 1; k <= n_experts[b]; ++k) {
+      const int e = c->exp_off[b] + k - 1;
+      exp_seq[e] = c->seq_off[b] + k;
+      exp_query[e] = b;
+      // gamma * ln(r) with r clipped to [1e-8, 1 - 1e-8], in double, rounded once
+      const double rr = std::min(std::max((double)relevance[e], 1e-8), 1.0 - 1e-8);
+      prior[e] = (float)((double)gamma * std::log(rr));
+      if (beta) bfix[e] = beta[e];
+    }
+  }
+  for (long s = 0; s < S; ++s)
+    for (int p = 0; p < ceil_div(cache_len[s], kPage); ++p) { items.push_back((int32_t)s); items.push_back(p); }
+  put(L.seq_query, seq_query.data(), S * 4);
+  put(L.query_seq0, c->seq_off.data(), (n_queries + 1) * 4);
+  put(L.query_exp0, c->exp_off.data(), (n_queries + 1) * 4);
+  put(L.exp_seq, exp_seq.data(), NE * 4);
+  put(L.exp_query, exp_query.data(), NE * 4);
+  put(L.prior, prior.data(), NE * 4);
+  put(L.beta_fixed, bfix.data(), NE * 4);
+  put(L.load_items, items.data(), items.size() * 4);
+  std::vector<uint64_t> sk(S), sv(S);
+  for (long s = 0; s < S; ++s) { sk[s] = (uint64_t)(uintptr_t)src_k[s]; sv[s] = (uint64_t)(uintptr_t)src_v[s]; }
+  put(L.src_k, sk.data(), S * 8);
+  put(L.src_v, sv.data(), S * 8);
+  HIP_OK(hipMemcpyAsync(c->ws, c->staging.data(), L.meta_end, hipMemcpyHostToDevice, st));
+
+  // per-batch device state
+  HIP_OK(launch_fill_i32(c->at<int32_t>(L.tick_attn), 0, (size_t)cfg.max_seqs * cfg.n_kv_heads, st));
+  HIP_OK(launch_fill_i32(c->at<int32_t>(L.tick_fuse), 0, cfg.max_queries, st));
+  HIP_OK(launch_fill_i32(c->at<int32_t>(L.tick_beta), 0, cfg.max_seqs, st));
+  HIP_OK(launch_fill_i32(c->at<int32_t>(L.prev_tok), -1, cfg.max_queries, st));
+  HIP_OK(launch_zero_bytes(c->at<void>(L.x), (size_t)L.rows_pad * cfg.hidden * esize_of(cfg), st));
+  HIP_OK(hipMemcpyAsync(c->at<float>(L.beta), c->at<float>(L.beta_fixed), (size_t)NE * 4,
+                        hipMemcpyDeviceToDevice, st));
+
+  LoadArgs la{};
+  la.src_k = c->at<uint64_t>(L.src_k);
+  la.src_v = c->at<uint64_t>(L.src_v);
+  la.items = c->at<int32_t>(L.load_items);
+  la.len0 = c->at<int32_t>(L.len0);
+  la.page_table = c->at<int32_t>(L.page_table);
+  la.kpool = k_pool;
+  la.vpool = v_pool;
+  la.n_layers = cfg.n_layers;
+  la.n_kv_heads = cfg.n_kv_heads;
+  la.head_dim = cfg.head_dim;
+  la.max_pages = cfg.max_pages;
+  la.maxpps = P;
+  HIP_OK(launch_load(la, (int)(items.size() / 2), c->bf16, st));
+
+  c->kpool = k_pool;
+  c->vpool = v_pool;
+  c->dynamic_beta = beta == nullptr;
+  c->beta_frozen = false;
+  c->t = 0;
+  c->loaded = true;
+  return PCED_OK;
+}
+
+pced_status pced_step(pced_ctx* c, const void* q, const void* k_new, const void* v_new,
+                      const void* lm_head, int32_t* tokens_out, const pced_step_out* extra,
+                      hipStream_t st) {
+  pced_status r = check_ctx(c, true);
+  if (r != PCED_OK) return r;
+  if (!q || !k_new || !v_new || !lm_head || !tokens_out) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  return run_step(c, q, k_new, v_new, lm_head, tokens_out, 1, extra, st);
+}
+
+pced_status pced_generate(pced_ctx* c, int32_t n_steps, const pced_synth* synth, const void* lm_head,
+                          int32_t* tokens_out, const pced_step_out* last_extra, hipStream_t st) {
+  pced_status r = check_ctx(c, true);
+  if (r != PCED_OK) return r;
+  if (!synth || !lm_head || !tokens_out) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  if (n_steps < 1) return fail(PCED_ERR_INVALID_ARG, "n_steps < 1");
+  if (synth->first_token < 0 || synth->first_token >= c->cfg.vocab)
+    return fail(PCED_ERR_INVALID_ARG, "first_token out of range");
+  const int P = c->cfg.max_pages_per_seq;
+  for (int s = 0; s < c->S; ++s) {
+    const long last = (long)c->len[s] + n_steps - 1;
+    const long pidx = last / kPage;
+    if (pidx >= P) return fail(PCED_ERR_CAPACITY, "sequence %d cannot hold %d more tokens", s, n_steps);
+    for (long p = c->len[s] / kPage; p <= pidx; ++p)
+      if (c->page_table[(size_t)s * P + p] < 0)
+        return fail(PCED_ERR_CAPACITY, "sequence %d cannot hold %d more tokens", s, n_steps);
+  }
+  const pced_config& cfg = c->cfg;
+  SynthArgs sa{};
+  sa.q = c->at<void>(c->lay.syn_q);
+  sa.k_new = c->at<void>(c->lay.syn_k);
+  sa.v_new = c->at<void>(c->lay.syn_v);
+  sa.seq_query = c->at<int32_t>(c->lay.seq_query);
+  sa.prev_tok = c->at<int32_t>(c->lay.prev_tok);
+  sa.seed = synth->seed;
+  sa.value_scale = (float)(std::sqrt(3.0) / 65536.0);
+  sa.n_layers = cfg.n_layers;
+  sa.qdim = cfg.n_q_heads * cfg.head_dim;
+  sa.kvdim = cfg.n_kv_heads * cfg.head_dim;
+  sa.first_token = synth->first_token;
+  sa.bf16 = c->bf16;
+  const double es = (double)esize_of(cfg);
+  for (int i = 0; i < n_steps; ++i) {
+    sa.t = c->t;
+    sa.use_first = c->t == 0;
+    {
+      ProfScope ps(c, PCED_PROF_SYNTH, st, (double)c->S * cfg.n_layers * (sa.qdim + 2.0 * sa.kvdim) * es, 0);
+      HIP_OK(launch_synth(sa, c->S, st));
+    }
+    r = run_step(c, sa.q, sa.k_new, sa.v_new, lm_head, tokens_out + i, n_steps,
+                 i == n_steps - 1 ? last_extra : nullptr, st);
+    if (r != PCED_OK) return r;
+  }
+  return PCED_OK;
+}
+
+pced_status pced_lmhead(pced_ctx* c, const void* x, int32_t n_rows, const void* lm_head, float* logits,
+                        hipStream_t st) {
+  pced_status r = check_ctx(c, false);
+  if (r != PCED_OK) return r;
+  if (!x || !lm_head || !logits) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  if (n_rows < 1 || n_rows > c->cfg.max_seqs)
+    return fail(PCED_ERR_INVALID_ARG, "n_rows %d not in [1, %d]", n_rows, c->cfg.max_seqs);
+  // the kernel reads whole 48-row tiles of x: stage the rows in the padded buffer
+  void* xw = c->at<void>(c->lay.x);
+  HIP_OK(launch_copy_rows(x, xw, (size_t)n_rows * c->cfg.hidden * esize_of(c->cfg), st));
+  return run_lmhead(c, xw, n_rows, lm_head, logits, st);
+}
+
+pced_status pced_fuse(pced_ctx* c, const float* logits, int32_t refresh_beta, int32_t* tokens_out,
+                      const pced_step_out* extra, hipStream_t st) {
+  pced_status r = check_ctx(c, true);
+  if (r != PCED_OK) return r;
+  if (!logits || !tokens_out) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  if (c->dynamic_beta && !refresh_beta && !c->beta_frozen)
+    return fail(PCED_ERR_STATE, "dynamic beta has not been computed yet (pass refresh_beta)");
+  return run_fuse(c, logits, refresh_beta != 0, tokens_out, 1, extra, st);
+}
+
+pced_status pced_get_lengths(const pced_ctx* c, int32_t* out, int32_t capacity) {
+  pced_status r = check_ctx(c, true);
+  if (r != PCED_OK) return r;
+  if (!out || capacity < c->S) return fail(PCED_ERR_INVALID_ARG, "output too small");
+  std::copy(c->len.begin(), c->len.end(), out);
+  return PCED_OK;
+}
+
+pced_status pced_profile_enable(pced_ctx* c, int32_t on) {
+  pced_status r = check_ctx(c, false);
+  if (r != PCED_OK) return r;
+  if (on) {
+    for (auto& rec : c->recs) { c->ev_free.push_back(rec.a); c->ev_free.push_back(rec.b); }
+    c->recs.clear();
+    c->totals = pced_profile{};
+  }
+  c->prof = on != 0;
+  return PCED_OK;
+}
+
+pced_status pced_profile_read(pced_ctx* c, pced_profile* out) {
+  pced_status r = check_ctx(c, false);
+  if (r != PCED_OK) return r;
+  if (!out) return fail(PCED_ERR_INVALID_ARG, "out is NULL");
+  for (auto& rec : c->recs) {
+    float ms = 0.f;
+    HIP_OK(hipEventElapsedTime(&ms, rec.a, rec.b));
+    c->totals.launches[rec.cls] += 1;
+    c->totals.total_ms[rec.cls] += ms;
+    c->totals.bytes[rec.cls] += rec.bytes;
+    c->totals.flops[rec.cls] += rec.flops;
+    c->ev_free.push_back(rec.a);
+    c->ev_free.push_back(rec.b);
+  }
+  c->recs.clear();
+  *out = c->totals;
+  return PCED_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,115 @@
+// Internal interface between the host library (pced_api.cpp) and the gfx950
+// kernels (pced_kernels.hip). Not installed; the public ABI is include/pced.h.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pced {
+
+constexpr int kPage = 16;          // tokens per KV page (= MFMA M/K tile edge)
+constexpr int kMaxGroup = 16;      // q-heads per kv-head (MFMA N edge)
+constexpr int kFuseBlock = 256;    // vocab entries per fuse work-group
+constexpr int kBetaChunk = 4096;   // vocab entries per beta work-group
+constexpr int kLmRowsPad = 48;     // hidden-state rows are padded to a multiple of this
+
+// Per-step attention launch arguments (one launch per layer).
+struct AttnArgs {
+  const void* q;            // [S][L][Hq][D]
+  const void* kpool;        // [L][max_pages][Hkv][tile]
+  const void* vpool;
+  const int32_t* len0;      // [S] lengths at load
+  const int32_t* page_table;// [S][maxpps]
+  const int32_t* work_off;  // [S+1] prefix of splits per sequence (this step)
+  float* part_acc;          // [work*Hkv][G][D]
+  float* part_ml;           // [work*Hkv][G][2]  (running max in log2 units, sum)
+  int32_t* tickets;         // [S*Hkv], zero between launches
+  void* x_out;              // [S][Hq*D] layer output, storage type
+  float* attn_out;          // optional [S][L][Hq][D]
+  float* hidden_out;        // optional [S][Hq*D] (last layer only)
+  int n_seqs, n_layers, layer, n_q_heads, n_kv_heads, group;
+  int max_pages, maxpps, t, split_tokens, is_last_layer;
+  float scale_log2;         // log2(e) / sqrt(D)
+};
+
+struct AppendArgs {
+  const void* k_new;        // [S][L][Hkv][D]
+  const void* v_new;
+  void* kpool;
+  void* vpool;
+  const int32_t* len0;
+  const int32_t* page_table;
+  int32_t* work_off;        // [S+1] written by the planning block
+  int n_seqs, n_layers, n_kv_heads, head_dim, max_pages, maxpps, t, split_tokens;
+};
+
+struct LoadArgs {
+  const uint64_t* src_k;    // [S] device pointers to [L][len][Hkv][D]
+  const uint64_t* src_v;
+  const int32_t* items;     // [n_items][2] (sequence, logical page)
+  const int32_t* len0;
+  const int32_t* page_table;
+  void* kpool;
+  void* vpool;
+  int n_layers, n_kv_heads, head_dim, max_pages, maxpps;
+};
+
+struct LmArgs {
+  const void* x;            // [rows_pad][K] storage type, rows >= M zero
+  const void* w;            // [V][K]
+  float* logits;            // [M][V]
+  int M, V, K, rms;
+};
+
+struct FuseArgs {
+  const float* logits;      // [S][V]
+  const int32_t* query_seq0;// [B+1]
+  const int32_t* query_exp0;// [B+1]
+  const float* beta;        // [sum N]
+  const float* prior;       // [sum N] gamma * ln(clip(r)) rounded to fp32
+  float* part;              // [B][nblk][5]
+  int32_t* tickets;         // [B]
+  int32_t* tokens_out;      // [B] with stride
+  int32_t* prev_tok;        // [B]
+  int32_t* winner;          // optional [B]
+  float* top1;              // optional [B]
+  float* top2;              // optional [B]
+  int V, nblk, tok_stride;
+};
+
+struct BetaArgs {
+  const float* logits;      // [S][V]
+  const int32_t* query_seq0;
+  const int32_t* exp_seq;   // [sum N] sequence of each expert slot
+  const int32_t* exp_query; // [sum N] query of each expert slot
+  float* lse_part;          // [S][nchunk][2]
+  float* jsd_part;          // [sum N][nchunk]
+  int32_t* tickets;         // [sum N]
+  float* beta;              // [sum N]
+  int V, nchunk;
+};
+
+struct SynthArgs {
+  void* q;                  // [S][L][Hq*D]
+  void* k_new;              // [S][L][Hkv*D]
+  void* v_new;
+  const int32_t* seq_query; // [S]
+  const int32_t* prev_tok;  // [B]
+  uint64_t seed;
+  float value_scale;        // sqrt(3)/65536 rounded to fp32
+  int n_layers, qdim, kvdim, t, first_token, use_first, bf16;
+};
+
+// launchers (pced_kernels.hip); each returns hipGetLastError() after the launch
+hipError_t launch_fill_i32(int32_t* p, int32_t v, size_t n, hipStream_t st);
+hipError_t launch_zero_bytes(void* p, size_t nbytes, hipStream_t st);
+hipError_t launch_load(const LoadArgs& a, int n_items, bool bf16, hipStream_t st);
+hipError_t launch_append(const AppendArgs& a, bool bf16, hipStream_t st);
+hipError_t launch_attn(const AttnArgs& a, int n_blocks, int head_dim, bool bf16, hipStream_t st);
+hipError_t launch_lmhead(const LmArgs& a, bool bf16, hipStream_t st);
+hipError_t launch_beta(const BetaArgs& a, int n_seqs, int n_exp, hipStream_t st);
+hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st);
+hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st);
+hipError_t launch_copy_rows(const void* src, void* dst, size_t nbytes, hipStream_t st);
+
+}  // namespace pced

@@ -1,0 +1,865 @@
+// gfx950 kernels of the PCED decode step (Parallel Context-of-Experts Decoding,
+// arXiv 2601.08670, Section 3).
+//
+// KV pool tile layout. A tile is one (layer, page, kv-head): 16 tokens x D.
+//   bf16 K tile: element (t, d) at ((d/32)*64 + t + 16*((d%32)/8))*8 + d%8.
+//     Lane l's 16-byte load number i is exactly the A operand of
+//     v_mfma_f32_16x16x32_bf16 for the 16x32 block (tokens, dims 32i..32i+31):
+//     row t = l%16, k = 8*(l/16)..+7.
+//   bf16 V tile: element (t, d) at ((j/2*64 + d%16 + 16*(t/4))*2 + j%2)*4 + t%4,
+//     j = d/16. Lane l's 16-byte load number jj holds the A operands of two
+//     v_mfma_f32_16x16x16_bf16 for V^T blocks j = 2jj, 2jj+1: row d = 16j + l%16,
+//     k = tokens 4*(l/16)..+3.
+//   f32 tiles are row-major [t][d].
+// Every wave load of a page is therefore a contiguous 1 KiB.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "pced_internal.h"
+
+namespace pced {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kNegInf = -INFINITY;
+
+__device__ __forceinline__ float bf2f(uint32_t b) { return __uint_as_float(b << 16); }
+
+// round-to-nearest-even float -> bf16 bits (finite inputs)
+__device__ __forceinline__ uint32_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ int kswz(int t, int d) {
+  return ((d >> 5) * 64 + t + 16 * ((d & 31) >> 3)) * 8 + (d & 7);
+}
+__device__ __forceinline__ int vswz(int t, int d) {
+  const int j = d >> 4;
+  return (((j >> 1) * 64 + (d & 15) + 16 * (t >> 2)) * 2 + (j & 1)) * 4 + (t & 3);
+}
+
+// ------------------------------------------------------------------ utilities
+
+__global__ void k_fill_i32(int32_t* p, int32_t v, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+__global__ void k_zero_u32(uint32_t* p, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+// ------------------------------------------------------------- cache loading
+
+// One block per (sequence, logical page) item and layer: copies the page's
+// tokens of every kv-head from the contiguous [L][len][Hkv][D] source into the
+// pool tiles, zero-filling slots past the sequence's length.
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_load(LoadArgs a) {
+  const int item = blockIdx.x, l = blockIdx.y;
+  const int s = a.items[2 * item], p = a.items[2 * item + 1];
+  const int len = a.len0[s];
+  const int phys = a.page_table[(size_t)s * a.maxpps + p];
+  const int Hkv = a.n_kv_heads, D = a.head_dim;
+  const size_t tile = (size_t)kPage * D;
+  const size_t tile0 = ((size_t)l * a.max_pages + phys) * Hkv;
+  const int n = Hkv * kPage * D;
+  for (int idx = threadIdx.x; idx < n; idx += blockDim.x) {
+    const int g = idx / (kPage * D), rem = idx % (kPage * D);
+    const int t = rem / D, d = rem % D;
+    const int tok = p * kPage + t;
+    const size_t src = (((size_t)l * len + tok) * Hkv + g) * D + d;
+    const size_t base = (tile0 + g) * tile;
+    if (BF16) {
+      const uint16_t* sk = (const uint16_t*)a.src_k[s];
+      const uint16_t* sv = (const uint16_t*)a.src_v[s];
+      const uint16_t kv = tok < len ? sk[src] : 0, vv = tok < len ? sv[src] : 0;
+      ((uint16_t*)a.kpool)[base + kswz(t, d)] = kv;
+      ((uint16_t*)a.vpool)[base + vswz(t, d)] = vv;
+    } else {
+      const float* sk = (const float*)a.src_k[s];
+      const float* sv = (const float*)a.src_v[s];
+      ((float*)a.kpool)[base + (size_t)t * D + d] = tok < len ? sk[src] : 0.f;
+      ((float*)a.vpool)[base + (size_t)t * D + d] = tok < len ? sv[src] : 0.f;
+    }
+  }
+}
+
+// --------------------------------------------- shared-history append + plan
+
+// Blocks 0 .. S*L-1: write step t's K/V row of (sequence, layer) into slot
+// len0 + t of the sequence's pages (Section 3: the chosen token joins every
+// expert's history). Block S*L: prefix of attention splits per sequence for
+// this step's lengths len0 + t + 1.
+template <bool BF16>
+__global__ __launch_bounds__(128) void k_append(AppendArgs a) {
+  const int S = a.n_seqs, L = a.n_layers;
+  if ((int)blockIdx.x == S * L) {
+    if (threadIdx.x == 0) {
+      int off = 0;
+      for (int s = 0; s < S; ++s) {
+        a.work_off[s] = off;
+        off += (a.len0[s] + a.t + 1 + a.split_tokens - 1) / a.split_tokens;
+      }
+      a.work_off[S] = off;
+    }
+    return;
+  }
+  const int s = blockIdx.x / L, l = blockIdx.x % L;
+  const int pos = a.len0[s] + a.t;
+  const int phys = a.page_table[(size_t)s * a.maxpps + pos / kPage];
+  const int slot = pos % kPage;
+  const int Hkv = a.n_kv_heads, D = a.head_dim;
+  const size_t tile = (size_t)kPage * D;
+  const size_t tile0 = ((size_t)l * a.max_pages + phys) * Hkv;
+  const size_t src0 = ((size_t)s * L + l) * Hkv * D;
+  for (int idx = threadIdx.x; idx < Hkv * D; idx += blockDim.x) {
+    const int g = idx / D, d = idx % D;
+    const size_t base = (tile0 + g) * tile;
+    if (BF16) {
+      ((uint16_t*)a.kpool)[base + kswz(slot, d)] = ((const uint16_t*)a.k_new)[src0 + idx];
+      ((uint16_t*)a.vpool)[base + vswz(slot, d)] = ((const uint16_t*)a.v_new)[src0 + idx];
+    } else {
+      ((float*)a.kpool)[base + (size_t)slot * D + d] = ((const float*)a.k_new)[src0 + idx];
+      ((float*)a.vpool)[base + (size_t)slot * D + d] = ((const float*)a.v_new)[src0 + idx];
+    }
+  }
+}
+
+// ----------------------------------------------------------- decode attention
+
+struct WorkItem {
+  int s, g, split, nsplit, tok_begin, tok_end;
+};
+
+__device__ __forceinline__ WorkItem decode_work(const AttnArgs& a, int w) {
+  WorkItem it;
+  it.g = w % a.n_kv_heads;
+  const int item = w / a.n_kv_heads;
+  int lo = 0, hi = a.n_seqs;  // largest s with work_off[s] <= item
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (a.work_off[mid] <= item) lo = mid; else hi = mid;
+  }
+  it.s = lo;
+  it.split = item - a.work_off[lo];
+  it.nsplit = a.work_off[lo + 1] - a.work_off[lo];
+  const int len = a.len0[lo] + a.t + 1;
+  it.tok_begin = it.split * a.split_tokens;
+  it.tok_end = min(len, it.tok_begin + a.split_tokens);
+  return it;
+}
+
+// Write 4 consecutive output dims of one q-head: fp32 debug copy, the layer
+// output in the storage type, and (last layer) the fp32 value of the stored x.
+template <bool BF16>
+__device__ __forceinline__ void write_o4(const AttnArgs& a, int s, int head, int d, int D, float4 o) {
+  const int Hq = a.n_q_heads;
+  const size_t xo = (size_t)s * Hq * D + (size_t)head * D + d;
+  if (a.attn_out) {
+    float4* p = (float4*)(a.attn_out + (((size_t)s * a.n_layers + a.layer) * Hq + head) * D + d);
+    *p = o;
+  }
+  if (BF16) {
+    const uint32_t b0 = f2bf(o.x), b1 = f2bf(o.y), b2 = f2bf(o.z), b3 = f2bf(o.w);
+    uint2 pk;
+    pk.x = b0 | (b1 << 16);
+    pk.y = b2 | (b3 << 16);
+    *(uint2*)((uint16_t*)a.x_out + xo) = pk;
+    if (a.is_last_layer && a.hidden_out)
+      *(float4*)(a.hidden_out + xo) = make_float4(bf2f(b0), bf2f(b1), bf2f(b2), bf2f(b3));
+  } else {
+    *(float4*)((float*)a.x_out + xo) = o;
+    if (a.is_last_layer && a.hidden_out) *(float4*)(a.hidden_out + xo) = o;
+  }
+}
+
+// The last of a sequence's split waves to finish (atomic ticket) merges the
+// partial softmax states of all splits in split order:
+//   m* = max_j m_j,  o = sum_j acc_j 2^(m_j - m*) / sum_j l_j 2^(m_j - m*).
+template <bool BF16>
+__device__ void ticket_and_combine(const AttnArgs& a, const WorkItem& it, int D) {
+  const int lane = threadIdx.x;
+  const int G = a.group, Hkv = a.n_kv_heads;
+  __threadfence();
+  int prev = 0;
+  if (lane == 0)
+    prev = __hip_atomic_fetch_add(a.tickets + it.s * Hkv + it.g, 1, __ATOMIC_ACQ_REL,
+                                  __HIP_MEMORY_SCOPE_AGENT);
+  prev = __shfl(prev, 0);
+  if (prev != it.nsplit - 1) return;
+  __threadfence();
+  const int w0 = a.work_off[it.s] * Hkv + it.g;
+  const int n4 = G * D / 4;
+  for (int idx = lane; idx < n4; idx += 64) {
+    const int h = (idx * 4) / D, d = (idx * 4) % D;
+    float mstar = kNegInf;
+    for (int j = 0; j < it.nsplit; ++j)
+      mstar = fmaxf(mstar, a.part_ml[((size_t)(w0 + j * Hkv) * G + h) * 2]);
+    float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+    float den = 0.f;
+    for (int j = 0; j < it.nsplit; ++j) {
+      const size_t wj = (size_t)(w0 + j * Hkv);
+      const float sc = exp2f(a.part_ml[(wj * G + h) * 2] - mstar);
+      den += a.part_ml[(wj * G + h) * 2 + 1] * sc;
+      const float4 v = *(const float4*)(a.part_acc + (wj * G + h) * D + d);
+      num.x += v.x * sc; num.y += v.y * sc; num.z += v.z * sc; num.w += v.w * sc;
+    }
+    const float inv = 1.0f / den;
+    write_o4<BF16>(a, it.s, it.g * G + h, d, D,
+                   make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv));
+  }
+  if (lane == 0) a.tickets[it.s * Hkv + it.g] = 0;
+}
+
+// Split-K flash decoding for bf16 caches, one wave per (sequence, kv-head,
+// split). The G q-heads of the kv-head ride in the N dimension of the matrix
+// cores, so every K/V byte is read once for all of them:
+//   S^T[16 tok x 16 heads] = K[16 x D] Q^T          (D/32 x 16x16x32 MFMA)
+//   O^T[D x 16 heads]     += V^T[D x 16 tok] P^T    (D/16 x 16x16x16 MFMA)
+// P comes straight out of the S^T accumulator layout (lane l: head l%16,
+// tokens 4*(l/16)..+3), which is the B operand layout of the second product.
+// Online softmax in base 2 with log2(e)/sqrt(D) folded into the score scale.
+template <int D>
+__global__ __launch_bounds__(64) void k_attn_bf16(AttnArgs a) {
+  constexpr int NC = D / 32;
+  constexpr int NJ = D / 16;
+  const int lane = threadIdx.x;
+  const int col = lane & 15, quad = lane >> 4;
+  const int G = a.group, Hkv = a.n_kv_heads;
+  const WorkItem it = decode_work(a, blockIdx.x);
+  const int pg0 = it.tok_begin / kPage, pg1 = (it.tok_end + kPage - 1) / kPage;
+
+  bf16x8 qop[NC];
+  {
+    const uint16_t* q = (const uint16_t*)a.q +
+        (((size_t)it.s * a.n_layers + a.layer) * a.n_q_heads + (size_t)it.g * G + col) * D;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      uint4 v = make_uint4(0u, 0u, 0u, 0u);
+      if (col < G) v = *(const uint4*)(q + 32 * i + 8 * quad);
+      qop[i] = as_bf16x8(v);
+    }
+  }
+  const size_t tile = (size_t)kPage * D;
+  const uint4* kp = (const uint4*)a.kpool;
+  const uint4* vp = (const uint4*)a.vpool;
+  const size_t lay = (size_t)a.layer * a.max_pages * Hkv + it.g;
+  const int32_t* pt = a.page_table + (size_t)it.s * a.maxpps;
+  const size_t tile16 = tile / 8;  // tile size in 16-byte units
+
+  uint4 kc[NC], vc[NC];
+  {
+    const size_t t0 = (lay + (size_t)pt[pg0] * Hkv) * tile16;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      kc[i] = kp[t0 + i * 64 + lane];
+      vc[i] = vp[t0 + i * 64 + lane];
+    }
+  }
+  f32x4 acc[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = kNegInf, l_part = 0.f;
+
+  for (int p = pg0; p < pg1; ++p) {
+    uint4 kn[NC], vn[NC];
+    const bool more = p + 1 < pg1;
+    if (more) {
+      const size_t t1 = (lay + (size_t)pt[p + 1] * Hkv) * tile16;
+#pragma unroll
+      for (int i = 0; i < NC; ++i) {
+        kn[i] = kp[t1 + i * 64 + lane];
+        vn[i] = vp[t1 + i * 64 + lane];
+      }
+    }
+    f32x4 sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < NC; ++i)
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kc[i]), qop[i], sc, 0, 0, 0);
+    const int tb = p * kPage + 4 * quad;
+    float z[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) z[r] = (tb + r < it.tok_end) ? sc[r] * a.scale_log2 : kNegInf;
+    float mx = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = exp2f(m_run - m_new);
+    uint32_t pb[4];
+    float psum = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      pb[r] = f2bf(exp2f(z[r] - m_new));
+      psum += bf2f(pb[r]);   // normaliser uses exactly the weights fed to the MFMA
+    }
+    l_part = l_part * alpha + psum;
+    m_run = m_new;
+    s16x4 pop;
+    pop[0] = (short)pb[0]; pop[1] = (short)pb[1]; pop[2] = (short)pb[2]; pop[3] = (short)pb[3];
+    if (p * kPage + kPage > it.tok_end) {
+      // Partial last page: slots past the sequence end hold stale or never-written
+      // bits. Their weights are 0, but 0 * NaN is NaN inside the matrix core, so
+      // clear the V elements of those tokens (lane elements r = 0..3 are the same
+      // tokens tb + r as its weights).
+      const uint32_t m01 = (tb + 0 < it.tok_end ? 0x0000FFFFu : 0u) | (tb + 1 < it.tok_end ? 0xFFFF0000u : 0u);
+      const uint32_t m23 = (tb + 2 < it.tok_end ? 0x0000FFFFu : 0u) | (tb + 3 < it.tok_end ? 0xFFFF0000u : 0u);
+#pragma unroll
+      for (int jj = 0; jj < NC; ++jj) {
+        vc[jj].x &= m01; vc[jj].y &= m23; vc[jj].z &= m01; vc[jj].w &= m23;
+      }
+    }
+#pragma unroll
+    for (int jj = 0; jj < NC; ++jj) {
+      const s16x4 va = __builtin_bit_cast(s16x4, make_uint2(vc[jj].x, vc[jj].y));
+      const s16x4 vb = __builtin_bit_cast(s16x4, make_uint2(vc[jj].z, vc[jj].w));
+      acc[2 * jj] *= alpha;
+      acc[2 * jj + 1] *= alpha;
+      acc[2 * jj] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pop, acc[2 * jj], 0, 0, 0);
+      acc[2 * jj + 1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vb, pop, acc[2 * jj + 1], 0, 0, 0);
+    }
+    if (more) {
+#pragma unroll
+      for (int i = 0; i < NC; ++i) { kc[i] = kn[i]; vc[i] = vn[i]; }
+    }
+  }
+  float l_tot = l_part + __shfl_xor(l_part, 16);
+  l_tot += __shfl_xor(l_tot, 32);
+
+  if (it.nsplit == 1) {
+    if (col < G) {
+      const float inv = 1.0f / l_tot;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        write_o4<true>(a, it.s, it.g * G + col, 16 * j + 4 * quad, D,
+                       make_float4(acc[j][0] * inv, acc[j][1] * inv, acc[j][2] * inv, acc[j][3] * inv));
+    }
+    return;
+  }
+  const size_t w = blockIdx.x;
+  if (col < G) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      *(float4*)(a.part_acc + (w * G + col) * D + 16 * j + 4 * quad) =
+          make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+    if (quad == 0) {
+      a.part_ml[(w * G + col) * 2] = m_run;
+      a.part_ml[(w * G + col) * 2 + 1] = l_tot;
+    }
+  }
+  ticket_and_combine<true>(a, it, D);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// fp32 caches (small/validation shapes): one wave per work item, lanes over
+// head dims (D <= 128), one token at a time, per-head online softmax in base 2.
+__global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a, int D) {
+  const int lane = threadIdx.x;
+  const int G = a.group, Hkv = a.n_kv_heads;
+  const WorkItem it = decode_work(a, blockIdx.x);
+  const float* q = (const float*)a.q +
+      (((size_t)it.s * a.n_layers + a.layer) * a.n_q_heads + (size_t)it.g * G) * D;
+  const bool has0 = lane < D, has1 = lane + 64 < D;
+  float qv[kMaxGroup][2], m[kMaxGroup], l[kMaxGroup], acc[kMaxGroup][2];
+#pragma unroll
+  for (int h = 0; h < kMaxGroup; ++h) {
+    qv[h][0] = (h < G && has0) ? q[h * D + lane] : 0.f;
+    qv[h][1] = (h < G && has1) ? q[h * D + lane + 64] : 0.f;
+    m[h] = kNegInf; l[h] = 0.f; acc[h][0] = 0.f; acc[h][1] = 0.f;
+  }
+  const size_t tile = (size_t)kPage * D;
+  const float* kp = (const float*)a.kpool;
+  const float* vp = (const float*)a.vpool;
+  const size_t lay = (size_t)a.layer * a.max_pages * Hkv + it.g;
+  const int32_t* pt = a.page_table + (size_t)it.s * a.maxpps;
+  for (int tok = it.tok_begin; tok < it.tok_end; ++tok) {
+    const size_t base = (lay + (size_t)pt[tok / kPage] * Hkv) * tile + (size_t)(tok % kPage) * D;
+    const float k0 = has0 ? kp[base + lane] : 0.f, k1 = has1 ? kp[base + lane + 64] : 0.f;
+    const float v0 = has0 ? vp[base + lane] : 0.f, v1 = has1 ? vp[base + lane + 64] : 0.f;
+#pragma unroll
+    for (int h = 0; h < kMaxGroup; ++h) {
+      if (h >= G) break;
+      const float z = wave_sum(qv[h][0] * k0 + qv[h][1] * k1) * a.scale_log2;
+      const float mn = fmaxf(m[h], z);
+      const float al = exp2f(m[h] - mn), pz = exp2f(z - mn);
+      l[h] = l[h] * al + pz;
+      acc[h][0] = acc[h][0] * al + pz * v0;
+      acc[h][1] = acc[h][1] * al + pz * v1;
+      m[h] = mn;
+    }
+  }
+  if (it.nsplit == 1) {
+#pragma unroll
+    for (int h = 0; h < kMaxGroup; ++h) {
+      if (h >= G) break;
+      const float inv = 1.0f / l[h];
+      const int head = it.g * G + h;
+      const size_t xo = (size_t)it.s * a.n_q_heads * D + (size_t)head * D;
+      const size_t ao = (((size_t)it.s * a.n_layers + a.layer) * a.n_q_heads + head) * D;
+      for (int c = 0; c < 2; ++c) {
+        const int d = lane + 64 * c;
+        if (d >= D) break;
+        const float o = acc[h][c] * inv;
+        ((float*)a.x_out)[xo + d] = o;
+        if (a.attn_out) a.attn_out[ao + d] = o;
+        if (a.is_last_layer && a.hidden_out) a.hidden_out[xo + d] = o;
+      }
+    }
+    return;
+  }
+  const size_t w = blockIdx.x;
+#pragma unroll
+  for (int h = 0; h < kMaxGroup; ++h) {
+    if (h >= G) break;
+    if (has0) a.part_acc[(w * G + h) * D + lane] = acc[h][0];
+    if (has1) a.part_acc[(w * G + h) * D + lane + 64] = acc[h][1];
+    if (lane == 0) {
+      a.part_ml[(w * G + h) * 2] = m[h];
+      a.part_ml[(w * G + h) * 2 + 1] = l[h];
+    }
+  }
+  ticket_and_combine<false>(a, it, D);
+}
+
+// ------------------------------------------------------------------- LM head
+
+__device__ __forceinline__ float sumsq8(bf16x8 v) {
+  const uint4 u = __builtin_bit_cast(uint4, v);
+  float s = 0.f;
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float lo = __uint_as_float(w[i] << 16), hi = __uint_as_float(w[i] & 0xFFFF0000u);
+    s += lo * lo + hi * hi;
+  }
+  return s;
+}
+
+// logits[m][v] = rho_m * sum_k x[m][k] W[v][k] on the matrix cores:
+// C^T[16 vocab x 16 rows] += W[16 x 32] X^T[32 x 16] (v_mfma_f32_16x16x32_bf16).
+// A wave owns 16*VT vocab rows and streams each W byte once per 16*NT rows of x;
+// each lane reads 32 contiguous bytes of a W row per 64-wide k step, so a row's
+// four lanes cover one 128-byte line. rho (RMS scale) is accumulated from the
+// same x operand loads.
+template <int VT, int NT>
+__global__ __launch_bounds__(256) void k_lmhead_bf16(LmArgs a) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = lane & 15, quad = lane >> 4;
+  const int vbase = (blockIdx.x * 4 + wave) * (16 * VT);
+  if (vbase >= a.V) return;
+  const int K = a.K;
+  const uint16_t* W = (const uint16_t*)a.w;
+  const uint16_t* X = (const uint16_t*)a.x;
+  const uint16_t* wrow[VT];
+#pragma unroll
+  for (int vt = 0; vt < VT; ++vt) {
+    const int row = min(vbase + 16 * vt + col, a.V - 1);
+    wrow[vt] = W + (size_t)row * K + 16 * quad;
+  }
+  for (int m0 = 0; m0 < a.M; m0 += 16 * NT) {
+    f32x4 acc[VT][NT];
+    float ss[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      ss[nt] = 0.f;
+#pragma unroll
+      for (int vt = 0; vt < VT; ++vt) acc[vt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    const uint16_t* xrow[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) xrow[nt] = X + (size_t)(m0 + 16 * nt + col) * K + 16 * quad;
+    for (int k0 = 0; k0 < K; k0 += 64) {
+      bf16x8 a0[VT], a1[VT], b0[NT], b1[NT];
+#pragma unroll
+      for (int vt = 0; vt < VT; ++vt) {
+        a0[vt] = as_bf16x8(*(const uint4*)(wrow[vt] + k0));
+        a1[vt] = as_bf16x8(*(const uint4*)(wrow[vt] + k0 + 8));
+      }
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        b0[nt] = as_bf16x8(*(const uint4*)(xrow[nt] + k0));
+        b1[nt] = as_bf16x8(*(const uint4*)(xrow[nt] + k0 + 8));
+        ss[nt] += sumsq8(b0[nt]) + sumsq8(b1[nt]);
+      }
+#pragma unroll
+      for (int vt = 0; vt < VT; ++vt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          acc[vt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[vt], b0[nt], acc[vt][nt], 0, 0, 0);
+          acc[vt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[vt], b1[nt], acc[vt][nt], 0, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      float t = ss[nt] + __shfl_xor(ss[nt], 16);
+      t += __shfl_xor(t, 32);
+      const float rho = a.rms ? 1.0f / sqrtf(t / (float)K + 1e-5f) : 1.0f;
+      const int m = m0 + 16 * nt + col;
+      if (m >= a.M) continue;
+#pragma unroll
+      for (int vt = 0; vt < VT; ++vt) {
+        const int v = vbase + 16 * vt + 4 * quad;
+        float* out = a.logits + (size_t)m * a.V + v;
+        const f32x4 c = acc[vt][nt];
+        if (v + 3 < a.V && (a.V & 3) == 0) {
+          *(float4*)out = make_float4(c[0] * rho, c[1] * rho, c[2] * rho, c[3] * rho);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (v + r < a.V) out[r] = c[r] * rho;
+        }
+      }
+    }
+  }
+}
+
+// fp32 LM head for small validation shapes: one thread per vocab row.
+__global__ __launch_bounds__(256) void k_lmhead_f32(LmArgs a) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= a.V) return;
+  const float* W = (const float*)a.w + (size_t)v * a.K;
+  for (int m = 0; m < a.M; ++m) {
+    const float* x = (const float*)a.x + (size_t)m * a.K;
+    float ss = 0.f, dot = 0.f;
+    for (int k = 0; k < a.K; ++k) {
+      ss += x[k] * x[k];
+      dot += x[k] * W[k];
+    }
+    const float rho = a.rms ? 1.0f / sqrtf(ss / (float)a.K + 1e-5f) : 1.0f;
+    a.logits[(size_t)m * a.V + v] = dot * rho;
+  }
+}
+
+// ---------------------------------------------------------- Eq. 2 and Eq. 3
+
+struct Top2 {
+  float v1; int i1; int k1; float v2; int i2;
+};
+
+// order: higher score first, lower token id on equal scores
+__device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
+  return va > vb || (va == vb && ia < ib);
+}
+
+__device__ __forceinline__ Top2 merge(const Top2& A, const Top2& B) {
+  Top2 R;
+  if (better(A.v1, A.i1, B.v1, B.i1)) {
+    R.v1 = A.v1; R.i1 = A.i1; R.k1 = A.k1;
+    if (better(A.v2, A.i2, B.v1, B.i1)) { R.v2 = A.v2; R.i2 = A.i2; } else { R.v2 = B.v1; R.i2 = B.i1; }
+  } else {
+    R.v1 = B.v1; R.i1 = B.i1; R.k1 = B.k1;
+    if (better(B.v2, B.i2, A.v1, A.i1)) { R.v2 = B.v2; R.i2 = B.i2; } else { R.v2 = A.v1; R.i2 = A.i1; }
+  }
+  return R;
+}
+
+__device__ __forceinline__ Top2 shfl_top2(const Top2& x, int o) {
+  Top2 y;
+  y.v1 = __shfl_xor(x.v1, o); y.i1 = __shfl_xor(x.i1, o); y.k1 = __shfl_xor(x.k1, o);
+  y.v2 = __shfl_xor(x.v2, o); y.i2 = __shfl_xor(x.i2, o);
+  return y;
+}
+
+// Two-level argmax: a wave merges its lanes' candidates with shuffles, the block
+// merges its waves through LDS. Deterministic for any merge order: "better" is a
+// total order on (score, token).
+__device__ Top2 block_top2(Top2 c) {
+  __shared__ Top2 red[kFuseBlock / 64];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) c = merge(c, shfl_top2(c, o));
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[wave] = c;
+  __syncthreads();
+  Top2 r = red[0];
+  for (int i = 1; i < (int)(blockDim.x >> 6); ++i) r = merge(r, red[i]);
+  __syncthreads();
+  return r;
+}
+
+// One block per (query, 256-token vocab slice). Per token v:
+//   s_hat_k(v) = ((1 + beta_k) s_k(v) - beta_k s_0(v)) + gamma ln r_k     (Eq. 2)
+// evaluated in float32 in exactly that order without fused multiply-adds,
+// S(v) = max over experts 1..N (lowest k on ties), then the block's best and
+// second-best tokens. The last block of a query (atomic ticket) merges all
+// slices and writes y_t (Eq. 3), the expert, and the two scores.
+__global__ __launch_bounds__(kFuseBlock) void k_fuse(FuseArgs a) {
+#pragma clang fp contract(off)
+  const int b = blockIdx.y;
+  const int s0 = a.query_seq0[b];
+  const int N = a.query_seq0[b + 1] - s0 - 1;
+  const int e0 = a.query_exp0[b];
+  const int v = blockIdx.x * kFuseBlock + threadIdx.x;
+  Top2 c{kNegInf, 0x7FFFFFFF, 0, kNegInf, 0x7FFFFFFF};
+  if (v < a.V) {
+    const float sa = a.logits[(size_t)s0 * a.V + v];
+    float best = kNegInf;
+    int bk = 0;
+    for (int k = 1; k <= N; ++k) {
+      const float beta = a.beta[e0 + k - 1];
+      const float coef = 1.0f + beta;
+      const float t1 = coef * a.logits[(size_t)(s0 + k) * a.V + v];
+      const float t2 = beta * sa;
+      const float val = (t1 - t2) + a.prior[e0 + k - 1];
+      if (val > best) { best = val; bk = k; }
+    }
+    c.v1 = best; c.i1 = v; c.k1 = bk;
+  }
+  c = block_top2(c);
+  __shared__ int is_last;
+  if (threadIdx.x == 0) {
+    float* p = a.part + ((size_t)b * a.nblk + blockIdx.x) * 5;
+    p[0] = c.v1; p[1] = __int_as_float(c.i1); p[2] = __int_as_float(c.k1);
+    p[3] = c.v2; p[4] = __int_as_float(c.i2);
+    __threadfence();
+    const int prev = __hip_atomic_fetch_add(a.tickets + b, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    is_last = prev == a.nblk - 1;
+  }
+  __syncthreads();
+  if (!is_last) return;
+  __threadfence();
+  Top2 r{kNegInf, 0x7FFFFFFF, 0, kNegInf, 0x7FFFFFFF};
+  for (int i = threadIdx.x; i < a.nblk; i += blockDim.x) {
+    const float* p = a.part + ((size_t)b * a.nblk + i) * 5;
+    Top2 x{p[0], __float_as_int(p[1]), __float_as_int(p[2]), p[3], __float_as_int(p[4])};
+    r = merge(r, x);
+  }
+  r = block_top2(r);
+  if (threadIdx.x == 0) {
+    a.tokens_out[(size_t)b * a.tok_stride] = r.i1;
+    a.prev_tok[b] = r.i1;
+    if (a.winner) a.winner[b] = r.k1;
+    if (a.top1) a.top1[b] = r.v1;
+    if (a.top2) a.top2[b] = r.v2;
+    a.tickets[b] = 0;
+  }
+}
+
+// ---------------------------------------------------------------- dynamic beta
+
+__device__ float block_reduce_max(float v) {
+  __shared__ float red[4];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  const float r = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  __syncthreads();
+  return r;
+}
+
+__device__ float block_reduce_sum(float v) {
+  __shared__ float red[4];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  const float r = (red[0] + red[1]) + (red[2] + red[3]);
+  __syncthreads();
+  return r;
+}
+
+// Per (row, vocab chunk): chunk max M_c and sum exp(s - M_c).
+__global__ __launch_bounds__(256) void k_beta_lse(BetaArgs a) {
+  const int s = blockIdx.y, ch = blockIdx.x;
+  const float* row = a.logits + (size_t)s * a.V;
+  const int v0 = ch * kBetaChunk, v1 = min(a.V, v0 + kBetaChunk);
+  float m = kNegInf;
+  for (int v = v0 + threadIdx.x; v < v1; v += blockDim.x) m = fmaxf(m, row[v]);
+  m = block_reduce_max(m);
+  float sum = 0.f;
+  for (int v = v0 + threadIdx.x; v < v1; v += blockDim.x) sum += expf(row[v] - m);
+  sum = block_reduce_sum(sum);
+  if (threadIdx.x == 0) {
+    a.lse_part[((size_t)s * a.nchunk + ch) * 2] = m;
+    a.lse_part[((size_t)s * a.nchunk + ch) * 2 + 1] = sum;
+  }
+}
+
+__device__ __forceinline__ float row_lse(const BetaArgs& a, int s) {
+  const float* p = a.lse_part + (size_t)s * a.nchunk * 2;
+  float m = kNegInf;
+  for (int c = 0; c < a.nchunk; ++c) m = fmaxf(m, p[2 * c]);
+  float sum = 0.f;
+  for (int c = 0; c < a.nchunk; ++c) sum += p[2 * c + 1] * expf(p[2 * c] - m);
+  return m + logf(sum);
+}
+
+// beta_k = JSD(p_k || p_0) in bits (first step, dynamic mode; Section 3 reads
+// beta from AdaCAD's with-context vs no-context divergence). Per (expert, chunk)
+// partial sums of 1/2 p (ln p - ln m) + 1/2 q (ln q - ln m), m = (p + q) / 2,
+// with ln m = max(ln p, ln q) + log1p(exp(-|ln p - ln q|)) - ln 2; the last
+// chunk block of an expert adds the partials in chunk order and divides by ln 2.
+__global__ __launch_bounds__(256) void k_beta_jsd(BetaArgs a) {
+  const int e = blockIdx.y, ch = blockIdx.x;
+  const int sk = a.exp_seq[e];
+  const int s0 = a.query_seq0[a.exp_query[e]];
+  const float lk = row_lse(a, sk), l0 = row_lse(a, s0);
+  const float* rk = a.logits + (size_t)sk * a.V;
+  const float* r0 = a.logits + (size_t)s0 * a.V;
+  const int v0 = ch * kBetaChunk, v1 = min(a.V, v0 + kBetaChunk);
+  const float ln2 = 0.69314718055994530942f;
+  float acc = 0.f;
+  for (int v = v0 + threadIdx.x; v < v1; v += blockDim.x) {
+    const float lp = rk[v] - lk, lq = r0[v] - l0;
+    const float p = expf(lp), q = expf(lq);
+    const float lm = fmaxf(lp, lq) + log1pf(expf(-fabsf(lp - lq))) - ln2;
+    acc += 0.5f * (p * (lp - lm) + q * (lq - lm));
+  }
+  acc = block_reduce_sum(acc);
+  __shared__ int is_last;
+  if (threadIdx.x == 0) {
+    a.jsd_part[(size_t)e * a.nchunk + ch] = acc;
+    __threadfence();
+    const int prev = __hip_atomic_fetch_add(a.tickets + e, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    is_last = prev == a.nchunk - 1;
+  }
+  __syncthreads();
+  if (!is_last) return;
+  if (threadIdx.x == 0) {
+    __threadfence();
+    float tot = 0.f;
+    for (int c = 0; c < a.nchunk; ++c) tot += a.jsd_part[(size_t)e * a.nchunk + c];
+    a.beta[e] = tot / ln2;
+    a.tickets[e] = 0;
+  }
+}
+
+// --------------------------------------------------- generation input synth
+
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
+__device__ __forceinline__ uint64_t fold(uint64_t k, uint64_t f) { return mix64((k ^ f) + kGolden); }
+
+template <bool BF16>
+__device__ void synth_fill(void* dst, size_t off, uint64_t key, int n, float scale) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const uint64_t h = mix64(key + (uint64_t)(i + 1) * kGolden);
+    const int u = (int)(h & 0xFFFF) + (int)((h >> 16) & 0xFFFF) + (int)((h >> 32) & 0xFFFF) + (int)(h >> 48);
+    const float v = (float)(u - 131070) * scale;
+    if (BF16) ((uint16_t*)dst)[off + i] = (uint16_t)f2bf(v);
+    else ((float*)dst)[off + i] = v;
+  }
+}
+
+// Step-t inputs of sequence s, layer l from the previous token of its query:
+// q = stream(fold(seed, 0x51, t, s, l, y)), k_new with tag 0x4B, v_new with 0x56.
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_synth(SynthArgs a) {
+  const int s = blockIdx.x / a.n_layers, l = blockIdx.x % a.n_layers;
+  const int y = a.use_first ? a.first_token : a.prev_tok[a.seq_query[s]];
+  uint64_t base[3];
+  const uint64_t tags[3] = {0x51, 0x4B, 0x56};
+#pragma unroll
+  for (int i = 0; i < 3; ++i) {
+    uint64_t k = fold(a.seed, tags[i]);
+    k = fold(k, (uint64_t)a.t);
+    k = fold(k, (uint64_t)s);
+    k = fold(k, (uint64_t)l);
+    base[i] = fold(k, (uint64_t)y);
+  }
+  const size_t row = (size_t)s * a.n_layers + l;
+  synth_fill<BF16>(a.q, row * a.qdim, base[0], a.qdim, a.value_scale);
+  synth_fill<BF16>(a.k_new, row * a.kvdim, base[1], a.kvdim, a.value_scale);
+  synth_fill<BF16>(a.v_new, row * a.kvdim, base[2], a.kvdim, a.value_scale);
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------ launchers
+
+hipError_t launch_fill_i32(int32_t* p, int32_t v, size_t n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  const int blocks = (int)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
+  k_fill_i32<<<blocks, 256, 0, st>>>(p, v, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_bytes(void* p, size_t nbytes, hipStream_t st) {
+  const size_t n = nbytes / 4;
+  if (n == 0) return hipSuccess;
+  const int blocks = (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
+  k_zero_u32<<<blocks, 256, 0, st>>>((uint32_t*)p, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_load(const LoadArgs& a, int n_items, bool bf16, hipStream_t st) {
+  if (n_items == 0) return hipSuccess;
+  dim3 grid(n_items, a.n_layers);
+  if (bf16) k_load<true><<<grid, 256, 0, st>>>(a);
+  else k_load<false><<<grid, 256, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_append(const AppendArgs& a, bool bf16, hipStream_t st) {
+  const int blocks = a.n_seqs * a.n_layers + 1;
+  if (bf16) k_append<true><<<blocks, 128, 0, st>>>(a);
+  else k_append<false><<<blocks, 128, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn(const AttnArgs& a, int n_blocks, int head_dim, bool bf16, hipStream_t st) {
+  if (bf16) {
+    if (head_dim == 128) k_attn_bf16<128><<<n_blocks, 64, 0, st>>>(a);
+    else if (head_dim == 64) k_attn_bf16<64><<<n_blocks, 64, 0, st>>>(a);
+    else return hipErrorInvalidValue;
+  } else {
+    k_attn_f32<<<n_blocks, 64, 0, st>>>(a, head_dim);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_lmhead(const LmArgs& a, bool bf16, hipStream_t st) {
+  if (bf16) {
+    constexpr int VT = 4, NT = 3;
+    const int rows_per_block = 4 * 16 * VT;
+    const int blocks = (a.V + rows_per_block - 1) / rows_per_block;
+    k_lmhead_bf16<VT, NT><<<blocks, 256, 0, st>>>(a);
+  } else {
+    k_lmhead_f32<<<(a.V + 255) / 256, 256, 0, st>>>(a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_beta(const BetaArgs& a, int n_seqs, int n_exp, hipStream_t st) {
+  k_beta_lse<<<dim3(a.nchunk, n_seqs), 256, 0, st>>>(a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  k_beta_jsd<<<dim3(a.nchunk, n_exp), 256, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st) {
+  k_fuse<<<dim3(a.nblk, n_queries), kFuseBlock, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st) {
+  const int blocks = n_seqs * a.n_layers;
+  if (a.bf16) k_synth<true><<<blocks, 256, 0, st>>>(a);
+  else k_synth<false><<<blocks, 256, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_rows(const void* src, void* dst, size_t nbytes, hipStream_t st) {
+  return hipMemcpyAsync(dst, src, nbytes, hipMemcpyDeviceToDevice, st);
+}
+
+}  // namespace pced

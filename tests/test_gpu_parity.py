@@ -1,0 +1,174 @@
+"""GPU path vs CPU oracle, element by element, on seeded synthetic inputs.
+
+Every GPU computation goes through the C ABI (libpced). Inputs come from
+``pced_inputs``; expected values come only from the oracle."""
+import numpy as np
+import pytest
+
+from oracle import pced_oracle as O
+from pced_inputs import counter
+from pced_inputs import workloads as W
+from tests.helpers import REL_TOL, check_tokens, make_oracle, rel_err_rows
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _session(wl, **kw):
+    from paper_2601_08670_amd.session import session_for_workload
+    kw.setdefault("poison", True)
+    return session_for_workload(wl, device=DEV, **kw)
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def _run_steps(wl, steps, want=("logits", "attn_out", "winner", "top1", "top2", "beta_used", "hidden"),
+               attn_layers=None, sess=None):
+    """Run `steps` GPU steps and the oracle beside them; check every stage."""
+    sess = sess or _session(wl)
+    Wt = wl.lm_head_device(DEV)
+    Wh = wl.lm_head_host()
+    orc = make_oracle(wl)
+    tol = REL_TOL[wl.geom.dtype]
+    exempt = 0
+    for t in range(steps):
+        q, kn, vn = wl.step_inputs_device(t, DEV)
+        out = sess.step(q, kn, vn, Wt, want=want)
+        torch.cuda.synchronize()
+        ref = orc.step(*wl.step_inputs_host(t), Wh, attn_layers=attn_layers)
+        if "attn_out" in out:
+            a = _np(out["attn_out"])
+            for l, ra in ref.attn.items():
+                err = rel_err_rows(a[:, l].reshape(-1, wl.geom.head_dim), ra.reshape(-1, wl.geom.head_dim))
+                assert err <= tol, f"step {t} layer {l}: attention rel err {err}"
+        err = rel_err_rows(_np(out["logits"]), ref.logits)
+        assert err <= tol, f"step {t}: logits rel err {err}"
+        np.testing.assert_allclose(_np(out["beta_used"]), ref.beta, rtol=0, atol=1e-4)
+        exempt += check_tokens(_np(out["tokens"]), ref.logits, wl, ref.beta, ref.tokens, ref.gaps)
+        win = _np(out["winner"])
+        for b in range(wl.n_queries):
+            if int(out["tokens"][b]) == ref.tokens[b] and ref.gaps[b] > 1e-3:
+                assert win[b] == ref.winners[b]
+                assert abs(float(out["top1"][b]) - ref.top1[b]) <= 2 * tol * max(1.0, abs(ref.top1[b]))
+    return sess, exempt
+
+
+def test_device_generator_matches_host():
+    for dtype in ("bf16", "f32"):
+        for (k, start, n, scale) in [(counter.key(0, 13), 0, 100_003, 0.02), (12345, 777, 5000, 1.0)]:
+            h = W.host_values(k, start, n, scale, dtype)
+            d = _np(W.device_values(k, start, n, scale, dtype, DEV))
+            assert np.array_equal(h.view(np.uint8), d.view(np.uint8))
+
+
+def test_config1_tiny_fp32_all_steps():
+    wl = W.config1()
+    _run_steps(wl, wl.steps)
+
+
+def test_bf16_multi_query_ragged_two_layers():
+    geom = W.Geometry(2, 8, 2, 64, 512, 3000, "bf16")
+    wl = W.custom(geom, [3, 2], [40, 300, 17, 5, 129], amateur_len=16, steps=3, seed=7)
+    _run_steps(wl, wl.steps)
+
+
+def test_bf16_llama_heads_fixed_beta_shuffled_pages():
+    geom = W.Geometry(1, 32, 8, 128, 4096, 2048, "bf16")
+    wl = W.custom(geom, [4], [1, 16, 257, 700], amateur_len=64, steps=2, seed=3,
+                  beta=[0.25, 0.5, 0.75, 1.0], shuffle_pages=True)
+    _run_steps(wl, wl.steps)
+
+
+def test_lmhead_stage_bf16_and_tails():
+    from paper_2601_08670_amd.session import PcedSession
+    for (M, V, hidden) in [(1, 1000, 256), (33, 4104, 512), (50, 1003, 256), (101, 2048, 4096)]:
+        hq = hidden // 64
+        hkv = max(1, hq // 4)
+        geom = W.Geometry(1, hq, hkv, 64, hidden, V, "bf16")
+        wl = W.custom(geom, [M - 1 if M > 1 else 1], [1] * max(M - 1, 1), 1, 1, seed=M)
+        sess = PcedSession(n_layers=1, n_q_heads=hq, n_kv_heads=hkv, head_dim=64, vocab=V, dtype="bf16",
+                           max_queries=1, max_seqs=max(M, 2), max_pages=4, max_pages_per_seq=2, device=DEV,
+                           poison=True)
+        xk = counter.key(99, M)
+        xh = W.host_values(xk, 0, M * hidden, 1.0, "bf16").reshape(M, hidden)
+        xd = W.device_values(xk, 0, M * hidden, 1.0, "bf16", DEV).reshape(M, hidden)
+        logits = torch.empty((M, V), dtype=torch.float32, device=DEV)
+        sess.ctx.pced_lmhead(xd, M, wl.lm_head_device(DEV), logits)
+        torch.cuda.synchronize()
+        ref = O.lm_head(O.decode_stored(xh, "bf16"), O.decode_stored(wl.lm_head_host(), "bf16"), "rms")
+        err = rel_err_rows(_np(logits), ref)
+        assert err <= 2e-2, (M, V, hidden, err)
+        # fp32 accumulation of exact bf16 products: far inside the contract
+        assert err <= 1e-4, (M, V, hidden, err)
+
+
+def _fuse_session(n_experts, V, beta, seed, rel=None):
+    from paper_2601_08670_amd.session import PcedSession
+    S = sum(n + 1 for n in n_experts)
+    sess = PcedSession(n_layers=1, n_q_heads=1, n_kv_heads=1, head_dim=64, vocab=V, dtype="bf16",
+                       max_queries=len(n_experts), max_seqs=S, max_pages=S, max_pages_per_seq=1, device=DEV,
+                       poison=True)
+    src = [torch.zeros((1, 1, 1, 64), dtype=torch.int16, device=DEV) for _ in range(S)]
+    if rel is None:
+        rel = np.random.default_rng(seed).random(sum(n_experts)).astype(np.float32)
+        rel[0] = 0.0  # clipped to 1e-8
+    sess.load(n_experts, [1] * S, src, src, rel.tolist(), gamma=2.5, beta=beta)
+    return sess, rel
+
+
+def test_fuse_stage_bit_exact_fixed_beta_with_ties():
+    n_experts = [5, 1, 16]
+    V = 3001
+    S = sum(n + 1 for n in n_experts)
+    rng = np.random.default_rng(1)
+    beta = rng.random(sum(n_experts)).astype(np.float32)
+    rel = rng.random(sum(n_experts)).astype(np.float32)
+    rel[0] = 0.0  # clipped to 1e-8
+    # query 2: beta = 0 and equal relevance, so equal logits give exactly equal fused scores
+    beta[6:] = 0.0
+    rel[6:] = 0.5
+    beta = beta.tolist()
+    sess, rel = _fuse_session(n_experts, V, beta, seed=2, rel=rel)
+    lk = counter.key(5, 5)
+    host = W.host_values(lk, 0, S * V, 1.3, "f32").reshape(S, V)
+    host = host.copy()
+    # exact ties across tokens (100, 2000) and across experts (4 and 6) of query 2
+    s2 = 8  # amateur of query 2; expert k is row s2 + k
+    host[s2 + 4, 100] = host[s2 + 4, 2000] = 50.0
+    host[s2 + 6, 100] = 50.0
+    dev = torch.from_numpy(host).to(DEV)
+    tokens = torch.empty(3, dtype=torch.int32, device=DEV)
+    extra = {k: torch.empty(3, dtype=torch.float32 if k != "winner" else torch.int32, device=DEV)
+             for k in ("winner", "top1", "top2")}
+    sess.ctx.pced_fuse(dev, 0, tokens, extra)
+    torch.cuda.synchronize()
+    off = np.concatenate([[0], np.cumsum([n + 1 for n in n_experts])])
+    e0 = 0
+    for b, n in enumerate(n_experts):
+        sel = O.fuse_query(host[off[b]:off[b + 1]], rel[e0:e0 + n], 2.5, np.array(beta[e0:e0 + n], np.float32),
+                           precision=np.float32)
+        assert int(tokens[b]) == sel.token
+        assert int(extra["winner"][b]) == sel.winner
+        assert float(extra["top1"][b]) == np.float32(sel.top1)
+        assert float(extra["top2"][b]) == np.float32(sel.top2)
+        e0 += n
+    assert int(tokens[2]) == 100 and int(extra["winner"][2]) == 4
+    assert float(extra["top2"][2]) == float(extra["top1"][2])
+
+
+def test_fuse_stage_dynamic_beta():
+    n_experts = [7, 3]
+    V = 20000
+    S = sum(n + 1 for n in n_experts)
+    sess, rel = _fuse_session(n_experts, V, None, seed=3)
+    host = W.host_values(counter.key(6, 6), 0, S * V, 1.3, "f32").reshape(S, V)
+    tokens = torch.empty(2, dtype=torch.int32, device=DEV)
+    bu = torch.empty(sum(n_experts), dtype=torch.float32, device=DEV)
+    sess.ctx.pced_fuse(torch.from_numpy(host).to(DEV), 1, tokens, {"beta_used": bu})
+    torch.cuda.synchronize()
+    off = np.concatenate([[0], np.cumsum([n + 1 for n in n_experts])])
+    ref_beta = np.concatenate([O.dynamic_beta(host[off[b]:off[b + 1]].astype(np.float64)) for b in range(2)])
+    np.testing.assert_allclose(_np(bu), ref_beta, rtol=1e-4, atol=1e-6)
