@@ -10,9 +10,11 @@ LM head + (first step) dynamic beta + Eq. 2/3 fusion.
 
 Timing: W warm-up steps, then the caches are reloaded (lengths back to the
 preloaded ones) and exactly K steps are timed between two device
-synchronisations; inputs for every step are already resident in HBM. Every
-launch in that region is bracketed by HIP events on its own stream, from which
-the per-kernel average durations and roofline fractions are computed.
+synchronisations; inputs for every step are already resident in HBM. That
+region gives `value`. The same K steps are then run once more with every launch
+bracketed by HIP events on the launch stream (the events add a little time per
+launch, so they are kept out of `value`); per-kernel average durations and the
+roofline fractions come from that second region.
 
 Prints one JSON line on stdout.
 """
@@ -129,7 +131,7 @@ def main():
     t0 = time.time()
     sess = session_for_workload(wl, device=dev, extra_tokens=max(K, Wm) + 1, load_now=False)
     src = load_workload(sess, wl)
-    Wt = wl.lm_head_device(dev)
+    Wt = sess.pack_lm_head(wl.lm_head_device(dev))
     n_inputs = max(K, Wm)
     inputs = [wl.step_inputs_device(t, dev) for t in range(n_inputs)]
     torch.cuda.synchronize()
@@ -164,7 +166,7 @@ def main():
     else:
         ms_total, prof = timed(True)
         log(f"[bench] timed {K} steps with per-launch events: {ms_total / K:.3f} ms/step")
-    ms_step = ms_total / K
+    ms_step = ms_plain / K
 
     kernels = {}
     if prof:
@@ -196,13 +198,13 @@ def main():
 
     out = {
         "metric": "PCED decode steps/sec at N docs",
-        "value": K / (ms_total * 1e-3),
+        "value": K / (ms_plain * 1e-3),
         "unit": "steps/s",
         "n_gpus": 1,
         "steps": K,
         "warmup": Wm,
         "ms_per_step": ms_step,
-        "ms_per_step_without_events": ms_plain / K,
+        "ms_per_step_with_launch_events": ms_total / K,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

@@ -75,7 +75,8 @@ typedef struct pced_config {
   int32_t n_kv_heads;        /* Hkv; Hq / Hkv <= 16                              */
   int32_t head_dim;          /* D: 64 or 128                                     */
   int32_t hidden;            /* must equal Hq * D (the hidden state is the
-                                concatenated per-head attention output)         */
+                                concatenated per-head attention output); a
+                                multiple of 256 for bf16                        */
   int32_t vocab;             /* V >= 2                                           */
   int32_t dtype;             /* pced_dtype                                       */
   int32_t page_size;         /* tokens per KV page; must be 16                   */
@@ -94,6 +95,20 @@ typedef struct pced_ctx pced_ctx;
  * ordered so that each matrix-core operand is one contiguous 16-byte load per
  * lane. Returns 0 for an invalid cfg. */
 size_t pced_pool_bytes(const pced_config* cfg);
+
+/* Bytes of the packed LM-head weights for cfg (0 for an invalid cfg). */
+size_t pced_lm_head_bytes(const pced_config* cfg);
+
+/*
+ * Re-lay the LM-head weights once (at model load) into the form every step
+ * reads. w: device [V][hidden] row-major, storage type; w_packed: device,
+ * pced_lm_head_bytes(cfg), caller-owned, must not overlap w. For bf16 the
+ * packed form is 2 KiB tiles, one per (16 vocabulary rows, 64 hidden columns),
+ * each holding two matrix-core operands in lane order, so that the LM head
+ * streams W with contiguous 1 KiB wave loads (rows past V are zero); for f32 it
+ * is a plain copy. Asynchronous on `stream`. Errors: INVALID_ARG, HIP.
+ */
+pced_status pced_pack_lm_head(const pced_config* cfg, const void* w, void* w_packed, hipStream_t stream);
 
 /* Bytes of device workspace a context needs (0 for an invalid cfg). */
 size_t pced_workspace_bytes(const pced_config* cfg);
@@ -164,7 +179,7 @@ typedef struct pced_step_out {
  *   q          device [S][L][Hq][D]    this step's query vectors
  *   k_new      device [S][L][Hkv][D]   this step's K row (the shared token's)
  *   v_new      device [S][L][Hkv][D]   this step's V row
- *   lm_head    device [V][hidden]      row-major output projection
+ *   lm_head    device                  LM-head weights packed by pced_pack_lm_head
  *   tokens_out device [B]              chosen token y_t per query
  *   extra      optional outputs, may be NULL
  * All in the storage type except the fp32 outputs. Errors: STATE (nothing
@@ -199,7 +214,8 @@ pced_status pced_generate(pced_ctx* ctx, int32_t n_steps, const pced_synth* synt
 /*
  * Stage entry: full-vocabulary logits for given hidden states (paper, Section 3:
  * per-expert logits s_k). x: device [n_rows][hidden] storage type; lm_head:
- * device [V][hidden]; logits: device [n_rows][V] fp32; n_rows <= max_seqs.
+ * device, packed by pced_pack_lm_head; logits: device [n_rows][V] fp32;
+ * n_rows <= max_seqs.
  */
 pced_status pced_lmhead(pced_ctx* ctx, const void* x, int32_t n_rows, const void* lm_head,
                         float* logits, hipStream_t stream);
@@ -227,7 +243,8 @@ enum {
   PCED_PROF_BETA = 3,    /* dynamic beta (first step only)         */
   PCED_PROF_FUSE = 4,    /* Eq. 2 + Eq. 3                          */
   PCED_PROF_SYNTH = 5,   /* pced_generate's input synthesis        */
-  PCED_PROF_NCLASS = 6
+  PCED_PROF_COMBINE = 6, /* merge of split attention partials      */
+  PCED_PROF_NCLASS = 7
 };
 typedef struct pced_profile {
   int64_t launches[PCED_PROF_NCLASS];

@@ -16,9 +16,9 @@ LIB_PATH = os.path.join(_HERE, "libpced.so")
 PCED_F32, PCED_BF16 = 0, 1
 PCED_NORM_NONE, PCED_NORM_RMS = 0, 1
 STATUS = {0: "OK", 1: "INVALID_ARG", 2: "CAPACITY", 3: "HIP", 4: "UNSUPPORTED", 5: "STATE"}
-PROF_CLASSES = ("append", "attn", "lmhead", "beta", "fuse", "synth")
+PROF_CLASSES = ("append", "attn", "lmhead", "beta", "fuse", "synth", "combine")
 
-EXPORTED = ("pced_pool_bytes", "pced_workspace_bytes", "pced_create", "pced_destroy", "pced_last_error",
+EXPORTED = ("pced_pool_bytes", "pced_lm_head_bytes", "pced_pack_lm_head", "pced_workspace_bytes", "pced_create", "pced_destroy", "pced_last_error",
             "pced_load_caches", "pced_step", "pced_generate", "pced_lmhead", "pced_fuse",
             "pced_get_lengths", "pced_profile_enable", "pced_profile_read")
 
@@ -46,8 +46,8 @@ class pced_synth(ctypes.Structure):
 
 
 class pced_profile(ctypes.Structure):
-    _fields_ = [("launches", ctypes.c_int64 * 6), ("total_ms", ctypes.c_double * 6),
-                ("bytes", ctypes.c_double * 6), ("flops", ctypes.c_double * 6)]
+    _fields_ = [("launches", ctypes.c_int64 * 7), ("total_ms", ctypes.c_double * 7),
+                ("bytes", ctypes.c_double * 7), ("flops", ctypes.c_double * 7)]
 
 
 _lib = None
@@ -66,6 +66,8 @@ def load_library() -> ctypes.CDLL:
     sig = {
         "pced_pool_bytes": (ctypes.c_size_t, [ctypes.POINTER(pced_config)]),
         "pced_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(pced_config)]),
+        "pced_lm_head_bytes": (ctypes.c_size_t, [ctypes.POINTER(pced_config)]),
+        "pced_pack_lm_head": (I, [ctypes.POINTER(pced_config), P, P, V]),
         "pced_create": (I, [ctypes.POINTER(pced_config), P, ctypes.c_size_t, ctypes.POINTER(P)]),
         "pced_destroy": (None, [P]),
         "pced_last_error": (ctypes.c_char_p, []),
@@ -107,6 +109,15 @@ def pced_pool_bytes(cfg: pced_config) -> int:
 
 def pced_workspace_bytes(cfg: pced_config) -> int:
     return load_library().pced_workspace_bytes(ctypes.byref(cfg))
+
+
+def pced_lm_head_bytes(cfg: pced_config) -> int:
+    return load_library().pced_lm_head_bytes(ctypes.byref(cfg))
+
+
+def pced_pack_lm_head(cfg: pced_config, w, w_packed, stream=None):
+    """Re-lay row-major [V][hidden] LM-head weights into the packed form the steps read."""
+    _check(load_library().pced_pack_lm_head(ctypes.byref(cfg), w.data_ptr(), w_packed.data_ptr(), _stream(stream)))
 
 
 def _ptr(t) -> Optional[int]:

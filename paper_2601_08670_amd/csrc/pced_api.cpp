@@ -52,7 +52,7 @@ bool cfg_valid(const pced_config* c, std::string* why) {
   if (c->dtype == PCED_BF16 && c->head_dim != 64 && c->head_dim != 128) return bad("bf16 needs head_dim 64 or 128");
   if (c->dtype == PCED_F32 && (c->head_dim < 4 || c->head_dim > 128 || c->head_dim % 4)) return bad("f32 needs head_dim in [4,128], a multiple of 4");
   if (c->hidden != c->n_q_heads * c->head_dim) return bad("hidden must equal n_q_heads * head_dim");
-  if (c->dtype == PCED_BF16 && c->hidden % 64) return bad("bf16 hidden must be a multiple of 64");
+  if (c->dtype == PCED_BF16 && c->hidden % 256) return bad("bf16 hidden must be a multiple of 256");
   if (c->vocab < 2) return bad("vocab < 2");
   if (c->page_size != kPage) return bad("page_size must be 16");
   if (c->max_queries < 1) return bad("max_queries < 1");
@@ -67,7 +67,7 @@ bool cfg_valid(const pced_config* c, std::string* why) {
 struct Layout {
   size_t len0, page_table, seq_query, query_seq0, query_exp0, exp_seq, exp_query, prior, beta_fixed,
       load_items, src_k, src_v, meta_end;
-  size_t work_off, tick_attn, tick_fuse, tick_beta, prev_tok, beta, part_acc, part_ml, x, logits,
+  size_t work_off, work_list, work_pages, tick_attn, tick_fuse, tick_beta, prev_tok, beta, part_acc, part_ml, x, logits,
       fuse_part, lse_part, jsd_part, syn_q, syn_k, syn_v, total;
   int rows_pad, nblk_fuse, nchunk, max_work;
 };
@@ -97,6 +97,8 @@ Layout make_layout(const pced_config& c) {
   L.src_v = take(S * 8);
   L.meta_end = o;
   L.work_off = take((S + 1) * 4);
+  L.work_list = take((size_t)L.max_work * 16);
+  L.work_pages = take((size_t)L.max_work * kMaxSplitPages * 4);
   L.tick_attn = take(S * c.n_kv_heads * 4);
   L.tick_fuse = take(B * 4);
   L.tick_beta = take(S * 4);
@@ -140,6 +142,7 @@ struct pced_ctx {
   void* vpool = nullptr;
   std::vector<char> staging;
   int num_cus = 0;
+  int attn_waves_per_cu = 8;
   // profiling
   bool prof = false;
   std::vector<ProfRec> recs;
@@ -151,32 +154,33 @@ struct pced_ctx {
 
 namespace {
 
-// Event pair around one launch when profiling is on.
+// Start/stop events of one kernel class launch when profiling is on. They are
+// handed to the launcher, which attaches them to the dispatch itself
+// (hipExtLaunchKernelGGL), so they time the kernels and not the queue.
 struct ProfScope {
   pced_ctx* c;
   ProfRec rec;
-  hipStream_t st;
+  Timing tm;
   bool on;
-  ProfScope(pced_ctx* ctx, int cls, hipStream_t s, double bytes, double flops)
-      : c(ctx), st(s), on(ctx->prof) {
+  ProfScope(pced_ctx* ctx, int cls, double bytes, double flops) : c(ctx), on(ctx->prof) {
     if (!on) return;
     rec.cls = cls;
     rec.bytes = bytes;
     rec.flops = flops;
     rec.a = take();
     rec.b = take();
-    hipEventRecord(rec.a, st);
+    tm.start = rec.a;
+    tm.stop = rec.b;
   }
+  const Timing* timing() const { return on ? &tm : nullptr; }
   hipEvent_t take() {
     if (!c->ev_free.empty()) { hipEvent_t e = c->ev_free.back(); c->ev_free.pop_back(); return e; }
     hipEvent_t e = nullptr;
-    hipEventCreate(&e);
+    hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
     return e;
   }
   ~ProfScope() {
-    if (!on) return;
-    hipEventRecord(rec.b, st);
-    c->recs.push_back(rec);
+    if (on) c->recs.push_back(rec);
   }
 };
 
@@ -187,23 +191,31 @@ int device_cus() {
   return n;
 }
 
-// Tokens per attention split: enough work items to fill the chip several times
-// over (the ragged tail of the last wave of work items is what limits a launch),
-// while keeping each split long enough to amortise its partial-state write.
+int count_work(const pced_ctx* c, int split_tokens, int* max_splits) {
+  long n = 0;
+  int mx = 0;
+  for (int s = 0; s < c->S; ++s) {
+    const int k = ceil_div(c->len[s] + 1, split_tokens);
+    n += k;
+    mx = std::max(mx, k);
+  }
+  if (max_splits) *max_splits = mx;
+  return (int)n;
+}
+
+// Pages per attention split: the smallest split whose work items (one wave each)
+// all fit on the chip at once, so every wave starts in the first round and the
+// launch ends when the longest split does; sequences shorter than a split are
+// not split at all.
 int choose_split_tokens(const pced_ctx* c) {
   long page_heads = 0;
   for (int s = 0; s < c->S; ++s) page_heads += ceil_div(c->len[s] + 1, kPage);
   page_heads *= c->cfg.n_kv_heads;
-  const long target = (long)c->num_cus * 8;
-  int sp = (int)std::max<long>(1, (page_heads + target - 1) / target);
-  sp = std::min(sp, 64);
+  const long cap = (long)c->num_cus * c->attn_waves_per_cu;
+  int sp = (int)std::max<long>(1, (page_heads + cap - 1) / cap);
+  sp = std::min(sp, kMaxSplitPages);
+  while (sp < kMaxSplitPages && (long)count_work(c, sp * kPage, nullptr) * c->cfg.n_kv_heads > cap) ++sp;
   return sp * kPage;
-}
-
-int count_work(const pced_ctx* c, int split_tokens) {
-  long n = 0;
-  for (int s = 0; s < c->S; ++s) n += ceil_div(c->len[s] + 1, split_tokens);
-  return (int)n;
 }
 
 pced_status check_ctx(const pced_ctx* c, bool need_loaded) {
@@ -228,8 +240,8 @@ pced_status run_fuse(pced_ctx* c, const float* logits, bool refresh_beta, int32_
     b.beta = c->at<float>(c->lay.beta);
     b.V = cfg.vocab;
     b.nchunk = c->lay.nchunk;
-    ProfScope ps(c, PCED_PROF_BETA, st, (double)(c->S + 2.0 * c->NE) * cfg.vocab * 4, 0);
-    HIP_OK(launch_beta(b, c->S, c->NE, st));
+    ProfScope ps(c, PCED_PROF_BETA, (double)(c->S + 2.0 * c->NE) * cfg.vocab * 4, 0);
+    HIP_OK(launch_beta(b, c->S, c->NE, st, ps.timing()));
     c->beta_frozen = true;
   }
   FuseArgs f{};
@@ -249,8 +261,8 @@ pced_status run_fuse(pced_ctx* c, const float* logits, bool refresh_beta, int32_
   f.nblk = c->lay.nblk_fuse;
   f.tok_stride = tok_stride;
   {
-    ProfScope ps(c, PCED_PROF_FUSE, st, (double)c->S * cfg.vocab * 4, 0);
-    HIP_OK(launch_fuse(f, c->B, st));
+    ProfScope ps(c, PCED_PROF_FUSE, (double)c->S * cfg.vocab * 4, 0);
+    HIP_OK(launch_fuse(f, c->B, st, ps.timing()));
   }
   if (extra && extra->beta_used)
     HIP_OK(hipMemcpyAsync(extra->beta_used, c->at<float>(c->lay.beta), (size_t)c->NE * 4,
@@ -269,10 +281,10 @@ pced_status run_lmhead(pced_ctx* c, const void* x, int M, const void* w, float* 
   a.K = cfg.hidden;
   a.rms = cfg.norm == PCED_NORM_RMS;
   const double es = (double)esize_of(cfg);
-  ProfScope ps(c, PCED_PROF_LMHEAD, st,
+  ProfScope ps(c, PCED_PROF_LMHEAD,
                (double)cfg.vocab * cfg.hidden * es + (double)M * cfg.hidden * es + (double)M * cfg.vocab * 4,
                2.0 * M * cfg.vocab * cfg.hidden);
-  HIP_OK(launch_lmhead(a, c->bf16, st));
+  HIP_OK(launch_lmhead(a, c->bf16, st, ps.timing()));
   return PCED_OK;
 }
 
@@ -287,7 +299,8 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
       return fail(PCED_ERR_CAPACITY, "sequence %d has no page for token %d", s, c->len[s]);
   }
   const int split = choose_split_tokens(c);
-  const int n_work = count_work(c, split);
+  int max_splits = 1;
+  const int n_work = count_work(c, split, &max_splits);
   if (n_work > c->lay.max_work) return fail(PCED_ERR_CAPACITY, "attention work list exceeds workspace");
   const double es = (double)esize_of(cfg);
 
@@ -299,6 +312,8 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
   ap.len0 = c->at<int32_t>(c->lay.len0);
   ap.page_table = c->at<int32_t>(c->lay.page_table);
   ap.work_off = c->at<int32_t>(c->lay.work_off);
+  ap.work_list = c->at<int4>(c->lay.work_list);
+  ap.work_pages = c->at<int32_t>(c->lay.work_pages);
   ap.n_seqs = c->S;
   ap.n_layers = cfg.n_layers;
   ap.n_kv_heads = cfg.n_kv_heads;
@@ -308,9 +323,8 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
   ap.t = c->t;
   ap.split_tokens = split;
   {
-    ProfScope ps(c, PCED_PROF_APPEND, st,
-                 4.0 * c->S * cfg.n_layers * cfg.n_kv_heads * cfg.head_dim * es, 0);
-    HIP_OK(launch_append(ap, c->bf16, st));
+    ProfScope ps(c, PCED_PROF_APPEND, 4.0 * c->S * cfg.n_layers * cfg.n_kv_heads * cfg.head_dim * es, 0);
+    HIP_OK(launch_append(ap, c->bf16, st, ps.timing()));
   }
 
   AttnArgs at{};
@@ -320,9 +334,10 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
   at.len0 = ap.len0;
   at.page_table = ap.page_table;
   at.work_off = ap.work_off;
+  at.work_list = ap.work_list;
+  at.work_pages = ap.work_pages;
   at.part_acc = c->at<float>(c->lay.part_acc);
   at.part_ml = c->at<float>(c->lay.part_ml);
-  at.tickets = c->at<int32_t>(c->lay.tick_attn);
   at.x_out = c->at<void>(c->lay.x);
   at.attn_out = extra ? extra->attn_out : nullptr;
   at.hidden_out = extra ? extra->hidden : nullptr;
@@ -344,8 +359,14 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
   for (int l = 0; l < cfg.n_layers; ++l) {
     at.layer = l;
     at.is_last_layer = l == cfg.n_layers - 1;
-    ProfScope ps(c, PCED_PROF_ATTN, st, attn_bytes, attn_flops);
-    HIP_OK(launch_attn(at, n_work * cfg.n_kv_heads, cfg.head_dim, c->bf16, st));
+    {
+      ProfScope ps(c, PCED_PROF_ATTN, attn_bytes, attn_flops);
+      HIP_OK(launch_attn(at, n_work * cfg.n_kv_heads, cfg.head_dim, c->bf16, st, ps.timing()));
+    }
+    if (n_work > c->S) {  // some sequence has more than one split
+      ProfScope ps(c, PCED_PROF_COMBINE, 0, 0);
+      HIP_OK(launch_attn_combine(at, cfg.head_dim, max_splits, c->bf16, st, ps.timing()));
+    }
   }
 
   float* logits = (extra && extra->logits) ? extra->logits : c->at<float>(c->lay.logits);
@@ -365,6 +386,24 @@ extern "C" {
 size_t pced_pool_bytes(const pced_config* cfg) {
   if (!cfg_valid(cfg, nullptr)) return 0;
   return (size_t)cfg->n_layers * cfg->max_pages * cfg->n_kv_heads * kPage * cfg->head_dim * esize_of(*cfg);
+}
+
+size_t pced_lm_head_bytes(const pced_config* cfg) {
+  if (!cfg_valid(cfg, nullptr)) return 0;
+  if (cfg->dtype == PCED_BF16) return (size_t)ceil_div(cfg->vocab, 16) * 16 * cfg->hidden * 2;
+  return (size_t)cfg->vocab * cfg->hidden * 4;
+}
+
+pced_status pced_pack_lm_head(const pced_config* cfg, const void* w, void* w_packed, hipStream_t st) {
+  std::string why;
+  if (!cfg_valid(cfg, &why)) return fail(PCED_ERR_INVALID_ARG, "invalid config: %s", why.c_str());
+  if (!w || !w_packed) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  const char* a = (const char*)w;
+  const char* b = (const char*)w_packed;
+  const size_t na = (size_t)cfg->vocab * cfg->hidden * esize_of(*cfg), nb = pced_lm_head_bytes(cfg);
+  if (a < b + nb && b < a + na) return fail(PCED_ERR_INVALID_ARG, "w and w_packed overlap");
+  HIP_OK(launch_pack_lm_head(w, w_packed, cfg->vocab, cfg->hidden, cfg->dtype == PCED_BF16, st));
+  return PCED_OK;
 }
 
 size_t pced_workspace_bytes(const pced_config* cfg) {
@@ -460,7 +499,10 @@ pced_status pced_load_caches(pced_ctx* c, int32_t n_queries, const int32_t* n_ex
       next += need;
     }
   }
-  if (c->num_cus == 0) c->num_cus = device_cus();
+  if (c->num_cus == 0) {
+    c->num_cus = device_cus();
+    c->attn_waves_per_cu = attn_blocks_per_cu(cfg.head_dim, c->bf16);
+  }
 
   // host mirror
   c->B = n_queries;
@@ -591,8 +633,8 @@ pced_status pced_generate(pced_ctx* c, int32_t n_steps, const pced_synth* synth,
     sa.t = c->t;
     sa.use_first = c->t == 0;
     {
-      ProfScope ps(c, PCED_PROF_SYNTH, st, (double)c->S * cfg.n_layers * (sa.qdim + 2.0 * sa.kvdim) * es, 0);
-      HIP_OK(launch_synth(sa, c->S, st));
+      ProfScope ps(c, PCED_PROF_SYNTH, (double)c->S * cfg.n_layers * (sa.qdim + 2.0 * sa.kvdim) * es, 0);
+      HIP_OK(launch_synth(sa, c->S, st, ps.timing()));
     }
     r = run_step(c, sa.q, sa.k_new, sa.v_new, lm_head, tokens_out + i, n_steps,
                  i == n_steps - 1 ? last_extra : nullptr, st);

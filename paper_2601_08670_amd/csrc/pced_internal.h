@@ -12,6 +12,7 @@ constexpr int kMaxGroup = 16;      // q-heads per kv-head (MFMA N edge)
 constexpr int kFuseBlock = 256;    // vocab entries per fuse work-group
 constexpr int kBetaChunk = 4096;   // vocab entries per beta work-group
 constexpr int kLmRowsPad = 48;     // hidden-state rows are padded to a multiple of this
+constexpr int kMaxSplitPages = 64; // pages per attention split (one page id per lane)
 
 // Per-step attention launch arguments (one launch per layer).
 struct AttnArgs {
@@ -21,9 +22,10 @@ struct AttnArgs {
   const int32_t* len0;      // [S] lengths at load
   const int32_t* page_table;// [S][maxpps]
   const int32_t* work_off;  // [S+1] prefix of splits per sequence (this step)
+  const int4* work_list;    // [work] (sequence, first token, end token, splits of the sequence)
+  const int32_t* work_pages;// [work][kMaxSplitPages] physical pages of each work item
   float* part_acc;          // [work*Hkv][G][D]
   float* part_ml;           // [work*Hkv][G][2]  (running max in log2 units, sum)
-  int32_t* tickets;         // [S*Hkv], zero between launches
   void* x_out;              // [S][Hq*D] layer output, storage type
   float* attn_out;          // optional [S][L][Hq][D]
   float* hidden_out;        // optional [S][Hq*D] (last layer only)
@@ -40,6 +42,8 @@ struct AppendArgs {
   const int32_t* len0;
   const int32_t* page_table;
   int32_t* work_off;        // [S+1] written by the planning block
+  int4* work_list;          // [work] written by the planning blocks
+  int32_t* work_pages;      // [work][kMaxSplitPages] written by the planning blocks
   int n_seqs, n_layers, n_kv_heads, head_dim, max_pages, maxpps, t, split_tokens;
 };
 
@@ -56,7 +60,7 @@ struct LoadArgs {
 
 struct LmArgs {
   const void* x;            // [rows_pad][K] storage type, rows >= M zero
-  const void* w;            // [V][K]
+  const void* w;            // packed bf16 tiles (see pced_pack_lm_head) or f32 [V][K]
   float* logits;            // [M][V]
   int M, V, K, rms;
 };
@@ -100,16 +104,25 @@ struct SynthArgs {
   int n_layers, qdim, kvdim, t, first_token, use_first, bf16;
 };
 
+// Optional timing events attached to the first / last dispatch of a launcher.
+struct Timing {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+
 // launchers (pced_kernels.hip); each returns hipGetLastError() after the launch
 hipError_t launch_fill_i32(int32_t* p, int32_t v, size_t n, hipStream_t st);
 hipError_t launch_zero_bytes(void* p, size_t nbytes, hipStream_t st);
-hipError_t launch_load(const LoadArgs& a, int n_items, bool bf16, hipStream_t st);
-hipError_t launch_append(const AppendArgs& a, bool bf16, hipStream_t st);
-hipError_t launch_attn(const AttnArgs& a, int n_blocks, int head_dim, bool bf16, hipStream_t st);
-hipError_t launch_lmhead(const LmArgs& a, bool bf16, hipStream_t st);
-hipError_t launch_beta(const BetaArgs& a, int n_seqs, int n_exp, hipStream_t st);
-hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st);
-hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st);
+hipError_t launch_load(const LoadArgs& a, int n_items, bool bf16, hipStream_t st, const Timing* tm = nullptr);
+hipError_t launch_append(const AppendArgs& a, bool bf16, hipStream_t st, const Timing* tm = nullptr);
+hipError_t launch_attn(const AttnArgs& a, int n_blocks, int head_dim, bool bf16, hipStream_t st, const Timing* tm = nullptr);
+int attn_blocks_per_cu(int head_dim, bool bf16);  // resident one-wave blocks per CU
+hipError_t launch_attn_combine(const AttnArgs& a, int head_dim, int max_splits, bool bf16, hipStream_t st, const Timing* tm = nullptr);
+hipError_t launch_pack_lm_head(const void* w, void* wp, int V, int K, bool bf16, hipStream_t st);
+hipError_t launch_lmhead(const LmArgs& a, bool bf16, hipStream_t st, const Timing* tm = nullptr);
+hipError_t launch_beta(const BetaArgs& a, int n_seqs, int n_exp, hipStream_t st, const Timing* tm = nullptr);
+hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st, const Timing* tm = nullptr);
+hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st, const Timing* tm = nullptr);
 hipError_t launch_copy_rows(const void* src, void* dst, size_t nbytes, hipStream_t st);
 
 }  // namespace pced

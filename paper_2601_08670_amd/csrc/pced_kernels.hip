@@ -98,20 +98,36 @@ __global__ __launch_bounds__(256) void k_load(LoadArgs a) {
 
 // Blocks 0 .. S*L-1: write step t's K/V row of (sequence, layer) into slot
 // len0 + t of the sequence's pages (Section 3: the chosen token joins every
-// expert's history). Block S*L: prefix of attention splits per sequence for
-// this step's lengths len0 + t + 1.
+// expert's history). Blocks S*L + s plan sequence s for this step's length
+// len0 + t + 1: its splits' descriptors and physical page ids, which every
+// layer's attention launch of the step reads.
 template <bool BF16>
 __global__ __launch_bounds__(128) void k_append(AppendArgs a) {
   const int S = a.n_seqs, L = a.n_layers;
-  if ((int)blockIdx.x == S * L) {
+  if ((int)blockIdx.x >= S * L) {
+    const int s = blockIdx.x - S * L;
+    const int st = a.split_tokens, sp = st / kPage;
+    // offset of this sequence's first split: sum over earlier sequences
+    __shared__ int red[2];
+    int part = 0;
+    for (int r = threadIdx.x; r < s; r += blockDim.x) part += (a.len0[r] + a.t + 1 + st - 1) / st;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) part += __shfl_xor(part, o);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = part;
+    __syncthreads();
+    const int off = red[0] + red[1];
+    const int len = a.len0[s] + a.t + 1;
+    const int n = (len + st - 1) / st;
+    const int npages = (len + kPage - 1) / kPage;
     if (threadIdx.x == 0) {
-      int off = 0;
-      for (int s = 0; s < S; ++s) {
-        a.work_off[s] = off;
-        off += (a.len0[s] + a.t + 1 + a.split_tokens - 1) / a.split_tokens;
-      }
-      a.work_off[S] = off;
+      a.work_off[s] = off;
+      if (s == S - 1) a.work_off[S] = off + n;
     }
+    for (int j = threadIdx.x; j < n; j += blockDim.x)
+      a.work_list[off + j] = make_int4(s, j * st, min(len, (j + 1) * st), n);
+    const int32_t* pt = a.page_table + (size_t)s * a.maxpps;
+    for (int p = threadIdx.x; p < npages; p += blockDim.x)
+      a.work_pages[(size_t)(off + p / sp) * kMaxSplitPages + p % sp] = pt[p];
     return;
   }
   const int s = blockIdx.x / L, l = blockIdx.x % L;
@@ -144,18 +160,12 @@ struct WorkItem {
 __device__ __forceinline__ WorkItem decode_work(const AttnArgs& a, int w) {
   WorkItem it;
   it.g = w % a.n_kv_heads;
-  const int item = w / a.n_kv_heads;
-  int lo = 0, hi = a.n_seqs;  // largest s with work_off[s] <= item
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (a.work_off[mid] <= item) lo = mid; else hi = mid;
-  }
-  it.s = lo;
-  it.split = item - a.work_off[lo];
-  it.nsplit = a.work_off[lo + 1] - a.work_off[lo];
-  const int len = a.len0[lo] + a.t + 1;
-  it.tok_begin = it.split * a.split_tokens;
-  it.tok_end = min(len, it.tok_begin + a.split_tokens);
+  const int4 e = a.work_list[w / a.n_kv_heads];
+  it.s = e.x;
+  it.tok_begin = e.y;
+  it.tok_end = e.z;
+  it.nsplit = e.w;
+  it.split = e.y / a.split_tokens;
   return it;
 }
 
@@ -183,42 +193,54 @@ __device__ __forceinline__ void write_o4(const AttnArgs& a, int s, int head, int
   }
 }
 
-// The last of a sequence's split waves to finish (atomic ticket) merges the
-// partial softmax states of all splits in split order:
+// Merge of a sequence's split partial states, in split order:
 //   m* = max_j m_j,  o = sum_j acc_j 2^(m_j - m*) / sum_j l_j 2^(m_j - m*).
+// One block per (sequence, kv-head); sequences that fit one split were written
+// directly by the attention kernel. Each thread owns 4 output dims of one head
+// and issues the loads of up to 16 splits at once (one memory round trip for
+// the usual split counts), merging further groups of 16 online.
 template <bool BF16>
-__device__ void ticket_and_combine(const AttnArgs& a, const WorkItem& it, int D) {
-  const int lane = threadIdx.x;
+__global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a, int D) {
+  constexpr int J = 16;
+  const int s = blockIdx.x / a.n_kv_heads, g = blockIdx.x % a.n_kv_heads;
+  const int nsplit = a.work_off[s + 1] - a.work_off[s];
+  if (nsplit <= 1) return;
   const int G = a.group, Hkv = a.n_kv_heads;
-  __threadfence();
-  int prev = 0;
-  if (lane == 0)
-    prev = __hip_atomic_fetch_add(a.tickets + it.s * Hkv + it.g, 1, __ATOMIC_ACQ_REL,
-                                  __HIP_MEMORY_SCOPE_AGENT);
-  prev = __shfl(prev, 0);
-  if (prev != it.nsplit - 1) return;
-  __threadfence();
-  const int w0 = a.work_off[it.s] * Hkv + it.g;
-  const int n4 = G * D / 4;
-  for (int idx = lane; idx < n4; idx += 64) {
+  const int w0 = a.work_off[s] * Hkv + g;
+  for (int idx = threadIdx.x; idx < G * D / 4; idx += blockDim.x) {
     const int h = (idx * 4) / D, d = (idx * 4) % D;
-    float mstar = kNegInf;
-    for (int j = 0; j < it.nsplit; ++j)
-      mstar = fmaxf(mstar, a.part_ml[((size_t)(w0 + j * Hkv) * G + h) * 2]);
+    float m_run = kNegInf, den = 0.f;
     float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
-    float den = 0.f;
-    for (int j = 0; j < it.nsplit; ++j) {
-      const size_t wj = (size_t)(w0 + j * Hkv);
-      const float sc = exp2f(a.part_ml[(wj * G + h) * 2] - mstar);
-      den += a.part_ml[(wj * G + h) * 2 + 1] * sc;
-      const float4 v = *(const float4*)(a.part_acc + (wj * G + h) * D + d);
-      num.x += v.x * sc; num.y += v.y * sc; num.z += v.z * sc; num.w += v.w * sc;
+    for (int j0 = 0; j0 < nsplit; j0 += J) {
+      float mj[J], lj[J];
+      float4 vj[J];
+#pragma unroll
+      for (int u = 0; u < J; ++u) {
+        if (j0 + u < nsplit) {
+          const size_t wj = (size_t)(w0 + (j0 + u) * Hkv);
+          mj[u] = a.part_ml[(wj * G + h) * 2];
+          lj[u] = a.part_ml[(wj * G + h) * 2 + 1];
+          vj[u] = *(const float4*)(a.part_acc + (wj * G + h) * D + d);
+        } else {
+          mj[u] = kNegInf; lj[u] = 0.f; vj[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+      float mg = m_run;
+#pragma unroll
+      for (int u = 0; u < J; ++u) mg = fmaxf(mg, mj[u]);
+      const float r = exp2f(m_run - mg);
+      den *= r; num.x *= r; num.y *= r; num.z *= r; num.w *= r;
+#pragma unroll
+      for (int u = 0; u < J; ++u) {
+        const float w = exp2f(mj[u] - mg);
+        den += lj[u] * w;
+        num.x += vj[u].x * w; num.y += vj[u].y * w; num.z += vj[u].z * w; num.w += vj[u].w * w;
+      }
+      m_run = mg;
     }
     const float inv = 1.0f / den;
-    write_o4<BF16>(a, it.s, it.g * G + h, d, D,
-                   make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv));
+    write_o4<BF16>(a, s, g * G + h, d, D, make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv));
   }
-  if (lane == 0) a.tickets[it.s * Hkv + it.g] = 0;
 }
 
 // Split-K flash decoding for bf16 caches, one wave per (sequence, kv-head,
@@ -230,14 +252,18 @@ __device__ void ticket_and_combine(const AttnArgs& a, const WorkItem& it, int D)
 // tokens 4*(l/16)..+3), which is the B operand layout of the second product.
 // Online softmax in base 2 with log2(e)/sqrt(D) folded into the score scale.
 template <int D>
-__global__ __launch_bounds__(64) void k_attn_bf16(AttnArgs a) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_attn_bf16(AttnArgs a) {
   constexpr int NC = D / 32;
   constexpr int NJ = D / 16;
   const int lane = threadIdx.x;
   const int col = lane & 15, quad = lane >> 4;
   const int G = a.group, Hkv = a.n_kv_heads;
   const WorkItem it = decode_work(a, blockIdx.x);
-  const int pg0 = it.tok_begin / kPage, pg1 = (it.tok_end + kPage - 1) / kPage;
+  const int pg0 = it.tok_begin / kPage;
+  const int np = (it.tok_end + kPage - 1) / kPage - pg0;  // 1 .. kMaxSplitPages
+  // the split's physical page ids, one per lane (written by the planner),
+  // read back with readlane
+  const int my_pid = a.work_pages[(size_t)(blockIdx.x / Hkv) * kMaxSplitPages + lane];
 
   bf16x8 qop[NC];
   {
@@ -250,63 +276,63 @@ __global__ __launch_bounds__(64) void k_attn_bf16(AttnArgs a) {
       qop[i] = as_bf16x8(v);
     }
   }
-  const size_t tile = (size_t)kPage * D;
   const uint4* kp = (const uint4*)a.kpool;
   const uint4* vp = (const uint4*)a.vpool;
   const size_t lay = (size_t)a.layer * a.max_pages * Hkv + it.g;
-  const int32_t* pt = a.page_table + (size_t)it.s * a.maxpps;
-  const size_t tile16 = tile / 8;  // tile size in 16-byte units
+  constexpr size_t tile16 = (size_t)kPage * D / 8;  // tile size in 16-byte units
 
-  uint4 kc[NC], vc[NC];
-  {
-    const size_t t0 = (lay + (size_t)pt[pg0] * Hkv) * tile16;
+  // Loads are issued unconditionally (past the end: the last page again, an L2
+  // hit) so that the wait before each page's use leaves the next page in flight.
+  auto load_page = [&](int i, uint4 (&kb)[NC], uint4 (&vb)[NC]) {
+    const int phys = __builtin_amdgcn_readlane(my_pid, min(i, np - 1));
+    const size_t t0 = (lay + (size_t)phys * Hkv) * tile16;
 #pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      kc[i] = kp[t0 + i * 64 + lane];
-      vc[i] = vp[t0 + i * 64 + lane];
+    for (int c = 0; c < NC; ++c) {
+      kb[c] = kp[t0 + c * 64 + lane];
+      vb[c] = vp[t0 + c * 64 + lane];
     }
-  }
+  };
+
   f32x4 acc[NJ];
 #pragma unroll
   for (int j = 0; j < NJ; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = kNegInf, l_part = 0.f;
+  // Online softmax with a lazily moved reference: weights are 2^(z - m_ref) with
+  // m_ref per head, shared by the head's four lanes. m_ref (and the accumulators)
+  // only move when some score of the page exceeds m_ref + 8, so weights stay
+  // <= 2^8 and the common page needs neither cross-lane traffic nor a rescale.
+  float m_ref = kNegInf, l_part = 0.f;
 
-  for (int p = pg0; p < pg1; ++p) {
-    uint4 kn[NC], vn[NC];
-    const bool more = p + 1 < pg1;
-    if (more) {
-      const size_t t1 = (lay + (size_t)pt[p + 1] * Hkv) * tile16;
-#pragma unroll
-      for (int i = 0; i < NC; ++i) {
-        kn[i] = kp[t1 + i * 64 + lane];
-        vn[i] = vp[t1 + i * 64 + lane];
-      }
-    }
+  auto process = [&](int i, uint4 (&kc)[NC], uint4 (&vc)[NC]) {
     f32x4 sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < NC; ++i)
-      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kc[i]), qop[i], sc, 0, 0, 0);
-    const int tb = p * kPage + 4 * quad;
+    for (int c = 0; c < NC; ++c)
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kc[c]), qop[c], sc, 0, 0, 0);
+    const int tb = (pg0 + i) * kPage + 4 * quad;
     float z[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) z[r] = (tb + r < it.tok_end) ? sc[r] * a.scale_log2 : kNegInf;
-    float mx = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f(m_run - m_new);
+    const float zmax = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+    if (__builtin_amdgcn_ballot_w64(zmax > m_ref + 8.0f) != 0) {
+      float mx = fmaxf(zmax, __shfl_xor(zmax, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_ref, mx);
+      const float alpha = exp2f(m_ref - m_new);
+      l_part *= alpha;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) acc[j] *= alpha;
+      m_ref = m_new;
+    }
     uint32_t pb[4];
     float psum = 0.f;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      pb[r] = f2bf(exp2f(z[r] - m_new));
+      pb[r] = f2bf(exp2f(z[r] - m_ref));
       psum += bf2f(pb[r]);   // normaliser uses exactly the weights fed to the MFMA
     }
-    l_part = l_part * alpha + psum;
-    m_run = m_new;
+    l_part += psum;
     s16x4 pop;
     pop[0] = (short)pb[0]; pop[1] = (short)pb[1]; pop[2] = (short)pb[2]; pop[3] = (short)pb[3];
-    if (p * kPage + kPage > it.tok_end) {
+    if ((pg0 + i) * kPage + kPage > it.tok_end) {
       // Partial last page: slots past the sequence end hold stale or never-written
       // bits. Their weights are 0, but 0 * NaN is NaN inside the matrix core, so
       // clear the V elements of those tokens (lane elements r = 0..3 are the same
@@ -314,23 +340,35 @@ __global__ __launch_bounds__(64) void k_attn_bf16(AttnArgs a) {
       const uint32_t m01 = (tb + 0 < it.tok_end ? 0x0000FFFFu : 0u) | (tb + 1 < it.tok_end ? 0xFFFF0000u : 0u);
       const uint32_t m23 = (tb + 2 < it.tok_end ? 0x0000FFFFu : 0u) | (tb + 3 < it.tok_end ? 0xFFFF0000u : 0u);
 #pragma unroll
-      for (int jj = 0; jj < NC; ++jj) {
-        vc[jj].x &= m01; vc[jj].y &= m23; vc[jj].z &= m01; vc[jj].w &= m23;
+      for (int c = 0; c < NC; ++c) {
+        vc[c].x &= m01; vc[c].y &= m23; vc[c].z &= m01; vc[c].w &= m23;
       }
     }
 #pragma unroll
-    for (int jj = 0; jj < NC; ++jj) {
-      const s16x4 va = __builtin_bit_cast(s16x4, make_uint2(vc[jj].x, vc[jj].y));
-      const s16x4 vb = __builtin_bit_cast(s16x4, make_uint2(vc[jj].z, vc[jj].w));
-      acc[2 * jj] *= alpha;
-      acc[2 * jj + 1] *= alpha;
-      acc[2 * jj] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pop, acc[2 * jj], 0, 0, 0);
-      acc[2 * jj + 1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vb, pop, acc[2 * jj + 1], 0, 0, 0);
+    for (int c = 0; c < NC; ++c) {
+      const s16x4 va = __builtin_bit_cast(s16x4, make_uint2(vc[c].x, vc[c].y));
+      const s16x4 vb = __builtin_bit_cast(s16x4, make_uint2(vc[c].z, vc[c].w));
+      acc[2 * c] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pop, acc[2 * c], 0, 0, 0);
+      acc[2 * c + 1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vb, pop, acc[2 * c + 1], 0, 0, 0);
     }
-    if (more) {
-#pragma unroll
-      for (int i = 0; i < NC; ++i) { kc[i] = kn[i]; vc[i] = vn[i]; }
-    }
+  };
+
+  // four-page register ring: the refill of page i+3 (into the buffer of page
+  // i-1, already consumed) is issued before page i is consumed, so three pages
+  // are always in flight
+  uint4 kA[NC], vA[NC], kB[NC], vB[NC], kC[NC], vC[NC], kD[NC], vD[NC];
+  load_page(0, kA, vA);
+  load_page(1, kB, vB);
+  load_page(2, kC, vC);
+  for (int i = 0; i < np; i += 4) {
+    load_page(i + 3, kD, vD);
+    process(i, kA, vA);
+    load_page(i + 4, kA, vA);
+    if (i + 1 < np) process(i + 1, kB, vB);
+    load_page(i + 5, kB, vB);
+    if (i + 2 < np) process(i + 2, kC, vC);
+    load_page(i + 6, kC, vC);
+    if (i + 3 < np) process(i + 3, kD, vD);
   }
   float l_tot = l_part + __shfl_xor(l_part, 16);
   l_tot += __shfl_xor(l_tot, 32);
@@ -352,11 +390,10 @@ __global__ __launch_bounds__(64) void k_attn_bf16(AttnArgs a) {
       *(float4*)(a.part_acc + (w * G + col) * D + 16 * j + 4 * quad) =
           make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
     if (quad == 0) {
-      a.part_ml[(w * G + col) * 2] = m_run;
+      a.part_ml[(w * G + col) * 2] = m_ref;
       a.part_ml[(w * G + col) * 2 + 1] = l_tot;
     }
   }
-  ticket_and_combine<true>(a, it, D);
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -432,7 +469,6 @@ __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a, int D) {
       a.part_ml[(w * G + h) * 2 + 1] = l[h];
     }
   }
-  ticket_and_combine<false>(a, it, D);
 }
 
 // ------------------------------------------------------------------- LM head
@@ -449,27 +485,51 @@ __device__ __forceinline__ float sumsq8(bf16x8 v) {
   return s;
 }
 
+// Packed LM-head layout (bf16). W [V][K] is re-laid once into 2 KiB tiles, one
+// per (16-row vocab block vb, 64-wide k step ks), tiles ordered [vb][ks]. Inside
+// a tile, half h (0, 1) and lane l = col + 16*quad hold the 8 elements
+// W[16*vb + col][64*ks + 16*quad + 8*h .. +7]: each half is exactly the A operand
+// of one v_mfma_f32_16x16x32_bf16, read as one contiguous 1 KiB wave load.
+// Rows past V are zero.
+__global__ __launch_bounds__(256) void k_pack_w_bf16(const uint16_t* __restrict__ w, uint16_t* __restrict__ wp,
+                                                     int V, int K) {
+  const int KS = K / 64;
+  const size_t n16 = (size_t)((V + 15) / 16) * KS * 2 * 64;  // 16-byte units of the packed matrix
+  for (size_t u = blockIdx.x * (size_t)blockDim.x + threadIdx.x; u < n16; u += (size_t)gridDim.x * blockDim.x) {
+    const int lane = (int)(u & 63);
+    const size_t t = u >> 6;
+    const int h = (int)(t & 1);
+    const size_t tile = t >> 1;
+    const int ks = (int)(tile % KS);
+    const int vb = (int)(tile / KS);
+    const int v = 16 * vb + (lane & 15);
+    const int k = 64 * ks + 16 * (lane >> 4) + 8 * h;
+    uint4 val = make_uint4(0u, 0u, 0u, 0u);
+    if (v < V) val = *(const uint4*)(w + (size_t)v * K + k);
+    *(uint4*)(wp + u * 8) = val;
+  }
+}
+
 // logits[m][v] = rho_m * sum_k x[m][k] W[v][k] on the matrix cores:
 // C^T[16 vocab x 16 rows] += W[16 x 32] X^T[32 x 16] (v_mfma_f32_16x16x32_bf16).
-// A wave owns 16*VT vocab rows and streams each W byte once per 16*NT rows of x;
-// each lane reads 32 contiguous bytes of a W row per 64-wide k step, so a row's
-// four lanes cover one 128-byte line. rho (RMS scale) is accumulated from the
-// same x operand loads.
+// A wave owns VT consecutive 16-row vocab blocks and streams their packed tiles
+// (contiguous 1 KiB loads) exactly once per 16*NT rows of x, through a 3-stage
+// register ring (two 64-wide k steps in flight); the x operands (a few hundred
+// KiB, L2-resident) are loaded one step ahead.
+// rho (the RMS scale) is accumulated from the same x operands.
 template <int VT, int NT>
-__global__ __launch_bounds__(256) void k_lmhead_bf16(LmArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_lmhead_bf16(LmArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, quad = lane >> 4;
-  const int vbase = (blockIdx.x * 4 + wave) * (16 * VT);
-  if (vbase >= a.V) return;
-  const int K = a.K;
-  const uint16_t* W = (const uint16_t*)a.w;
+  const int vb0 = (blockIdx.x * 4 + wave) * VT;   // first 16-row vocab block of the wave
+  const int nvb = (a.V + 15) / 16;
+  if (vb0 >= nvb) return;
+  const int K = a.K, KS = K / 64;
+  const uint4* Wp = (const uint4*)a.w;
   const uint16_t* X = (const uint16_t*)a.x;
-  const uint16_t* wrow[VT];
+  const uint4* wt[VT];
 #pragma unroll
-  for (int vt = 0; vt < VT; ++vt) {
-    const int row = min(vbase + 16 * vt + col, a.V - 1);
-    wrow[vt] = W + (size_t)row * K + 16 * quad;
-  }
+  for (int vt = 0; vt < VT; ++vt) wt[vt] = Wp + (size_t)min(vb0 + vt, nvb - 1) * KS * 128 + lane;
   for (int m0 = 0; m0 < a.M; m0 += 16 * NT) {
     f32x4 acc[VT][NT];
     float ss[NT];
@@ -482,26 +542,53 @@ __global__ __launch_bounds__(256) void k_lmhead_bf16(LmArgs a) {
     const uint16_t* xrow[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) xrow[nt] = X + (size_t)(m0 + 16 * nt + col) * K + 16 * quad;
-    for (int k0 = 0; k0 < K; k0 += 64) {
-      bf16x8 a0[VT], a1[VT], b0[NT], b1[NT];
+    struct WS { uint4 w[VT][2]; };
+    struct XS { uint4 x[NT][2]; };
+    auto load_w = [&](WS& S, int ks) {
+      ks = min(ks, KS - 1);  // past the end: the last step again (cache hit), keeps the ring branch-free
 #pragma unroll
       for (int vt = 0; vt < VT; ++vt) {
-        a0[vt] = as_bf16x8(*(const uint4*)(wrow[vt] + k0));
-        a1[vt] = as_bf16x8(*(const uint4*)(wrow[vt] + k0 + 8));
+        S.w[vt][0] = wt[vt][(size_t)ks * 128];
+        S.w[vt][1] = wt[vt][(size_t)ks * 128 + 64];
       }
+    };
+    auto load_x = [&](XS& S, int ks) {
+      ks = min(ks, KS - 1);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        b0[nt] = as_bf16x8(*(const uint4*)(xrow[nt] + k0));
-        b1[nt] = as_bf16x8(*(const uint4*)(xrow[nt] + k0 + 8));
-        ss[nt] += sumsq8(b0[nt]) + sumsq8(b1[nt]);
+        S.x[nt][0] = *(const uint4*)(xrow[nt] + ks * 64);
+        S.x[nt][1] = *(const uint4*)(xrow[nt] + ks * 64 + 8);
       }
+    };
+    auto step = [&](const WS& A, const XS& B) {
 #pragma unroll
-      for (int vt = 0; vt < VT; ++vt)
+      for (int nt = 0; nt < NT; ++nt) {
+        ss[nt] += sumsq8(as_bf16x8(B.x[nt][0])) + sumsq8(as_bf16x8(B.x[nt][1]));
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          acc[vt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[vt], b0[nt], acc[vt][nt], 0, 0, 0);
-          acc[vt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[vt], b1[nt], acc[vt][nt], 0, 0, 0);
+        for (int vt = 0; vt < VT; ++vt) {
+          acc[vt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(A.w[vt][0]), as_bf16x8(B.x[nt][0]),
+                                                                acc[vt][nt], 0, 0, 0);
+          acc[vt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(A.w[vt][1]), as_bf16x8(B.x[nt][1]),
+                                                                acc[vt][nt], 0, 0, 0);
         }
+      }
+    };
+    // W: three-stage ring (two 64-wide k steps in flight while one is consumed);
+    // x: two stages (one step ahead). Each step's x is issued before the W of
+    // two steps later: vector loads retire in order, so waiting for x never
+    // waits for W that is not needed yet. The pattern repeats every 6 steps.
+    WS w0, w1, w2;
+    XS xa, xb;
+    load_x(xa, 0);
+    load_w(w0, 0);
+    load_w(w1, 1);
+    for (int ks = 0; ks < KS; ks += 6) {
+      load_x(xb, ks + 1); load_w(w2, ks + 2); step(w0, xa);
+      load_x(xa, ks + 2); load_w(w0, ks + 3); if (ks + 1 < KS) step(w1, xb);
+      load_x(xb, ks + 3); load_w(w1, ks + 4); if (ks + 2 < KS) step(w2, xa);
+      load_x(xa, ks + 4); load_w(w2, ks + 5); if (ks + 3 < KS) step(w0, xb);
+      load_x(xb, ks + 5); load_w(w0, ks + 6); if (ks + 4 < KS) step(w1, xa);
+      load_x(xa, ks + 6); load_w(w1, ks + 7); if (ks + 5 < KS) step(w2, xb);
     }
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -512,15 +599,15 @@ __global__ __launch_bounds__(256) void k_lmhead_bf16(LmArgs a) {
       if (m >= a.M) continue;
 #pragma unroll
       for (int vt = 0; vt < VT; ++vt) {
-        const int v = vbase + 16 * vt + 4 * quad;
+        const int v = 16 * (vb0 + vt) + 4 * quad;
         float* out = a.logits + (size_t)m * a.V + v;
-        const f32x4 c = acc[vt][nt];
+        const f32x4 cc = acc[vt][nt];
         if (v + 3 < a.V && (a.V & 3) == 0) {
-          *(float4*)out = make_float4(c[0] * rho, c[1] * rho, c[2] * rho, c[3] * rho);
+          *(float4*)out = make_float4(cc[0] * rho, cc[1] * rho, cc[2] * rho, cc[3] * rho);
         } else {
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            if (v + r < a.V) out[r] = c[r] * rho;
+            if (v + r < a.V) out[r] = cc[r] * rho;
         }
       }
     }
@@ -556,14 +643,18 @@ __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
 }
 
 __device__ __forceinline__ Top2 merge(const Top2& A, const Top2& B) {
+  // winner's best, then the better of the winner's second and the loser's best
+  // (written with selects only, so the candidates stay in registers)
+  const bool af = better(A.v1, A.i1, B.v1, B.i1);
+  const float wv2 = af ? A.v2 : B.v2, lv1 = af ? B.v1 : A.v1;
+  const int wi2 = af ? A.i2 : B.i2, li1 = af ? B.i1 : A.i1;
+  const bool w2 = better(wv2, wi2, lv1, li1);
   Top2 R;
-  if (better(A.v1, A.i1, B.v1, B.i1)) {
-    R.v1 = A.v1; R.i1 = A.i1; R.k1 = A.k1;
-    if (better(A.v2, A.i2, B.v1, B.i1)) { R.v2 = A.v2; R.i2 = A.i2; } else { R.v2 = B.v1; R.i2 = B.i1; }
-  } else {
-    R.v1 = B.v1; R.i1 = B.i1; R.k1 = B.k1;
-    if (better(B.v2, B.i2, A.v1, A.i1)) { R.v2 = B.v2; R.i2 = B.i2; } else { R.v2 = A.v1; R.i2 = A.i1; }
-  }
+  R.v1 = af ? A.v1 : B.v1;
+  R.i1 = af ? A.i1 : B.i1;
+  R.k1 = af ? A.k1 : B.k1;
+  R.v2 = w2 ? wv2 : lv1;
+  R.i2 = w2 ? wi2 : li1;
   return R;
 }
 
@@ -594,8 +685,7 @@ __device__ Top2 block_top2(Top2 c) {
 //   s_hat_k(v) = ((1 + beta_k) s_k(v) - beta_k s_0(v)) + gamma ln r_k     (Eq. 2)
 // evaluated in float32 in exactly that order without fused multiply-adds,
 // S(v) = max over experts 1..N (lowest k on ties), then the block's best and
-// second-best tokens. The last block of a query (atomic ticket) merges all
-// slices and writes y_t (Eq. 3), the expert, and the two scores.
+// second-best tokens, merged per query by k_fuse_final.
 __global__ __launch_bounds__(kFuseBlock) void k_fuse(FuseArgs a) {
 #pragma clang fp contract(off)
   const int b = blockIdx.y;
@@ -605,32 +695,41 @@ __global__ __launch_bounds__(kFuseBlock) void k_fuse(FuseArgs a) {
   const int v = blockIdx.x * kFuseBlock + threadIdx.x;
   Top2 c{kNegInf, 0x7FFFFFFF, 0, kNegInf, 0x7FFFFFFF};
   if (v < a.V) {
-    const float sa = a.logits[(size_t)s0 * a.V + v];
+    const float* colp = a.logits + v;
+    const float sa = colp[(size_t)s0 * a.V];
     float best = kNegInf;
     int bk = 0;
-    for (int k = 1; k <= N; ++k) {
-      const float beta = a.beta[e0 + k - 1];
-      const float coef = 1.0f + beta;
-      const float t1 = coef * a.logits[(size_t)(s0 + k) * a.V + v];
-      const float t2 = beta * sa;
-      const float val = (t1 - t2) + a.prior[e0 + k - 1];
-      if (val > best) { best = val; bk = k; }
+    // experts in batches of 16 independent loads, so their latencies overlap
+    for (int kb = 1; kb <= N; kb += 16) {
+      float x[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) x[j] = (kb + j <= N) ? colp[(size_t)(s0 + kb + j) * a.V] : 0.f;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int k = kb + j;
+        if (k > N) continue;
+        const float beta = a.beta[e0 + k - 1];
+        const float coef = 1.0f + beta;
+        const float t1 = coef * x[j];
+        const float t2 = beta * sa;
+        const float val = (t1 - t2) + a.prior[e0 + k - 1];
+        if (val > best) { best = val; bk = k; }
+      }
     }
     c.v1 = best; c.i1 = v; c.k1 = bk;
   }
   c = block_top2(c);
-  __shared__ int is_last;
   if (threadIdx.x == 0) {
     float* p = a.part + ((size_t)b * a.nblk + blockIdx.x) * 5;
     p[0] = c.v1; p[1] = __int_as_float(c.i1); p[2] = __int_as_float(c.k1);
     p[3] = c.v2; p[4] = __int_as_float(c.i2);
-    __threadfence();
-    const int prev = __hip_atomic_fetch_add(a.tickets + b, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    is_last = prev == a.nblk - 1;
   }
-  __syncthreads();
-  if (!is_last) return;
-  __threadfence();
+}
+
+// One block per query: merges the vocabulary slices' candidates and writes
+// y_t (Eq. 3), the expert that scored it, and the two best distinct scores.
+__global__ __launch_bounds__(kFuseBlock) void k_fuse_final(FuseArgs a) {
+  const int b = blockIdx.x;
   Top2 r{kNegInf, 0x7FFFFFFF, 0, kNegInf, 0x7FFFFFFF};
   for (int i = threadIdx.x; i < a.nblk; i += blockDim.x) {
     const float* p = a.part + ((size_t)b * a.nblk + i) * 5;
@@ -644,7 +743,6 @@ __global__ __launch_bounds__(kFuseBlock) void k_fuse(FuseArgs a) {
     if (a.winner) a.winner[b] = r.k1;
     if (a.top1) a.top1[b] = r.v1;
     if (a.top2) a.top2[b] = r.v2;
-    a.tickets[b] = 0;
   }
 }
 
@@ -701,8 +799,7 @@ __device__ __forceinline__ float row_lse(const BetaArgs& a, int s) {
 // beta_k = JSD(p_k || p_0) in bits (first step, dynamic mode; Section 3 reads
 // beta from AdaCAD's with-context vs no-context divergence). Per (expert, chunk)
 // partial sums of 1/2 p (ln p - ln m) + 1/2 q (ln q - ln m), m = (p + q) / 2,
-// with ln m = max(ln p, ln q) + log1p(exp(-|ln p - ln q|)) - ln 2; the last
-// chunk block of an expert adds the partials in chunk order and divides by ln 2.
+// with ln m = max(ln p, ln q) + log1p(exp(-|ln p - ln q|)) - ln 2.
 __global__ __launch_bounds__(256) void k_beta_jsd(BetaArgs a) {
   const int e = blockIdx.y, ch = blockIdx.x;
   const int sk = a.exp_seq[e];
@@ -720,22 +817,16 @@ __global__ __launch_bounds__(256) void k_beta_jsd(BetaArgs a) {
     acc += 0.5f * (p * (lp - lm) + q * (lq - lm));
   }
   acc = block_reduce_sum(acc);
-  __shared__ int is_last;
-  if (threadIdx.x == 0) {
-    a.jsd_part[(size_t)e * a.nchunk + ch] = acc;
-    __threadfence();
-    const int prev = __hip_atomic_fetch_add(a.tickets + e, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    is_last = prev == a.nchunk - 1;
-  }
-  __syncthreads();
-  if (!is_last) return;
-  if (threadIdx.x == 0) {
-    __threadfence();
-    float tot = 0.f;
-    for (int c = 0; c < a.nchunk; ++c) tot += a.jsd_part[(size_t)e * a.nchunk + c];
-    a.beta[e] = tot / ln2;
-    a.tickets[e] = 0;
-  }
+  if (threadIdx.x == 0) a.jsd_part[(size_t)e * a.nchunk + ch] = acc;
+}
+
+// beta_k = (sum of expert k's chunk partials, in chunk order) / ln 2.
+__global__ __launch_bounds__(256) void k_beta_final(BetaArgs a, int n_exp) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= n_exp) return;
+  float tot = 0.f;
+  for (int c = 0; c < a.nchunk; ++c) tot += a.jsd_part[(size_t)e * a.nchunk + c];
+  a.beta[e] = tot / 0.69314718055994530942f;
 }
 
 // --------------------------------------------------- generation input synth
@@ -785,6 +876,21 @@ __global__ __launch_bounds__(256) void k_synth(SynthArgs a) {
 
 // ------------------------------------------------------------------ launchers
 
+namespace {
+// Launch, bracketed by the timing events (recorded on the launch stream) when given.
+template <typename Kern, typename... Args>
+hipError_t go(Kern kernel, dim3 grid, dim3 block, size_t shm, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1,
+              Args... args) {
+  if (ev0) hipEventRecord(ev0, st);
+  hipLaunchKernelGGL(kernel, grid, block, shm, st, args...);
+  hipError_t e = hipGetLastError();
+  if (ev1) hipEventRecord(ev1, st);
+  return e;
+}
+hipEvent_t t0(const Timing* tm) { return tm ? tm->start : nullptr; }
+hipEvent_t t1(const Timing* tm) { return tm ? tm->stop : nullptr; }
+}  // namespace
+
 hipError_t launch_fill_i32(int32_t* p, int32_t v, size_t n, hipStream_t st) {
   if (n == 0) return hipSuccess;
   const int blocks = (int)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
@@ -800,62 +906,79 @@ hipError_t launch_zero_bytes(void* p, size_t nbytes, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_load(const LoadArgs& a, int n_items, bool bf16, hipStream_t st) {
+hipError_t launch_load(const LoadArgs& a, int n_items, bool bf16, hipStream_t st, const Timing* tm) {
   if (n_items == 0) return hipSuccess;
   dim3 grid(n_items, a.n_layers);
-  if (bf16) k_load<true><<<grid, 256, 0, st>>>(a);
-  else k_load<false><<<grid, 256, 0, st>>>(a);
-  return hipGetLastError();
+  if (bf16) return go(k_load<true>, grid, dim3(256), 0, st, t0(tm), t1(tm), a);
+  return go(k_load<false>, grid, dim3(256), 0, st, t0(tm), t1(tm), a);
 }
 
-hipError_t launch_append(const AppendArgs& a, bool bf16, hipStream_t st) {
-  const int blocks = a.n_seqs * a.n_layers + 1;
-  if (bf16) k_append<true><<<blocks, 128, 0, st>>>(a);
-  else k_append<false><<<blocks, 128, 0, st>>>(a);
-  return hipGetLastError();
+hipError_t launch_append(const AppendArgs& a, bool bf16, hipStream_t st, const Timing* tm) {
+  const int blocks = a.n_seqs * a.n_layers + a.n_seqs;
+  if (bf16) return go(k_append<true>, dim3(blocks), dim3(128), 0, st, t0(tm), t1(tm), a);
+  return go(k_append<false>, dim3(blocks), dim3(128), 0, st, t0(tm), t1(tm), a);
 }
 
-hipError_t launch_attn(const AttnArgs& a, int n_blocks, int head_dim, bool bf16, hipStream_t st) {
+hipError_t launch_attn(const AttnArgs& a, int n_blocks, int head_dim, bool bf16, hipStream_t st, const Timing* tm) {
   if (bf16) {
-    if (head_dim == 128) k_attn_bf16<128><<<n_blocks, 64, 0, st>>>(a);
-    else if (head_dim == 64) k_attn_bf16<64><<<n_blocks, 64, 0, st>>>(a);
-    else return hipErrorInvalidValue;
-  } else {
-    k_attn_f32<<<n_blocks, 64, 0, st>>>(a, head_dim);
+    if (head_dim == 128) return go(k_attn_bf16<128>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a);
+    if (head_dim == 64) return go(k_attn_bf16<64>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a);
+    return hipErrorInvalidValue;
   }
+  return go(k_attn_f32, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a, head_dim);
+}
+
+int attn_blocks_per_cu(int head_dim, bool bf16) {
+  int n = 0;
+  hipError_t e;
+  if (bf16 && head_dim == 128) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_bf16<128>, 64, 0);
+  else if (bf16) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_bf16<64>, 64, 0);
+  else e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_f32, 64, 0);
+  return (e == hipSuccess && n > 0) ? n : 8;
+}
+
+hipError_t launch_attn_combine(const AttnArgs& a, int head_dim, int max_splits, bool bf16, hipStream_t st,
+                               const Timing* tm) {
+  const int blocks = a.n_seqs * a.n_kv_heads;
+  (void)max_splits;
+  if (bf16) return go(k_attn_combine<true>, dim3(blocks), dim3(128), 0, st, t0(tm), t1(tm), a, head_dim);
+  return go(k_attn_combine<false>, dim3(blocks), dim3(128), 0, st, t0(tm), t1(tm), a, head_dim);
+}
+
+hipError_t launch_pack_lm_head(const void* w, void* wp, int V, int K, bool bf16, hipStream_t st) {
+  if (!bf16) return hipMemcpyAsync(wp, w, (size_t)V * K * 4, hipMemcpyDeviceToDevice, st);
+  k_pack_w_bf16<<<2048, 256, 0, st>>>((const uint16_t*)w, (uint16_t*)wp, V, K);
   return hipGetLastError();
 }
 
-hipError_t launch_lmhead(const LmArgs& a, bool bf16, hipStream_t st) {
+hipError_t launch_lmhead(const LmArgs& a, bool bf16, hipStream_t st, const Timing* tm) {
   if (bf16) {
     constexpr int VT = 4, NT = 3;
-    const int rows_per_block = 4 * 16 * VT;
-    const int blocks = (a.V + rows_per_block - 1) / rows_per_block;
-    k_lmhead_bf16<VT, NT><<<blocks, 256, 0, st>>>(a);
-  } else {
-    k_lmhead_f32<<<(a.V + 255) / 256, 256, 0, st>>>(a);
+    const int nvb = (a.V + 15) / 16;
+    const int blocks = (nvb + 4 * VT - 1) / (4 * VT);
+    return go(k_lmhead_bf16<VT, NT>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), a);
   }
-  return hipGetLastError();
+  return go(k_lmhead_f32, dim3((a.V + 255) / 256), dim3(256), 0, st, t0(tm), t1(tm), a);
 }
 
-hipError_t launch_beta(const BetaArgs& a, int n_seqs, int n_exp, hipStream_t st) {
-  k_beta_lse<<<dim3(a.nchunk, n_seqs), 256, 0, st>>>(a);
-  hipError_t e = hipGetLastError();
+hipError_t launch_beta(const BetaArgs& a, int n_seqs, int n_exp, hipStream_t st, const Timing* tm) {
+  hipError_t e = go(k_beta_lse, dim3(a.nchunk, n_seqs), dim3(256), 0, st, t0(tm), nullptr, a);
   if (e != hipSuccess) return e;
-  k_beta_jsd<<<dim3(a.nchunk, n_exp), 256, 0, st>>>(a);
-  return hipGetLastError();
+  e = go(k_beta_jsd, dim3(a.nchunk, n_exp), dim3(256), 0, st, nullptr, nullptr, a);
+  if (e != hipSuccess) return e;
+  return go(k_beta_final, dim3((n_exp + 255) / 256), dim3(256), 0, st, nullptr, t1(tm), a, n_exp);
 }
 
-hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st) {
-  k_fuse<<<dim3(a.nblk, n_queries), kFuseBlock, 0, st>>>(a);
-  return hipGetLastError();
+hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st, const Timing* tm) {
+  hipError_t e = go(k_fuse, dim3(a.nblk, n_queries), dim3(kFuseBlock), 0, st, t0(tm), nullptr, a);
+  if (e != hipSuccess) return e;
+  return go(k_fuse_final, dim3(n_queries), dim3(kFuseBlock), 0, st, nullptr, t1(tm), a);
 }
 
-hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st) {
+hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st, const Timing* tm) {
   const int blocks = n_seqs * a.n_layers;
-  if (a.bf16) k_synth<true><<<blocks, 256, 0, st>>>(a);
-  else k_synth<false><<<blocks, 256, 0, st>>>(a);
-  return hipGetLastError();
+  if (a.bf16) return go(k_synth<true>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), a);
+  return go(k_synth<false>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), a);
 }
 
 hipError_t launch_copy_rows(const void* src, void* dst, size_t nbytes, hipStream_t st) {

@@ -43,6 +43,13 @@ class PcedSession:
         self.B = 0
         self.NE = 0
 
+    def pack_lm_head(self, w):
+        """Packed copy (device) of row-major [V][hidden] LM-head weights."""
+        torch = _torch()
+        out = torch.empty(_lib.pced_lm_head_bytes(self.cfg), dtype=torch.uint8, device=self.device)
+        _lib.pced_pack_lm_head(self.cfg, w, out)
+        return out
+
     # ------------------------------------------------------------------ load
     def load(self, n_experts: Sequence[int], cache_len: Sequence[int], src_k, src_v, relevance,
              gamma=2.5, beta=None, page_table=None, reserve_tokens=0):

@@ -29,7 +29,7 @@ def _run_steps(wl, steps, want=("logits", "attn_out", "winner", "top1", "top2", 
                attn_layers=None, sess=None):
     """Run `steps` GPU steps and the oracle beside them; check every stage."""
     sess = sess or _session(wl)
-    Wt = wl.lm_head_device(DEV)
+    Wt = sess.pack_lm_head(wl.lm_head_device(DEV))
     Wh = wl.lm_head_host()
     orc = make_oracle(wl)
     tol = REL_TOL[wl.geom.dtype]
@@ -96,7 +96,7 @@ def test_lmhead_stage_bf16_and_tails():
         xh = W.host_values(xk, 0, M * hidden, 1.0, "bf16").reshape(M, hidden)
         xd = W.device_values(xk, 0, M * hidden, 1.0, "bf16", DEV).reshape(M, hidden)
         logits = torch.empty((M, V), dtype=torch.float32, device=DEV)
-        sess.ctx.pced_lmhead(xd, M, wl.lm_head_device(DEV), logits)
+        sess.ctx.pced_lmhead(xd, M, sess.pack_lm_head(wl.lm_head_device(DEV)), logits)
         torch.cuda.synchronize()
         ref = O.lm_head(O.decode_stored(xh, "bf16"), O.decode_stored(wl.lm_head_host(), "bf16"), "rms")
         err = rel_err_rows(_np(logits), ref)
@@ -108,7 +108,7 @@ def test_lmhead_stage_bf16_and_tails():
 def _fuse_session(n_experts, V, beta, seed, rel=None):
     from paper_2601_08670_amd.session import PcedSession
     S = sum(n + 1 for n in n_experts)
-    sess = PcedSession(n_layers=1, n_q_heads=1, n_kv_heads=1, head_dim=64, vocab=V, dtype="bf16",
+    sess = PcedSession(n_layers=1, n_q_heads=4, n_kv_heads=1, head_dim=64, vocab=V, dtype="bf16",
                        max_queries=len(n_experts), max_seqs=S, max_pages=S, max_pages_per_seq=1, device=DEV,
                        poison=True)
     src = [torch.zeros((1, 1, 1, 64), dtype=torch.int16, device=DEV) for _ in range(S)]
