@@ -1,0 +1,172 @@
+"""C ABI checks that need no GPU: the library loads, exports every function the
+header declares, and rejects invalid arguments on the host before anything is
+enqueued (nothing here launches a kernel)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2601_08670_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pced.h")
+
+OK, INVALID, CAPACITY, HIPERR, UNSUPPORTED, STATE = 0, 1, 2, 3, 4, 5
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pced_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declarations_are_exported():
+    lib = _lib.load_library()
+    names = declared_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in pced.h but not exported"
+    assert sorted(_lib.EXPORTED) == names
+
+
+def cfg(**kw):
+    base = dict(n_layers=2, n_q_heads=8, n_kv_heads=2, head_dim=64, vocab=1000, dtype="bf16",
+                max_queries=2, max_seqs=8, max_pages=64, max_pages_per_seq=16)
+    base.update(kw)
+    return _lib.make_config(**base)
+
+
+def test_sizes():
+    c = cfg()
+    assert _lib.pced_pool_bytes(c) == 2 * 64 * 2 * 16 * 64 * 2
+    assert _lib.pced_lm_head_bytes(c) == 1008 * 512 * 2          # vocab padded to 16 rows
+    assert _lib.pced_lm_head_bytes(cfg(dtype="f32", n_q_heads=4, head_dim=16)) == 1000 * 64 * 4
+    assert _lib.pced_workspace_bytes(c) > 0
+
+
+@pytest.mark.parametrize("bad", [
+    dict(n_layers=0), dict(n_kv_heads=3), dict(n_q_heads=64, n_kv_heads=2), dict(head_dim=96),
+    dict(hidden=1000), dict(n_q_heads=2, n_kv_heads=1), dict(vocab=1), dict(max_queries=0),
+    dict(max_seqs=1), dict(max_pages=0), dict(dtype="f32", head_dim=130),
+])
+def test_invalid_config_sizes_are_zero(bad):
+    c = cfg(**bad)
+    assert _lib.pced_workspace_bytes(c) == 0
+    assert _lib.pced_pool_bytes(c) == 0
+    assert _lib.pced_lm_head_bytes(c) == 0
+
+
+def test_page_size_must_be_16():
+    c = cfg()
+    c.page_size = 32
+    assert _lib.pced_workspace_bytes(c) == 0
+
+
+class FakeCtx:
+    """A context over a fake (never dereferenced) workspace address."""
+
+    def __init__(self, c=None):
+        self.lib = _lib.load_library()
+        self.cfg = c or cfg()
+        self.ws = 1 << 40  # 256-byte aligned; create() does not touch device memory
+        h = ctypes.c_void_p()
+        st = self.lib.pced_create(ctypes.byref(self.cfg), self.ws, _lib.pced_workspace_bytes(self.cfg),
+                                  ctypes.byref(h))
+        assert st == OK, self.lib.pced_last_error()
+        self.h = h
+
+    def close(self):
+        self.lib.pced_destroy(self.h)
+
+
+def test_create_errors():
+    lib = _lib.load_library()
+    c = cfg()
+    n = _lib.pced_workspace_bytes(c)
+    h = ctypes.c_void_p()
+    assert lib.pced_create(ctypes.byref(c), 1 << 40, n, None) == INVALID
+    assert lib.pced_create(ctypes.byref(c), None, n, ctypes.byref(h)) == INVALID
+    assert lib.pced_create(ctypes.byref(c), (1 << 40) + 16, n, ctypes.byref(h)) == INVALID
+    assert lib.pced_create(ctypes.byref(c), 1 << 40, n - 1, ctypes.byref(h)) == CAPACITY
+    assert b"too small" in lib.pced_last_error()
+    bad = cfg(n_kv_heads=3)
+    assert lib.pced_create(ctypes.byref(bad), 1 << 40, n, ctypes.byref(h)) == INVALID
+    assert b"invalid config" in lib.pced_last_error()
+    lib.pced_destroy(None)
+
+
+def _arr(t, vals):
+    return (t * len(vals))(*vals)
+
+
+def _load(fc, n_experts, cache_len, pt=None, reserve=0, rel=None, beta=None, gamma=2.5, srcs=True):
+    S = len(cache_len)
+    ptrs = (ctypes.c_void_p * S)(*([1 << 30] * S)) if srcs else None
+    rel = rel if rel is not None else [0.5] * sum(n_experts)
+    return fc.lib.pced_load_caches(
+        fc.h, len(n_experts), _arr(ctypes.c_int32, n_experts), _arr(ctypes.c_int32, cache_len), ptrs, ptrs,
+        1 << 41, 1 << 41, None if pt is None else _arr(ctypes.c_int32, pt), reserve,
+        _arr(ctypes.c_float, rel), ctypes.c_float(gamma), None if beta is None else _arr(ctypes.c_float, beta), None)
+
+
+def test_load_validation_before_any_launch():
+    fc = FakeCtx()
+    lib = fc.lib
+    assert _load(fc, [], []) == INVALID                                  # zero queries
+    assert _load(fc, [1, 1, 1], [1] * 6) == INVALID                      # more than max_queries
+    assert _load(fc, [0], [4]) == INVALID                                # a query without documents
+    assert _load(fc, [8], [4] * 9) == CAPACITY                           # 9 sequences > max_seqs 8
+    assert b"max_seqs" in lib.pced_last_error()
+    assert _load(fc, [2], [4, 0, 4]) == INVALID                          # empty cache
+    assert _load(fc, [2], [4, 4, 4], srcs=False) == INVALID              # no source pointers
+    assert _load(fc, [2], [4, 4, 300]) == CAPACITY                       # 19 pages > 16 per sequence
+    assert _load(fc, [2], [4, 4, 4], reserve=300) == CAPACITY
+    assert _load(fc, [2], [200, 200, 250], reserve=10) == CAPACITY       # 13+13+17 > 16 or pool
+    assert _load(fc, [1], [4, 4], rel=[float("nan")]) == INVALID
+    assert _load(fc, [1], [4, 4], beta=[float("inf")]) == INVALID
+    assert _load(fc, [1], [4, 4], gamma=float("nan")) == INVALID
+    # caller page tables: duplicate ids, ids out of range, missing pages of a cache
+    P = 16
+    pt = [-1] * (2 * P)
+    pt[0], pt[P] = 3, 3
+    assert _load(fc, [1], [4, 4], pt=pt) == INVALID
+    assert b"twice" in lib.pced_last_error()
+    pt[P] = 64
+    assert _load(fc, [1], [4, 4], pt=pt) == INVALID
+    pt[P] = -1
+    assert _load(fc, [1], [4, 4], pt=pt) == INVALID
+    # nothing was loaded: the step entry points still report STATE
+    tok = ctypes.c_void_p(1 << 42)
+    assert lib.pced_step(fc.h, 1, 1, 1, 1, tok, None, None) == STATE
+    out = (ctypes.c_int32 * 8)()
+    assert lib.pced_get_lengths(fc.h, out, 8) == STATE
+    fc.close()
+
+
+def test_entry_points_before_load_report_state():
+    fc = FakeCtx()
+    lib = fc.lib
+    syn = _lib.pced_synth(seed=1, first_token=0)
+    assert lib.pced_step(fc.h, 1, 1, 1, 1, 1, None, None) == STATE
+    assert lib.pced_generate(fc.h, 2, ctypes.byref(syn), 1, 1, None, None) == STATE
+    assert lib.pced_fuse(fc.h, 1, 1, 1, None, None) == STATE
+    assert b"pced_load_caches" in lib.pced_last_error()
+    assert lib.pced_step(None, 1, 1, 1, 1, 1, None, None) == INVALID
+    assert lib.pced_lmhead(fc.h, None, 1, 1, 1, None) == INVALID
+    assert lib.pced_lmhead(fc.h, 1, 0, 1, 1, None) == INVALID
+    assert lib.pced_lmhead(fc.h, 1, 9, 1, 1, None) == INVALID           # > max_seqs
+    assert lib.pced_profile_read(fc.h, None) == INVALID
+    assert lib.pced_profile_enable(None, 1) == INVALID
+    fc.close()
+
+
+def test_pack_lm_head_validation():
+    lib = _lib.load_library()
+    c = cfg()
+    assert lib.pced_pack_lm_head(ctypes.byref(c), None, 1 << 40, None) == INVALID
+    # overlapping source and destination
+    assert lib.pced_pack_lm_head(ctypes.byref(c), 1 << 40, (1 << 40) + 64, None) == INVALID
+    assert b"overlap" in lib.pced_last_error()
+    bad = cfg(vocab=1)
+    assert lib.pced_pack_lm_head(ctypes.byref(bad), 1 << 40, 1 << 41, None) == INVALID
