@@ -50,7 +50,36 @@ def parse():
     p.add_argument("--cpu-sample-layers", type=int, default=12)
     p.add_argument("--cpu-sample-vocab", type=int, default=32768)
     p.add_argument("--no-events", action="store_true", help="time without per-launch events")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="after the timed steps, run one plain 256 MiB device copy (scale reference for "
+                        "the FETCH_SIZE / WRITE_SIZE counters)")
     return p.parse_args()
+
+
+def kernel_source_sha256() -> str:
+    import hashlib
+    path = os.path.join(ROOT, "paper_2601_08670_amd", "csrc", "pced_kernels.hip")
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per decode-attention launch from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known size), or None if
+    there is none for this workload or the kernels changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if line.startswith("- ") and ": " in line:
+            k, v = line[2:].strip().split(": ", 1)
+            vals[k.strip("` ")] = v.strip("` ")
+    if vals.get("kernel source sha256") != kernel_source_sha256():
+        return None
+    try:
+        return float(vals["pced_decode_attn HBM bytes per launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(wl, n_layers_sample: int, vocab_sample: int) -> dict:
@@ -186,9 +215,20 @@ def main():
     roofline = None
     if attn:
         roofline = {"bound": "hbm", "achieved": attn["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": attn["GB/s"] / HBM_PEAK_GBS, "traffic": None, "kernel": "pced_decode_attn",
+                    "frac": attn["GB/s"] / HBM_PEAK_GBS, "traffic": measured_traffic(wl.name),
+                    "kernel": "pced_decode_attn",
                     "bytes_per_launch": prof["attn"]["bytes"] / prof["attn"]["launches"],
                     "avg_launch_us": attn["avg_us"]}
+
+    if args.copy_calibration:
+        n = 256 << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log("[bench] calibration copy of 256 MiB done")
 
     cpu = None
     if not args.no_cpu_baseline:
