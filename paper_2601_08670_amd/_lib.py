@@ -11,7 +11,8 @@ import os
 from typing import Optional, Sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libpced.so")
+# PCED_LIBRARY may name another build of the same library (e.g. a debug build)
+LIB_PATH = os.environ.get("PCED_LIBRARY") or os.path.join(_HERE, "libpced.so")
 
 PCED_F32, PCED_BF16 = 0, 1
 PCED_NORM_NONE, PCED_NORM_RMS = 0, 1

@@ -70,6 +70,7 @@ struct Layout {
   size_t work_off, work_list, work_pages, tick_attn, tick_fuse, tick_beta, prev_tok, beta, part_acc, part_ml, x, logits,
       fuse_part, lse_part, jsd_part, syn_q, syn_k, syn_v, total;
   int rows_pad, nblk_fuse, nchunk, max_work;
+  size_t part_slots;
 };
 
 Layout make_layout(const pced_config& c) {
@@ -104,8 +105,10 @@ Layout make_layout(const pced_config& c) {
   L.tick_beta = take(S * 4);
   L.prev_tok = take(B * 4);
   L.beta = take(S * 4);
-  L.part_acc = take((size_t)L.max_work * c.n_kv_heads * G * c.head_dim * 4);
-  L.part_ml = take((size_t)L.max_work * c.n_kv_heads * G * 2 * 4);
+  // split partials: [S*Hkv][stride][G][D] with stride <= pages per sequence
+  L.part_slots = (size_t)c.max_seqs * c.n_kv_heads * c.max_pages_per_seq;
+  L.part_acc = take(L.part_slots * G * c.head_dim * 4);
+  L.part_ml = take(L.part_slots * G * 2 * 4);
   L.x = take((size_t)L.rows_pad * c.hidden * es);
   L.logits = take(S * c.vocab * 4);
   L.fuse_part = take(B * L.nblk_fuse * 5 * 4);
@@ -350,6 +353,7 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
   at.maxpps = P;
   at.t = c->t;
   at.split_tokens = split;
+  at.split_stride = max_splits;
   at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)cfg.head_dim));
   double kv_tokens = 0;
   for (int s = 0; s < c->S; ++s) kv_tokens += c->len[s] + 1;

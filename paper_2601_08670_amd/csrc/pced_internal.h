@@ -24,13 +24,13 @@ struct AttnArgs {
   const int32_t* work_off;  // [S+1] prefix of splits per sequence (this step)
   const int4* work_list;    // [work] (sequence, first token, end token, splits of the sequence)
   const int32_t* work_pages;// [work][kMaxSplitPages] physical pages of each work item
-  float* part_acc;          // [work*Hkv][G][D]
-  float* part_ml;           // [work*Hkv][G][2]  (running max in log2 units, sum)
+  float* part_acc;          // [S*Hkv][split_stride][G][D] partial outputs of split work items
+  float* part_ml;           // [S*Hkv][split_stride][G][2] (running max in log2 units, sum)
   void* x_out;              // [S][Hq*D] layer output, storage type
   float* attn_out;          // optional [S][L][Hq][D]
   float* hidden_out;        // optional [S][Hq*D] (last layer only)
   int n_seqs, n_layers, layer, n_q_heads, n_kv_heads, group;
-  int max_pages, maxpps, t, split_tokens, is_last_layer;
+  int max_pages, maxpps, t, split_tokens, split_stride, is_last_layer;
   float scale_log2;         // log2(e) / sqrt(D)
 };
 

@@ -198,43 +198,46 @@ __device__ __forceinline__ void write_o4(const AttnArgs& a, int s, int head, int
 // One block per (sequence, kv-head); sequences that fit one split were written
 // directly by the attention kernel. Each thread owns 4 output dims of one head
 // and issues the loads of up to 16 splits at once (one memory round trip for
-// the usual split counts), merging further groups of 16 online.
+// the usual split counts), merging further groups of 16 online. Slots past the
+// split count are read but never used (no arithmetic touches them).
 template <bool BF16>
 __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a, int D) {
   constexpr int J = 16;
   const int s = blockIdx.x / a.n_kv_heads, g = blockIdx.x % a.n_kv_heads;
-  const int nsplit = a.work_off[s + 1] - a.work_off[s];
-  if (nsplit <= 1) return;
-  const int G = a.group, Hkv = a.n_kv_heads;
-  const int w0 = a.work_off[s] * Hkv + g;
+  const int G = a.group, stride = a.split_stride;
+  // partial slots of (s, g) are contiguous, so their loads do not wait for the
+  // split count: the first J are read at once (clamped inside the slot range)
+  // together with the sequence length
+  const size_t w0 = (size_t)blockIdx.x * stride;
+  const int nsplit = (a.len0[s] + a.t + 1 + a.split_tokens - 1) / a.split_tokens;
   for (int idx = threadIdx.x; idx < G * D / 4; idx += blockDim.x) {
     const int h = (idx * 4) / D, d = (idx * 4) % D;
     float m_run = kNegInf, den = 0.f;
     float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int j0 = 0; j0 < nsplit; j0 += J) {
+    for (int j0 = 0; j0 < max(nsplit, 1); j0 += J) {
       float mj[J], lj[J];
       float4 vj[J];
 #pragma unroll
       for (int u = 0; u < J; ++u) {
-        if (j0 + u < nsplit) {
-          const size_t wj = (size_t)(w0 + (j0 + u) * Hkv);
-          mj[u] = a.part_ml[(wj * G + h) * 2];
-          lj[u] = a.part_ml[(wj * G + h) * 2 + 1];
-          vj[u] = *(const float4*)(a.part_acc + (wj * G + h) * D + d);
-        } else {
-          mj[u] = kNegInf; lj[u] = 0.f; vj[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+        const size_t wj = w0 + min(j0 + u, stride - 1);
+        mj[u] = a.part_ml[(wj * G + h) * 2];
+        lj[u] = a.part_ml[(wj * G + h) * 2 + 1];
+        vj[u] = *(const float4*)(a.part_acc + (wj * G + h) * D + d);
       }
+      if (nsplit <= 1) return;  // written directly by the attention kernel
       float mg = m_run;
 #pragma unroll
-      for (int u = 0; u < J; ++u) mg = fmaxf(mg, mj[u]);
+      for (int u = 0; u < J; ++u)
+        if (j0 + u < nsplit) mg = fmaxf(mg, mj[u]);
       const float r = exp2f(m_run - mg);
       den *= r; num.x *= r; num.y *= r; num.z *= r; num.w *= r;
 #pragma unroll
       for (int u = 0; u < J; ++u) {
-        const float w = exp2f(mj[u] - mg);
-        den += lj[u] * w;
-        num.x += vj[u].x * w; num.y += vj[u].y * w; num.z += vj[u].z * w; num.w += vj[u].w * w;
+        if (j0 + u < nsplit) {
+          const float w = exp2f(mj[u] - mg);
+          den += lj[u] * w;
+          num.x += vj[u].x * w; num.y += vj[u].y * w; num.z += vj[u].z * w; num.w += vj[u].w * w;
+        }
       }
       m_run = mg;
     }
@@ -383,7 +386,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
     }
     return;
   }
-  const size_t w = blockIdx.x;
+  const size_t w = (size_t)(it.s * Hkv + it.g) * a.split_stride + it.split;
   if (col < G) {
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
@@ -458,7 +461,7 @@ __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a, int D) {
     }
     return;
   }
-  const size_t w = blockIdx.x;
+  const size_t w = (size_t)(it.s * Hkv + it.g) * a.split_stride + it.split;
 #pragma unroll
   for (int h = 0; h < kMaxGroup; ++h) {
     if (h >= G) break;
@@ -881,10 +884,10 @@ namespace {
 template <typename Kern, typename... Args>
 hipError_t go(Kern kernel, dim3 grid, dim3 block, size_t shm, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1,
               Args... args) {
-  if (ev0) hipEventRecord(ev0, st);
+  if (ev0) (void)hipEventRecord(ev0, st);
   hipLaunchKernelGGL(kernel, grid, block, shm, st, args...);
   hipError_t e = hipGetLastError();
-  if (ev1) hipEventRecord(ev1, st);
+  if (ev1) (void)hipEventRecord(ev1, st);
   return e;
 }
 hipEvent_t t0(const Timing* tm) { return tm ? tm->start : nullptr; }
