@@ -85,6 +85,11 @@ typedef struct pced_config {
   int32_t max_pages;         /* pool capacity in pages (per layer)               */
   int32_t max_pages_per_seq; /* page-table row length                            */
   int32_t norm;              /* pced_norm                                        */
+  int32_t max_attn_chunks;   /* cap on the attention launch's work chunks (waves
+                                per kv-head), >= 0; 0 = as many as fit on the
+                                GPU at once. A smaller cap leaves compute units
+                                to other work; each chunk then streams more
+                                pages and may span more sequences            */
 } pced_config;
 
 typedef struct pced_ctx pced_ctx;

@@ -59,6 +59,7 @@ bool cfg_valid(const pced_config* c, std::string* why) {
   if (c->max_seqs < 2) return bad("max_seqs < 2");
   if (c->max_pages < 1 || c->max_pages_per_seq < 1) return bad("max_pages and max_pages_per_seq must be >= 1");
   if (c->norm != PCED_NORM_NONE && c->norm != PCED_NORM_RMS) return bad("unknown norm");
+  if (c->max_attn_chunks < 0) return bad("max_attn_chunks must be >= 0");
   // 32-bit index guards used by the kernels
   if ((double)c->max_seqs * c->vocab > 2147483647.0) return bad("max_seqs * vocab exceeds 2^31");
   return true;
@@ -67,7 +68,7 @@ bool cfg_valid(const pced_config* c, std::string* why) {
 struct Layout {
   size_t len0, page_table, seq_query, query_seq0, query_exp0, exp_seq, exp_query, prior, beta_fixed,
       load_items, src_k, src_v, meta_end;
-  size_t work_off, work_list, work_pages, tick_attn, tick_fuse, tick_beta, prev_tok, beta, part_acc, part_ml, x, logits,
+  size_t chunk_info, seg, nparts, work_pages, tick_fuse, tick_beta, prev_tok, beta, part_acc, part_ml, x, logits,
       fuse_part, lse_part, jsd_part, syn_q, syn_k, syn_v, total;
   int rows_pad, nblk_fuse, nchunk, max_work;
   size_t part_slots;
@@ -80,7 +81,7 @@ Layout make_layout(const pced_config& c) {
   L.rows_pad = ceil_div(c.max_seqs, kLmRowsPad) * kLmRowsPad;
   L.nblk_fuse = ceil_div(c.vocab, kFuseBlock);
   L.nchunk = ceil_div(c.vocab, kBetaChunk);
-  L.max_work = c.max_pages;  // every split covers at least one page of its sequence
+  L.max_work = c.max_pages;  // every attention chunk holds at least one page
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes); return r; };
   // metadata block, uploaded by one copy at load
@@ -97,10 +98,10 @@ Layout make_layout(const pced_config& c) {
   L.src_k = take(S * 8);
   L.src_v = take(S * 8);
   L.meta_end = o;
-  L.work_off = take((S + 1) * 4);
-  L.work_list = take((size_t)L.max_work * 16);
+  L.chunk_info = take((size_t)L.max_work * 8);
+  L.seg = take((size_t)L.max_work * kMaxSeg * 2 * 16);
+  L.nparts = take(S * 4);
   L.work_pages = take((size_t)L.max_work * kMaxSplitPages * 4);
-  L.tick_attn = take(S * c.n_kv_heads * 4);
   L.tick_fuse = take(B * 4);
   L.tick_beta = take(S * 4);
   L.prev_tok = take(B * 4);
@@ -194,31 +195,60 @@ int device_cus() {
   return n;
 }
 
-int count_work(const pced_ctx* c, int split_tokens, int* max_splits) {
-  long n = 0;
-  int mx = 0;
-  for (int s = 0; s < c->S; ++s) {
-    const int k = ceil_div(c->len[s] + 1, split_tokens);
-    n += k;
-    mx = std::max(mx, k);
+// Balanced attention plan for the coming step (lengths after its append): the
+// P pages of all sequences, concatenated in sequence order, are cut into C
+// chunks of floor(P/C) or ceil(P/C) pages, one wave per (chunk, kv-head). The
+// device planner uses the same chunk bounds (chunk c starts at floor(c P / C)).
+struct AttnPlan {
+  long pages = 0;     // P
+  int chunks = 0;     // C
+  int max_seg = 0;    // most sequences met by one chunk
+  int max_parts = 0;  // most chunks met by one sequence (partial slots per sequence)
+};
+
+void plan_stats(const std::vector<long>& pre, long P, long C, AttnPlan* out) {
+  const int S = (int)pre.size() - 1;
+  auto lo = [&](long c) { return c * P / C; };
+  auto chunk_of = [&](long u) { return (long)(((u + 1) * C - 1) / P); };
+  int max_seg = 0, max_parts = 0;
+  int s = 0;
+  for (long c = 0; c < C; ++c) {
+    const long b = lo(c), e = lo(c + 1);
+    while (pre[s + 1] <= b) ++s;  // first sequence of the chunk
+    int n = 0;
+    for (int r = s; r < S && pre[r] < e; ++r) ++n;
+    max_seg = std::max(max_seg, n);
   }
-  if (max_splits) *max_splits = mx;
-  return (int)n;
+  for (int r = 0; r < S; ++r)
+    max_parts = std::max(max_parts, (int)(chunk_of(pre[r + 1] - 1) - chunk_of(pre[r]) + 1));
+  out->pages = P;
+  out->chunks = (int)C;
+  out->max_seg = max_seg;
+  out->max_parts = max_parts;
 }
 
-// Pages per attention split: the smallest split whose work items (one wave each)
-// all fit on the chip at once, so every wave starts in the first round and the
-// launch ends when the longest split does; sequences shorter than a split are
-// not split at all.
-int choose_split_tokens(const pced_ctx* c) {
-  long page_heads = 0;
-  for (int s = 0; s < c->S; ++s) page_heads += ceil_div(c->len[s] + 1, kPage);
-  page_heads *= c->cfg.n_kv_heads;
-  const long cap = (long)c->num_cus * c->attn_waves_per_cu;
-  int sp = (int)std::max<long>(1, (page_heads + cap - 1) / cap);
-  sp = std::min(sp, kMaxSplitPages);
-  while (sp < kMaxSplitPages && (long)count_work(c, sp * kPage, nullptr) * c->cfg.n_kv_heads > cap) ++sp;
-  return sp * kPage;
+// C is the number of chunks whose waves all fit on the chip at once (so every
+// wave starts in the first round and streams the same number of pages), at
+// least P/64 (one page id per lane), raised when a chunk would meet more
+// sequences than a wave can stage q rows for.
+AttnPlan plan_attention(const pced_ctx* c) {
+  const int S = c->S;
+  std::vector<long> pre(S + 1, 0);
+  for (int s = 0; s < S; ++s) pre[s + 1] = pre[s] + ceil_div(c->len[s] + 1, kPage);
+  const long P = pre[S];
+  long cap = std::max<long>(1, (long)c->num_cus * c->attn_waves_per_cu / c->cfg.n_kv_heads);
+  if (c->cfg.max_attn_chunks > 0) cap = std::min<long>(cap, c->cfg.max_attn_chunks);
+  long C = std::max<long>(std::min(cap, P), ceil_div(P, (long)kMaxSplitPages));
+  // bf16: the later segments' q rows of a chunk are staged by its wave in LDS
+  const int per_seg_units = c->G * c->cfg.head_dim / 8;
+  const int seg_limit = c->bf16 ? std::min(kMaxSeg, 1 + 64 * kStageUnits / per_seg_units) : kMaxSeg;
+  AttnPlan plan;
+  for (;;) {
+    plan_stats(pre, P, C, &plan);
+    if (plan.max_seg <= seg_limit || C >= P) break;
+    C = std::min(P, C + std::max<long>(1, C / 16));
+  }
+  return plan;
 }
 
 pced_status check_ctx(const pced_ctx* c, bool need_loaded) {
@@ -301,10 +331,8 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
     if (pidx >= P || c->page_table[(size_t)s * P + pidx] < 0)
       return fail(PCED_ERR_CAPACITY, "sequence %d has no page for token %d", s, c->len[s]);
   }
-  const int split = choose_split_tokens(c);
-  int max_splits = 1;
-  const int n_work = count_work(c, split, &max_splits);
-  if (n_work > c->lay.max_work) return fail(PCED_ERR_CAPACITY, "attention work list exceeds workspace");
+  const AttnPlan plan = plan_attention(c);
+  if (plan.chunks > c->lay.max_work) return fail(PCED_ERR_CAPACITY, "attention plan exceeds workspace");
   const double es = (double)esize_of(cfg);
 
   AppendArgs ap{};
@@ -314,8 +342,9 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
   ap.vpool = c->vpool;
   ap.len0 = c->at<int32_t>(c->lay.len0);
   ap.page_table = c->at<int32_t>(c->lay.page_table);
-  ap.work_off = c->at<int32_t>(c->lay.work_off);
-  ap.work_list = c->at<int4>(c->lay.work_list);
+  ap.chunk_info = c->at<int2>(c->lay.chunk_info);
+  ap.seg = c->at<int4>(c->lay.seg);
+  ap.nparts = c->at<int32_t>(c->lay.nparts);
   ap.work_pages = c->at<int32_t>(c->lay.work_pages);
   ap.n_seqs = c->S;
   ap.n_layers = cfg.n_layers;
@@ -324,7 +353,8 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
   ap.max_pages = cfg.max_pages;
   ap.maxpps = P;
   ap.t = c->t;
-  ap.split_tokens = split;
+  ap.n_chunks = plan.chunks;
+  ap.total_pages = (int)plan.pages;
   {
     ProfScope ps(c, PCED_PROF_APPEND, 4.0 * c->S * cfg.n_layers * cfg.n_kv_heads * cfg.head_dim * es, 0);
     HIP_OK(launch_append(ap, c->bf16, st, ps.timing()));
@@ -336,8 +366,9 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
   at.vpool = c->vpool;
   at.len0 = ap.len0;
   at.page_table = ap.page_table;
-  at.work_off = ap.work_off;
-  at.work_list = ap.work_list;
+  at.chunk_info = ap.chunk_info;
+  at.seg = ap.seg;
+  at.nparts = ap.nparts;
   at.work_pages = ap.work_pages;
   at.part_acc = c->at<float>(c->lay.part_acc);
   at.part_ml = c->at<float>(c->lay.part_ml);
@@ -352,8 +383,7 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
   at.max_pages = cfg.max_pages;
   at.maxpps = P;
   at.t = c->t;
-  at.split_tokens = split;
-  at.split_stride = max_splits;
+  at.split_stride = plan.max_parts;
   at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)cfg.head_dim));
   double kv_tokens = 0;
   for (int s = 0; s < c->S; ++s) kv_tokens += c->len[s] + 1;
@@ -365,11 +395,11 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
     at.is_last_layer = l == cfg.n_layers - 1;
     {
       ProfScope ps(c, PCED_PROF_ATTN, attn_bytes, attn_flops);
-      HIP_OK(launch_attn(at, n_work * cfg.n_kv_heads, cfg.head_dim, c->bf16, st, ps.timing()));
+      HIP_OK(launch_attn(at, plan.chunks * cfg.n_kv_heads, cfg.head_dim, c->bf16, st, ps.timing()));
     }
-    if (n_work > c->S) {  // some sequence has more than one split
+    if (plan.max_parts > 1) {  // some sequence spans more than one chunk
       ProfScope ps(c, PCED_PROF_COMBINE, 0, 0);
-      HIP_OK(launch_attn_combine(at, cfg.head_dim, max_splits, c->bf16, st, ps.timing()));
+      HIP_OK(launch_attn_combine(at, cfg.head_dim, plan.max_parts, c->bf16, st, ps.timing()));
     }
   }
 
@@ -560,7 +590,6 @@ pced_status pced_load_caches(pced_ctx* c, int32_t n_queries, const int32_t* n_ex
   HIP_OK(hipMemcpyAsync(c->ws, c->staging.data(), L.meta_end, hipMemcpyHostToDevice, st));
 
   // per-batch device state
-  HIP_OK(launch_fill_i32(c->at<int32_t>(L.tick_attn), 0, (size_t)cfg.max_seqs * cfg.n_kv_heads, st));
   HIP_OK(launch_fill_i32(c->at<int32_t>(L.tick_fuse), 0, cfg.max_queries, st));
   HIP_OK(launch_fill_i32(c->at<int32_t>(L.tick_beta), 0, cfg.max_seqs, st));
   HIP_OK(launch_fill_i32(c->at<int32_t>(L.prev_tok), -1, cfg.max_queries, st));

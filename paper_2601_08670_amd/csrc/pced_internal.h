@@ -12,7 +12,9 @@ constexpr int kMaxGroup = 16;      // q-heads per kv-head (MFMA N edge)
 constexpr int kFuseBlock = 256;    // vocab entries per fuse work-group
 constexpr int kBetaChunk = 4096;   // vocab entries per beta work-group
 constexpr int kLmRowsPad = 48;     // hidden-state rows are padded to a multiple of this
-constexpr int kMaxSplitPages = 64; // pages per attention split (one page id per lane)
+constexpr int kMaxSplitPages = 64; // pages per attention chunk (one page id per lane)
+constexpr int kMaxSeg = 8;         // sequences one attention chunk may span
+constexpr int kStageUnits = 4;     // 16-byte q units per lane staged in LDS for a chunk's later sequences
 
 // Per-step attention launch arguments (one launch per layer).
 struct AttnArgs {
@@ -21,16 +23,24 @@ struct AttnArgs {
   const void* vpool;
   const int32_t* len0;      // [S] lengths at load
   const int32_t* page_table;// [S][maxpps]
-  const int32_t* work_off;  // [S+1] prefix of splits per sequence (this step)
-  const int4* work_list;    // [work] (sequence, first token, end token, splits of the sequence)
-  const int32_t* work_pages;// [work][kMaxSplitPages] physical pages of each work item
-  float* part_acc;          // [S*Hkv][split_stride][G][D] partial outputs of split work items
+  // Balanced plan of the step (written by the planning blocks of the append
+  // launch): the pages of all sequences, concatenated in sequence order, are cut
+  // into C chunks of equal size (+-1 page); one wave per (chunk, kv-head). A
+  // chunk meets up to kMaxSeg sequences ("segments"); each segment yields one
+  // partial state of its sequence, or the final output when the sequence lies
+  // in a single chunk.
+  const int2* chunk_info;   // [C] (segments, pages) of each chunk
+  const int4* seg;          // [C][kMaxSeg][2]: {s, first page in chunk, page offset in s - first page,
+                            //  token end}, {partial index in s, partials of s, 0, 0}
+  const int32_t* nparts;    // [S] partial states of each sequence (chunks it meets)
+  const int32_t* work_pages;// [C][kMaxSplitPages] physical pages of each chunk
+  float* part_acc;          // [S*Hkv][split_stride][G][D] partial outputs
   float* part_ml;           // [S*Hkv][split_stride][G][2] (running max in log2 units, sum)
   void* x_out;              // [S][Hq*D] layer output, storage type
   float* attn_out;          // optional [S][L][Hq][D]
   float* hidden_out;        // optional [S][Hq*D] (last layer only)
   int n_seqs, n_layers, layer, n_q_heads, n_kv_heads, group;
-  int max_pages, maxpps, t, split_tokens, split_stride, is_last_layer;
+  int max_pages, maxpps, t, split_stride, is_last_layer;
   float scale_log2;         // log2(e) / sqrt(D)
 };
 
@@ -41,10 +51,12 @@ struct AppendArgs {
   void* vpool;
   const int32_t* len0;
   const int32_t* page_table;
-  int32_t* work_off;        // [S+1] written by the planning block
-  int4* work_list;          // [work] written by the planning blocks
-  int32_t* work_pages;      // [work][kMaxSplitPages] written by the planning blocks
-  int n_seqs, n_layers, n_kv_heads, head_dim, max_pages, maxpps, t, split_tokens;
+  int2* chunk_info;         // plan outputs, see AttnArgs
+  int4* seg;
+  int32_t* nparts;
+  int32_t* work_pages;
+  int n_seqs, n_layers, n_kv_heads, head_dim, max_pages, maxpps, t;
+  int n_chunks, total_pages;  // C and P of the balanced plan (P = pages after the append)
 };
 
 struct LoadArgs {

@@ -96,38 +96,72 @@ __global__ __launch_bounds__(256) void k_load(LoadArgs a) {
 
 // --------------------------------------------- shared-history append + plan
 
+// Balanced attention plan. The pages of all sequences (after this step's
+// append), concatenated in sequence order, are cut into C chunks: chunk c holds
+// global pages [chunk_lo(c), chunk_lo(c + 1)) with chunk_lo(c) = floor(c P / C),
+// so chunk sizes differ by at most one page and every wave of the attention
+// launch streams the same amount of cache.
+__device__ __forceinline__ long chunk_lo(long c, long P, long C) { return c * P / C; }
+// the chunk holding global page u: the largest c with chunk_lo(c) <= u
+__device__ __forceinline__ int chunk_of(long u, long P, long C) { return (int)(((u + 1) * C - 1) / P); }
+
 // Blocks 0 .. S*L-1: write step t's K/V row of (sequence, layer) into slot
 // len0 + t of the sequence's pages (Section 3: the chosen token joins every
-// expert's history). Blocks S*L + s plan sequence s for this step's length
-// len0 + t + 1: its splits' descriptors and physical page ids, which every
-// layer's attention launch of the step reads.
+// expert's history). Block S*L + s plans sequence s for this step's length
+// len0 + t + 1: the chunks it meets, its segment descriptor in each (the
+// sequence's position among the chunk's segments comes from walking back over
+// the sequences that reach into the chunk), and the physical id of each of its
+// pages at the page's place in its chunk.
 template <bool BF16>
 __global__ __launch_bounds__(128) void k_append(AppendArgs a) {
   const int S = a.n_seqs, L = a.n_layers;
   if ((int)blockIdx.x >= S * L) {
     const int s = blockIdx.x - S * L;
-    const int st = a.split_tokens, sp = st / kPage;
-    // offset of this sequence's first split: sum over earlier sequences
+    const long P = a.total_pages, C = a.n_chunks;
+    auto pages_of = [&](int r) { return (a.len0[r] + a.t + 1 + kPage - 1) / kPage; };
+    // first global page of this sequence: sum over earlier sequences
     __shared__ int red[2];
+    __shared__ int k_first;
     int part = 0;
-    for (int r = threadIdx.x; r < s; r += blockDim.x) part += (a.len0[r] + a.t + 1 + st - 1) / st;
+    for (int r = threadIdx.x; r < s; r += blockDim.x) part += pages_of(r);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) part += __shfl_xor(part, o);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = part;
-    __syncthreads();
-    const int off = red[0] + red[1];
     const int len = a.len0[s] + a.t + 1;
-    const int n = (len + st - 1) / st;
-    const int npages = (len + kPage - 1) / kPage;
+    const int ps = (len + kPage - 1) / kPage;
+    __syncthreads();
+    const long pre = red[0] + red[1];
+    const int c0 = chunk_of(pre, P, C), c1 = chunk_of(pre + ps - 1, P, C);
     if (threadIdx.x == 0) {
-      a.work_off[s] = off;
-      if (s == S - 1) a.work_off[S] = off + n;
+      a.nparts[s] = c1 - c0 + 1;
+      // segments of chunk c0 before this one: earlier sequences ending after its start
+      const long b0 = chunk_lo(c0, P, C);
+      long end = pre;
+      int k = 0;
+      for (int r = s - 1; r >= 0 && end > b0 && k < kMaxSeg; --r) {
+        ++k;
+        end -= pages_of(r);
+      }
+      k_first = k;
     }
-    for (int j = threadIdx.x; j < n; j += blockDim.x)
-      a.work_list[off + j] = make_int4(s, j * st, min(len, (j + 1) * st), n);
+    __syncthreads();
+    for (int c = c0 + (int)threadIdx.x; c <= c1; c += blockDim.x) {
+      const long lo_c = chunk_lo(c, P, C), hi_c = chunk_lo(c + 1, P, C);
+      const long lo = max(pre, lo_c), hi = min(pre + ps, hi_c);
+      const int k = c == c0 ? k_first : 0;
+      const int i0 = (int)(lo - lo_c), pa = (int)(lo - pre);
+      if (k < kMaxSeg) {
+        a.seg[((size_t)c * kMaxSeg + k) * 2] = make_int4(s, i0, pa - i0, min(len, (int)(hi - pre) * kPage));
+        a.seg[((size_t)c * kMaxSeg + k) * 2 + 1] = make_int4(c - c0, c1 - c0 + 1, 0, 0);
+      }
+      if (hi == hi_c) a.chunk_info[c] = make_int2(k + 1, (int)(hi_c - lo_c));  // last segment of chunk c
+    }
     const int32_t* pt = a.page_table + (size_t)s * a.maxpps;
-    for (int p = threadIdx.x; p < npages; p += blockDim.x)
-      a.work_pages[(size_t)(off + p / sp) * kMaxSplitPages + p % sp] = pt[p];
+    for (int p = threadIdx.x; p < ps; p += blockDim.x) {
+      const long u = pre + p;
+      const int c = chunk_of(u, P, C);
+      a.work_pages[(size_t)c * kMaxSplitPages + (u - chunk_lo(c, P, C))] = pt[p];
+    }
     return;
   }
   const int s = blockIdx.x / L, l = blockIdx.x % L;
@@ -152,22 +186,6 @@ __global__ __launch_bounds__(128) void k_append(AppendArgs a) {
 }
 
 // ----------------------------------------------------------- decode attention
-
-struct WorkItem {
-  int s, g, split, nsplit, tok_begin, tok_end;
-};
-
-__device__ __forceinline__ WorkItem decode_work(const AttnArgs& a, int w) {
-  WorkItem it;
-  it.g = w % a.n_kv_heads;
-  const int4 e = a.work_list[w / a.n_kv_heads];
-  it.s = e.x;
-  it.tok_begin = e.y;
-  it.tok_end = e.z;
-  it.nsplit = e.w;
-  it.split = e.y / a.split_tokens;
-  return it;
-}
 
 // Write 4 consecutive output dims of one q-head: fp32 debug copy, the layer
 // output in the storage type, and (last layer) the fp32 value of the stored x.
@@ -209,7 +227,7 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a, int D) {
   // split count: the first J are read at once (clamped inside the slot range)
   // together with the sequence length
   const size_t w0 = (size_t)blockIdx.x * stride;
-  const int nsplit = (a.len0[s] + a.t + 1 + a.split_tokens - 1) / a.split_tokens;
+  const int nsplit = a.nparts[s];
   for (int idx = threadIdx.x; idx < G * D / 4; idx += blockDim.x) {
     const int h = (idx * 4) / D, d = (idx * 4) % D;
     float m_run = kNegInf, den = 0.f;
@@ -246,42 +264,58 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a, int D) {
   }
 }
 
-// Split-K flash decoding for bf16 caches, one wave per (sequence, kv-head,
-// split). The G q-heads of the kv-head ride in the N dimension of the matrix
+// Flash decoding for bf16 caches over the balanced plan, one wave per (chunk,
+// kv-head). The G q-heads of the kv-head ride in the N dimension of the matrix
 // cores, so every K/V byte is read once for all of them:
 //   S^T[16 tok x 16 heads] = K[16 x D] Q^T          (D/32 x 16x16x32 MFMA)
 //   O^T[D x 16 heads]     += V^T[D x 16 tok] P^T    (D/16 x 16x16x16 MFMA)
 // P comes straight out of the S^T accumulator layout (lane l: head l%16,
 // tokens 4*(l/16)..+3), which is the B operand layout of the second product.
 // Online softmax in base 2 with log2(e)/sqrt(D) folded into the score scale.
+// A chunk may span several sequences. At each segment switch the wave stores
+// the finished segment (the final output when the sequence lies in this chunk
+// alone, else a partial state for the merge kernel) and continues with the next
+// sequence's q, staged in LDS by the prologue, and a fresh softmax state; the
+// page stream itself does not stop at a switch.
 template <int D>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_attn_bf16(AttnArgs a) {
   constexpr int NC = D / 32;
   constexpr int NJ = D / 16;
+  // q rows of the chunk's later segments, [segment - 1][G][D]
+  __shared__ __align__(16) uint16_t q_lds[kStageUnits * 64 * 8];
+  // finished segments' softmax states, [segment][G][D] accumulators and
+  // [segment][G] (m, l): (segments - 1) G D <= 8 kStageUnits * 64 by the plan
+  __shared__ __align__(16) float st_acc[kStageUnits * 64 * 8];
+  __shared__ float st_ml[kMaxSeg * kMaxGroup * 2];
   const int lane = threadIdx.x;
   const int col = lane & 15, quad = lane >> 4;
   const int G = a.group, Hkv = a.n_kv_heads;
-  const WorkItem it = decode_work(a, blockIdx.x);
-  const int pg0 = it.tok_begin / kPage;
-  const int np = (it.tok_end + kPage - 1) / kPage - pg0;  // 1 .. kMaxSplitPages
-  // the split's physical page ids, one per lane (written by the planner),
-  // read back with readlane
-  const int my_pid = a.work_pages[(size_t)(blockIdx.x / Hkv) * kMaxSplitPages + lane];
+  const int c = blockIdx.x / Hkv, g = blockIdx.x % Hkv;
+  const int2 ci = a.chunk_info[c];
+  const int nseg = ci.x, np = ci.y;  // 1 .. kMaxSeg segments, 1 .. kMaxSplitPages pages
+  // the chunk's physical page ids and segment descriptors, lane k holding entry
+  // k (read back with readlane; entries past the chunk's counts are never used)
+  const int my_pid = a.work_pages[(size_t)c * kMaxSplitPages + lane];
+  const int4* sd = a.seg + (size_t)c * kMaxSeg * 2;
+  const int4 d0 = sd[2 * min(lane, kMaxSeg - 1)];
+  const int4 d1 = sd[2 * min(lane, kMaxSeg - 1) + 1];
+  const int4 e0 = sd[0], e1 = sd[1];  // segment 0, uniform loads
+  int cur_s = e0.x, cur_poff = e0.z, cur_end = e0.w, cur_j = e1.x, cur_parts = e1.y;
 
+  const size_t q_layer = (size_t)a.layer * a.n_q_heads + (size_t)g * G;
   bf16x8 qop[NC];
   {
+    // Columns past the group repeat its last head: their scores and outputs are
+    // never stored, and the loads stay unconditional, so waiting for the page
+    // ids below does not also wait for these.
     const uint16_t* q = (const uint16_t*)a.q +
-        (((size_t)it.s * a.n_layers + a.layer) * a.n_q_heads + (size_t)it.g * G + col) * D;
+        ((size_t)cur_s * a.n_layers * a.n_q_heads + q_layer + min(col, G - 1)) * D;
 #pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      uint4 v = make_uint4(0u, 0u, 0u, 0u);
-      if (col < G) v = *(const uint4*)(q + 32 * i + 8 * quad);
-      qop[i] = as_bf16x8(v);
-    }
+    for (int i = 0; i < NC; ++i) qop[i] = as_bf16x8(*(const uint4*)(q + 32 * i + 8 * quad));
   }
   const uint4* kp = (const uint4*)a.kpool;
   const uint4* vp = (const uint4*)a.vpool;
-  const size_t lay = (size_t)a.layer * a.max_pages * Hkv + it.g;
+  const size_t lay = (size_t)a.layer * a.max_pages * Hkv + g;
   constexpr size_t tile16 = (size_t)kPage * D / 8;  // tile size in 16-byte units
 
   // Loads are issued unconditionally (past the end: the last page again, an L2
@@ -290,9 +324,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
     const int phys = __builtin_amdgcn_readlane(my_pid, min(i, np - 1));
     const size_t t0 = (lay + (size_t)phys * Hkv) * tile16;
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      kb[c] = kp[t0 + c * 64 + lane];
-      vb[c] = vp[t0 + c * 64 + lane];
+    for (int cc = 0; cc < NC; ++cc) {
+      kb[cc] = kp[t0 + cc * 64 + lane];
+      vb[cc] = vp[t0 + cc * 64 + lane];
     }
   };
 
@@ -304,16 +338,88 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
   // only move when some score of the page exceeds m_ref + 8, so weights stay
   // <= 2^8 and the common page needs neither cross-lane traffic nor a rescale.
   float m_ref = kNegInf, l_part = 0.f;
+  int k = 0;
+  int next_i0 = nseg > 1 ? sd[2].y : 0x7fffffff;
 
-  auto process = [&](int i, uint4 (&kc)[NC], uint4 (&vc)[NC]) {
+  // Write a finished segment, whose state is in LDS slot `slot`: the final
+  // output when its sequence lies in this chunk alone, else its partial state
+  // for the merge kernel, copied by all 64 lanes as whole contiguous lines
+  // (the slot has the partial's [G][D] layout).
+  auto emit = [&](int slot, int s, int part, int parts) __attribute__((always_inline)) {
+    const float* sa = st_acc + slot * G * D;
+    const float* sm = st_ml + slot * G * 2;
+    if (parts == 1) {
+      if (col >= G) return;
+      const float inv = 1.0f / sm[2 * col + 1];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const float4 v = *(const float4*)(sa + col * D + 16 * j + 4 * quad);
+        write_o4<true>(a, s, g * G + col, 16 * j + 4 * quad, D, make_float4(v.x * inv, v.y * inv, v.z * inv, v.w * inv));
+      }
+      return;
+    }
+    const size_t w = (size_t)(s * Hkv + g) * a.split_stride + part;
+    float* dst = a.part_acc + w * G * D;
+    for (int e = 4 * lane; e < G * D; e += 256) *(float4*)(dst + e) = *(const float4*)(sa + e);
+    if (lane < 2 * G) a.part_ml[w * G * 2 + lane] = sm[lane];
+  };
+  auto reg_acc4 = [&](int j) __attribute__((always_inline)) {
+    return make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+  };
+  auto l_total = [&]() __attribute__((always_inline)) {
+    float l_tot = l_part + __shfl_xor(l_part, 16);
+    return l_tot + __shfl_xor(l_tot, 32);
+  };
+  // At a segment switch the finished state goes to LDS, not to memory: a store
+  // inside the page loop would make every later wait of that iteration drain the
+  // whole ring (stores and loads share the wave's memory counter). The states are
+  // written out after the loop.
+  auto save = [&](int slot) __attribute__((always_inline)) {
+    const float l_tot = l_total();
+    if (col < G) {
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        *(float4*)(st_acc + (slot * G + col) * D + 16 * j + 4 * quad) = reg_acc4(j);
+      if (quad == 0) {
+        st_ml[(slot * G + col) * 2] = m_ref;
+        st_ml[(slot * G + col) * 2 + 1] = l_tot;
+      }
+    }
+  };
+
+  uint4 stg0, stg1, stg2, stg3;  // staged q units of later segments (filled after the ring starts)
+  auto process = [&](int i, uint4 (&kc)[NC], uint4 (&vc)[NC]) __attribute__((always_inline)) {
+    if (i == next_i0) {  // first page of the next segment
+      save(k);
+      if (k == 0) {  // units past the count land in unused LDS
+        *(uint4*)(q_lds + 8 * lane) = stg0;
+        *(uint4*)(q_lds + 8 * (lane + 64)) = stg1;
+        *(uint4*)(q_lds + 8 * (lane + 128)) = stg2;
+        *(uint4*)(q_lds + 8 * (lane + 192)) = stg3;
+      }
+      ++k;
+      cur_s = __builtin_amdgcn_readlane(d0.x, k);
+      cur_poff = __builtin_amdgcn_readlane(d0.z, k);
+      cur_end = __builtin_amdgcn_readlane(d0.w, k);
+      cur_j = __builtin_amdgcn_readlane(d1.x, k);
+      cur_parts = __builtin_amdgcn_readlane(d1.y, k);
+      next_i0 = k + 1 < nseg ? __builtin_amdgcn_readlane(d0.y, k + 1) : 0x7fffffff;
+      const uint16_t* qs = q_lds + ((k - 1) * G + min(col, G - 1)) * D + 8 * quad;
+#pragma unroll
+      for (int cc = 0; cc < NC; ++cc) qop[cc] = as_bf16x8(*(const uint4*)(qs + 32 * cc));
+      m_ref = kNegInf;
+      l_part = 0.f;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
     f32x4 sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
-      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kc[c]), qop[c], sc, 0, 0, 0);
-    const int tb = (pg0 + i) * kPage + 4 * quad;
+    for (int cc = 0; cc < NC; ++cc)
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kc[cc]), qop[cc], sc, 0, 0, 0);
+    const int tb = (i + cur_poff) * kPage + 4 * quad;  // token of element r = 0 in the sequence
     float z[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) z[r] = (tb + r < it.tok_end) ? sc[r] * a.scale_log2 : kNegInf;
+    for (int r = 0; r < 4; ++r) z[r] = (tb + r < cur_end) ? sc[r] * a.scale_log2 : kNegInf;
     const float zmax = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
     if (__builtin_amdgcn_ballot_w64(zmax > m_ref + 8.0f) != 0) {
       float mx = fmaxf(zmax, __shfl_xor(zmax, 16));
@@ -335,68 +441,80 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
     l_part += psum;
     s16x4 pop;
     pop[0] = (short)pb[0]; pop[1] = (short)pb[1]; pop[2] = (short)pb[2]; pop[3] = (short)pb[3];
-    if ((pg0 + i) * kPage + kPage > it.tok_end) {
-      // Partial last page: slots past the sequence end hold stale or never-written
-      // bits. Their weights are 0, but 0 * NaN is NaN inside the matrix core, so
-      // clear the V elements of those tokens (lane elements r = 0..3 are the same
-      // tokens tb + r as its weights).
-      const uint32_t m01 = (tb + 0 < it.tok_end ? 0x0000FFFFu : 0u) | (tb + 1 < it.tok_end ? 0xFFFF0000u : 0u);
-      const uint32_t m23 = (tb + 2 < it.tok_end ? 0x0000FFFFu : 0u) | (tb + 3 < it.tok_end ? 0xFFFF0000u : 0u);
+    if ((i + cur_poff) * kPage + kPage > cur_end) {
+      // Partial last page: slots past the segment's end hold stale or never-written
+      // bits (or the next chunk's tokens). Their weights are 0, but 0 * NaN is NaN
+      // inside the matrix core, so clear the V elements of those tokens (lane
+      // elements r = 0..3 are the same tokens tb + r as its weights).
+      const uint32_t m01 = (tb + 0 < cur_end ? 0x0000FFFFu : 0u) | (tb + 1 < cur_end ? 0xFFFF0000u : 0u);
+      const uint32_t m23 = (tb + 2 < cur_end ? 0x0000FFFFu : 0u) | (tb + 3 < cur_end ? 0xFFFF0000u : 0u);
 #pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        vc[c].x &= m01; vc[c].y &= m23; vc[c].z &= m01; vc[c].w &= m23;
+      for (int cc = 0; cc < NC; ++cc) {
+        vc[cc].x &= m01; vc[cc].y &= m23; vc[cc].z &= m01; vc[cc].w &= m23;
       }
     }
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      const s16x4 va = __builtin_bit_cast(s16x4, make_uint2(vc[c].x, vc[c].y));
-      const s16x4 vb = __builtin_bit_cast(s16x4, make_uint2(vc[c].z, vc[c].w));
-      acc[2 * c] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pop, acc[2 * c], 0, 0, 0);
-      acc[2 * c + 1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vb, pop, acc[2 * c + 1], 0, 0, 0);
+    for (int cc = 0; cc < NC; ++cc) {
+      const s16x4 va = __builtin_bit_cast(s16x4, make_uint2(vc[cc].x, vc[cc].y));
+      const s16x4 vb = __builtin_bit_cast(s16x4, make_uint2(vc[cc].z, vc[cc].w));
+      acc[2 * cc] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pop, acc[2 * cc], 0, 0, 0);
+      acc[2 * cc + 1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vb, pop, acc[2 * cc + 1], 0, 0, 0);
     }
   };
 
   // four-page register ring: the refill of page i+3 (into the buffer of page
   // i-1, already consumed) is issued before page i is consumed, so three pages
-  // are always in flight
+  // are always in flight. The body is branch-free (a segment switch only touches
+  // registers, LDS and stores) so that every iteration ends with the same loads
+  // outstanding and the compiler's wait counts stay partial across the back
+  // edge: pages past the chunk's end are the last page again and contribute
+  // nothing (all their tokens are masked).
   uint4 kA[NC], vA[NC], kB[NC], vB[NC], kC[NC], vC[NC], kD[NC], vD[NC];
+  // the prologue keeps its A, B, C issue order (the scheduler would otherwise
+  // reverse it, and the wait at the loop head then has to drain every load)
   load_page(0, kA, vA);
+  __builtin_amdgcn_sched_barrier(0);
   load_page(1, kB, vB);
+  __builtin_amdgcn_sched_barrier(0);
   load_page(2, kC, vC);
+  __builtin_amdgcn_sched_barrier(0);
+  // Later segments' q rows: 16-byte units u = ((k - 1) G + h) D/8 + d/8, spread
+  // over lanes. Issued after the ring's first pages (loads complete in order, so
+  // page 0 does not wait for them) and stored to LDS at the first switch.
+  const int per_seg = G * (D / 8);
+  const int n_units = (nseg - 1) * per_seg;
+  // (unconditional loads: a unit past the count re-reads segment 0's first row)
+  static_assert(kStageUnits == 4, "staging registers below");
+  auto stage = [&](int r) __attribute__((always_inline)) {
+    const int u = lane + 64 * r;
+    const bool valid = u < n_units;
+    const int kk = min(1 + u / per_seg, kMaxSeg - 1), rem = valid ? u % per_seg : 0;
+    const int sk = valid ? __shfl(d0.x, kk) : e0.x;
+    return *(const uint4*)((const uint16_t*)a.q +
+                           ((size_t)sk * a.n_layers * a.n_q_heads + q_layer + rem / (D / 8)) * D +
+                           8 * (rem % (D / 8)));
+  };
+  stg0 = stage(0);
+  stg1 = stage(1);
+  stg2 = stage(2);
+  stg3 = stage(3);
   for (int i = 0; i < np; i += 4) {
     load_page(i + 3, kD, vD);
     process(i, kA, vA);
     load_page(i + 4, kA, vA);
-    if (i + 1 < np) process(i + 1, kB, vB);
+    process(i + 1, kB, vB);
     load_page(i + 5, kB, vB);
-    if (i + 2 < np) process(i + 2, kC, vC);
+    process(i + 2, kC, vC);
     load_page(i + 6, kC, vC);
-    if (i + 3 < np) process(i + 3, kD, vD);
+    process(i + 3, kD, vD);
   }
-  float l_tot = l_part + __shfl_xor(l_part, 16);
-  l_tot += __shfl_xor(l_tot, 32);
-
-  if (it.nsplit == 1) {
-    if (col < G) {
-      const float inv = 1.0f / l_tot;
-#pragma unroll
-      for (int j = 0; j < NJ; ++j)
-        write_o4<true>(a, it.s, it.g * G + col, 16 * j + 4 * quad, D,
-                       make_float4(acc[j][0] * inv, acc[j][1] * inv, acc[j][2] * inv, acc[j][3] * inv));
-    }
-    return;
-  }
-  const size_t w = (size_t)(it.s * Hkv + it.g) * a.split_stride + it.split;
-  if (col < G) {
-#pragma unroll
-    for (int j = 0; j < NJ; ++j)
-      *(float4*)(a.part_acc + (w * G + col) * D + 16 * j + 4 * quad) =
-          make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
-    if (quad == 0) {
-      a.part_ml[(w * G + col) * 2] = m_ref;
-      a.part_ml[(w * G + col) * 2 + 1] = l_tot;
-    }
-  }
+  // the saved segments, then the last one through slot 0 (LDS accesses of one
+  // wave stay in order, so slot 0 is read out before it is overwritten)
+  for (int kk = 0; kk < k; ++kk)
+    emit(kk, __builtin_amdgcn_readlane(d0.x, kk), __builtin_amdgcn_readlane(d1.x, kk),
+         __builtin_amdgcn_readlane(d1.y, kk));
+  save(0);
+  emit(0, cur_s, cur_j, cur_parts);
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -405,71 +523,76 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// fp32 caches (small/validation shapes): one wave per work item, lanes over
-// head dims (D <= 128), one token at a time, per-head online softmax in base 2.
+// fp32 caches (small/validation shapes): one wave per (chunk, kv-head) of the
+// balanced plan, lanes over head dims (D <= 128), one token at a time, per-head
+// online softmax in base 2; the chunk's segments one after another.
 __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a, int D) {
   const int lane = threadIdx.x;
   const int G = a.group, Hkv = a.n_kv_heads;
-  const WorkItem it = decode_work(a, blockIdx.x);
-  const float* q = (const float*)a.q +
-      (((size_t)it.s * a.n_layers + a.layer) * a.n_q_heads + (size_t)it.g * G) * D;
+  const int c = blockIdx.x / Hkv, g = blockIdx.x % Hkv;
+  const int nseg = a.chunk_info[c].x;
   const bool has0 = lane < D, has1 = lane + 64 < D;
-  float qv[kMaxGroup][2], m[kMaxGroup], l[kMaxGroup], acc[kMaxGroup][2];
-#pragma unroll
-  for (int h = 0; h < kMaxGroup; ++h) {
-    qv[h][0] = (h < G && has0) ? q[h * D + lane] : 0.f;
-    qv[h][1] = (h < G && has1) ? q[h * D + lane + 64] : 0.f;
-    m[h] = kNegInf; l[h] = 0.f; acc[h][0] = 0.f; acc[h][1] = 0.f;
-  }
   const size_t tile = (size_t)kPage * D;
   const float* kp = (const float*)a.kpool;
   const float* vp = (const float*)a.vpool;
-  const size_t lay = (size_t)a.layer * a.max_pages * Hkv + it.g;
-  const int32_t* pt = a.page_table + (size_t)it.s * a.maxpps;
-  for (int tok = it.tok_begin; tok < it.tok_end; ++tok) {
-    const size_t base = (lay + (size_t)pt[tok / kPage] * Hkv) * tile + (size_t)(tok % kPage) * D;
-    const float k0 = has0 ? kp[base + lane] : 0.f, k1 = has1 ? kp[base + lane + 64] : 0.f;
-    const float v0 = has0 ? vp[base + lane] : 0.f, v1 = has1 ? vp[base + lane + 64] : 0.f;
+  const size_t lay = (size_t)a.layer * a.max_pages * Hkv + g;
+  for (int k = 0; k < nseg; ++k) {
+    const int4 d0 = a.seg[((size_t)c * kMaxSeg + k) * 2], d1 = a.seg[((size_t)c * kMaxSeg + k) * 2 + 1];
+    const int s = d0.x, tok_end = d0.w;
+    const float* q = (const float*)a.q + (((size_t)s * a.n_layers + a.layer) * a.n_q_heads + (size_t)g * G) * D;
+    float qv[kMaxGroup][2], m[kMaxGroup], l[kMaxGroup], acc[kMaxGroup][2];
 #pragma unroll
     for (int h = 0; h < kMaxGroup; ++h) {
-      if (h >= G) break;
-      const float z = wave_sum(qv[h][0] * k0 + qv[h][1] * k1) * a.scale_log2;
-      const float mn = fmaxf(m[h], z);
-      const float al = exp2f(m[h] - mn), pz = exp2f(z - mn);
-      l[h] = l[h] * al + pz;
-      acc[h][0] = acc[h][0] * al + pz * v0;
-      acc[h][1] = acc[h][1] * al + pz * v1;
-      m[h] = mn;
+      qv[h][0] = (h < G && has0) ? q[h * D + lane] : 0.f;
+      qv[h][1] = (h < G && has1) ? q[h * D + lane + 64] : 0.f;
+      m[h] = kNegInf; l[h] = 0.f; acc[h][0] = 0.f; acc[h][1] = 0.f;
     }
-  }
-  if (it.nsplit == 1) {
+    const int32_t* pt = a.page_table + (size_t)s * a.maxpps;
+    for (int tok = (d0.y + d0.z) * kPage; tok < tok_end; ++tok) {
+      const size_t base = (lay + (size_t)pt[tok / kPage] * Hkv) * tile + (size_t)(tok % kPage) * D;
+      const float k0 = has0 ? kp[base + lane] : 0.f, k1 = has1 ? kp[base + lane + 64] : 0.f;
+      const float v0 = has0 ? vp[base + lane] : 0.f, v1 = has1 ? vp[base + lane + 64] : 0.f;
 #pragma unroll
-    for (int h = 0; h < kMaxGroup; ++h) {
-      if (h >= G) break;
-      const float inv = 1.0f / l[h];
-      const int head = it.g * G + h;
-      const size_t xo = (size_t)it.s * a.n_q_heads * D + (size_t)head * D;
-      const size_t ao = (((size_t)it.s * a.n_layers + a.layer) * a.n_q_heads + head) * D;
-      for (int c = 0; c < 2; ++c) {
-        const int d = lane + 64 * c;
-        if (d >= D) break;
-        const float o = acc[h][c] * inv;
-        ((float*)a.x_out)[xo + d] = o;
-        if (a.attn_out) a.attn_out[ao + d] = o;
-        if (a.is_last_layer && a.hidden_out) a.hidden_out[xo + d] = o;
+      for (int h = 0; h < kMaxGroup; ++h) {
+        if (h >= G) break;
+        const float z = wave_sum(qv[h][0] * k0 + qv[h][1] * k1) * a.scale_log2;
+        const float mn = fmaxf(m[h], z);
+        const float al = exp2f(m[h] - mn), pz = exp2f(z - mn);
+        l[h] = l[h] * al + pz;
+        acc[h][0] = acc[h][0] * al + pz * v0;
+        acc[h][1] = acc[h][1] * al + pz * v1;
+        m[h] = mn;
       }
     }
-    return;
-  }
-  const size_t w = (size_t)(it.s * Hkv + it.g) * a.split_stride + it.split;
+    if (d1.y == 1) {  // the sequence lies in this chunk alone: final output
 #pragma unroll
-  for (int h = 0; h < kMaxGroup; ++h) {
-    if (h >= G) break;
-    if (has0) a.part_acc[(w * G + h) * D + lane] = acc[h][0];
-    if (has1) a.part_acc[(w * G + h) * D + lane + 64] = acc[h][1];
-    if (lane == 0) {
-      a.part_ml[(w * G + h) * 2] = m[h];
-      a.part_ml[(w * G + h) * 2 + 1] = l[h];
+      for (int h = 0; h < kMaxGroup; ++h) {
+        if (h >= G) break;
+        const float inv = 1.0f / l[h];
+        const int head = g * G + h;
+        const size_t xo = (size_t)s * a.n_q_heads * D + (size_t)head * D;
+        const size_t ao = (((size_t)s * a.n_layers + a.layer) * a.n_q_heads + head) * D;
+        for (int cc = 0; cc < 2; ++cc) {
+          const int d = lane + 64 * cc;
+          if (d >= D) break;
+          const float o = acc[h][cc] * inv;
+          ((float*)a.x_out)[xo + d] = o;
+          if (a.attn_out) a.attn_out[ao + d] = o;
+          if (a.is_last_layer && a.hidden_out) a.hidden_out[xo + d] = o;
+        }
+      }
+      continue;
+    }
+    const size_t w = (size_t)(s * Hkv + g) * a.split_stride + d1.x;
+#pragma unroll
+    for (int h = 0; h < kMaxGroup; ++h) {
+      if (h >= G) break;
+      if (has0) a.part_acc[(w * G + h) * D + lane] = acc[h][0];
+      if (has1) a.part_acc[(w * G + h) * D + lane + 64] = acc[h][1];
+      if (lane == 0) {
+        a.part_ml[(w * G + h) * 2] = m[h];
+        a.part_ml[(w * G + h) * 2 + 1] = l[h];
+      }
     }
   }
 }

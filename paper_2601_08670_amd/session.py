@@ -21,7 +21,8 @@ class PcedSession:
     """A context plus its two KV pools for one model geometry and capacity."""
 
     def __init__(self, *, n_layers, n_q_heads, n_kv_heads, head_dim, vocab, dtype, max_queries,
-                 max_seqs, max_pages, max_pages_per_seq, norm="rms", device="cuda", poison=False):
+                 max_seqs, max_pages, max_pages_per_seq, norm="rms", device="cuda", poison=False,
+                 max_attn_chunks=0):
         torch = _torch()
         self.dtype = dtype
         self.device = device
@@ -30,7 +31,8 @@ class PcedSession:
         self.cfg = _lib.make_config(n_layers=n_layers, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads,
                                     head_dim=head_dim, vocab=vocab, dtype=dtype, max_queries=max_queries,
                                     max_seqs=max_seqs, max_pages=max_pages,
-                                    max_pages_per_seq=max_pages_per_seq, norm=norm)
+                                    max_pages_per_seq=max_pages_per_seq, norm=norm,
+                                    max_attn_chunks=max_attn_chunks)
         self.ctx = _lib.Context(self.cfg, device=device)
         pool = _lib.pced_pool_bytes(self.cfg)
         self.k_pool = torch.empty(pool, dtype=torch.uint8, device=device)
@@ -100,7 +102,7 @@ class PcedSession:
 
 
 def session_for_workload(wl, device="cuda", extra_tokens: Optional[int] = None, norm="rms",
-                         load_now=True, max_queries=None, poison=False):
+                         load_now=True, max_queries=None, poison=False, max_attn_chunks=0):
     """Build a session sized for a synthetic workload (duck-typed: any object with
     the attributes of ``pced_inputs.workloads.Workload``) and load its caches,
     materialised on ``device``."""
@@ -112,7 +114,7 @@ def session_for_workload(wl, device="cuda", extra_tokens: Optional[int] = None, 
                        head_dim=g.head_dim, vocab=g.vocab, dtype=g.dtype,
                        max_queries=max_queries or wl.n_queries, max_seqs=wl.n_seqs,
                        max_pages=int(need.sum()), max_pages_per_seq=maxpps, norm=norm, device=device,
-                       poison=poison)
+                       poison=poison, max_attn_chunks=max_attn_chunks)
     sess.workload_page_table = wl.page_table(extra, maxpps)
     if load_now:
         load_workload(sess, wl)

@@ -48,7 +48,7 @@ def test_sizes():
 @pytest.mark.parametrize("bad", [
     dict(n_layers=0), dict(n_kv_heads=3), dict(n_q_heads=64, n_kv_heads=2), dict(head_dim=96),
     dict(hidden=1000), dict(n_q_heads=2, n_kv_heads=1), dict(vocab=1), dict(max_queries=0),
-    dict(max_seqs=1), dict(max_pages=0), dict(dtype="f32", head_dim=130),
+    dict(max_seqs=1), dict(max_pages=0), dict(dtype="f32", head_dim=130), dict(max_attn_chunks=-1),
 ])
 def test_invalid_config_sizes_are_zero(bad):
     c = cfg(**bad)

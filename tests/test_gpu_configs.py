@@ -193,6 +193,26 @@ def test_edge_cases(name, geom, n_exp, lens, am, steps):
     _check_queries(wl, list(range(wl.n_queries)), steps)
 
 
+SPAN = [
+    # (name, geometry, n_experts, expert lengths, amateur length, steps, chunk cap, shuffled pages)
+    ("bf16-d64-3-chunks", W.Geometry(1, 8, 2, 64, 512, 700, "bf16"), [5, 4],
+     [1, 40, 17, 300, 16, 33, 5, 64, 130], 12, 3, 3, False),
+    ("bf16-d128-2-layers-shuffled", W.Geometry(2, 8, 2, 128, 1024, 600, "bf16"), [6],
+     [250, 9, 15, 17, 120, 48], 20, 2, 2, True),
+    ("bf16-more-segments-than-a-wave-stages", W.Geometry(1, 8, 2, 128, 1024, 600, "bf16"), [9],
+     [16, 1, 15, 17, 2, 31, 3, 16, 40], 5, 2, 1, False),
+    ("fp32-2-chunks", W.Geometry(1, 4, 2, 64, 256, 300, "f32"), [4], [3, 70, 18, 33], 10, 3, 2, True),
+]
+
+
+@pytest.mark.parametrize("name,geom,n_exp,lens,am,steps,cap,shuffle", SPAN, ids=[e[0] for e in SPAN])
+def test_chunks_spanning_sequences(name, geom, n_exp, lens, am, steps, cap, shuffle):
+    """A capped attention plan: each chunk streams the pages of several
+    sequences, switching q and softmax state at every sequence boundary."""
+    wl = W.custom(geom, n_exp, lens, am, steps, seed=11, shuffle_pages=shuffle)
+    _check_queries(wl, list(range(wl.n_queries)), steps, sess=_session(wl, max_attn_chunks=cap))
+
+
 def test_fixed_and_zero_beta():
     geom = W.Geometry(1, 8, 2, 64, 512, 900, "bf16")
     wl = W.custom(geom, [4], [30, 90, 200, 7], 10, 2, seed=8, beta=[0.0, 0.25, 1.0, 0.5])
