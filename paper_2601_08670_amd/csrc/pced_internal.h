@@ -12,6 +12,7 @@ constexpr int kMaxGroup = 16;      // q-heads per kv-head (MFMA N edge)
 constexpr int kFuseBlock = 256;    // vocab entries per fuse work-group
 constexpr int kBetaChunk = 4096;   // vocab entries per beta work-group
 constexpr int kLmRowsPad = 48;     // hidden-state rows are padded to a multiple of this
+constexpr int kLmRowsMTW = 9;      // many-row LM head: row tiles per wave (up to 32 * 9 = 288 rows at once)
 constexpr int kMaxSplitPages = 64; // pages per attention chunk (one page id per lane)
 constexpr int kMaxSeg = 8;         // sequences one attention chunk may span
 constexpr int kStageUnits = 4;     // 16-byte q units per lane staged in LDS for a chunk's later sequences
@@ -75,6 +76,7 @@ struct LmArgs {
   const void* w;            // packed bf16 tiles (see pced_pack_lm_head) or f32 [V][K]
   float* logits;            // [M][V]
   int M, V, K, rms;
+  int row_groups;           // >= 1: work-groups per vocab chunk, each taking every R-th 48-row group
 };
 
 struct FuseArgs {

@@ -647,7 +647,18 @@ template <int VT, int NT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_lmhead_bf16(LmArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, quad = lane >> 4;
-  const int vb0 = (blockIdx.x * 4 + wave) * VT;   // first 16-row vocab block of the wave
+  // Work-groups are dealt to the 8 XCDs round-robin. With R = a.row_groups > 1,
+  // the R row groups of one vocab chunk are consecutive work-groups of the same
+  // XCD, so they stream the same W tiles together and all but the first read
+  // them from that XCD's L2.
+  const int R = max(a.row_groups, 1);
+  int chunk = blockIdx.x, rg = 0;
+  if (R > 1) {
+    const int xcd = blockIdx.x % 8, i = blockIdx.x / 8;
+    chunk = xcd + 8 * (i / R);
+    rg = i % R;
+  }
+  const int vb0 = (chunk * 4 + wave) * VT;   // first 16-row vocab block of the wave
   const int nvb = (a.V + 15) / 16;
   if (vb0 >= nvb) return;
   const int K = a.K, KS = K / 64;
@@ -656,7 +667,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const uint4* wt[VT];
 #pragma unroll
   for (int vt = 0; vt < VT; ++vt) wt[vt] = Wp + (size_t)min(vb0 + vt, nvb - 1) * KS * 128 + lane;
-  for (int m0 = 0; m0 < a.M; m0 += 16 * NT) {
+  for (int m0 = rg * 16 * NT; m0 < a.M; m0 += 16 * NT * R) {
     f32x4 acc[VT][NT];
     float ss[NT];
 #pragma unroll
@@ -735,6 +746,154 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           for (int r = 0; r < 4; ++r)
             if (v + r < a.V) out[r] = cc[r] * rho;
         }
+      }
+    }
+  }
+}
+
+// LM head for many rows: W is streamed exactly once for all M <= 32 MTW rows.
+// A block of WPB waves owns WPB/2 * VTW consecutive 16-row vocab blocks; wave w takes
+// vocab blocks [VTW (w/2), +VTW) and the row tiles w%2, w%2 + 2, ... (interleaved,
+// so the two halves stay balanced for any M). The hidden dimension is walked in
+// stages of 64 KB columns. For every stage the block stages the x slice of all
+// rows in LDS (double buffered, in the lanes' B-operand order so each wave reads
+// it conflict-free), filled by all 512 threads with coalesced row pieces; each
+// wave streams its own packed W tiles straight from HBM through a 2-slot
+// register ring refilled right after each stage's products; the next x slice is
+// issued before that refill, so waiting for x never waits for W that is not
+// due, and long stages keep each W load a full stage ahead of its use. The
+// staging threads also accumulate every row's sum of squares (RMS scale).
+template <int VTW, int MTW, int KB, int WPB>
+__global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_lmhead_rows_bf16(LmArgs a) {
+  constexpr int NTH = 64 * WPB;          // threads per block
+  constexpr int MT = 2 * MTW;            // row tiles the kernel holds
+  constexpr int SUB = MT * 128;          // 16-byte x units of one 64-wide k step
+  constexpr int UNITS = SUB * KB;        // ... of one stage
+  constexpr int UPT = (UNITS + NTH - 1) / NTH;
+  constexpr int PIECES = 8 * KB;         // 16-byte pieces of a row's stage slice
+  // unit (k step sb, tile, half h, lane l) at sb*SUB + tile*128 + 64 h + l
+  __shared__ __align__(16) uint4 xs[2][UNITS];
+  __shared__ float rho_s[MT * 16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int col = lane & 15, quad = lane >> 4;
+  const int K = a.K, KS = K / (64 * KB), M = a.M;
+  const int nt = (M + 15) / 16;          // row tiles in use
+  const int n_units = nt * 16 * PIECES;  // units of the rows in use, per stage
+  const int nvb = (a.V + 15) / 16;
+  const int rh = wave & 1;
+  const int vb0 = (blockIdx.x * (WPB / 2) + (wave >> 1)) * VTW;
+  const uint4* Wp = (const uint4*)a.w;
+  const uint16_t* X = (const uint16_t*)a.x;
+  const uint4* wt[VTW];
+#pragma unroll
+  for (int vt = 0; vt < VTW; ++vt) wt[vt] = Wp + (size_t)min(vb0 + vt, nvb - 1) * (K / 64) * 128 + lane;
+
+  // staging: thread unit v = tid + NTH j is row v / PIECES, 16-byte piece v % PIECES
+  // of its stage slice (PIECES consecutive threads read one contiguous row piece);
+  // unit j of a thread is NTH / PIECES rows below unit 0
+  static_assert(NTH % (16 * PIECES) == 0, "whole tiles per staging round");
+  constexpr int ROWS_J = NTH / PIECES;
+  const int row0 = tid / PIECES, pc = tid % PIECES, sb0 = pc >> 3, c8 = pc & 7;
+  const uint16_t* xsrc = X + (size_t)row0 * K + 8 * pc;
+  const int xdst = sb0 * SUB + (row0 >> 4) * 128 + 64 * (c8 & 1) + 16 * (c8 >> 1) + (row0 & 15);
+  float ss[UPT];
+#pragma unroll
+  for (int j = 0; j < UPT; ++j) ss[j] = 0.f;
+  uint4 xr[UPT];
+  auto load_x = [&](int ks) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < UPT; ++j)
+      if (tid + NTH * j < n_units) xr[j] = *(const uint4*)(xsrc + (size_t)j * ROWS_J * K + ks * 64 * KB);
+  };
+  auto store_x = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < UPT; ++j)
+      if (tid + NTH * j < n_units) {
+        xs[buf][xdst + j * (ROWS_J / 16) * 128] = xr[j];
+        ss[j] += sumsq8(as_bf16x8(xr[j]));
+      }
+  };
+  struct WS { uint4 w[VTW][KB][2]; };
+  auto load_w = [&](WS& S, int ks) __attribute__((always_inline)) {
+    ks = min(ks, KS - 1);  // past the end: the last stage again (cache hit)
+#pragma unroll
+    for (int vt = 0; vt < VTW; ++vt)
+#pragma unroll
+      for (int sb = 0; sb < KB; ++sb) {
+        S.w[vt][sb][0] = wt[vt][(size_t)(ks * KB + sb) * 128];
+        S.w[vt][sb][1] = wt[vt][(size_t)(ks * KB + sb) * 128 + 64];
+      }
+  };
+  f32x4 acc[VTW][MTW];
+#pragma unroll
+  for (int i = 0; i < MTW; ++i)
+#pragma unroll
+    for (int vt = 0; vt < VTW; ++vt) acc[vt][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto step = [&](const WS& A, int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int sb = 0; sb < KB; ++sb)
+#pragma unroll
+      for (int i = 0; i < MTW; ++i) {
+        const int t = 2 * i + rh;
+        if (t < nt) {
+          const bf16x8 b0 = as_bf16x8(xs[buf][sb * SUB + t * 128 + lane]);
+          const bf16x8 b1 = as_bf16x8(xs[buf][sb * SUB + t * 128 + 64 + lane]);
+#pragma unroll
+          for (int vt = 0; vt < VTW; ++vt) {
+            acc[vt][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(A.w[vt][sb][0]), b0, acc[vt][i], 0, 0, 0);
+            acc[vt][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(A.w[vt][sb][1]), b1, acc[vt][i], 0, 0, 0);
+          }
+        }
+      }
+  };
+  // One stage with a two-slot W ring: issue x of ks+1, multiply stage ks, refill
+  // the consumed slot with W of ks+2, publish x of ks+1. The refill is younger
+  // than x of ks+1, so publishing x waits for W of ks+1 (used next) but not ks+2.
+  auto sub = [&](int ks, WS& use) __attribute__((always_inline)) {
+    if (ks >= KS) return;  // uniform
+    if (ks + 1 < KS) load_x(ks + 1);
+    step(use, ks & 1);
+    load_w(use, ks + 2);
+    if (ks + 1 < KS) store_x((ks + 1) & 1);
+    __syncthreads();
+  };
+  WS w0, w1;
+  load_x(0);
+  store_x(0);
+  load_w(w0, 0);
+  load_w(w1, 1);
+  __syncthreads();
+  for (int ks = 0; ks < KS; ks += 2) {
+    sub(ks, w0);
+    sub(ks + 1, w1);
+  }
+  // RMS scale per row: the PIECES threads of a row are consecutive lanes
+#pragma unroll
+  for (int j = 0; j < UPT; ++j) {
+    float t = ss[j];
+#pragma unroll
+    for (int o = 1; o < PIECES; o <<= 1) t += __shfl_xor(t, o);
+    const int v = tid + NTH * j;
+    if (v < n_units && v % PIECES == 0) rho_s[v / PIECES] = a.rms ? 1.0f / sqrtf(t / (float)K + 1e-5f) : 1.0f;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < MTW; ++i) {
+    const int m = 16 * (2 * i + rh) + col;
+    if (m >= M) continue;
+    const float rho = rho_s[m];
+#pragma unroll
+    for (int vt = 0; vt < VTW; ++vt) {
+      if (vb0 + vt >= nvb) continue;
+      const int v = 16 * (vb0 + vt) + 4 * quad;
+      float* out = a.logits + (size_t)m * a.V + v;
+      const f32x4 cc = acc[vt][i];
+      if (v + 3 < a.V && (a.V & 3) == 0) {
+        *(float4*)out = make_float4(cc[0] * rho, cc[1] * rho, cc[2] * rho, cc[3] * rho);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (v + r < a.V) out[r] = cc[r] * rho;
       }
     }
   }
@@ -1079,10 +1238,22 @@ hipError_t launch_pack_lm_head(const void* w, void* wp, int V, int K, bool bf16,
 
 hipError_t launch_lmhead(const LmArgs& a, bool bf16, hipStream_t st, const Timing* tm) {
   if (bf16) {
-    constexpr int VT = 4, NT = 3;
     const int nvb = (a.V + 15) / 16;
-    const int blocks = (nvb + 4 * VT - 1) / (4 * VT);
-    return go(k_lmhead_bf16<VT, NT>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), a);
+    if (a.M > kLmRowsPad && a.M <= 32 * kLmRowsMTW) {  // many rows: W streamed once for all of them
+      constexpr int VTW = 2, WPB = 8;
+      const int blocks = (nvb + WPB / 2 * VTW - 1) / (WPB / 2 * VTW);
+      if (a.K % 128 == 0)
+        return go(k_lmhead_rows_bf16<VTW, kLmRowsMTW, 2, WPB>, dim3(blocks), dim3(64 * WPB), 0, st, t0(tm), t1(tm), a);
+      return go(k_lmhead_rows_bf16<VTW, kLmRowsMTW, 1, WPB>, dim3(blocks), dim3(64 * WPB), 0, st, t0(tm), t1(tm), a);
+    }
+    // up to 48 rows, or beyond the many-row kernel: 48-row groups, the groups of
+    // one vocab chunk together on one XCD so that W comes from HBM once
+    constexpr int VT = 4, NT = 3;
+    const int chunks = (nvb + 4 * VT - 1) / (4 * VT);
+    LmArgs b = a;
+    b.row_groups = (a.M + 16 * NT - 1) / (16 * NT);
+    const int blocks = b.row_groups > 1 ? (chunks + 7) / 8 * 8 * b.row_groups : chunks;
+    return go(k_lmhead_bf16<VT, NT>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), b);
   }
   return go(k_lmhead_f32, dim3((a.V + 255) / 256), dim3(256), 0, st, t0(tm), t1(tm), a);
 }
