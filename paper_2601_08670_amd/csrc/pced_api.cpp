@@ -112,7 +112,8 @@ Layout make_layout(const pced_config& c) {
   L.part_ml = take(L.part_slots * G * 2 * 4);
   L.x = take((size_t)L.rows_pad * c.hidden * es);
   L.logits = take(S * c.vocab * 4);
-  L.fuse_part = take(B * L.nblk_fuse * 5 * 4);
+  // per-slice candidates: k_fuse uses 256-column slices, the fused LM-head epilogue 128-column ones
+  L.fuse_part = take(B * (size_t)ceil_div(c.vocab, 128) * 5 * 4);
   L.lse_part = take(S * L.nchunk * 2 * 4);
   L.jsd_part = take(S * L.nchunk * 4);
   L.syn_q = take(S * c.n_layers * c.n_q_heads * c.head_dim * es);
@@ -257,6 +258,34 @@ pced_status check_ctx(const pced_ctx* c, bool need_loaded) {
   return PCED_OK;
 }
 
+FuseArgs fuse_args(pced_ctx* c, const float* logits, int32_t* tokens_out, int tok_stride, const pced_step_out* extra,
+                   int nblk) {
+  FuseArgs f{};
+  f.logits = logits;
+  f.query_seq0 = c->at<int32_t>(c->lay.query_seq0);
+  f.query_exp0 = c->at<int32_t>(c->lay.query_exp0);
+  f.beta = c->at<float>(c->lay.beta);
+  f.prior = c->at<float>(c->lay.prior);
+  f.part = c->at<float>(c->lay.fuse_part);
+  f.tickets = c->at<int32_t>(c->lay.tick_fuse);
+  f.tokens_out = tokens_out;
+  f.prev_tok = c->at<int32_t>(c->lay.prev_tok);
+  f.winner = extra ? extra->winner : nullptr;
+  f.top1 = extra ? extra->top1 : nullptr;
+  f.top2 = extra ? extra->top2 : nullptr;
+  f.V = c->cfg.vocab;
+  f.nblk = nblk;
+  f.tok_stride = tok_stride;
+  return f;
+}
+
+pced_status copy_beta_used(pced_ctx* c, const pced_step_out* extra, hipStream_t st) {
+  if (extra && extra->beta_used)
+    HIP_OK(hipMemcpyAsync(extra->beta_used, c->at<float>(c->lay.beta), (size_t)c->NE * 4,
+                          hipMemcpyDeviceToDevice, st));
+  return PCED_OK;
+}
+
 // Launch the beta (first step) and fuse kernels over `logits`.
 pced_status run_fuse(pced_ctx* c, const float* logits, bool refresh_beta, int32_t* tokens_out,
                      int tok_stride, const pced_step_out* extra, hipStream_t st) {
@@ -277,33 +306,30 @@ pced_status run_fuse(pced_ctx* c, const float* logits, bool refresh_beta, int32_
     HIP_OK(launch_beta(b, c->S, c->NE, st, ps.timing()));
     c->beta_frozen = true;
   }
-  FuseArgs f{};
-  f.logits = logits;
-  f.query_seq0 = c->at<int32_t>(c->lay.query_seq0);
-  f.query_exp0 = c->at<int32_t>(c->lay.query_exp0);
-  f.beta = c->at<float>(c->lay.beta);
-  f.prior = c->at<float>(c->lay.prior);
-  f.part = c->at<float>(c->lay.fuse_part);
-  f.tickets = c->at<int32_t>(c->lay.tick_fuse);
-  f.tokens_out = tokens_out;
-  f.prev_tok = c->at<int32_t>(c->lay.prev_tok);
-  f.winner = extra ? extra->winner : nullptr;
-  f.top1 = extra ? extra->top1 : nullptr;
-  f.top2 = extra ? extra->top2 : nullptr;
-  f.V = cfg.vocab;
-  f.nblk = c->lay.nblk_fuse;
-  f.tok_stride = tok_stride;
+  FuseArgs f = fuse_args(c, logits, tokens_out, tok_stride, extra, c->lay.nblk_fuse);
   {
     ProfScope ps(c, PCED_PROF_FUSE, (double)c->S * cfg.vocab * 4, 0);
     HIP_OK(launch_fuse(f, c->B, st, ps.timing()));
   }
-  if (extra && extra->beta_used)
-    HIP_OK(hipMemcpyAsync(extra->beta_used, c->at<float>(c->lay.beta), (size_t)c->NE * 4,
-                          hipMemcpyDeviceToDevice, st));
-  return PCED_OK;
+  return copy_beta_used(c, extra, st);
 }
 
-pced_status run_lmhead(pced_ctx* c, const void* x, int M, const void* w, float* logits, hipStream_t st) {
+// After an LM head with the fused Eq. 2 epilogue: only the per-query merge of
+// its `nblk` slice candidates remains.
+pced_status run_fuse_final(pced_ctx* c, int nblk, int32_t* tokens_out, int tok_stride, const pced_step_out* extra,
+                           hipStream_t st) {
+  FuseArgs f = fuse_args(c, nullptr, tokens_out, tok_stride, extra, nblk);
+  {
+    ProfScope ps(c, PCED_PROF_FUSE, (double)c->B * nblk * 5 * 4, 0);
+    HIP_OK(launch_fuse_final(f, c->B, st, ps.timing()));
+  }
+  return copy_beta_used(c, extra, st);
+}
+
+// LM head over M rows of x. With fuse_nblk > 0 the kernel's epilogue applies
+// Eq. 2 and leaves per-slice candidates instead of writing the logits.
+pced_status run_lmhead(pced_ctx* c, const void* x, int M, const void* w, float* logits, hipStream_t st,
+                       int fuse_nblk = 0) {
   const pced_config& cfg = c->cfg;
   LmArgs a{};
   a.x = x;
@@ -313,9 +339,18 @@ pced_status run_lmhead(pced_ctx* c, const void* x, int M, const void* w, float* 
   a.V = cfg.vocab;
   a.K = cfg.hidden;
   a.rms = cfg.norm == PCED_NORM_RMS;
+  if (fuse_nblk > 0) {
+    a.query_seq0 = c->at<int32_t>(c->lay.query_seq0);
+    a.query_exp0 = c->at<int32_t>(c->lay.query_exp0);
+    a.beta = c->at<float>(c->lay.beta);
+    a.prior = c->at<float>(c->lay.prior);
+    a.fuse_part = c->at<float>(c->lay.fuse_part);
+    a.n_queries = c->B;
+    a.fuse_nblk = fuse_nblk;
+  }
   const double es = (double)esize_of(cfg);
-  ProfScope ps(c, PCED_PROF_LMHEAD,
-               (double)cfg.vocab * cfg.hidden * es + (double)M * cfg.hidden * es + (double)M * cfg.vocab * 4,
+  const double out_bytes = fuse_nblk > 0 ? (double)c->B * fuse_nblk * 5 * 4 : (double)M * cfg.vocab * 4;
+  ProfScope ps(c, PCED_PROF_LMHEAD, (double)cfg.vocab * cfg.hidden * es + (double)M * cfg.hidden * es + out_bytes,
                2.0 * M * cfg.vocab * cfg.hidden);
   HIP_OK(launch_lmhead(a, c->bf16, st, ps.timing()));
   return PCED_OK;
@@ -403,10 +438,22 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
     }
   }
 
-  float* logits = (extra && extra->logits) ? extra->logits : c->at<float>(c->lay.logits);
-  pced_status r = run_lmhead(c, at.x_out, c->S, w, logits, st);
-  if (r != PCED_OK) return r;
-  r = run_fuse(c, logits, c->dynamic_beta && !c->beta_frozen, tokens_out, tok_stride, extra, st);
+  // Eq. 2 and the slice argmax run in the LM head's epilogue when beta is known
+  // (fixed, or frozen after the first step) and the caller wants no logits;
+  // otherwise the logits are materialised (dynamic beta needs them at the first step)
+  const bool refresh = c->dynamic_beta && !c->beta_frozen;
+  const int fused_nblk = (c->bf16 && !refresh && !(extra && extra->logits)) ? lmhead_fused_nblk(c->S, cfg.vocab) : 0;
+  pced_status r;
+  if (fused_nblk > 0) {
+    r = run_lmhead(c, at.x_out, c->S, w, nullptr, st, fused_nblk);
+    if (r != PCED_OK) return r;
+    r = run_fuse_final(c, fused_nblk, tokens_out, tok_stride, extra, st);
+  } else {
+    float* logits = (extra && extra->logits) ? extra->logits : c->at<float>(c->lay.logits);
+    r = run_lmhead(c, at.x_out, c->S, w, logits, st);
+    if (r != PCED_OK) return r;
+    r = run_fuse(c, logits, refresh, tokens_out, tok_stride, extra, st);
+  }
   if (r != PCED_OK) return r;
   for (int s = 0; s < c->S; ++s) c->len[s] += 1;
   c->t += 1;

@@ -77,6 +77,15 @@ struct LmArgs {
   float* logits;            // [M][V]
   int M, V, K, rms;
   int row_groups;           // >= 1: work-groups per vocab chunk, each taking every R-th 48-row group
+  // Fused Eq. 2 epilogue (fuse_part != nullptr, M <= 288, one row group): the
+  // logits are not written; every block writes its best two tokens per query
+  // (over its vocabulary slice) to fuse_part [B][fuse_nblk][5] for k_fuse_final.
+  const int32_t* query_seq0;// [B+1]
+  const int32_t* query_exp0;// [B+1]
+  const float* beta;        // [sum N]
+  const float* prior;       // [sum N]
+  float* fuse_part;
+  int n_queries, fuse_nblk;
 };
 
 struct FuseArgs {
@@ -136,6 +145,10 @@ hipError_t launch_pack_lm_head(const void* w, void* wp, int V, int K, bool bf16,
 hipError_t launch_lmhead(const LmArgs& a, bool bf16, hipStream_t st, const Timing* tm = nullptr);
 hipError_t launch_beta(const BetaArgs& a, int n_seqs, int n_exp, hipStream_t st, const Timing* tm = nullptr);
 hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st, const Timing* tm = nullptr);
+// the final per-query merge alone (after an LM head with the fused epilogue)
+hipError_t launch_fuse_final(const FuseArgs& a, int n_queries, hipStream_t st, const Timing* tm = nullptr);
+// vocabulary slices (blocks) of the fused LM-head epilogue for M rows, or 0 if M rows cannot be fused
+int lmhead_fused_nblk(int M, int V);
 hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st, const Timing* tm = nullptr);
 hipError_t launch_copy_rows(const void* src, void* dst, size_t nbytes, hipStream_t st);
 

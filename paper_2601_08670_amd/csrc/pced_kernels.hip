@@ -597,7 +597,7 @@ __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a, int D) {
   }
 }
 
-// ------------------------------------------------------------------- LM head
+// --------------------------------------------------- LM head: sum of squares
 
 __device__ __forceinline__ float sumsq8(bf16x8 v) {
   const uint4 u = __builtin_bit_cast(uint4, v);
@@ -610,6 +610,130 @@ __device__ __forceinline__ float sumsq8(bf16x8 v) {
   }
   return s;
 }
+
+// ------------------------------------------------------ argmax helpers (Eq. 3)
+
+struct Top2 {
+  float v1; int i1; int k1; float v2; int i2;
+};
+
+// order: higher score first, lower token id on equal scores
+__device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
+  return va > vb || (va == vb && ia < ib);
+}
+
+__device__ __forceinline__ Top2 merge(const Top2& A, const Top2& B) {
+  // winner's best, then the better of the winner's second and the loser's best
+  // (written with selects only, so the candidates stay in registers)
+  const bool af = better(A.v1, A.i1, B.v1, B.i1);
+  const float wv2 = af ? A.v2 : B.v2, lv1 = af ? B.v1 : A.v1;
+  const int wi2 = af ? A.i2 : B.i2, li1 = af ? B.i1 : A.i1;
+  const bool w2 = better(wv2, wi2, lv1, li1);
+  Top2 R;
+  R.v1 = af ? A.v1 : B.v1;
+  R.i1 = af ? A.i1 : B.i1;
+  R.k1 = af ? A.k1 : B.k1;
+  R.v2 = w2 ? wv2 : lv1;
+  R.i2 = w2 ? wi2 : li1;
+  return R;
+}
+
+__device__ __forceinline__ Top2 shfl_top2(const Top2& x, int o) {
+  Top2 y;
+  y.v1 = __shfl_xor(x.v1, o); y.i1 = __shfl_xor(x.i1, o); y.k1 = __shfl_xor(x.k1, o);
+  y.v2 = __shfl_xor(x.v2, o); y.i2 = __shfl_xor(x.i2, o);
+  return y;
+}
+
+// Two-level argmax over a block of NW waves: a wave merges its lanes' candidates
+// with shuffles, the block merges its waves through LDS. Deterministic for any
+// merge order: "better" is a total order on (score, token).
+template <int NW>
+__device__ Top2 block_top2(Top2 c) {
+  __shared__ Top2 red[NW];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) c = merge(c, shfl_top2(c, o));
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[wave] = c;
+  __syncthreads();
+  Top2 r = red[0];
+#pragma unroll
+  for (int i = 1; i < NW; ++i) r = merge(r, red[i]);
+  __syncthreads();
+  return r;
+}
+
+// Eq. 2 and the best two tokens per query over a block's logits tile (the LM
+// head's fused epilogue). The NC columns are vocabulary ids v0 .. v0+NC-1; row m
+// of column j is read through at(m, j). The block's NW waves form groups of NC
+// threads, one column per thread, and the groups take the queries in turn; the
+// experts' scores are read eight at a time so their LDS latencies overlap. The
+// arithmetic is k_fuse's, in the same order and without contraction, so the
+// result is bit-identical to materialising the logits and fusing them
+// afterwards. Writes fuse_part[b][blk] for every query b.
+template <int NW, int NC, typename At>
+__device__ void fuse_tile(const LmArgs& a, int v0, int blk, At at) {
+#pragma clang fp contract(off)
+  constexpr int NG = 64 * NW / NC;  // thread groups (queries in flight)
+  constexpr int WG = NC / 64;       // waves per group
+  static_assert(NG >= 1 && NC % 64 == 0, "whole waves per group");
+  __shared__ Top2 red[NG][WG];
+  // beta and prior of every expert, staged once (fused launches have < 288 experts)
+  __shared__ float cb[32 * kLmRowsMTW], pr[32 * kLmRowsMTW];
+  const int n_exp = a.query_exp0[a.n_queries];
+  for (int i = threadIdx.x; i < n_exp; i += 64 * NW) {
+    cb[i] = a.beta[i];
+    pr[i] = a.prior[i];
+  }
+  __syncthreads();
+  const int g = threadIdx.x / NC, j = threadIdx.x % NC, wg = j >> 6;
+  const int v = v0 + j;
+  for (int b0 = 0; b0 < a.n_queries; b0 += NG) {
+    // one query per wave: uniform, so its row range, beta and prior come by scalar loads
+    const int b = __builtin_amdgcn_readfirstlane(b0 + g);
+    Top2 c{kNegInf, 0x7FFFFFFF, 0, kNegInf, 0x7FFFFFFF};
+    if (b < a.n_queries && v < a.V) {
+      const int s0 = a.query_seq0[b];
+      const int N = a.query_seq0[b + 1] - s0 - 1;
+      const int e0 = a.query_exp0[b];
+      const float sa = at(s0, j);
+      float best = kNegInf;
+      int bk = 0;
+      for (int kb = 1; kb <= N; kb += 8) {
+        float x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = (kb + u <= N) ? at(s0 + kb + u, j) : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int k = kb + u;
+          if (k > N) continue;
+          const float beta = cb[e0 + k - 1];
+          const float coef = 1.0f + beta;
+          const float t1 = coef * x[u];
+          const float t2 = beta * sa;
+          const float val = (t1 - t2) + pr[e0 + k - 1];
+          if (val > best) { best = val; bk = k; }
+        }
+      }
+      c.v1 = best; c.i1 = v; c.k1 = bk;
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) c = merge(c, shfl_top2(c, o));
+    if ((threadIdx.x & 63) == 0) red[g][wg] = c;
+    __syncthreads();
+    if (j == 0 && b < a.n_queries) {
+      Top2 r = red[g][0];
+#pragma unroll
+      for (int i = 1; i < WG; ++i) r = merge(r, red[g][i]);
+      float* p = a.fuse_part + ((size_t)b * a.fuse_nblk + blk) * 5;
+      p[0] = r.v1; p[1] = __int_as_float(r.i1); p[2] = __int_as_float(r.k1);
+      p[3] = r.v2; p[4] = __int_as_float(r.i2);
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------------- LM head
 
 // Packed LM-head layout (bf16). W [V][K] is re-laid once into 2 KiB tiles, one
 // per (16-row vocab block vb, 64-wide k step ks), tiles ordered [vb][ks]. Inside
@@ -643,7 +767,7 @@ __global__ __launch_bounds__(256) void k_pack_w_bf16(const uint16_t* __restrict_
 // register ring (two 64-wide k steps in flight); the x operands (a few hundred
 // KiB, L2-resident) are loaded one step ahead.
 // rho (the RMS scale) is accumulated from the same x operands.
-template <int VT, int NT>
+template <int VT, int NT, bool FUSED>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_lmhead_bf16(LmArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, quad = lane >> 4;
@@ -660,7 +784,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   }
   const int vb0 = (chunk * 4 + wave) * VT;   // first 16-row vocab block of the wave
   const int nvb = (a.V + 15) / 16;
-  if (vb0 >= nvb) return;
+  if (!FUSED && vb0 >= nvb) return;  // (fused: every wave reaches the block's barriers)
   const int K = a.K, KS = K / 64;
   const uint4* Wp = (const uint4*)a.w;
   const uint16_t* X = (const uint16_t*)a.x;
@@ -727,6 +851,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       load_x(xb, ks + 5); load_w(w0, ks + 6); if (ks + 4 < KS) step(w1, xa);
       load_x(xa, ks + 6); load_w(w1, ks + 7); if (ks + 5 < KS) step(w2, xb);
     }
+    if constexpr (FUSED) {
+      // logits tile of the block (rows x 256 columns, rows padded by 16 bytes
+      // against bank conflicts), then Eq. 2 per column (one row group: m0 = 0)
+      constexpr int LD = 64 * VT + 4;
+      __shared__ __align__(16) float tile[16 * NT * LD];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        float t = ss[nt] + __shfl_xor(ss[nt], 16);
+        t += __shfl_xor(t, 32);
+        const float rho = a.rms ? 1.0f / sqrtf(t / (float)K + 1e-5f) : 1.0f;
+        const int m = 16 * nt + col;
+        if (m >= a.M) continue;
+#pragma unroll
+        for (int vt = 0; vt < VT; ++vt) {
+          const f32x4 cc = acc[vt][nt];
+          *(float4*)(tile + m * LD + 64 * wave + 16 * vt + 4 * quad) =
+              make_float4(cc[0] * rho, cc[1] * rho, cc[2] * rho, cc[3] * rho);
+        }
+      }
+      __syncthreads();
+      fuse_tile<4, 64 * VT>(a, chunk * 256, chunk, [&](int m, int j) { return tile[m * LD + j]; });
+      continue;
+    }
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       float t = ss[nt] + __shfl_xor(ss[nt], 16);
@@ -763,7 +910,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 // issued before that refill, so waiting for x never waits for W that is not
 // due, and long stages keep each W load a full stage ahead of its use. The
 // staging threads also accumulate every row's sum of squares (RMS scale).
-template <int VTW, int MTW, int KB, int WPB>
+template <int VTW, int MTW, int KB, int WPB, bool FUSED>
 __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_lmhead_rows_bf16(LmArgs a) {
   constexpr int NTH = 64 * WPB;          // threads per block
   constexpr int MT = 2 * MTW;            // row tiles the kernel holds
@@ -877,6 +1024,30 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
     if (v < n_units && v % PIECES == 0) rho_s[v / PIECES] = a.rms ? 1.0f / sqrtf(t / (float)K + 1e-5f) : 1.0f;
   }
   __syncthreads();
+  if constexpr (FUSED) {
+    // logits tile of the block in the (now free) x buffers: rows x 128 columns,
+    // float4 groups XOR-swizzled by row against bank conflicts; then Eq. 2 per column
+    constexpr int NC = WPB / 2 * VTW * 16;  // columns of the block
+    static_assert(NC == 128 && 2 * UNITS * 4 >= 32 * MTW * NC, "tile fits the x buffers");
+    float* tile = (float*)&xs[0][0];
+    auto at = [&](int m, int j) { return tile[m * NC + ((((j >> 2) ^ (m & 31)) << 2) | (j & 3))]; };
+#pragma unroll
+    for (int i = 0; i < MTW; ++i) {
+      const int m = 16 * (2 * i + rh) + col;
+      if (m >= M) continue;
+      const float rho = rho_s[m];
+#pragma unroll
+      for (int vt = 0; vt < VTW; ++vt) {
+        const f32x4 cc = acc[vt][i];
+        const int c4 = 8 * (wave >> 1) + 4 * vt + quad;
+        *(float4*)(tile + m * NC + ((c4 ^ (m & 31)) << 2)) =
+            make_float4(cc[0] * rho, cc[1] * rho, cc[2] * rho, cc[3] * rho);
+      }
+    }
+    __syncthreads();
+    fuse_tile<WPB, NC>(a, blockIdx.x * NC, blockIdx.x, at);
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < MTW; ++i) {
     const int m = 16 * (2 * i + rh) + col;
@@ -918,54 +1089,6 @@ __global__ __launch_bounds__(256) void k_lmhead_f32(LmArgs a) {
 
 // ---------------------------------------------------------- Eq. 2 and Eq. 3
 
-struct Top2 {
-  float v1; int i1; int k1; float v2; int i2;
-};
-
-// order: higher score first, lower token id on equal scores
-__device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
-  return va > vb || (va == vb && ia < ib);
-}
-
-__device__ __forceinline__ Top2 merge(const Top2& A, const Top2& B) {
-  // winner's best, then the better of the winner's second and the loser's best
-  // (written with selects only, so the candidates stay in registers)
-  const bool af = better(A.v1, A.i1, B.v1, B.i1);
-  const float wv2 = af ? A.v2 : B.v2, lv1 = af ? B.v1 : A.v1;
-  const int wi2 = af ? A.i2 : B.i2, li1 = af ? B.i1 : A.i1;
-  const bool w2 = better(wv2, wi2, lv1, li1);
-  Top2 R;
-  R.v1 = af ? A.v1 : B.v1;
-  R.i1 = af ? A.i1 : B.i1;
-  R.k1 = af ? A.k1 : B.k1;
-  R.v2 = w2 ? wv2 : lv1;
-  R.i2 = w2 ? wi2 : li1;
-  return R;
-}
-
-__device__ __forceinline__ Top2 shfl_top2(const Top2& x, int o) {
-  Top2 y;
-  y.v1 = __shfl_xor(x.v1, o); y.i1 = __shfl_xor(x.i1, o); y.k1 = __shfl_xor(x.k1, o);
-  y.v2 = __shfl_xor(x.v2, o); y.i2 = __shfl_xor(x.i2, o);
-  return y;
-}
-
-// Two-level argmax: a wave merges its lanes' candidates with shuffles, the block
-// merges its waves through LDS. Deterministic for any merge order: "better" is a
-// total order on (score, token).
-__device__ Top2 block_top2(Top2 c) {
-  __shared__ Top2 red[kFuseBlock / 64];
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) c = merge(c, shfl_top2(c, o));
-  const int wave = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) red[wave] = c;
-  __syncthreads();
-  Top2 r = red[0];
-  for (int i = 1; i < (int)(blockDim.x >> 6); ++i) r = merge(r, red[i]);
-  __syncthreads();
-  return r;
-}
-
 // One block per (query, 256-token vocab slice). Per token v:
 //   s_hat_k(v) = ((1 + beta_k) s_k(v) - beta_k s_0(v)) + gamma ln r_k     (Eq. 2)
 // evaluated in float32 in exactly that order without fused multiply-adds,
@@ -1003,7 +1126,7 @@ __global__ __launch_bounds__(kFuseBlock) void k_fuse(FuseArgs a) {
     }
     c.v1 = best; c.i1 = v; c.k1 = bk;
   }
-  c = block_top2(c);
+  c = block_top2<kFuseBlock / 64>(c);
   if (threadIdx.x == 0) {
     float* p = a.part + ((size_t)b * a.nblk + blockIdx.x) * 5;
     p[0] = c.v1; p[1] = __int_as_float(c.i1); p[2] = __int_as_float(c.k1);
@@ -1021,7 +1144,7 @@ __global__ __launch_bounds__(kFuseBlock) void k_fuse_final(FuseArgs a) {
     Top2 x{p[0], __float_as_int(p[1]), __float_as_int(p[2]), p[3], __float_as_int(p[4])};
     r = merge(r, x);
   }
-  r = block_top2(r);
+  r = block_top2<kFuseBlock / 64>(r);
   if (threadIdx.x == 0) {
     a.tokens_out[(size_t)b * a.tok_stride] = r.i1;
     a.prev_tok[b] = r.i1;
@@ -1236,15 +1359,24 @@ hipError_t launch_pack_lm_head(const void* w, void* wp, int V, int K, bool bf16,
   return hipGetLastError();
 }
 
+int lmhead_fused_nblk(int M, int V) {
+  if (M <= kLmRowsPad) return (V + 255) / 256;         // 48-row kernel: 256 columns per block
+  if (M <= 32 * kLmRowsMTW) return (V + 127) / 128;    // many-row kernel: 128 columns per block
+  return 0;
+}
+
 hipError_t launch_lmhead(const LmArgs& a, bool bf16, hipStream_t st, const Timing* tm) {
   if (bf16) {
     const int nvb = (a.V + 15) / 16;
+    const bool fused = a.fuse_part != nullptr;
+    if (fused && lmhead_fused_nblk(a.M, a.V) == 0) return hipErrorInvalidValue;
     if (a.M > kLmRowsPad && a.M <= 32 * kLmRowsMTW) {  // many rows: W streamed once for all of them
       constexpr int VTW = 2, WPB = 8;
       const int blocks = (nvb + WPB / 2 * VTW - 1) / (WPB / 2 * VTW);
-      if (a.K % 128 == 0)
-        return go(k_lmhead_rows_bf16<VTW, kLmRowsMTW, 2, WPB>, dim3(blocks), dim3(64 * WPB), 0, st, t0(tm), t1(tm), a);
-      return go(k_lmhead_rows_bf16<VTW, kLmRowsMTW, 1, WPB>, dim3(blocks), dim3(64 * WPB), 0, st, t0(tm), t1(tm), a);
+      const dim3 g(blocks), b(64 * WPB);
+      if (a.K % 128 != 0) return hipErrorInvalidValue;  // bf16 hidden sizes are multiples of 256
+      if (fused) return go(k_lmhead_rows_bf16<VTW, kLmRowsMTW, 2, WPB, true>, g, b, 0, st, t0(tm), t1(tm), a);
+      return go(k_lmhead_rows_bf16<VTW, kLmRowsMTW, 2, WPB, false>, g, b, 0, st, t0(tm), t1(tm), a);
     }
     // up to 48 rows, or beyond the many-row kernel: 48-row groups, the groups of
     // one vocab chunk together on one XCD so that W comes from HBM once
@@ -1253,7 +1385,8 @@ hipError_t launch_lmhead(const LmArgs& a, bool bf16, hipStream_t st, const Timin
     LmArgs b = a;
     b.row_groups = (a.M + 16 * NT - 1) / (16 * NT);
     const int blocks = b.row_groups > 1 ? (chunks + 7) / 8 * 8 * b.row_groups : chunks;
-    return go(k_lmhead_bf16<VT, NT>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), b);
+    if (fused) return go(k_lmhead_bf16<VT, NT, true>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), b);
+    return go(k_lmhead_bf16<VT, NT, false>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), b);
   }
   return go(k_lmhead_f32, dim3((a.V + 255) / 256), dim3(256), 0, st, t0(tm), t1(tm), a);
 }
@@ -1270,6 +1403,10 @@ hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st, const T
   hipError_t e = go(k_fuse, dim3(a.nblk, n_queries), dim3(kFuseBlock), 0, st, t0(tm), nullptr, a);
   if (e != hipSuccess) return e;
   return go(k_fuse_final, dim3(n_queries), dim3(kFuseBlock), 0, st, nullptr, t1(tm), a);
+}
+
+hipError_t launch_fuse_final(const FuseArgs& a, int n_queries, hipStream_t st, const Timing* tm) {
+  return go(k_fuse_final, dim3(n_queries), dim3(kFuseBlock), 0, st, t0(tm), t1(tm), a);
 }
 
 hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st, const Timing* tm) {

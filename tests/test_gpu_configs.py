@@ -213,6 +213,40 @@ def test_chunks_spanning_sequences(name, geom, n_exp, lens, am, steps, cap, shuf
     _check_queries(wl, list(range(wl.n_queries)), steps, sess=_session(wl, max_attn_chunks=cap))
 
 
+FUSED = [
+    # (name, geometry, n_experts, expert lengths, amateur length, steps, fixed beta or None)
+    ("48-row-kernel-dynamic-beta", W.Geometry(1, 8, 2, 64, 512, 3001, "bf16"), [3, 2],
+     [40, 300, 17, 5, 129], 16, 3, None),
+    ("many-row-kernel-fixed-beta", W.Geometry(1, 8, 2, 64, 512, 1000, "bf16"), [20, 30, 10],
+     list(range(3, 183, 3)), 5, 2, "fixed"),
+    ("llama-heads-vocab-tail-dynamic-beta", W.Geometry(1, 32, 8, 128, 4096, 4103, "bf16"), [6],
+     [100, 7, 64, 300, 16, 45], 64, 3, None),
+]
+
+
+@pytest.mark.parametrize("name,geom,n_exp,lens,am,steps,beta", FUSED, ids=[e[0] for e in FUSED])
+def test_fused_lmhead_epilogue_matches_materialised_logits(name, geom, n_exp, lens, am, steps, beta):
+    """Without requested logits, Eq. 2 and the slice argmax run in the LM head's
+    epilogue (beta fixed, or frozen after the first step). Tokens, winners and
+    both scores must equal the materialised-logits path bit for bit."""
+    if beta == "fixed":
+        beta = np.random.default_rng(4).random(sum(n_exp)).astype(np.float32).tolist()
+    wl = W.custom(geom, n_exp, lens, am, steps, seed=12, beta=beta)
+    sa, sb = _session(wl), _session(wl)
+    Wt = sa.pack_lm_head(wl.lm_head_device(DEV))
+    Wh = lm_head_host(wl.seed, geom.vocab, geom.hidden, geom.dtype)
+    orc, seqs = _oracle_for_queries(wl, list(range(wl.n_queries)))
+    for t in range(steps):
+        q, kn, vn = wl.step_inputs_device(t, DEV)
+        oa = sa.step(q, kn, vn, Wt, want=("logits", "winner", "top1", "top2"))
+        ob = sb.step(q, kn, vn, Wt, want=("winner", "top1", "top2"))
+        torch.cuda.synchronize()
+        for k in ("tokens", "winner", "top1", "top2"):
+            assert np.array_equal(_np(oa[k]).view(np.uint8), _np(ob[k]).view(np.uint8)), (t, k)
+        ref = orc.step(*wl.step_inputs_host(t), Wh)
+        check_tokens(_np(ob["tokens"]), ref.logits, wl, ref.beta, ref.tokens, ref.gaps)
+
+
 def test_fixed_and_zero_beta():
     geom = W.Geometry(1, 8, 2, 64, 512, 900, "bf16")
     wl = W.custom(geom, [4], [30, 90, 200, 7], 10, 2, seed=8, beta=[0.0, 0.25, 1.0, 0.5])
