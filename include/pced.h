@@ -239,6 +239,30 @@ pced_status pced_fuse(pced_ctx* ctx, const float* logits, int32_t refresh_beta,
 /* Host mirror of the current cache length of every sequence: out [S]. */
 pced_status pced_get_lengths(const pced_ctx* ctx, int32_t* out, int32_t capacity);
 
+/* Retrieval score modes (paper, Appendix B: normalisation per scoring mode). */
+typedef enum pced_score_mode {
+  PCED_SCORE_DENSE = 0,    /* cosine similarity in [-1, 1]: r = clip((s + 1) / 2, 0, 1 - eps)     */
+  PCED_SCORE_COLBERT = 1,  /* same range and rescaling as dense                                  */
+  PCED_SCORE_SPARSE = 2    /* nonnegative, unbounded: r = clip((2/pi) atan(max(s, 0)), 0, 1 - eps) */
+} pced_score_mode;
+
+/*
+ * Host helper: relevance scores r_k for pced_load_caches from raw retrieval
+ * scores and reranker logits (paper: Section 3, "Retrieval and relevance
+ * scoring"; Appendix B, the per-mode normalisation, the reranker's sigmoid and
+ * the harmonic-mean fusion), eps = 1e-8:
+ *     r_ret = per mode (see pced_score_mode)
+ *     r_rer = clip(1 / (1 + exp(-z)), 0, 1 - eps)
+ *     r     = 2 r_ret r_rer / (r_ret + r_rer + eps)
+ * With reranker_logits NULL, r = r_ret. Evaluated in double precision, stored
+ * as float. All pointers are host memory of n elements; relevance may alias
+ * neither input. No device work and no context involved.
+ * Errors: INVALID_ARG (NULL retrieval or relevance, n < 0, unknown mode, a NaN
+ * input).
+ */
+pced_status pced_relevance(int32_t mode, int32_t n, const float* retrieval, const float* reranker_logits,
+                           float* relevance);
+
 /* Kernel timing with HIP events recorded around each launch on the launch
  * stream. Classes: */
 enum {

@@ -329,6 +329,47 @@ class Oracle:
             beta=np.array(beta, copy=True), logits=logits, hidden=hidden, attn=attn)
 
 
+# --------------------------------------------------------------------------
+# Relevance scores from raw retrieval and reranker outputs (Section 3,
+# "Retrieval and relevance scoring"; Appendix B). Every normalised score is
+# clipped to [0, 1 - eps]; the harmonic mean carries eps in its denominator as
+# Appendix B writes it (the Section 3 formula omits it).
+
+def normalise_retrieval(s, mode: str) -> np.ndarray:
+    """Appendix B: dense / ColBERT cosine scores in [-1, 1] are rescaled
+    affinely, (s + 1) / 2; sparse scores (nonnegative, unbounded) go through
+    (2 / pi) arctan(max(s, 0)). Both are clipped to [0, 1 - eps]."""
+    s = np.asarray(s, dtype=np.float64)
+    if mode in ("dense", "colbert"):
+        r = (s + 1.0) / 2.0
+    elif mode == "sparse":
+        r = (2.0 / math.pi) * np.arctan(np.maximum(s, 0.0))
+    else:
+        raise ValueError(mode)
+    return np.clip(r, 0.0, 1.0 - RELEVANCE_EPS)
+
+
+def normalise_reranker(z) -> np.ndarray:
+    """Appendix B: the reranker's logits through the logistic sigmoid, clipped
+    to [0, 1 - eps]."""
+    z = np.asarray(z, dtype=np.float64)
+    with np.errstate(over="ignore"):  # exp(-z) = inf for very negative z gives sigma = 0
+        return np.clip(1.0 / (1.0 + np.exp(-z)), 0.0, 1.0 - RELEVANCE_EPS)
+
+
+def fuse_relevance(r_ret, r_rer) -> np.ndarray:
+    """Appendix B: harmonic mean 2 r_ret r_rer / (r_ret + r_rer + eps)."""
+    a = np.asarray(r_ret, dtype=np.float64)
+    b = np.asarray(r_rer, dtype=np.float64)
+    return 2.0 * a * b / (a + b + RELEVANCE_EPS)
+
+
+def relevance(retrieval, mode: str, reranker_logits=None) -> np.ndarray:
+    """r_k for Eq. 2 from raw scores; retrieval only when there is no reranker."""
+    r = normalise_retrieval(retrieval, mode)
+    return r if reranker_logits is None else fuse_relevance(r, normalise_reranker(reranker_logits))
+
+
 def kv_bytes_per_token(n_layers: int, n_kv_heads: int, head_dim: int, bytes_per_value: int) -> int:
     """Bytes of K and V cached for one token across all layers."""
     return 2 * n_layers * n_kv_heads * head_dim * bytes_per_value

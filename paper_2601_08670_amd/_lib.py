@@ -21,7 +21,7 @@ PROF_CLASSES = ("append", "attn", "lmhead", "beta", "fuse", "synth", "combine")
 
 EXPORTED = ("pced_pool_bytes", "pced_lm_head_bytes", "pced_pack_lm_head", "pced_workspace_bytes", "pced_create", "pced_destroy", "pced_last_error",
             "pced_load_caches", "pced_step", "pced_generate", "pced_lmhead", "pced_fuse",
-            "pced_get_lengths", "pced_profile_enable", "pced_profile_read")
+            "pced_get_lengths", "pced_profile_enable", "pced_profile_read", "pced_relevance")
 
 
 class PcedError(RuntimeError):
@@ -80,6 +80,7 @@ def load_library() -> ctypes.CDLL:
         "pced_get_lengths": (I, [P, P, I]),
         "pced_profile_enable": (I, [P, I]),
         "pced_profile_read": (I, [P, ctypes.POINTER(pced_profile)]),
+        "pced_relevance": (I, [I, I, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -119,6 +120,24 @@ def pced_lm_head_bytes(cfg: pced_config) -> int:
 def pced_pack_lm_head(cfg: pced_config, w, w_packed, stream=None):
     """Re-lay row-major [V][hidden] LM-head weights into the packed form the steps read."""
     _check(load_library().pced_pack_lm_head(ctypes.byref(cfg), w.data_ptr(), w_packed.data_ptr(), _stream(stream)))
+
+
+SCORE_MODES = {"dense": 0, "colbert": 1, "sparse": 2}
+
+
+def pced_relevance(mode: str, retrieval, reranker_logits=None):
+    """Relevance scores r_k from raw retrieval scores (``mode`` dense, colbert or
+    sparse) and optional reranker logits, by the library's host helper; returns a
+    float32 NumPy array."""
+    import numpy as np
+    ret = np.ascontiguousarray(retrieval, dtype=np.float32)
+    rer = None if reranker_logits is None else np.ascontiguousarray(reranker_logits, dtype=np.float32)
+    if rer is not None and rer.shape != ret.shape:
+        raise ValueError("retrieval and reranker_logits differ in shape")
+    out = np.empty_like(ret)
+    _check(load_library().pced_relevance(SCORE_MODES[mode], ret.size, ret.ctypes.data,
+                                         None if rer is None else rer.ctypes.data, out.ctypes.data))
+    return out
 
 
 def _ptr(t) -> Optional[int]:

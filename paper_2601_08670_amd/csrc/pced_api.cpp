@@ -746,6 +746,31 @@ pced_status pced_fuse(pced_ctx* c, const float* logits, int32_t refresh_beta, in
   return run_fuse(c, logits, refresh_beta != 0, tokens_out, 1, extra, st);
 }
 
+pced_status pced_relevance(int32_t mode, int32_t n, const float* retrieval, const float* reranker_logits,
+                           float* relevance) {
+  if (!retrieval || !relevance) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  if (n < 0) return fail(PCED_ERR_INVALID_ARG, "n = %d", n);
+  if (mode != PCED_SCORE_DENSE && mode != PCED_SCORE_COLBERT && mode != PCED_SCORE_SPARSE)
+    return fail(PCED_ERR_INVALID_ARG, "unknown score mode %d", mode);
+  for (int32_t k = 0; k < n; ++k)
+    if (std::isnan(retrieval[k]) || (reranker_logits && std::isnan(reranker_logits[k])))
+      return fail(PCED_ERR_INVALID_ARG, "score %d is NaN", k);
+  const double eps = 1e-8, top = 1.0 - eps;
+  auto clip = [&](double x) { return std::min(std::max(x, 0.0), top); };
+  for (int32_t k = 0; k < n; ++k) {
+    const double s = retrieval[k];
+    const double r_ret = mode == PCED_SCORE_SPARSE ? clip(2.0 / M_PI * std::atan(std::max(s, 0.0)))
+                                                   : clip((s + 1.0) / 2.0);
+    double r = r_ret;
+    if (reranker_logits) {
+      const double r_rer = clip(1.0 / (1.0 + std::exp(-(double)reranker_logits[k])));
+      r = 2.0 * r_ret * r_rer / (r_ret + r_rer + eps);
+    }
+    relevance[k] = (float)r;
+  }
+  return PCED_OK;
+}
+
 pced_status pced_get_lengths(const pced_ctx* c, int32_t* out, int32_t capacity) {
   pced_status r = check_ctx(c, true);
   if (r != PCED_OK) return r;

@@ -170,3 +170,39 @@ def test_pack_lm_head_validation():
     assert b"overlap" in lib.pced_last_error()
     bad = cfg(vocab=1)
     assert lib.pced_pack_lm_head(ctypes.byref(bad), 1 << 40, 1 << 41, None) == INVALID
+
+
+def test_relevance_helper_matches_oracle():
+    """pced_relevance (host C) against the oracle's Appendix B functions: the
+    float32 results agree to one unit in the last place."""
+    from oracle import pced_oracle as O
+    import numpy as np
+    rng = np.random.default_rng(3)
+    n = 1000
+    for mode in ("dense", "colbert", "sparse"):
+        ret = (rng.random(n) * 2.4 - 1.2 if mode != "sparse" else rng.gamma(1.0, 20.0, n)).astype(np.float32)
+        ret[:4] = [-1.0, 1.0, 0.0, np.inf if mode == "sparse" else 5.0]
+        rer = (rng.normal(0, 4, n)).astype(np.float32)
+        for z in (None, rer):
+            got = _lib.pced_relevance(mode, ret, z)
+            want = O.relevance(ret.astype(np.float64), mode, None if z is None else z.astype(np.float64))
+            ulp = np.spacing(want.astype(np.float32))
+            assert np.all(np.abs(got.astype(np.float64) - want) <= ulp), mode
+
+
+def test_relevance_helper_errors():
+    import numpy as np
+    lib = _lib.load_library()
+    a = (ctypes.c_float * 2)(0.1, 0.2)
+    out = (ctypes.c_float * 2)()
+    assert lib.pced_relevance(7, 2, a, None, out) == INVALID
+    assert lib.pced_relevance(0, -1, a, None, out) == INVALID
+    assert lib.pced_relevance(0, 2, None, None, out) == INVALID
+    assert lib.pced_relevance(0, 2, a, None, None) == INVALID
+    bad = (ctypes.c_float * 2)(0.1, float("nan"))
+    assert lib.pced_relevance(2, 2, bad, None, out) == INVALID
+    assert lib.pced_relevance(0, 2, a, bad, out) == INVALID
+    assert b"NaN" in lib.pced_last_error()
+    assert lib.pced_relevance(0, 0, a, None, out) == OK
+    with pytest.raises(_lib.PcedError):
+        _lib.pced_relevance("dense", np.array([np.nan], np.float32))

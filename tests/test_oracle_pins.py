@@ -487,3 +487,47 @@ def test_kv_storage_figure_of_the_paper():
     assert per_token == 128 * 1024
     total = g["passages"] * g["tokens_per_passage"] * per_token
     assert round(total / 2 ** 30, 2) == g["reported_gb"]
+
+
+# ---------------------------------------------------------------- relevance
+# Appendix B normalisation and fusion, pinned by closed forms and invariants.
+
+def test_dense_and_colbert_rescaling_closed_forms():
+    for mode in ("dense", "colbert"):
+        r = O.normalise_retrieval([-1.0, 0.0, 0.5, -3.0, 1.0, 7.0], mode)
+        assert r[0] == 0.0 and r[1] == 0.5 and r[2] == 0.75 and r[3] == 0.0
+        assert r[4] == r[5] == 1.0 - 1e-8          # clipped below 1
+    s = np.linspace(-1, 1, 101)
+    assert np.all(np.diff(O.normalise_retrieval(s, "dense")) > 0)
+
+
+def test_sparse_arctan_closed_forms():
+    r = O.normalise_retrieval([0.0, 1.0, math.sqrt(3.0), 1.0 / math.sqrt(3.0), -5.0, 1e12], "sparse")
+    assert r[0] == 0.0 and r[4] == 0.0                  # max(s, 0)
+    assert abs(r[1] - 0.5) < 1e-15                      # atan(1) = pi/4
+    assert abs(r[2] - 2.0 / 3.0) < 1e-15                # atan(sqrt 3) = pi/3
+    assert abs(r[3] - 1.0 / 3.0) < 1e-15                # atan(1/sqrt 3) = pi/6
+    assert r[5] == 1.0 - 1e-8
+    assert np.all(np.diff(O.normalise_retrieval(np.linspace(0, 50, 200), "sparse")) > 0)
+
+
+def test_reranker_sigmoid_closed_forms():
+    r = O.normalise_reranker([0.0, math.log(3.0), -math.log(3.0), -800.0, 800.0])
+    assert r[0] == 0.5
+    assert abs(r[1] - 0.75) < 1e-15 and abs(r[2] - 0.25) < 1e-15
+    assert r[3] == 0.0 and r[4] == 1.0 - 1e-8
+    z = np.linspace(-6, 6, 25)
+    assert np.allclose(O.normalise_reranker(z) + O.normalise_reranker(-z), 1.0, atol=1e-15)
+
+
+def test_harmonic_mean_fusion():
+    assert O.fuse_relevance(0.0, 0.7) == 0.0
+    # harmonic mean of 1/3 and 1 is 1/2; eps only perturbs the 9th digit
+    assert abs(O.fuse_relevance(1.0 / 3.0, 1.0) - 0.5) < 1e-8
+    a, b = np.random.default_rng(0).random((2, 50))
+    assert np.array_equal(O.fuse_relevance(a, b), O.fuse_relevance(b, a))
+    h = O.fuse_relevance(a, b)
+    assert np.all(h <= np.maximum(a, b)) and np.all(h >= np.minimum(a, b) - 1e-7)
+    # equal inputs give (almost) that value; retrieval alone without a reranker
+    assert np.allclose(O.fuse_relevance(a, a), a, atol=1e-7)
+    assert np.array_equal(O.relevance([0.2, -0.4], "dense"), O.normalise_retrieval([0.2, -0.4], "dense"))
