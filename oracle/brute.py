@@ -79,3 +79,34 @@ def pick(rows, relevance, gamma, beta):
         if v != tok and best_v[v] > top2:
             top2 = best_v[v]
     return tok, best_k[tok], best_v[tok], top2
+
+
+def aggregate_pick(rows, relevance, gamma, beta, rule):
+    """The MoE / PoE aggregation variants with scalar loops (same reading as
+    pced_oracle.aggregate_query): weights w_k proportional to clip(r_k)^gamma,
+    distributions softmax((1 + beta_k) s_k - beta_k s_0); MoE score
+    log sum_k w_k p_k(v), PoE score sum_k w_k log p_k(v).
+    Returns (token, expert, best score, second-best score)."""
+    s0 = rows[0]
+    V, N = len(s0), len(rows) - 1
+    raw = [min(max(r, 1e-8), 1.0 - 1e-8) ** gamma for r in relevance]
+    w = [x / sum(raw) for x in raw]
+    probs = []
+    for k in range(1, N + 1):
+        c = [(1.0 + beta[k - 1]) * rows[k][v] - beta[k - 1] * s0[v] for v in range(V)]
+        m = max(c)
+        e = [math.exp(x - m) for x in c]
+        tot = sum(e)
+        probs.append([x / tot for x in e])
+    score = []
+    for v in range(V):
+        if rule == "moe":
+            score.append(math.log(sum(w[k] * probs[k][v] for k in range(N))))
+        else:
+            score.append(sum(w[k] * math.log(probs[k][v]) for k in range(N)))
+    best = max(score)
+    token = score.index(best)
+    contrib = [w[k] * probs[k][token] for k in range(N)]
+    expert = contrib.index(max(contrib)) + 1
+    second = max([score[v] for v in range(V) if v != token], default=-math.inf)
+    return token, expert, best, second

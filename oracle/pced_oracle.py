@@ -155,10 +155,13 @@ def jsd_bits(p: np.ndarray, q: np.ndarray) -> float:
     return 0.5 * kl(p) + 0.5 * kl(q)
 
 
-def dynamic_beta(logits_query: np.ndarray) -> np.ndarray:
-    """beta_k = JSD(softmax s_k, softmax s_0) for k = 1..N (one query's rows, amateur first)."""
+def dynamic_beta(logits_query: np.ndarray, scalar: bool = False) -> np.ndarray:
+    """beta_k = JSD(softmax s_k, softmax s_0) for k = 1..N (one query's rows, amateur first).
+    ``scalar``: one beta for the query, the mean of those divergences (the paper's
+    beta_0 read as a single number), repeated for every expert."""
     p0 = softmax(logits_query[0])
-    return np.array([jsd_bits(softmax(logits_query[k]), p0) for k in range(1, logits_query.shape[0])])
+    b = np.array([jsd_bits(softmax(logits_query[k]), p0) for k in range(1, logits_query.shape[0])])
+    return np.full_like(b, b.mean()) if scalar else b
 
 
 # ----------------------------------------------------------------- Eq. 2 / 3
@@ -216,9 +219,58 @@ def select(scores: np.ndarray) -> Selection:
     return Selection(token, winner, float(top1), top2)
 
 
+# ------------------------------------------- aggregation rules (Appendix C.4)
+# The ablation compares Max with a mixture (weighted sum) and a product
+# (weighted product) of the experts' distributions, weights from the retrieval
+# scores, without formulas. Reading used here: each expert's distribution is
+# the softmax of its contrastive logits c_k = (1 + beta_k) s_k - beta_k s_0
+# (Eq. 2 without the prior), and the weights are pi_k = r_k^gamma / sum_j r_j^gamma
+# (so log pi_k is Eq. 2's prior gamma log r_k up to a constant). Scores are
+# reported in log units:
+#     MoE: log sum_k pi_k softmax(c_k)(v)        PoE: sum_k pi_k log softmax(c_k)(v)
+# The token is the argmax (lowest token on ties); the reported expert is the one
+# with the largest weighted probability pi_k softmax(c_k)(y) (lowest k on ties).
+
+def expert_weights(relevance: np.ndarray, gamma: float) -> np.ndarray:
+    """pi_k = r_k^gamma / sum_j r_j^gamma over one query's clipped relevance."""
+    return softmax(prior_term(relevance, gamma))
+
+
+def log_softmax(c: np.ndarray) -> np.ndarray:
+    m = c.max(axis=-1, keepdims=True)
+    return c - (m + np.log(np.sum(np.exp(c - m), axis=-1, keepdims=True)))
+
+
+def aggregate_query(logits_query: np.ndarray, relevance: np.ndarray, gamma: float, beta: np.ndarray,
+                    rule: str) -> Selection:
+    """MoE or PoE aggregation and selection for one query (rows: amateur, experts)."""
+    s = np.asarray(logits_query, dtype=np.float64)
+    b = np.asarray(beta, dtype=np.float64)[:, None]
+    c = (1.0 + b) * s[1:] - b * s[0][None, :]            # contrastive logits [N, V]
+    logp = log_softmax(c)
+    logw = np.log(expert_weights(relevance, gamma))[:, None]
+    joint = logw + logp                                  # log(pi_k p_k(v))
+    if rule == "moe":
+        m = joint.max(axis=0)
+        score = m + np.log(np.sum(np.exp(joint - m[None, :]), axis=0))
+    elif rule == "poe":
+        score = np.sum(np.exp(logw) * logp, axis=0)
+    else:
+        raise ValueError(rule)
+    top1 = score.max()
+    token = int(np.flatnonzero(score == top1)[0])
+    col = joint[:, token]
+    winner = int(np.flatnonzero(col == col.max())[0]) + 1
+    others = np.delete(score, token)
+    return Selection(token, winner, float(top1), float(others.max()) if others.size else -math.inf)
+
+
 def fuse_query(logits_query: np.ndarray, relevance: np.ndarray, gamma: float,
-               beta: np.ndarray, precision=np.float64) -> Selection:
-    """Eq. 2 then Eq. 3 for one query (rows: amateur, expert 1..N)."""
+               beta: np.ndarray, precision=np.float64, rule: str = "max") -> Selection:
+    """Eq. 2 then Eq. 3 for one query (rows: amateur, expert 1..N); ``rule``
+    "moe" / "poe" select by the aggregation variants instead."""
+    if rule != "max":
+        return aggregate_query(logits_query, relevance, gamma, beta, rule)
     prior = prior_term(relevance, gamma)
     if precision is np.float32:
         prior = prior.astype(np.float32)
@@ -254,7 +306,8 @@ class Oracle:
 
     def __init__(self, *, n_layers, n_q_heads, n_kv_heads, head_dim, vocab, dtype,
                  n_experts: Sequence[int], cache_k: Callable, cache_v: Callable,
-                 relevance, gamma: float = 2.5, beta=None, norm: str = "rms"):
+                 relevance, gamma: float = 2.5, beta=None, norm: str = "rms", aggregation: str = "max",
+                 beta_scalar: bool = False):
         self.L, self.Hq, self.Hkv, self.D, self.V = n_layers, n_q_heads, n_kv_heads, head_dim, vocab
         self.dtype = dtype
         self.n_experts = list(n_experts)
@@ -266,6 +319,8 @@ class Oracle:
         self.fixed_beta = None if beta is None else np.asarray(beta, dtype=np.float64)
         self.frozen_beta = None
         self.norm = norm
+        self.aggregation = aggregation
+        self.beta_scalar = bool(beta_scalar)
         self.appended_k = [[[] for _ in range(self.L)] for _ in range(self.S)]
         self.appended_v = [[[] for _ in range(self.L)] for _ in range(self.S)]
         self.t = 0
@@ -313,14 +368,15 @@ class Oracle:
         else:
             if self.frozen_beta is None:
                 self.frozen_beta = np.concatenate([
-                    dynamic_beta(logits[self.seq_off[b]:self.seq_off[b + 1]])
+                    dynamic_beta(logits[self.seq_off[b]:self.seq_off[b + 1]], self.beta_scalar)
                     for b in range(len(self.n_experts))])
             beta = self.frozen_beta
         sels = []
         e0 = 0
         for b, n in enumerate(self.n_experts):
             rows = logits[self.seq_off[b]:self.seq_off[b + 1]]
-            sels.append(fuse_query(rows, self.relevance[e0:e0 + n], self.gamma, beta[e0:e0 + n]))
+            sels.append(fuse_query(rows, self.relevance[e0:e0 + n], self.gamma, beta[e0:e0 + n],
+                                   rule=self.aggregation))
             e0 += n
         self.t += 1
         return StepResult(

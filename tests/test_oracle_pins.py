@@ -531,3 +531,98 @@ def test_harmonic_mean_fusion():
     # equal inputs give (almost) that value; retrieval alone without a reranker
     assert np.allclose(O.fuse_relevance(a, a), a, atol=1e-7)
     assert np.array_equal(O.relevance([0.2, -0.4], "dense"), O.normalise_retrieval([0.2, -0.4], "dense"))
+
+
+# ------------------------------------------------- aggregation variants (NEXT-2)
+# MoE / PoE (Appendix C.4, read as in pced_oracle.aggregate_query), pinned by
+# reductions to the Max rule and to single distributions, by invariants of
+# mixtures and products of distributions, and by a scalar-loop brute force.
+
+def _rand_query(rng, N, V, scale=3.0):
+    rows = rng.normal(0, scale, (N + 1, V))
+    return rows, rng.random(N), rng.random(N)
+
+
+@pytest.mark.parametrize("rule", ["moe", "poe"])
+def test_aggregation_with_one_expert_is_the_max_rule(rule):
+    rng = np.random.default_rng(21)
+    for _ in range(5):
+        rows, rel, beta = _rand_query(rng, 1, 97)
+        sel = O.aggregate_query(rows, rel, 2.5, beta, rule)
+        ref = O.fuse_query(rows, rel, 2.5, beta)
+        assert sel.token == ref.token and sel.winner == 1
+        c = (1 + beta[0]) * rows[1] - beta[0] * rows[0]
+        assert abs(sel.top1 - O.log_softmax(c)[sel.token]) < 1e-12
+
+
+@pytest.mark.parametrize("rule", ["moe", "poe"])
+def test_identical_experts_reduce_to_one_distribution(rule):
+    rng = np.random.default_rng(22)
+    rows, rel, _ = _rand_query(rng, 4, 80)
+    rows[2:] = rows[1]
+    beta = np.full(4, 0.4)
+    sel = O.aggregate_query(rows, rel, 2.5, beta, rule)
+    c = 1.4 * rows[1] - 0.4 * rows[0]
+    assert sel.token == int(np.argmax(c))
+    assert abs(sel.top1 - O.log_softmax(c).max()) < 1e-12
+
+
+def test_mixture_is_a_distribution_and_product_is_below_it():
+    rng = np.random.default_rng(23)
+    rows, rel, beta = _rand_query(rng, 6, 50)
+    s = rows
+    c = (1 + beta[:, None]) * s[1:] - beta[:, None] * s[0][None, :]
+    lp = O.log_softmax(c)
+    w = O.expert_weights(rel, 2.5)
+    assert abs(w.sum() - 1.0) < 1e-15
+    moe = np.log(np.sum(w[:, None] * np.exp(lp), axis=0))
+    poe = np.sum(w[:, None] * lp, axis=0)
+    assert abs(np.exp(moe).sum() - 1.0) < 1e-12           # a mixture of distributions sums to 1
+    assert np.all(poe <= moe + 1e-12)                        # weighted AM-GM
+    assert O.aggregate_query(rows, rel, 2.5, beta, "moe").top1 == pytest.approx(moe.max(), abs=1e-12)
+    assert O.aggregate_query(rows, rel, 2.5, beta, "poe").top1 == pytest.approx(poe.max(), abs=1e-12)
+
+
+def test_weights_follow_the_prior_and_a_dominant_expert_decides():
+    rel = np.array([0.2, 0.8, 0.4])
+    w = O.expert_weights(rel, 2.0)
+    assert np.allclose(w, rel ** 2 / np.sum(rel ** 2), rtol=1e-14)
+    assert np.allclose(O.expert_weights(rel, 0.0), 1.0 / 3.0)
+    rng = np.random.default_rng(24)
+    rows, _, _ = _rand_query(rng, 3, 64)
+    rel = np.array([0.01, 1.0, 0.01])
+    for rule in ("moe", "poe"):
+        sel = O.aggregate_query(rows, rel, 60.0, np.zeros(3), rule)
+        assert sel.token == int(np.argmax(rows[2])) and sel.winner == 2
+
+
+@pytest.mark.parametrize("rule", ["moe", "poe"])
+def test_aggregation_permutation_invariant(rule):
+    rng = np.random.default_rng(25)
+    rows, rel, beta = _rand_query(rng, 5, 70)
+    perm = rng.permutation(5)
+    a = O.aggregate_query(rows, rel, 2.5, beta, rule)
+    b = O.aggregate_query(np.concatenate([rows[:1], rows[1:][perm]]), rel[perm], 2.5, beta[perm], rule)
+    assert a.token == b.token and perm[b.winner - 1] + 1 == a.winner
+    assert abs(a.top1 - b.top1) < 1e-12
+
+
+@pytest.mark.parametrize("rule", ["moe", "poe"])
+@pytest.mark.parametrize("N,V", [(1, 5), (2, 7), (5, 13)])
+def test_aggregation_brute_force_agrees(rule, N, V):
+    rng = np.random.default_rng(26 + N)
+    rows, rel, beta = _rand_query(rng, N, V)
+    tok, exp_k, top1, top2 = brute.aggregate_pick(rows.tolist(), rel.tolist(), 1.7, beta.tolist(), rule)
+    sel = O.aggregate_query(rows, rel, 1.7, beta, rule)
+    assert (sel.token, sel.winner) == (tok, exp_k)
+    assert abs(sel.top1 - top1) < 1e-12 and abs(sel.top2 - top2) < 1e-12
+
+
+def test_scalar_beta_is_the_mean_of_the_divergences():
+    rng = np.random.default_rng(27)
+    rows, _, _ = _rand_query(rng, 4, 40, scale=1.0)
+    per = O.dynamic_beta(rows)
+    sc = O.dynamic_beta(rows, scalar=True)
+    assert np.allclose(sc, per.mean()) and sc.shape == per.shape
+    one = rows[:2]
+    assert np.array_equal(O.dynamic_beta(one, scalar=True), O.dynamic_beta(one))
