@@ -63,6 +63,12 @@ typedef enum pced_dtype {
   PCED_BF16 = 1   /* bfloat16 storage (raw 16-bit patterns)   */
 } pced_dtype;
 
+typedef enum pced_aggregation {
+  PCED_AGG_MAX = 0,  /* Eq. 3: y = argmax_v max_k s_hat_k(v) (the method)                        */
+  PCED_AGG_MOE = 1,  /* mixture: argmax_v log sum_k pi_k softmax(c_k)(v)  (Appendix C.4 ablation) */
+  PCED_AGG_POE = 2   /* product: argmax_v sum_k pi_k log softmax(c_k)(v)  (Appendix C.4 ablation) */
+} pced_aggregation;
+
 typedef enum pced_norm {
   PCED_NORM_NONE = 0,  /* logits = x W^T                               */
   PCED_NORM_RMS = 1    /* logits = x W^T / sqrt(mean(x^2) + 1e-5) per row */
@@ -90,6 +96,17 @@ typedef struct pced_config {
                                 GPU at once. A smaller cap leaves compute units
                                 to other work; each chunk then streams more
                                 pages and may span more sequences            */
+  int32_t aggregation;       /* pced_aggregation. For MoE / PoE (the paper
+                                compares them with Max in Appendix C.4 without
+                                formulas; reading): c_k = (1 + beta_k) s_k -
+                                beta_k s_0, pi_k = r_k^gamma / sum_j r_j^gamma
+                                over the query's clipped r; scores (top1, top2)
+                                in log units; the reported expert maximises
+                                pi_k softmax(c_k)(y)                            */
+  int32_t beta_scalar;       /* dynamic beta only: 0 = one beta per expert
+                                (beta_k = JSD(p_k || p_0)); 1 = one beta per
+                                query, the mean of those divergences (the
+                                paper's beta_0 read as a single number)       */
 } pced_config;
 
 typedef struct pced_ctx pced_ctx;

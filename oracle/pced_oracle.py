@@ -241,9 +241,10 @@ def log_softmax(c: np.ndarray) -> np.ndarray:
     return c - (m + np.log(np.sum(np.exp(c - m), axis=-1, keepdims=True)))
 
 
-def aggregate_query(logits_query: np.ndarray, relevance: np.ndarray, gamma: float, beta: np.ndarray,
-                    rule: str) -> Selection:
-    """MoE or PoE aggregation and selection for one query (rows: amateur, experts)."""
+def aggregate_scores(logits_query: np.ndarray, relevance: np.ndarray, gamma: float, beta: np.ndarray,
+                     rule: str):
+    """MoE or PoE score of every token [V] and log(pi_k p_k(v)) [N, V] for one
+    query (rows: amateur, experts)."""
     s = np.asarray(logits_query, dtype=np.float64)
     b = np.asarray(beta, dtype=np.float64)[:, None]
     c = (1.0 + b) * s[1:] - b * s[0][None, :]            # contrastive logits [N, V]
@@ -257,6 +258,13 @@ def aggregate_query(logits_query: np.ndarray, relevance: np.ndarray, gamma: floa
         score = np.sum(np.exp(logw) * logp, axis=0)
     else:
         raise ValueError(rule)
+    return score, joint
+
+
+def aggregate_query(logits_query: np.ndarray, relevance: np.ndarray, gamma: float, beta: np.ndarray,
+                    rule: str) -> Selection:
+    """MoE or PoE aggregation and selection for one query (rows: amateur, experts)."""
+    score, joint = aggregate_scores(logits_query, relevance, gamma, beta, rule)
     top1 = score.max()
     token = int(np.flatnonzero(score == top1)[0])
     col = joint[:, token]

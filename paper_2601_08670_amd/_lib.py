@@ -33,7 +33,8 @@ class PcedError(RuntimeError):
 class pced_config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_layers", "n_q_heads", "n_kv_heads", "head_dim", "hidden", "vocab", "dtype", "page_size",
-        "max_queries", "max_seqs", "max_pages", "max_pages_per_seq", "norm", "max_attn_chunks")]
+        "max_queries", "max_seqs", "max_pages", "max_pages_per_seq", "norm", "max_attn_chunks",
+        "aggregation", "beta_scalar")]
 
 
 class pced_step_out(ctypes.Structure):
@@ -96,13 +97,15 @@ def _check(status: int):
 
 
 def make_config(*, n_layers, n_q_heads, n_kv_heads, head_dim, vocab, dtype, max_queries, max_seqs,
-                max_pages, max_pages_per_seq, norm="rms", hidden=None, max_attn_chunks=0) -> pced_config:
+                max_pages, max_pages_per_seq, norm="rms", hidden=None, max_attn_chunks=0, aggregation="max",
+                beta_scalar=False) -> pced_config:
     return pced_config(
         n_layers=n_layers, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads, head_dim=head_dim,
         hidden=hidden if hidden is not None else n_q_heads * head_dim, vocab=vocab,
         dtype=PCED_BF16 if dtype == "bf16" else PCED_F32, page_size=16, max_queries=max_queries,
         max_seqs=max_seqs, max_pages=max_pages, max_pages_per_seq=max_pages_per_seq,
-        norm=PCED_NORM_RMS if norm == "rms" else PCED_NORM_NONE, max_attn_chunks=max_attn_chunks)
+        norm=PCED_NORM_RMS if norm == "rms" else PCED_NORM_NONE, max_attn_chunks=max_attn_chunks,
+        aggregation=AGGREGATIONS[aggregation], beta_scalar=int(bool(beta_scalar)))
 
 
 def pced_pool_bytes(cfg: pced_config) -> int:
@@ -123,6 +126,7 @@ def pced_pack_lm_head(cfg: pced_config, w, w_packed, stream=None):
 
 
 SCORE_MODES = {"dense": 0, "colbert": 1, "sparse": 2}
+AGGREGATIONS = {"max": 0, "moe": 1, "poe": 2}
 
 
 def pced_relevance(mode: str, retrieval, reranker_logits=None):

@@ -60,16 +60,19 @@ bool cfg_valid(const pced_config* c, std::string* why) {
   if (c->max_pages < 1 || c->max_pages_per_seq < 1) return bad("max_pages and max_pages_per_seq must be >= 1");
   if (c->norm != PCED_NORM_NONE && c->norm != PCED_NORM_RMS) return bad("unknown norm");
   if (c->max_attn_chunks < 0) return bad("max_attn_chunks must be >= 0");
+  if (c->aggregation != PCED_AGG_MAX && c->aggregation != PCED_AGG_MOE && c->aggregation != PCED_AGG_POE)
+    return bad("unknown aggregation");
+  if (c->beta_scalar != 0 && c->beta_scalar != 1) return bad("beta_scalar must be 0 or 1");
   // 32-bit index guards used by the kernels
   if ((double)c->max_seqs * c->vocab > 2147483647.0) return bad("max_seqs * vocab exceeds 2^31");
   return true;
 }
 
 struct Layout {
-  size_t len0, page_table, seq_query, query_seq0, query_exp0, exp_seq, exp_query, prior, beta_fixed,
+  size_t len0, page_table, seq_query, query_seq0, query_exp0, exp_seq, exp_query, prior, logw, beta_fixed,
       load_items, src_k, src_v, meta_end;
   size_t chunk_info, seg, nparts, work_pages, tick_fuse, tick_beta, prev_tok, beta, part_acc, part_ml, x, logits,
-      fuse_part, lse_part, jsd_part, syn_q, syn_k, syn_v, total;
+      fuse_part, lse_part, jsd_part, agg_lse, syn_q, syn_k, syn_v, total;
   int rows_pad, nblk_fuse, nchunk, max_work;
   size_t part_slots;
 };
@@ -93,6 +96,7 @@ Layout make_layout(const pced_config& c) {
   L.exp_seq = take(S * 4);
   L.exp_query = take(S * 4);
   L.prior = take(S * 4);
+  L.logw = take(S * 4);
   L.beta_fixed = take(S * 4);
   L.load_items = take((size_t)c.max_pages * 2 * 4);
   L.src_k = take(S * 8);
@@ -116,6 +120,7 @@ Layout make_layout(const pced_config& c) {
   L.fuse_part = take(B * (size_t)ceil_div(c.vocab, 128) * 5 * 4);
   L.lse_part = take(S * L.nchunk * 2 * 4);
   L.jsd_part = take(S * L.nchunk * 4);
+  L.agg_lse = take(S * 4);
   L.syn_q = take(S * c.n_layers * c.n_q_heads * c.head_dim * es);
   L.syn_k = take(S * c.n_layers * c.n_kv_heads * c.head_dim * es);
   L.syn_v = take(S * c.n_layers * c.n_kv_heads * c.head_dim * es);
@@ -302,11 +307,39 @@ pced_status run_fuse(pced_ctx* c, const float* logits, bool refresh_beta, int32_
     b.beta = c->at<float>(c->lay.beta);
     b.V = cfg.vocab;
     b.nchunk = c->lay.nchunk;
+    b.query_exp0 = c->at<int32_t>(c->lay.query_exp0);
     ProfScope ps(c, PCED_PROF_BETA, (double)(c->S + 2.0 * c->NE) * cfg.vocab * 4, 0);
     HIP_OK(launch_beta(b, c->S, c->NE, st, ps.timing()));
+    if (cfg.beta_scalar) HIP_OK(launch_beta_mean(b, c->B, st));
     c->beta_frozen = true;
   }
   FuseArgs f = fuse_args(c, logits, tokens_out, tok_stride, extra, c->lay.nblk_fuse);
+  if (cfg.aggregation != PCED_AGG_MAX) {
+    AggArgs g{};
+    g.logits = logits;
+    g.query_seq0 = f.query_seq0;
+    g.query_exp0 = f.query_exp0;
+    g.exp_seq = c->at<int32_t>(c->lay.exp_seq);
+    g.exp_query = c->at<int32_t>(c->lay.exp_query);
+    g.beta = f.beta;
+    g.logw = c->at<float>(c->lay.logw);
+    g.lse_part = c->at<float>(c->lay.lse_part);
+    g.lse = c->at<float>(c->lay.agg_lse);
+    g.part = f.part;
+    g.V = cfg.vocab;
+    g.nchunk = c->lay.nchunk;
+    g.nblk = c->lay.nblk_fuse;
+    g.product = cfg.aggregation == PCED_AGG_POE;
+    {
+      ProfScope ps(c, PCED_PROF_FUSE, 2.0 * (c->NE + c->S) * cfg.vocab * 4, 0);
+      HIP_OK(launch_agg(g, c->NE, c->B, st, ps.timing()));
+    }
+    {
+      ProfScope ps(c, PCED_PROF_FUSE, (double)c->B * f.nblk * 5 * 4, 0);
+      HIP_OK(launch_fuse_final(f, c->B, st, ps.timing()));
+    }
+    return copy_beta_used(c, extra, st);
+  }
   {
     ProfScope ps(c, PCED_PROF_FUSE, (double)c->S * cfg.vocab * 4, 0);
     HIP_OK(launch_fuse(f, c->B, st, ps.timing()));
@@ -442,7 +475,8 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
   // (fixed, or frozen after the first step) and the caller wants no logits;
   // otherwise the logits are materialised (dynamic beta needs them at the first step)
   const bool refresh = c->dynamic_beta && !c->beta_frozen;
-  const int fused_nblk = (c->bf16 && !refresh && !(extra && extra->logits)) ? lmhead_fused_nblk(c->S, cfg.vocab) : 0;
+  const int fused_nblk = (c->bf16 && !refresh && !(extra && extra->logits) && cfg.aggregation == PCED_AGG_MAX)
+                             ? lmhead_fused_nblk(c->S, cfg.vocab) : 0;
   pced_status r;
   if (fused_nblk > 0) {
     r = run_lmhead(c, at.x_out, c->S, w, nullptr, st, fused_nblk);
@@ -606,7 +640,7 @@ pced_status pced_load_caches(pced_ctx* c, int32_t n_queries, const int32_t* n_ex
   put(L.len0, cache_len, S * 4);
   put(L.page_table, pt.data(), pt.size() * 4);
   std::vector<int32_t> seq_query(S), exp_seq(NE), exp_query(NE);
-  std::vector<float> prior(NE), bfix(NE, 0.f);
+  std::vector<float> prior(NE), logw(NE), bfix(NE, 0.f);
   std::vector<int32_t> items;
   for (int b = 0; b < n_queries; ++b) {
     for (int k = 0; k <= n_experts[b]; ++k) seq_query[c->seq_off[b] + k] = b;
@@ -619,6 +653,22 @@ pced_status pced_load_caches(pced_ctx* c, int32_t n_queries, const int32_t* n_ex
       prior[e] = (float)((double)gamma * std::log(rr));
       if (beta) bfix[e] = beta[e];
     }
+    // MoE / PoE weights: log pi_k = gamma ln r_k - log sum_j exp(gamma ln r_j) over the query, in double
+    double mx = -INFINITY;
+    for (int k = 1; k <= n_experts[b]; ++k) {
+      const double rr = std::min(std::max((double)relevance[c->exp_off[b] + k - 1], 1e-8), 1.0 - 1e-8);
+      mx = std::max(mx, (double)gamma * std::log(rr));
+    }
+    double z = 0.0;
+    for (int k = 1; k <= n_experts[b]; ++k) {
+      const double rr = std::min(std::max((double)relevance[c->exp_off[b] + k - 1], 1e-8), 1.0 - 1e-8);
+      z += std::exp((double)gamma * std::log(rr) - mx);
+    }
+    for (int k = 1; k <= n_experts[b]; ++k) {
+      const int e = c->exp_off[b] + k - 1;
+      const double rr = std::min(std::max((double)relevance[e], 1e-8), 1.0 - 1e-8);
+      logw[e] = (float)((double)gamma * std::log(rr) - mx - std::log(z));
+    }
   }
   for (long s = 0; s < S; ++s)
     for (int p = 0; p < ceil_div(cache_len[s], kPage); ++p) { items.push_back((int32_t)s); items.push_back(p); }
@@ -628,6 +678,7 @@ pced_status pced_load_caches(pced_ctx* c, int32_t n_queries, const int32_t* n_ex
   put(L.exp_seq, exp_seq.data(), NE * 4);
   put(L.exp_query, exp_query.data(), NE * 4);
   put(L.prior, prior.data(), NE * 4);
+  put(L.logw, logw.data(), NE * 4);
   put(L.beta_fixed, bfix.data(), NE * 4);
   put(L.load_items, items.data(), items.size() * 4);
   std::vector<uint64_t> sk(S), sv(S);

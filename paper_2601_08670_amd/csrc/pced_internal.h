@@ -104,6 +104,23 @@ struct FuseArgs {
   int V, nblk, tok_stride;
 };
 
+// MoE / PoE aggregation (the alternatives to Eq. 3's max): per-expert
+// log-sum-exp of the contrastive logits c_k = (1 + beta_k) s_k - beta_k s_0,
+// then per vocabulary slice the aggregated score and its best two tokens.
+struct AggArgs {
+  const float* logits;      // [S][V]
+  const int32_t* query_seq0;// [B+1]
+  const int32_t* query_exp0;// [B+1]
+  const int32_t* exp_seq;   // [sum N]
+  const int32_t* exp_query; // [sum N]
+  const float* beta;        // [sum N]
+  const float* logw;        // [sum N] log pi_k, pi_k = r_k^gamma / sum_j r_j^gamma within the query
+  float* lse_part;          // [sum N][nchunk][2]
+  float* lse;               // [sum N]
+  float* part;              // [B][nblk][5] slice candidates for k_fuse_final
+  int V, nchunk, nblk, product;  // product: 0 = mixture (MoE), 1 = product (PoE)
+};
+
 struct BetaArgs {
   const float* logits;      // [S][V]
   const int32_t* query_seq0;
@@ -113,6 +130,7 @@ struct BetaArgs {
   float* jsd_part;          // [sum N][nchunk]
   int32_t* tickets;         // [sum N]
   float* beta;              // [sum N]
+  const int32_t* query_exp0;// [B+1] (scalar mode)
   int V, nchunk;
 };
 
@@ -145,6 +163,8 @@ hipError_t launch_pack_lm_head(const void* w, void* wp, int V, int K, bool bf16,
 hipError_t launch_lmhead(const LmArgs& a, bool bf16, hipStream_t st, const Timing* tm = nullptr);
 hipError_t launch_beta(const BetaArgs& a, int n_seqs, int n_exp, hipStream_t st, const Timing* tm = nullptr);
 hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st, const Timing* tm = nullptr);
+hipError_t launch_beta_mean(const BetaArgs& a, int n_queries, hipStream_t st);
+hipError_t launch_agg(const AggArgs& a, int n_exp, int n_queries, hipStream_t st, const Timing* tm = nullptr);
 // the final per-query merge alone (after an LM head with the fused epilogue)
 hipError_t launch_fuse_final(const FuseArgs& a, int n_queries, hipStream_t st, const Timing* tm = nullptr);
 // vocabulary slices (blocks) of the fused LM-head epilogue for M rows, or 0 if M rows cannot be fused

@@ -1237,6 +1237,102 @@ __global__ __launch_bounds__(256) void k_beta_final(BetaArgs a, int n_exp) {
   a.beta[e] = tot / 0.69314718055994530942f;
 }
 
+// Scalar beta (one per query): the mean of the query's per-expert divergences,
+// summed in expert order, written back to every expert of the query.
+__global__ __launch_bounds__(64) void k_beta_mean(BetaArgs a) {
+  const int b = blockIdx.x;
+  const int e0 = a.query_exp0[b], e1 = a.query_exp0[b + 1];
+  if (threadIdx.x == 0) {
+    float tot = 0.f;
+    for (int e = e0; e < e1; ++e) tot += a.beta[e];
+    const float m = tot / (float)(e1 - e0);
+    for (int e = e0; e < e1; ++e) a.beta[e] = m;
+  }
+}
+
+// ------------------------------------------------ MoE / PoE aggregation
+
+// Per (expert, vocabulary chunk): max and sum of exp(c - max) of the contrastive
+// logits c = (1 + beta) s_k - beta s_0 (Eq. 2's order, no contraction).
+__global__ __launch_bounds__(256) void k_agg_lse(AggArgs a) {
+#pragma clang fp contract(off)
+  const int e = blockIdx.y, ch = blockIdx.x;
+  const float* rk = a.logits + (size_t)a.exp_seq[e] * a.V;
+  const float* r0 = a.logits + (size_t)a.query_seq0[a.exp_query[e]] * a.V;
+  const float beta = a.beta[e], coef = 1.0f + beta;
+  const int v0 = ch * kBetaChunk, v1 = min(a.V, v0 + kBetaChunk);
+  auto cval = [&](int v) { const float t1 = coef * rk[v]; const float t2 = beta * r0[v]; return t1 - t2; };
+  float m = kNegInf;
+  for (int v = v0 + threadIdx.x; v < v1; v += blockDim.x) m = fmaxf(m, cval(v));
+  m = block_reduce_max(m);
+  float sum = 0.f;
+  for (int v = v0 + threadIdx.x; v < v1; v += blockDim.x) sum += expf(cval(v) - m);
+  sum = block_reduce_sum(sum);
+  if (threadIdx.x == 0) {
+    a.lse_part[((size_t)e * a.nchunk + ch) * 2] = m;
+    a.lse_part[((size_t)e * a.nchunk + ch) * 2 + 1] = sum;
+  }
+}
+
+// lse_k from the chunk partials, in chunk order.
+__global__ __launch_bounds__(256) void k_agg_lse_final(AggArgs a, int n_exp) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= n_exp) return;
+  const float* p = a.lse_part + (size_t)e * a.nchunk * 2;
+  float m = kNegInf;
+  for (int c = 0; c < a.nchunk; ++c) m = fmaxf(m, p[2 * c]);
+  float sum = 0.f;
+  for (int c = 0; c < a.nchunk; ++c) sum += p[2 * c + 1] * expf(p[2 * c] - m);
+  a.lse[e] = m + logf(sum);
+}
+
+// One block per (query, 256-token slice): per token v the experts' weighted
+// log-probabilities j_k = log pi_k + c_k(v) - lse_k, then
+//   MoE: log sum_k exp(j_k)  (running max and rescaled sum, expert order)
+//   PoE: sum_k pi_k (c_k(v) - lse_k)
+// and the expert with the largest j_k (lowest k on ties); the block's best two
+// tokens go to the same partial buffer k_fuse_final merges.
+__global__ __launch_bounds__(kFuseBlock) void k_agg(AggArgs a) {
+#pragma clang fp contract(off)
+  const int b = blockIdx.y;
+  const int s0 = a.query_seq0[b];
+  const int N = a.query_seq0[b + 1] - s0 - 1;
+  const int e0 = a.query_exp0[b];
+  const int v = blockIdx.x * kFuseBlock + threadIdx.x;
+  Top2 c{kNegInf, 0x7FFFFFFF, 0, kNegInf, 0x7FFFFFFF};
+  if (v < a.V) {
+    const float sa = a.logits[(size_t)s0 * a.V + v];
+    float m = kNegInf, sum = 0.f, prod = 0.f, jbest = kNegInf;
+    int bk = 0;
+    for (int k = 1; k <= N; ++k) {
+      const int e = e0 + k - 1;
+      const float beta = a.beta[e], coef = 1.0f + beta;
+      const float t1 = coef * a.logits[(size_t)(s0 + k) * a.V + v];
+      const float t2 = beta * sa;
+      const float lp = (t1 - t2) - a.lse[e];
+      const float j = a.logw[e] + lp;
+      if (j > jbest) { jbest = j; bk = k; }
+      if (a.product) {
+        prod += expf(a.logw[e]) * lp;
+      } else if (j > m) {
+        sum = sum * expf(m - j) + 1.0f;
+        m = j;
+      } else {
+        sum += expf(j - m);
+      }
+    }
+    c.v1 = a.product ? prod : m + logf(sum);
+    c.i1 = v;
+    c.k1 = bk;
+  }
+  c = block_top2<kFuseBlock / 64>(c);
+  if (threadIdx.x == 0) {
+    float* p = a.part + ((size_t)b * a.nblk + blockIdx.x) * 5;
+    p[0] = c.v1; p[1] = __int_as_float(c.i1); p[2] = __int_as_float(c.k1);
+    p[3] = c.v2; p[4] = __int_as_float(c.i2);
+  }
+}
+
 // --------------------------------------------------- generation input synth
 
 __device__ __forceinline__ uint64_t mix64(uint64_t z) {
@@ -1403,6 +1499,18 @@ hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st, const T
   hipError_t e = go(k_fuse, dim3(a.nblk, n_queries), dim3(kFuseBlock), 0, st, t0(tm), nullptr, a);
   if (e != hipSuccess) return e;
   return go(k_fuse_final, dim3(n_queries), dim3(kFuseBlock), 0, st, nullptr, t1(tm), a);
+}
+
+hipError_t launch_beta_mean(const BetaArgs& a, int n_queries, hipStream_t st) {
+  return go(k_beta_mean, dim3(n_queries), dim3(64), 0, st, nullptr, nullptr, a);
+}
+
+hipError_t launch_agg(const AggArgs& a, int n_exp, int n_queries, hipStream_t st, const Timing* tm) {
+  hipError_t e = go(k_agg_lse, dim3(a.nchunk, n_exp), dim3(256), 0, st, t0(tm), nullptr, a);
+  if (e != hipSuccess) return e;
+  e = go(k_agg_lse_final, dim3((n_exp + 255) / 256), dim3(256), 0, st, nullptr, nullptr, a, n_exp);
+  if (e != hipSuccess) return e;
+  return go(k_agg, dim3(a.nblk, n_queries), dim3(kFuseBlock), 0, st, nullptr, t1(tm), a);
 }
 
 hipError_t launch_fuse_final(const FuseArgs& a, int n_queries, hipStream_t st, const Timing* tm) {

@@ -22,7 +22,7 @@ class PcedSession:
 
     def __init__(self, *, n_layers, n_q_heads, n_kv_heads, head_dim, vocab, dtype, max_queries,
                  max_seqs, max_pages, max_pages_per_seq, norm="rms", device="cuda", poison=False,
-                 max_attn_chunks=0):
+                 max_attn_chunks=0, aggregation="max", beta_scalar=False):
         torch = _torch()
         self.dtype = dtype
         self.device = device
@@ -32,7 +32,8 @@ class PcedSession:
                                     head_dim=head_dim, vocab=vocab, dtype=dtype, max_queries=max_queries,
                                     max_seqs=max_seqs, max_pages=max_pages,
                                     max_pages_per_seq=max_pages_per_seq, norm=norm,
-                                    max_attn_chunks=max_attn_chunks)
+                                    max_attn_chunks=max_attn_chunks, aggregation=aggregation,
+                                    beta_scalar=beta_scalar)
         self.ctx = _lib.Context(self.cfg, device=device)
         pool = _lib.pced_pool_bytes(self.cfg)
         self.k_pool = torch.empty(pool, dtype=torch.uint8, device=device)
@@ -102,7 +103,8 @@ class PcedSession:
 
 
 def session_for_workload(wl, device="cuda", extra_tokens: Optional[int] = None, norm="rms",
-                         load_now=True, max_queries=None, poison=False, max_attn_chunks=0):
+                         load_now=True, max_queries=None, poison=False, max_attn_chunks=0, aggregation="max",
+                         beta_scalar=False):
     """Build a session sized for a synthetic workload (duck-typed: any object with
     the attributes of ``pced_inputs.workloads.Workload``) and load its caches,
     materialised on ``device``."""
@@ -114,7 +116,8 @@ def session_for_workload(wl, device="cuda", extra_tokens: Optional[int] = None, 
                        head_dim=g.head_dim, vocab=g.vocab, dtype=g.dtype,
                        max_queries=max_queries or wl.n_queries, max_seqs=wl.n_seqs,
                        max_pages=int(need.sum()), max_pages_per_seq=maxpps, norm=norm, device=device,
-                       poison=poison, max_attn_chunks=max_attn_chunks)
+                       poison=poison, max_attn_chunks=max_attn_chunks, aggregation=aggregation,
+                       beta_scalar=beta_scalar)
     sess.workload_page_table = wl.page_table(extra, maxpps)
     if load_now:
         load_workload(sess, wl)

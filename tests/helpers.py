@@ -54,9 +54,10 @@ def fused_best(logits_query, relevance, gamma, beta):
     return O.contrastive_scores(logits_query, beta, O.prior_term(relevance, gamma)).max(axis=0)
 
 
-def check_tokens(gpu_tokens, ref_logits, wl: W.Workload, beta, ref_sel_tokens, ref_gaps):
+def check_tokens(gpu_tokens, ref_logits, wl: W.Workload, beta, ref_sel_tokens, ref_gaps, rule="max"):
     """Token contract: identical unless the oracle's top-2 gap is below 1e-3; in
-    that case the GPU token must score within 1e-3 of the oracle's best.
+    that case the GPU token must score within 1e-3 of the oracle's best (under
+    the selection rule: Eq. 3's max, or the MoE / PoE aggregation).
     Returns the number of exempted queries."""
     exempt = 0
     off = wl.seq_offsets
@@ -66,7 +67,10 @@ def check_tokens(gpu_tokens, ref_logits, wl: W.Workload, beta, ref_sel_tokens, r
         if int(gpu_tokens[b]) != int(ref_sel_tokens[b]):
             assert ref_gaps[b] < GAP_EXEMPT, (
                 f"query {b}: gpu token {gpu_tokens[b]} != oracle {ref_sel_tokens[b]} with gap {ref_gaps[b]}")
-            S = fused_best(rows, wl.relevance[e0:e0 + n], wl.gamma, beta[e0:e0 + n])
+            if rule == "max":
+                S = fused_best(rows, wl.relevance[e0:e0 + n], wl.gamma, beta[e0:e0 + n])
+            else:
+                S = O.aggregate_scores(rows, wl.relevance[e0:e0 + n], wl.gamma, beta[e0:e0 + n], rule)[0]
             assert S[int(gpu_tokens[b])] >= S.max() - GAP_EXEMPT
             exempt += 1
         e0 += n

@@ -57,6 +57,15 @@ def test_invalid_config_sizes_are_zero(bad):
     assert _lib.pced_lm_head_bytes(c) == 0
 
 
+def test_aggregation_and_beta_mode_fields_validated():
+    for field, value in (("aggregation", 3), ("aggregation", -1), ("beta_scalar", 2)):
+        c = cfg()
+        setattr(c, field, value)
+        assert _lib.pced_workspace_bytes(c) == 0, field
+    for rule in ("max", "moe", "poe"):
+        assert _lib.pced_workspace_bytes(cfg(aggregation=rule, beta_scalar=True)) > 0
+
+
 def test_page_size_must_be_16():
     c = cfg()
     c.page_size = 32

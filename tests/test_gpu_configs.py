@@ -247,6 +247,49 @@ def test_fused_lmhead_epilogue_matches_materialised_logits(name, geom, n_exp, le
         check_tokens(_np(ob["tokens"]), ref.logits, wl, ref.beta, ref.tokens, ref.gaps)
 
 
+AGG = [
+    # (name, rule, scalar beta, fixed beta, n_experts, expert lengths)
+    ("moe-dynamic-beta", "moe", False, False, [4, 3], [40, 300, 17, 90, 5, 129, 64]),
+    ("poe-dynamic-beta", "poe", False, False, [4, 3], [40, 300, 17, 90, 5, 129, 64]),
+    ("moe-scalar-beta", "moe", True, False, [5], [12, 200, 31, 77, 150]),
+    ("poe-fixed-beta", "poe", False, True, [6, 1], [33, 8, 250, 16, 47, 90, 21]),
+    ("max-scalar-beta", "max", True, False, [5, 2], [12, 200, 31, 77, 150, 64, 9]),
+]
+
+
+@pytest.mark.parametrize("name,rule,scalar,fixed,n_exp,lens", AGG, ids=[e[0] for e in AGG])
+def test_aggregation_variants_and_scalar_beta(name, rule, scalar, fixed, n_exp, lens):
+    """MoE / PoE aggregation (Appendix C.4 ablation) and the scalar dynamic beta
+    against the oracle: tokens, winners, both scores and beta."""
+    geom = W.Geometry(1, 8, 2, 64, 512, 2000, "bf16")
+    beta = np.random.default_rng(9).random(sum(n_exp)).astype(np.float32).tolist() if fixed else None
+    wl = W.custom(geom, n_exp, lens, 16, 3, seed=14, beta=beta)
+    sess = _session(wl, aggregation=rule, beta_scalar=scalar)
+    Wt = sess.pack_lm_head(wl.lm_head_device(DEV))
+    Wh = lm_head_host(wl.seed, geom.vocab, geom.hidden, geom.dtype)
+    g = wl.geom
+    orc = O.Oracle(n_layers=g.n_layers, n_q_heads=g.n_q_heads, n_kv_heads=g.n_kv_heads, head_dim=g.head_dim,
+                   vocab=g.vocab, dtype=g.dtype, n_experts=wl.n_experts,
+                   cache_k=lambda s, l: wl.kcache_host(s, l), cache_v=lambda s, l: wl.vcache_host(s, l),
+                   relevance=wl.relevance, gamma=wl.gamma, beta=wl.beta, aggregation=rule, beta_scalar=scalar)
+    for t in range(wl.steps):
+        q, kn, vn = wl.step_inputs_device(t, DEV)
+        want = ("logits", "winner", "top1", "top2", "beta_used") if t != 1 else ("winner", "top1", "top2", "beta_used")
+        out = sess.step(q, kn, vn, Wt, want=want)
+        torch.cuda.synchronize()
+        ref = orc.step(*wl.step_inputs_host(t), Wh)
+        np.testing.assert_allclose(_np(out["beta_used"]), ref.beta, rtol=0, atol=1e-4)
+        check_tokens(_np(out["tokens"]), ref.logits, wl, ref.beta, ref.tokens, ref.gaps, rule=rule)
+        toks, win = _np(out["tokens"]), _np(out["winner"])
+        for b in range(wl.n_queries):
+            if toks[b] == ref.tokens[b] and ref.gaps[b] > 1e-3:
+                assert win[b] == ref.winners[b], (t, b)
+                # scores inherit the logits' error (bf16 contract: 2e-2 relative), as in the Max-rule tests
+                tol = 2 * REL_TOL[g.dtype]
+                assert abs(float(out["top1"][b]) - ref.top1[b]) <= tol * max(1.0, abs(ref.top1[b]))
+                assert abs(float(out["top2"][b]) - ref.top2[b]) <= tol * max(1.0, abs(ref.top2[b]))
+
+
 def test_fixed_and_zero_beta():
     geom = W.Geometry(1, 8, 2, 64, 512, 900, "bf16")
     wl = W.custom(geom, [4], [30, 90, 200, 7], 10, 2, seed=8, beta=[0.0, 0.25, 1.0, 0.5])
