@@ -50,6 +50,9 @@ def parse():
     p.add_argument("--cpu-sample-layers", type=int, default=12)
     p.add_argument("--cpu-sample-vocab", type=int, default=32768)
     p.add_argument("--no-events", action="store_true", help="time without per-launch events")
+    p.add_argument("--generate", action="store_true",
+                   help="also time pced_generate over the K steps, launched directly and as one replay of a "
+                        "captured HIP graph")
     p.add_argument("--copy-calibration", action="store_true",
                    help="after the timed steps, run one plain 256 MiB device copy (scale reference for "
                         "the FETCH_SIZE / WRITE_SIZE counters)")
@@ -140,6 +143,60 @@ def cpu_baseline(wl, n_layers_sample: int, vocab_sample: int) -> dict:
     }
 
 
+def generate_timing(sess, wl, src, Wt, K, dev) -> dict:
+    """K steps of pced_generate (device-side synthetic q / k_new / v_new from the
+    previous token) from the freshly loaded caches: once launched directly, then
+    captured into a HIP graph from the same state and replayed three times, the
+    caches reloaded before each replay (a replay repeats exactly the captured
+    steps). Every replay's tokens must equal the direct run's."""
+    import torch
+
+    from paper_2601_08670_amd.session import load_workload
+
+    seed, first = 1234, 1
+
+    def elapsed(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(torch.cuda.current_stream())
+        fn()
+        b.record(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        return a.elapsed_time(b)
+
+    toks = torch.empty((sess.B, K), dtype=torch.int32, device=dev)
+    load_workload(sess, wl, src=src)
+    torch.cuda.synchronize()
+    ms_direct = elapsed(lambda: sess.ctx.pced_generate(K, seed, first, Wt, toks))
+    ref = toks.clone()
+    log(f"[bench] pced_generate direct: {ms_direct / K:.3f} ms/step")
+
+    load_workload(sess, wl, src=src)
+    torch.cuda.synchronize()
+    gtoks = torch.empty_like(toks)
+    graph = torch.cuda.CUDAGraph()
+    t0 = time.perf_counter()
+    with torch.cuda.graph(graph):
+        sess.ctx.pced_generate(K, seed, first, Wt, gtoks)
+    torch.cuda.synchronize()
+    capture_s = time.perf_counter() - t0
+    replays, match = [], True
+    for _ in range(3):
+        load_workload(sess, wl, src=src)
+        gtoks.fill_(-1)
+        torch.cuda.synchronize()
+        replays.append(elapsed(graph.replay))
+        match = match and bool(torch.equal(gtoks, ref))
+    del graph
+    load_workload(sess, wl, src=src)
+    torch.cuda.synchronize()
+    ms_graph = min(replays)
+    log(f"[bench] pced_generate graph replay: {ms_graph / K:.3f} ms/step (capture {capture_s:.2f}s, "
+        f"tokens match: {match})")
+    return {"steps": K, "direct_steps_per_s": K / (ms_direct * 1e-3),
+            "graph_replay_steps_per_s": K / (ms_graph * 1e-3),
+            "graph_replay_ms": replays, "capture_s": capture_s, "tokens_match_direct": match}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -220,6 +277,8 @@ def main():
                     "bytes_per_launch": prof["attn"]["bytes"] / prof["attn"]["launches"],
                     "avg_launch_us": attn["avg_us"]}
 
+    gen = generate_timing(sess, wl, src, Wt, K, dev) if args.generate else None
+
     if args.copy_calibration:
         n = 256 << 20
         src = torch.ones(n // 4, dtype=torch.float32, device=dev)
@@ -259,6 +318,8 @@ def main():
         "kernels": kernels,
         "cpu_baseline": cpu,
     }
+    if gen is not None:
+        out["generate"] = gen
     print(json.dumps(out), flush=True)
 
 

@@ -172,6 +172,40 @@ def test_generate_then_step_continues_history():
     assert sess.lengths() == [9, 24, 37]
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_generate_graph_replay_matches_direct(dtype):
+    # the whole generation captured into one HIP graph: dynamic beta at the first
+    # step (logits materialised), fused LM-head epilogue afterwards (bf16); each
+    # replay starts from reloaded caches and must reproduce the direct run
+    from paper_2601_08670_amd.session import load_workload
+    geom = W.Geometry(2, 8, 2, 64, 512, 3000, dtype)
+    wl = W.custom(geom, [3, 2], [40, 300, 17, 5, 129], amateur_len=16, steps=5, seed=13)
+    sess = _session(wl)
+    Wt = sess.pack_lm_head(wl.lm_head_device(DEV))
+    src = load_workload(sess, wl)
+    direct = sess.generate(wl.steps, 77, 3, Wt, want=("top1",))
+    torch.cuda.synchronize()
+    ref_tok, ref_top1 = direct["tokens"].clone(), direct["top1"].clone()
+    load_workload(sess, wl, src=src)
+    torch.cuda.synchronize()
+    toks = torch.empty_like(ref_tok)
+    top1 = torch.empty_like(ref_top1)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        sess.ctx.pced_generate(wl.steps, 77, 3, Wt, toks, {"top1": top1})
+    torch.cuda.synchronize()
+    for _ in range(3):
+        load_workload(sess, wl, src=src)
+        toks.fill_(-1)
+        top1.fill_(0.0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(toks, ref_tok)
+        assert torch.equal(top1, ref_top1)
+    del graph
+
+
 # ------------------------------------------------------------------ edge cases
 
 EDGE = [
