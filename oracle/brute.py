@@ -110,3 +110,67 @@ def aggregate_pick(rows, relevance, gamma, beta, rule):
     expert = contrib.index(max(contrib)) + 1
     second = max([score[v] for v in range(V) if v != token], default=-math.inf)
     return token, expert, best, second
+
+
+# ------------------------------------------------------- decoder around the step
+
+def bf16(x: float) -> float:
+    """Round a Python float to bfloat16 (through float32, nearest-even)."""
+    import struct
+    u = struct.unpack("<I", struct.pack("<f", x))[0]
+    # float64 -> float32 rounding happened in pack; now float32 -> bfloat16
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return struct.unpack("<f", struct.pack("<I", u))[0]
+
+
+def decoder_layer(h, pos, W, cacheK, cacheV, Hq, Hkv, D, theta, eps=1e-5):
+    """One decoder layer for one sequence, scalar loops.
+
+    h[j]: residual stream; pos: the new token's position (cache length);
+    W: dict of nested lists (attn_norm[j], wq[r][j], wk, wv, wo[j][r], mlp_norm,
+    w_gate[f][j], w_up, w_down[j][f]); cacheK/cacheV: lists of [g][d] rows,
+    extended in place. Returns (new h, attention output o[h][d])."""
+    n = len(h)
+
+    def rho_of(x):
+        return 1.0 / math.sqrt(sum(v * v for v in x) / n + eps)
+
+    def normed(x, g, M):
+        a = [bf16(x[j] * g[j]) for j in range(n)]
+        r = rho_of(x)
+        return [r * sum(a[j] * row[j] for j in range(n)) for row in M]
+
+    def rot(vec, p):
+        out = list(vec)
+        for i in range(D // 2):
+            ang = p * theta ** (-2.0 * i / D)
+            c, s = math.cos(ang), math.sin(ang)
+            x0, x1 = vec[2 * i], vec[2 * i + 1]
+            out[2 * i] = x0 * c - x1 * s
+            out[2 * i + 1] = x0 * s + x1 * c
+        return out
+
+    q = normed(h, W["attn_norm"], W["wq"])
+    k = normed(h, W["attn_norm"], W["wk"])
+    v = normed(h, W["attn_norm"], W["wv"])
+    qh = [[bf16(x) for x in rot(q[hh * D:(hh + 1) * D], pos)] for hh in range(Hq)]
+    kh = [[bf16(x) for x in rot(k[g * D:(g + 1) * D], pos)] for g in range(Hkv)]
+    vh = [[bf16(x) for x in v[g * D:(g + 1) * D]] for g in range(Hkv)]
+    cacheK.append(kh)
+    cacheV.append(vh)
+    o = attention(qh, cacheK, cacheV)
+    oflat = [bf16(x) for row in o for x in row]
+    h2 = [h[j] + sum(oflat[r] * W["wo"][j][r] for r in range(len(oflat))) for j in range(n)]
+    gate = normed(h2, W["mlp_norm"], W["w_gate"])
+    up = normed(h2, W["mlp_norm"], W["w_up"])
+    act = [bf16(gv / (1.0 + math.exp(-gv)) * uv) for gv, uv in zip(gate, up)]
+    h3 = [h2[j] + sum(act[f] * W["w_down"][j][f] for f in range(len(act))) for j in range(n)]
+    return h3, o
+
+
+def model_logits(h, final_norm, lm_head, eps=1e-5):
+    """RMSNorm(h) * g W^T for one sequence under the same rounding contract."""
+    n = len(h)
+    a = [bf16(h[j] * final_norm[j]) for j in range(n)]
+    r = 1.0 / math.sqrt(sum(v * v for v in h) / n + eps)
+    return [r * sum(a[j] * row[j] for j in range(n)) for row in lm_head]

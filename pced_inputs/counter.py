@@ -109,9 +109,13 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     return ((u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)).astype(np.uint16)
 
 
-def values_np(k: int, start: int, count: int, scale: float, dtype: str) -> np.ndarray:
-    """Values as stored: uint16 bf16 bits for ``dtype='bf16'``, float32 for ``'f32'``."""
+def values_np(k: int, start: int, count: int, scale: float, dtype: str, offset: float = 0.0) -> np.ndarray:
+    """Values as stored: uint16 bf16 bits for ``dtype='bf16'``, float32 for ``'f32'``.
+    A non-zero ``offset`` is added in float32 before the rounding to storage
+    (distributions centred away from 0, such as norm weights around 1)."""
     v = values_f32_np(k, start, count, scale)
+    if offset:
+        v = v + np.float32(offset)
     if dtype == "bf16":
         return f32_to_bf16_bits(v)
     if dtype == "f32":
@@ -139,7 +143,7 @@ def _mix64_torch(z):
     return z ^ lsr(z, 31)
 
 
-def values_torch(k: int, start: int, count: int, scale: float, dtype: str, device):
+def values_torch(k: int, start: int, count: int, scale: float, dtype: str, device, offset: float = 0.0):
     """Same bits as :func:`values_np`, computed on ``device`` with int64 torch ops.
 
     int64 multiply wraps modulo 2**64 in two's complement, which gives the same bit
@@ -156,6 +160,8 @@ def values_torch(k: int, start: int, count: int, scale: float, dtype: str, devic
     del h
     v = (u - IH_CENTER).to(torch.float32) * float(value_scale(scale))
     del u
+    if offset:
+        v = v + float(np.float32(offset))
     if dtype == "f32":
         return v
     if dtype == "bf16":

@@ -180,28 +180,28 @@ _TORCH_HOST_THRESHOLD = 1 << 20
 _CHUNK = 1 << 24
 
 
-def host_values(k: int, start: int, count: int, scale: float, dtype: str) -> np.ndarray:
+def host_values(k: int, start: int, count: int, scale: float, dtype: str, offset: float = 0.0) -> np.ndarray:
     """Host array of stored values (uint16 bf16 bits or float32)."""
     if count <= _TORCH_HOST_THRESHOLD:
-        return counter.values_np(k, start, count, scale, dtype)
+        return counter.values_np(k, start, count, scale, dtype, offset)
     import torch  # multi-threaded CPU path, bit-identical to the numpy one
 
     out = np.empty(count, dtype=np.uint16 if dtype == "bf16" else np.float32)
     for c0 in range(0, count, _CHUNK):
         n = min(_CHUNK, count - c0)
-        v = counter.values_torch(k, start + c0, n, scale, dtype, "cpu").numpy()
+        v = counter.values_torch(k, start + c0, n, scale, dtype, "cpu", offset).numpy()
         out[c0:c0 + n] = v.view(out.dtype)
     return out
 
 
-def device_values(k: int, start: int, count: int, scale: float, dtype: str, device):
+def device_values(k: int, start: int, count: int, scale: float, dtype: str, device, offset: float = 0.0):
     """Device tensor of stored values: torch.int16 holding bf16 bits, or float32."""
     import torch
 
     out = torch.empty(count, dtype=torch.int16 if dtype == "bf16" else torch.float32, device=device)
     for c0 in range(0, count, _CHUNK):
         n = min(_CHUNK, count - c0)
-        out[c0:c0 + n] = counter.values_torch(k, start + c0, n, scale, dtype, device)
+        out[c0:c0 + n] = counter.values_torch(k, start + c0, n, scale, dtype, device, offset)
     return out
 
 
