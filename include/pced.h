@@ -107,6 +107,12 @@ typedef struct pced_config {
                                 (beta_k = JSD(p_k || p_0)); 1 = one beta per
                                 query, the mean of those divergences (the
                                 paper's beta_0 read as a single number)       */
+  int32_t ffn_dim;           /* F, MLP width of the decoder stack run by the
+                                pced_model_* calls (bf16 only, a multiple of
+                                64); 0 = no decoder stack (pced_step with given
+                                q / k_new / v_new only)                        */
+  int32_t rope_theta;        /* RoPE base of the decoder stack (500000 for
+                                Llama 3); used when ffn_dim > 0               */
 } pced_config;
 
 typedef struct pced_ctx pced_ctx;
@@ -192,7 +198,8 @@ typedef struct pced_step_out {
   float* top1;            /* [B] fused score of the chosen token                   */
   float* top2;            /* [B] best fused score over all other tokens            */
   float* beta_used;       /* [sum N_b] beta_k used by this step                    */
-  float* hidden;          /* [S][hidden] fp32 copy of the stored hidden state x    */
+  float* hidden;          /* [S][hidden] fp32 copy of the stored hidden state x;
+                             pced_model_*: the final residual stream h        */
 } pced_step_out;
 
 /*
@@ -280,6 +287,85 @@ typedef enum pced_score_mode {
 pced_status pced_relevance(int32_t mode, int32_t n, const float* retrieval, const float* reranker_logits,
                            float* relevance);
 
+/*
+ * Decoder stack around the step (bf16, cfg.ffn_dim > 0). The paper runs the
+ * N+1 experts through the language model in one batched forward pass and
+ * processes the query into every expert's cache (Section 3); it does not
+ * restate the model. The stack here is a Llama-3-style decoder:
+ *   h = E[y];  per layer:
+ *     a = RMSNorm(h) g_attn;  q, k, v = a Wq^T, a Wk^T, a Wv^T;
+ *     q, k rotated (RoPE, pairs (2i, 2i+1), angle pos * rope_theta^(-2i/D));
+ *     k, v appended to the layer's cache at position pos;
+ *     h += Attn(q, cache) Wo^T;
+ *     b = RMSNorm(h) g_mlp;  h += (silu(b Wg^T) * (b Wu^T)) Wd^T;
+ *   logits = RMSNorm(h) g_final W_lm^T, then Eq. 2 / Eq. 3 as in pced_step.
+ * RMSNorm(h) = h / sqrt(mean(h^2) + 1e-5). pos is the sequence's own cache
+ * length before the append (each expert's document was encoded from
+ * position 0). Precision: h is fp32; a normalised product is computed as
+ * rho * (bf16(h * g) W^T) with rho from the fp32 h; q, k, v are rounded to bf16
+ * after RoPE, the attention output and silu(gate) * up to bf16 before their
+ * projections; products accumulate in fp32.
+ *
+ * Weights live in one caller-owned device buffer of pced_model_bytes(cfg),
+ * filled once by pced_pack_model_layer (every layer) and pced_pack_model_globals.
+ */
+
+/* Bytes of the packed decoder-stack weights (0 if cfg is invalid or ffn_dim == 0). */
+size_t pced_model_bytes(const pced_config* cfg);
+
+/*
+ * Pack layer `layer`'s weights into `model`. tensors: host array of 9 DEVICE
+ * pointers to bf16 row-major tensors, in this order:
+ *   attn_norm [hidden], wq [Hq*D][hidden], wk [Hkv*D][hidden], wv [Hkv*D][hidden],
+ *   wo [hidden][Hq*D], mlp_norm [hidden], w_gate [F][hidden], w_up [F][hidden],
+ *   w_down [hidden][F]
+ * (matrices are [out][in]). The sources may be freed once the stream has
+ * executed the call. Errors: INVALID_ARG (NULL, layer out of range, no stack
+ * configured), HIP.
+ */
+pced_status pced_pack_model_layer(const pced_config* cfg, int32_t layer, const void* const* tensors, void* model,
+                                  hipStream_t stream);
+
+/* Pack the token embedding (device bf16 [V][hidden]) and the final norm weight
+ * (device bf16 [hidden]) into `model`. Errors: INVALID_ARG, HIP. */
+pced_status pced_pack_model_globals(const pced_config* cfg, const void* embed, const void* final_norm, void* model,
+                                    hipStream_t stream);
+
+/*
+ * Query-suffix prefill (paper, Section 3: the query is processed into every
+ * expert's cache): appends tokens[b][0 .. n_tokens-1] to every sequence of
+ * query b, one token position at a time through the whole stack (each token
+ * attends to the cache and the suffix tokens before it). No logits.
+ *   model   device, packed weights
+ *   tokens  device int32 [B][n_tokens]; ids outside [0, V) are clamped
+ * Errors: STATE (nothing loaded), CAPACITY (pages), INVALID_ARG, HIP.
+ */
+pced_status pced_model_prefill(pced_ctx* ctx, const void* model, int32_t n_tokens, const int32_t* tokens,
+                               hipStream_t stream);
+
+/*
+ * One decode step through the decoder stack: in_tokens[b] (the query's last
+ * token: the final suffix token, then each chosen token) is appended to every
+ * sequence of query b, the stack and the LM head run for all S sequences, and
+ * Eq. 2 / Eq. 3 pick tokens_out[b]. Dynamic beta is computed at the first step
+ * that produces logits after a load.
+ *   in_tokens   device int32 [B] (clamped to [0, V))
+ *   tokens_out  device int32 [B]
+ *   lm_head     device, packed by pced_pack_lm_head
+ * Errors: as pced_model_prefill.
+ */
+pced_status pced_model_step(pced_ctx* ctx, const void* model, const void* lm_head, const int32_t* in_tokens,
+                            int32_t* tokens_out, const pced_step_out* extra, hipStream_t stream);
+
+/*
+ * n_steps of pced_model_step, each feeding the previous chosen token; the
+ * first step feeds first_tokens (device int32 [B]). tokens_out: device int32
+ * [B][n_steps]; last_extra: optional outputs of the last step.
+ */
+pced_status pced_model_generate(pced_ctx* ctx, const void* model, const void* lm_head, int32_t n_steps,
+                                const int32_t* first_tokens, int32_t* tokens_out,
+                                const pced_step_out* last_extra, hipStream_t stream);
+
 /* Kernel timing with HIP events recorded around each launch on the launch
  * stream. Classes: */
 enum {
@@ -290,7 +376,12 @@ enum {
   PCED_PROF_FUSE = 4,    /* Eq. 2 + Eq. 3                          */
   PCED_PROF_SYNTH = 5,   /* pced_generate's input synthesis        */
   PCED_PROF_COMBINE = 6, /* merge of split attention partials      */
-  PCED_PROF_NCLASS = 7
+  PCED_PROF_EMBED = 7,   /* decoder stack: token embedding          */
+  PCED_PROF_QKV = 8,     /* decoder stack: norm + QKV + RoPE + append */
+  PCED_PROF_OPROJ = 9,   /* decoder stack: O projection + residual  */
+  PCED_PROF_GATEUP = 10, /* decoder stack: norm + gate/up + SwiGLU  */
+  PCED_PROF_DOWN = 11,   /* decoder stack: down projection + residual */
+  PCED_PROF_NCLASS = 12
 };
 typedef struct pced_profile {
   int64_t launches[PCED_PROF_NCLASS];

@@ -17,11 +17,14 @@ LIB_PATH = os.environ.get("PCED_LIBRARY") or os.path.join(_HERE, "libpced.so")
 PCED_F32, PCED_BF16 = 0, 1
 PCED_NORM_NONE, PCED_NORM_RMS = 0, 1
 STATUS = {0: "OK", 1: "INVALID_ARG", 2: "CAPACITY", 3: "HIP", 4: "UNSUPPORTED", 5: "STATE"}
-PROF_CLASSES = ("append", "attn", "lmhead", "beta", "fuse", "synth", "combine")
+PROF_CLASSES = ("append", "attn", "lmhead", "beta", "fuse", "synth", "combine", "embed", "qkv", "oproj",
+                "gateup", "down")
 
 EXPORTED = ("pced_pool_bytes", "pced_lm_head_bytes", "pced_pack_lm_head", "pced_workspace_bytes", "pced_create", "pced_destroy", "pced_last_error",
             "pced_load_caches", "pced_step", "pced_generate", "pced_lmhead", "pced_fuse",
-            "pced_get_lengths", "pced_profile_enable", "pced_profile_read", "pced_relevance")
+            "pced_get_lengths", "pced_profile_enable", "pced_profile_read", "pced_relevance",
+            "pced_model_bytes", "pced_pack_model_layer", "pced_pack_model_globals", "pced_model_prefill",
+            "pced_model_step", "pced_model_generate")
 
 
 class PcedError(RuntimeError):
@@ -34,7 +37,7 @@ class pced_config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_layers", "n_q_heads", "n_kv_heads", "head_dim", "hidden", "vocab", "dtype", "page_size",
         "max_queries", "max_seqs", "max_pages", "max_pages_per_seq", "norm", "max_attn_chunks",
-        "aggregation", "beta_scalar")]
+        "aggregation", "beta_scalar", "ffn_dim", "rope_theta")]
 
 
 class pced_step_out(ctypes.Structure):
@@ -48,8 +51,8 @@ class pced_synth(ctypes.Structure):
 
 
 class pced_profile(ctypes.Structure):
-    _fields_ = [("launches", ctypes.c_int64 * 7), ("total_ms", ctypes.c_double * 7),
-                ("bytes", ctypes.c_double * 7), ("flops", ctypes.c_double * 7)]
+    _fields_ = [("launches", ctypes.c_int64 * 12), ("total_ms", ctypes.c_double * 12),
+                ("bytes", ctypes.c_double * 12), ("flops", ctypes.c_double * 12)]
 
 
 _lib = None
@@ -82,6 +85,12 @@ def load_library() -> ctypes.CDLL:
         "pced_profile_enable": (I, [P, I]),
         "pced_profile_read": (I, [P, ctypes.POINTER(pced_profile)]),
         "pced_relevance": (I, [I, I, P, P, P]),
+        "pced_model_bytes": (ctypes.c_size_t, [ctypes.POINTER(pced_config)]),
+        "pced_pack_model_layer": (I, [ctypes.POINTER(pced_config), I, P, P, V]),
+        "pced_pack_model_globals": (I, [ctypes.POINTER(pced_config), P, P, P, V]),
+        "pced_model_prefill": (I, [P, P, I, P, V]),
+        "pced_model_step": (I, [P, P, P, P, P, ctypes.POINTER(pced_step_out), V]),
+        "pced_model_generate": (I, [P, P, P, I, P, P, ctypes.POINTER(pced_step_out), V]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -98,14 +107,15 @@ def _check(status: int):
 
 def make_config(*, n_layers, n_q_heads, n_kv_heads, head_dim, vocab, dtype, max_queries, max_seqs,
                 max_pages, max_pages_per_seq, norm="rms", hidden=None, max_attn_chunks=0, aggregation="max",
-                beta_scalar=False) -> pced_config:
+                beta_scalar=False, ffn_dim=0, rope_theta=500000) -> pced_config:
     return pced_config(
         n_layers=n_layers, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads, head_dim=head_dim,
         hidden=hidden if hidden is not None else n_q_heads * head_dim, vocab=vocab,
         dtype=PCED_BF16 if dtype == "bf16" else PCED_F32, page_size=16, max_queries=max_queries,
         max_seqs=max_seqs, max_pages=max_pages, max_pages_per_seq=max_pages_per_seq,
         norm=PCED_NORM_RMS if norm == "rms" else PCED_NORM_NONE, max_attn_chunks=max_attn_chunks,
-        aggregation=AGGREGATIONS[aggregation], beta_scalar=int(bool(beta_scalar)))
+        aggregation=AGGREGATIONS[aggregation], beta_scalar=int(bool(beta_scalar)), ffn_dim=ffn_dim,
+        rope_theta=int(rope_theta))
 
 
 def pced_pool_bytes(cfg: pced_config) -> int:
@@ -123,6 +133,23 @@ def pced_lm_head_bytes(cfg: pced_config) -> int:
 def pced_pack_lm_head(cfg: pced_config, w, w_packed, stream=None):
     """Re-lay row-major [V][hidden] LM-head weights into the packed form the steps read."""
     _check(load_library().pced_pack_lm_head(ctypes.byref(cfg), w.data_ptr(), w_packed.data_ptr(), _stream(stream)))
+
+
+def pced_model_bytes(cfg: pced_config) -> int:
+    return load_library().pced_model_bytes(ctypes.byref(cfg))
+
+
+def pced_pack_model_layer(cfg: pced_config, layer: int, tensors, model, stream=None):
+    """Pack one decoder layer's 9 bf16 tensors (attn_norm, wq, wk, wv, wo,
+    mlp_norm, w_gate, w_up, w_down; device, row-major [out][in]) into ``model``."""
+    arr = (ctypes.c_void_p * 9)(*[t.data_ptr() for t in tensors])
+    _check(load_library().pced_pack_model_layer(ctypes.byref(cfg), int(layer), arr, model.data_ptr(),
+                                                _stream(stream)))
+
+
+def pced_pack_model_globals(cfg: pced_config, embed, final_norm, model, stream=None):
+    _check(load_library().pced_pack_model_globals(ctypes.byref(cfg), embed.data_ptr(), final_norm.data_ptr(),
+                                                  model.data_ptr(), _stream(stream)))
 
 
 SCORE_MODES = {"dense": 0, "colbert": 1, "sparse": 2}
@@ -242,6 +269,22 @@ class Context:
         so = _step_out(extra)
         _check(self.lib.pced_fuse(self.handle, logits.data_ptr(), int(refresh_beta), tokens_out.data_ptr(),
                                   so[0] if so else None, _stream(stream)))
+
+    def pced_model_prefill(self, model, n_tokens, tokens, stream=None):
+        _check(self.lib.pced_model_prefill(self.handle, model.data_ptr(), int(n_tokens), tokens.data_ptr(),
+                                           _stream(stream)))
+
+    def pced_model_step(self, model, lm_head, in_tokens, tokens_out, extra: Optional[dict] = None, stream=None):
+        so = _step_out(extra)
+        _check(self.lib.pced_model_step(self.handle, model.data_ptr(), lm_head.data_ptr(), in_tokens.data_ptr(),
+                                        tokens_out.data_ptr(), so[0] if so else None, _stream(stream)))
+
+    def pced_model_generate(self, model, lm_head, n_steps, first_tokens, tokens_out, last_extra=None,
+                            stream=None):
+        so = _step_out(last_extra)
+        _check(self.lib.pced_model_generate(self.handle, model.data_ptr(), lm_head.data_ptr(), int(n_steps),
+                                            first_tokens.data_ptr(), tokens_out.data_ptr(), so[0] if so else None,
+                                            _stream(stream)))
 
     def pced_get_lengths(self, n_seqs):
         out = (ctypes.c_int32 * n_seqs)()

@@ -63,6 +63,12 @@ bool cfg_valid(const pced_config* c, std::string* why) {
   if (c->aggregation != PCED_AGG_MAX && c->aggregation != PCED_AGG_MOE && c->aggregation != PCED_AGG_POE)
     return bad("unknown aggregation");
   if (c->beta_scalar != 0 && c->beta_scalar != 1) return bad("beta_scalar must be 0 or 1");
+  if (c->ffn_dim < 0) return bad("ffn_dim must be >= 0");
+  if (c->ffn_dim > 0) {
+    if (c->dtype != PCED_BF16) return bad("the decoder stack (ffn_dim > 0) needs bf16");
+    if (c->ffn_dim % 64) return bad("ffn_dim must be a multiple of 64");
+    if (c->rope_theta < 2) return bad("rope_theta must be >= 2");
+  }
   // 32-bit index guards used by the kernels
   if ((double)c->max_seqs * c->vocab > 2147483647.0) return bad("max_seqs * vocab exceeds 2^31");
   return true;
@@ -72,7 +78,7 @@ struct Layout {
   size_t len0, page_table, seq_query, query_seq0, query_exp0, exp_seq, exp_query, prior, logw, beta_fixed,
       load_items, src_k, src_v, meta_end;
   size_t chunk_info, seg, nparts, work_pages, tick_fuse, tick_beta, prev_tok, beta, part_acc, part_ml, x, logits,
-      fuse_part, lse_part, jsd_part, agg_lse, syn_q, syn_k, syn_v, total;
+      fuse_part, lse_part, jsd_part, agg_lse, syn_q, syn_k, syn_v, dec_h, dec_a, dec_act, dec_ss, dec_rho, total;
   int rows_pad, nblk_fuse, nchunk, max_work;
   size_t part_slots;
 };
@@ -124,6 +130,15 @@ Layout make_layout(const pced_config& c) {
   L.syn_q = take(S * c.n_layers * c.n_q_heads * c.head_dim * es);
   L.syn_k = take(S * c.n_layers * c.n_kv_heads * c.head_dim * es);
   L.syn_v = take(S * c.n_layers * c.n_kv_heads * c.head_dim * es);
+  // decoder stack (ffn_dim > 0): residual stream, next projection's bf16 input
+  // (padded rows: it is also the LM head's x), MLP activation, per-16-column
+  // sums of h^2 and the final row scales; the attention's query buffer is syn_q
+  const size_t dec = c.ffn_dim > 0 ? 1 : 0;
+  L.dec_h = take(dec * S * c.hidden * 4);
+  L.dec_a = take(dec * L.rows_pad * c.hidden * 2);
+  L.dec_act = take(dec * S * c.ffn_dim * 2);
+  L.dec_ss = take(dec * (c.hidden / 16) * S * 4);
+  L.dec_rho = take(dec * S * 4);
   L.total = o;
   return L;
 }
@@ -362,7 +377,7 @@ pced_status run_fuse_final(pced_ctx* c, int nblk, int32_t* tokens_out, int tok_s
 // LM head over M rows of x. With fuse_nblk > 0 the kernel's epilogue applies
 // Eq. 2 and leaves per-slice candidates instead of writing the logits.
 pced_status run_lmhead(pced_ctx* c, const void* x, int M, const void* w, float* logits, hipStream_t st,
-                       int fuse_nblk = 0) {
+                       int fuse_nblk = 0, const float* rho_in = nullptr) {
   const pced_config& cfg = c->cfg;
   LmArgs a{};
   a.x = x;
@@ -372,6 +387,7 @@ pced_status run_lmhead(pced_ctx* c, const void* x, int M, const void* w, float* 
   a.V = cfg.vocab;
   a.K = cfg.hidden;
   a.rms = cfg.norm == PCED_NORM_RMS;
+  a.rho_in = rho_in;
   if (fuse_nblk > 0) {
     a.query_seq0 = c->at<int32_t>(c->lay.query_seq0);
     a.query_exp0 = c->at<int32_t>(c->lay.query_exp0);
@@ -386,6 +402,273 @@ pced_status run_lmhead(pced_ctx* c, const void* x, int M, const void* w, float* 
   ProfScope ps(c, PCED_PROF_LMHEAD, (double)cfg.vocab * cfg.hidden * es + (double)M * cfg.hidden * es + out_bytes,
                2.0 * M * cfg.vocab * cfg.hidden);
   HIP_OK(launch_lmhead(a, c->bf16, st, ps.timing()));
+  return PCED_OK;
+}
+
+// LM head and token choice of a step over the S rows of x (rho_in: optional
+// row scales). Eq. 2 and the slice argmax run in the LM head's epilogue when
+// beta is known (fixed, or frozen after the first step) and the caller wants no
+// logits; otherwise the logits are materialised (dynamic beta needs them at the
+// first step).
+pced_status run_head(pced_ctx* c, const void* x, const float* rho_in, const void* w, int32_t* tokens_out,
+                     int tok_stride, const pced_step_out* extra, hipStream_t st) {
+  const pced_config& cfg = c->cfg;
+  const bool refresh = c->dynamic_beta && !c->beta_frozen;
+  const int fused_nblk = (c->bf16 && !refresh && !(extra && extra->logits) && cfg.aggregation == PCED_AGG_MAX)
+                             ? lmhead_fused_nblk(c->S, cfg.vocab) : 0;
+  pced_status r;
+  if (fused_nblk > 0) {
+    r = run_lmhead(c, x, c->S, w, nullptr, st, fused_nblk, rho_in);
+    if (r != PCED_OK) return r;
+    return run_fuse_final(c, fused_nblk, tokens_out, tok_stride, extra, st);
+  }
+  float* logits = (extra && extra->logits) ? extra->logits : c->at<float>(c->lay.logits);
+  r = run_lmhead(c, x, c->S, w, logits, st, 0, rho_in);
+  if (r != PCED_OK) return r;
+  return run_fuse(c, logits, refresh, tokens_out, tok_stride, extra, st);
+}
+
+pced_status check_room(const pced_ctx* c, int n_tokens) {
+  const int P = c->cfg.max_pages_per_seq;
+  for (int s = 0; s < c->S; ++s) {
+    const long last = (long)c->len[s] + n_tokens - 1;
+    if (last / kPage >= P) return fail(PCED_ERR_CAPACITY, "sequence %d cannot hold %d more tokens", s, n_tokens);
+    for (long p = c->len[s] / kPage; p <= last / kPage; ++p)
+      if (c->page_table[(size_t)s * P + p] < 0)
+        return fail(PCED_ERR_CAPACITY, "sequence %d cannot hold %d more tokens", s, n_tokens);
+  }
+  return PCED_OK;
+}
+
+// Byte offsets of the decoder-stack weights inside the packed model buffer:
+// per layer the two norm weights and the packed QKV (q, k, v tiles
+// concatenated), O, gate/up (gate and up tiles alternating) and down
+// matrices; then the embedding [V][hidden] and the final norm weight.
+struct ModelLayout {
+  size_t attn_norm, mlp_norm, qkv, o, gu, down, layer_bytes;
+  size_t embed, final_norm, total;
+};
+
+ModelLayout model_layout(const pced_config& c) {
+  ModelLayout m{};
+  const size_t H = c.hidden, F = c.ffn_dim, qd = (size_t)c.n_q_heads * c.head_dim,
+               kd = (size_t)c.n_kv_heads * c.head_dim;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes); return r; };
+  m.attn_norm = take(H * 2);
+  m.mlp_norm = take(H * 2);
+  m.qkv = take((qd + 2 * kd) * H * 2);
+  m.o = take(H * qd * 2);
+  m.gu = take(2 * F * H * 2);
+  m.down = take(H * F * 2);
+  m.layer_bytes = o;
+  o = m.layer_bytes * c.n_layers;
+  m.embed = take((size_t)c.vocab * H * 2);
+  m.final_norm = take(H * 2);
+  m.total = o;
+  return m;
+}
+
+// Embedding plus every decoder layer for the new token of each sequence
+// (appending its K/V rows). in_tok: the queries' tokens, stride tok_stride.
+// Leaves the residual stream in dec_h and bf16(h * g_final) in dec_a.
+pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_tok, int tok_stride,
+                              float* attn_out, hipStream_t st) {
+  const pced_config& cfg = c->cfg;
+  const ModelLayout ml = model_layout(cfg);
+  const int S = c->S, H = cfg.hidden, D = cfg.head_dim;
+  const int qd = cfg.n_q_heads * D, kd = cfg.n_kv_heads * D;
+  const AttnPlan plan = plan_attention(c);
+  if (plan.chunks > c->lay.max_work) return fail(PCED_ERR_CAPACITY, "attention plan exceeds workspace");
+
+  // planning blocks of the append launch only: K/V rows come from the QKV epilogue
+  AppendArgs ap{};
+  ap.kpool = c->kpool;
+  ap.vpool = c->vpool;
+  ap.len0 = c->at<int32_t>(c->lay.len0);
+  ap.page_table = c->at<int32_t>(c->lay.page_table);
+  ap.chunk_info = c->at<int2>(c->lay.chunk_info);
+  ap.seg = c->at<int4>(c->lay.seg);
+  ap.nparts = c->at<int32_t>(c->lay.nparts);
+  ap.work_pages = c->at<int32_t>(c->lay.work_pages);
+  ap.n_seqs = S;
+  ap.n_layers = cfg.n_layers;
+  ap.n_kv_heads = cfg.n_kv_heads;
+  ap.head_dim = D;
+  ap.max_pages = cfg.max_pages;
+  ap.maxpps = cfg.max_pages_per_seq;
+  ap.t = c->t;
+  ap.n_chunks = plan.chunks;
+  ap.total_pages = (int)plan.pages;
+  {
+    ProfScope ps(c, PCED_PROF_APPEND, 0, 0);
+    HIP_OK(launch_append(ap, true, st, ps.timing()));
+  }
+
+  float* h = c->at<float>(c->lay.dec_h);
+  uint16_t* an = c->at<uint16_t>(c->lay.dec_a);
+  uint16_t* act = c->at<uint16_t>(c->lay.dec_act);
+  float* ss = c->at<float>(c->lay.dec_ss);
+  {
+    EmbedArgs e{};
+    e.embed = (const uint16_t*)(model + ml.embed);
+    e.g = (const uint16_t*)(model + ml.attn_norm);
+    e.tokens = in_tok;
+    e.seq_query = c->at<int32_t>(c->lay.seq_query);
+    e.h = h;
+    e.a_out = an;
+    e.ss_out = ss;
+    e.hidden = H;
+    e.vocab = cfg.vocab;
+    e.tok_stride = tok_stride;
+    e.ld_ss = cfg.max_seqs;
+    ProfScope ps(c, PCED_PROF_EMBED, (double)S * H * (2 + 4 + 2), 0);
+    HIP_OK(launch_embed(e, S, st, ps.timing()));
+  }
+
+  AttnArgs at{};
+  at.q = c->at<void>(c->lay.syn_q);
+  at.kpool = c->kpool;
+  at.vpool = c->vpool;
+  at.len0 = ap.len0;
+  at.page_table = ap.page_table;
+  at.chunk_info = ap.chunk_info;
+  at.seg = ap.seg;
+  at.nparts = ap.nparts;
+  at.work_pages = ap.work_pages;
+  at.part_acc = c->at<float>(c->lay.part_acc);
+  at.part_ml = c->at<float>(c->lay.part_ml);
+  at.x_out = c->at<void>(c->lay.x);
+  at.attn_out = attn_out;
+  at.hidden_out = nullptr;
+  at.n_seqs = S;
+  at.n_layers = cfg.n_layers;
+  at.n_q_heads = cfg.n_q_heads;
+  at.n_kv_heads = cfg.n_kv_heads;
+  at.group = c->G;
+  at.max_pages = cfg.max_pages;
+  at.maxpps = cfg.max_pages_per_seq;
+  at.t = c->t;
+  at.split_stride = plan.max_parts;
+  at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
+  double kv_tokens = 0;
+  for (int s = 0; s < S; ++s) kv_tokens += c->len[s] + 1;
+  const double attn_bytes = kv_tokens * 2.0 * kd * 2 + 2.0 * S * qd * 2;
+  const double attn_flops = kv_tokens * 4.0 * qd;
+
+  GemmArgs g{};
+  g.M = S;
+  g.ld_ss = cfg.max_seqs;
+  g.ss_parts = H / 16;
+  g.inv_norm_dim = 1.0f / (float)H;
+  g.eps = 1e-5f;
+  g.h = h;
+  g.a_out = an;
+  g.ss_out = ss;
+  g.act = act;
+  g.F = cfg.ffn_dim;
+  g.q_out = c->at<uint16_t>(c->lay.syn_q);
+  g.kpool = (uint16_t*)c->kpool;
+  g.vpool = (uint16_t*)c->vpool;
+  g.len0 = ap.len0;
+  g.page_table = ap.page_table;
+  g.n_layers = cfg.n_layers;
+  g.n_q_heads = cfg.n_q_heads;
+  g.n_kv_heads = cfg.n_kv_heads;
+  g.head_dim = D;
+  g.max_pages = cfg.max_pages;
+  g.maxpps = cfg.max_pages_per_seq;
+  g.t = c->t;
+  g.log2_theta = std::log2((double)cfg.rope_theta);
+  const double F = cfg.ffn_dim;
+  for (int l = 0; l < cfg.n_layers; ++l) {
+    const char* lw = model + (size_t)l * ml.layer_bytes;
+    const uint16_t* g_next = (const uint16_t*)(l + 1 < cfg.n_layers ? model + (size_t)(l + 1) * ml.layer_bytes +
+                                                                          ml.attn_norm
+                                                                    : model + ml.final_norm);
+    g.layer = l;
+    {  // norm + QKV + RoPE + append
+      GemmArgs q = g;
+      q.w = lw + ml.qkv;
+      q.x = an;
+      q.K = H;
+      q.n_tiles = (qd + 2 * kd) / 16;
+      q.ss_in = ss;
+      ProfScope ps(c, PCED_PROF_QKV, (double)(qd + 2 * kd) * H * 2 + (double)S * (H * 2 + (qd + 2 * kd) * 2),
+                   2.0 * S * (qd + 2 * kd) * H);
+      HIP_OK(launch_gemm(q, kEpiQkv, st, ps.timing()));
+    }
+    at.layer = l;
+    at.is_last_layer = l == cfg.n_layers - 1;
+    {
+      ProfScope ps(c, PCED_PROF_ATTN, attn_bytes, attn_flops);
+      HIP_OK(launch_attn(at, plan.chunks * cfg.n_kv_heads, D, true, st, ps.timing()));
+    }
+    if (plan.max_parts > 1) {
+      ProfScope ps(c, PCED_PROF_COMBINE, 0, 0);
+      HIP_OK(launch_attn_combine(at, D, plan.max_parts, true, st, ps.timing()));
+    }
+    {  // O projection + residual; the MLP norm's input
+      GemmArgs o = g;
+      o.w = lw + ml.o;
+      o.x = c->at<uint16_t>(c->lay.x);
+      o.K = qd;
+      o.n_tiles = H / 16;
+      o.g_next = (const uint16_t*)(lw + ml.mlp_norm);
+      ProfScope ps(c, PCED_PROF_OPROJ, (double)H * qd * 2 + (double)S * (qd * 2 + H * 10),
+                   2.0 * S * H * qd);
+      HIP_OK(launch_gemm(o, kEpiResid, st, ps.timing()));
+    }
+    {  // norm + gate/up + SwiGLU
+      GemmArgs u = g;
+      u.w = lw + ml.gu;
+      u.x = an;
+      u.K = H;
+      u.n_tiles = 2 * cfg.ffn_dim / 16;
+      u.ss_in = ss;
+      ProfScope ps(c, PCED_PROF_GATEUP, 2.0 * F * H * 2 + (double)S * (H * 2 + F * 2), 4.0 * S * F * H);
+      HIP_OK(launch_gemm(u, kEpiSwiglu, st, ps.timing()));
+    }
+    {  // down projection + residual; the next norm's input
+      GemmArgs d = g;
+      d.w = lw + ml.down;
+      d.x = act;
+      d.K = cfg.ffn_dim;
+      d.n_tiles = H / 16;
+      d.g_next = g_next;
+      ProfScope ps(c, PCED_PROF_DOWN, F * H * 2 + (double)S * (F * 2 + H * 10), 2.0 * S * H * F);
+      HIP_OK(launch_gemm(d, kEpiResid, st, ps.timing()));
+    }
+  }
+  return PCED_OK;
+}
+
+pced_status check_model(const pced_ctx* c, const void* model) {
+  pced_status r = check_ctx(c, true);
+  if (r != PCED_OK) return r;
+  if (c->cfg.ffn_dim <= 0) return fail(PCED_ERR_STATE, "no decoder stack configured (ffn_dim == 0)");
+  if (!model) return fail(PCED_ERR_INVALID_ARG, "model is NULL");
+  return PCED_OK;
+}
+
+// One decode step through the decoder stack (shared by step and generate).
+pced_status run_model_step(pced_ctx* c, const void* model, const void* w, const int32_t* in_tok, int32_t* tokens_out,
+                           int tok_stride, const pced_step_out* extra, hipStream_t st) {
+  pced_status r = check_room(c, 1);
+  if (r != PCED_OK) return r;
+  r = run_model_forward(c, (const char*)model, in_tok, 1, extra ? extra->attn_out : nullptr, st);
+  if (r != PCED_OK) return r;
+  const pced_config& cfg = c->cfg;
+  float* rho = c->at<float>(c->lay.dec_rho);
+  HIP_OK(launch_rho(c->at<float>(c->lay.dec_ss), cfg.hidden / 16, cfg.max_seqs, c->S, 1.0f / (float)cfg.hidden,
+                    1e-5f, rho, st));
+  r = run_head(c, c->at<void>(c->lay.dec_a), rho, w, tokens_out, tok_stride, extra, st);
+  if (r != PCED_OK) return r;
+  if (extra && extra->hidden)
+    HIP_OK(hipMemcpyAsync(extra->hidden, c->at<float>(c->lay.dec_h), (size_t)c->S * cfg.hidden * 4,
+                          hipMemcpyDeviceToDevice, st));
+  for (int s = 0; s < c->S; ++s) c->len[s] += 1;
+  c->t += 1;
   return PCED_OK;
 }
 
@@ -471,23 +754,7 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
     }
   }
 
-  // Eq. 2 and the slice argmax run in the LM head's epilogue when beta is known
-  // (fixed, or frozen after the first step) and the caller wants no logits;
-  // otherwise the logits are materialised (dynamic beta needs them at the first step)
-  const bool refresh = c->dynamic_beta && !c->beta_frozen;
-  const int fused_nblk = (c->bf16 && !refresh && !(extra && extra->logits) && cfg.aggregation == PCED_AGG_MAX)
-                             ? lmhead_fused_nblk(c->S, cfg.vocab) : 0;
-  pced_status r;
-  if (fused_nblk > 0) {
-    r = run_lmhead(c, at.x_out, c->S, w, nullptr, st, fused_nblk);
-    if (r != PCED_OK) return r;
-    r = run_fuse_final(c, fused_nblk, tokens_out, tok_stride, extra, st);
-  } else {
-    float* logits = (extra && extra->logits) ? extra->logits : c->at<float>(c->lay.logits);
-    r = run_lmhead(c, at.x_out, c->S, w, logits, st);
-    if (r != PCED_OK) return r;
-    r = run_fuse(c, logits, refresh, tokens_out, tok_stride, extra, st);
-  }
+  const pced_status r = run_head(c, at.x_out, nullptr, w, tokens_out, tok_stride, extra, st);
   if (r != PCED_OK) return r;
   for (int s = 0; s < c->S; ++s) c->len[s] += 1;
   c->t += 1;
@@ -769,6 +1036,96 @@ pced_status pced_generate(pced_ctx* c, int32_t n_steps, const pced_synth* synth,
     }
     r = run_step(c, sa.q, sa.k_new, sa.v_new, lm_head, tokens_out + i, n_steps,
                  i == n_steps - 1 ? last_extra : nullptr, st);
+    if (r != PCED_OK) return r;
+  }
+  return PCED_OK;
+}
+
+size_t pced_model_bytes(const pced_config* cfg) {
+  if (!cfg_valid(cfg, nullptr) || cfg->ffn_dim <= 0) return 0;
+  return model_layout(*cfg).total;
+}
+
+pced_status pced_pack_model_layer(const pced_config* cfg, int32_t layer, const void* const* tensors, void* model,
+                                  hipStream_t st) {
+  std::string why;
+  if (!cfg_valid(cfg, &why)) return fail(PCED_ERR_INVALID_ARG, "invalid config: %s", why.c_str());
+  if (cfg->ffn_dim <= 0) return fail(PCED_ERR_INVALID_ARG, "no decoder stack configured (ffn_dim == 0)");
+  if (layer < 0 || layer >= cfg->n_layers) return fail(PCED_ERR_INVALID_ARG, "layer %d out of range", layer);
+  if (!tensors || !model) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  for (int i = 0; i < 9; ++i)
+    if (!tensors[i]) return fail(PCED_ERR_INVALID_ARG, "tensor %d is NULL", i);
+  const ModelLayout ml = model_layout(*cfg);
+  char* lw = (char*)model + (size_t)layer * ml.layer_bytes;
+  const int H = cfg->hidden, F = cfg->ffn_dim;
+  const int qd = cfg->n_q_heads * cfg->head_dim, kd = cfg->n_kv_heads * cfg->head_dim;
+  HIP_OK(hipMemcpyAsync(lw + ml.attn_norm, tensors[0], (size_t)H * 2, hipMemcpyDeviceToDevice, st));
+  HIP_OK(hipMemcpyAsync(lw + ml.mlp_norm, tensors[5], (size_t)H * 2, hipMemcpyDeviceToDevice, st));
+  // QKV: q tiles, then k tiles, then v tiles (all row counts are multiples of 16)
+  HIP_OK(launch_pack_tiles(tensors[1], lw + ml.qkv, qd, H, 1, 0, st));
+  HIP_OK(launch_pack_tiles(tensors[2], lw + ml.qkv, kd, H, 1, qd / 16, st));
+  HIP_OK(launch_pack_tiles(tensors[3], lw + ml.qkv, kd, H, 1, (qd + kd) / 16, st));
+  HIP_OK(launch_pack_tiles(tensors[4], lw + ml.o, H, qd, 1, 0, st));
+  // gate and up tiles alternate, so a block owning tiles 2j, 2j+1 has both halves of 16 MLP columns
+  HIP_OK(launch_pack_tiles(tensors[6], lw + ml.gu, F, H, 2, 0, st));
+  HIP_OK(launch_pack_tiles(tensors[7], lw + ml.gu, F, H, 2, 1, st));
+  HIP_OK(launch_pack_tiles(tensors[8], lw + ml.down, H, F, 1, 0, st));
+  return PCED_OK;
+}
+
+pced_status pced_pack_model_globals(const pced_config* cfg, const void* embed, const void* final_norm, void* model,
+                                    hipStream_t st) {
+  std::string why;
+  if (!cfg_valid(cfg, &why)) return fail(PCED_ERR_INVALID_ARG, "invalid config: %s", why.c_str());
+  if (cfg->ffn_dim <= 0) return fail(PCED_ERR_INVALID_ARG, "no decoder stack configured (ffn_dim == 0)");
+  if (!embed || !final_norm || !model) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  const ModelLayout ml = model_layout(*cfg);
+  HIP_OK(hipMemcpyAsync((char*)model + ml.embed, embed, (size_t)cfg->vocab * cfg->hidden * 2,
+                        hipMemcpyDeviceToDevice, st));
+  HIP_OK(hipMemcpyAsync((char*)model + ml.final_norm, final_norm, (size_t)cfg->hidden * 2,
+                        hipMemcpyDeviceToDevice, st));
+  return PCED_OK;
+}
+
+pced_status pced_model_prefill(pced_ctx* c, const void* model, int32_t n_tokens, const int32_t* tokens,
+                               hipStream_t st) {
+  pced_status r = check_model(c, model);
+  if (r != PCED_OK) return r;
+  if (!tokens) return fail(PCED_ERR_INVALID_ARG, "tokens is NULL");
+  if (n_tokens < 0) return fail(PCED_ERR_INVALID_ARG, "n_tokens < 0");
+  r = check_room(c, n_tokens);
+  if (r != PCED_OK) return r;
+  for (int i = 0; i < n_tokens; ++i) {
+    r = run_model_forward(c, (const char*)model, tokens + i, n_tokens, nullptr, st);
+    if (r != PCED_OK) return r;
+    for (int s = 0; s < c->S; ++s) c->len[s] += 1;
+    c->t += 1;
+  }
+  return PCED_OK;
+}
+
+pced_status pced_model_step(pced_ctx* c, const void* model, const void* lm_head, const int32_t* in_tokens,
+                            int32_t* tokens_out, const pced_step_out* extra, hipStream_t st) {
+  pced_status r = check_model(c, model);
+  if (r != PCED_OK) return r;
+  if (!lm_head || !in_tokens || !tokens_out) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  return run_model_step(c, model, lm_head, in_tokens, tokens_out, 1, extra, st);
+}
+
+pced_status pced_model_generate(pced_ctx* c, const void* model, const void* lm_head, int32_t n_steps,
+                                const int32_t* first_tokens, int32_t* tokens_out, const pced_step_out* last_extra,
+                                hipStream_t st) {
+  pced_status r = check_model(c, model);
+  if (r != PCED_OK) return r;
+  if (!lm_head || !first_tokens || !tokens_out) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  if (n_steps < 1) return fail(PCED_ERR_INVALID_ARG, "n_steps < 1");
+  r = check_room(c, n_steps);
+  if (r != PCED_OK) return r;
+  // step i > 0 feeds the token step i-1 chose, which the fuse also leaves in prev_tok
+  const int32_t* prev = c->at<int32_t>(c->lay.prev_tok);
+  for (int i = 0; i < n_steps; ++i) {
+    r = run_model_step(c, model, lm_head, i == 0 ? first_tokens : prev, tokens_out + i, n_steps,
+                       i == n_steps - 1 ? last_extra : nullptr, st);
     if (r != PCED_OK) return r;
   }
   return PCED_OK;

@@ -86,6 +86,7 @@ struct LmArgs {
   const float* prior;       // [sum N]
   float* fuse_part;
   int n_queries, fuse_nblk;
+  const float* rho_in;      // optional [M] row scales used instead of rms (bf16 kernels)
 };
 
 struct FuseArgs {
@@ -145,6 +146,46 @@ struct SynthArgs {
   int n_layers, qdim, kvdim, t, first_token, use_first, bf16;
 };
 
+// Decoder-stack projections of one decode step: out[m][n] = rho_m sum_k x[m][k] W[n][k]
+// for the M step rows, W packed in 16-row tiles (k_pack_w_bf16 layout), with an
+// epilogue per projection.
+enum GemmEpi { kEpiQkv = 0, kEpiResid = 1, kEpiSwiglu = 2 };
+struct GemmArgs {
+  const void* w;            // packed tiles of this projection
+  const uint16_t* x;        // [M][K] bf16 input rows
+  int M, K, n_tiles;        // rows, inner dimension, 16-column output tiles
+  // row scale rho_m = 1/sqrt(sum_p ss_in[p][m] * inv_norm_dim + eps), or 1 without ss_in
+  const float* ss_in;       // [ss_parts][ld_ss]
+  int ss_parts, ld_ss;
+  float inv_norm_dim, eps;
+  // kEpiResid: h[m][n] += out; a_out = bf16(h * g_next); ss_out[n / 16][m] = sum of h^2 over the tile
+  float* h;                 // [M][hidden]
+  uint16_t* a_out;          // [M][hidden]
+  const uint16_t* g_next;   // [hidden]
+  float* ss_out;            // [hidden/16][ld_ss]
+  // kEpiSwiglu: tiles alternate gate / up; act[m][f] = bf16(silu(gate) * up)
+  uint16_t* act;            // [M][F]
+  int F;
+  // kEpiQkv: columns [0, Hq*D) q, then k, then v; RoPE at pos = len0[m] + t;
+  // q to q_out, k / v into the paged pool at that position
+  uint16_t* q_out;          // [S][L][Hq][D]
+  uint16_t* kpool;
+  uint16_t* vpool;
+  const int32_t* len0;
+  const int32_t* page_table;
+  int layer, n_layers, n_q_heads, n_kv_heads, head_dim, max_pages, maxpps, t;
+  double log2_theta;
+};
+struct EmbedArgs {
+  const uint16_t* embed;    // [V][hidden]
+  const uint16_t* g;        // [hidden] first layer's attention norm weight
+  const int32_t* tokens;    // [B] with stride
+  const int32_t* seq_query; // [S]
+  float* h;                 // [S][hidden]
+  uint16_t* a_out;          // [S][hidden] bf16(h * g)
+  float* ss_out;            // [hidden/16][ld_ss]
+  int hidden, vocab, tok_stride, ld_ss;
+};
 // Optional timing events attached to the first / last dispatch of a launcher.
 struct Timing {
   hipEvent_t start = nullptr;
@@ -171,5 +212,12 @@ hipError_t launch_fuse_final(const FuseArgs& a, int n_queries, hipStream_t st, c
 int lmhead_fused_nblk(int M, int V);
 hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st, const Timing* tm = nullptr);
 hipError_t launch_copy_rows(const void* src, void* dst, size_t nbytes, hipStream_t st);
+// pack a [rows][K] bf16 matrix into 16-row tiles, tile i going to slot i * stride + offset
+hipError_t launch_pack_tiles(const void* w, void* wp, int rows, int K, int stride, int offset, hipStream_t st);
+hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Timing* tm = nullptr);
+hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Timing* tm = nullptr);
+// rho[m] = 1/sqrt(sum_p ss[p][m] * inv_dim + eps) for m < M
+hipError_t launch_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps, float* rho,
+                      hipStream_t st);
 
 }  // namespace pced

@@ -105,7 +105,7 @@ __device__ __forceinline__ long chunk_lo(long c, long P, long C) { return c * P 
 // the chunk holding global page u: the largest c with chunk_lo(c) <= u
 __device__ __forceinline__ int chunk_of(long u, long P, long C) { return (int)(((u + 1) * C - 1) / P); }
 
-// Blocks 0 .. S*L-1: write step t's K/V row of (sequence, layer) into slot
+// Blocks 0 .. S*L-1 (when k_new is given): write step t's K/V row of (sequence, layer) into slot
 // len0 + t of the sequence's pages (Section 3: the chosen token joins every
 // expert's history). Block S*L + s plans sequence s for this step's length
 // len0 + t + 1: the chunks it meets, its segment descriptor in each (the
@@ -115,8 +115,9 @@ __device__ __forceinline__ int chunk_of(long u, long P, long C) { return (int)((
 template <bool BF16>
 __global__ __launch_bounds__(128) void k_append(AppendArgs a) {
   const int S = a.n_seqs, L = a.n_layers;
-  if ((int)blockIdx.x >= S * L) {
-    const int s = blockIdx.x - S * L;
+  const int n_app = a.k_new ? S * L : 0;  // without K/V rows (written elsewhere) only the planning blocks run
+  if ((int)blockIdx.x >= n_app) {
+    const int s = blockIdx.x - n_app;
     const long P = a.total_pages, C = a.n_chunks;
     auto pages_of = [&](int r) { return (a.len0[r] + a.t + 1 + kPage - 1) / kPage; };
     // first global page of this sequence: sum over earlier sequences
@@ -741,8 +742,10 @@ __device__ void fuse_tile(const LmArgs& a, int v0, int blk, At at) {
 // W[16*vb + col][64*ks + 16*quad + 8*h .. +7]: each half is exactly the A operand
 // of one v_mfma_f32_16x16x32_bf16, read as one contiguous 1 KiB wave load.
 // Rows past V are zero.
+// Row tile vb of the source goes to tile slot vb * stride + offset of wp (the
+// decoder projections interleave or concatenate several matrices this way).
 __global__ __launch_bounds__(256) void k_pack_w_bf16(const uint16_t* __restrict__ w, uint16_t* __restrict__ wp,
-                                                     int V, int K) {
+                                                     int V, int K, int stride, int offset) {
   const int KS = K / 64;
   const size_t n16 = (size_t)((V + 15) / 16) * KS * 2 * 64;  // 16-byte units of the packed matrix
   for (size_t u = blockIdx.x * (size_t)blockDim.x + threadIdx.x; u < n16; u += (size_t)gridDim.x * blockDim.x) {
@@ -756,7 +759,8 @@ __global__ __launch_bounds__(256) void k_pack_w_bf16(const uint16_t* __restrict_
     const int k = 64 * ks + 16 * (lane >> 4) + 8 * h;
     uint4 val = make_uint4(0u, 0u, 0u, 0u);
     if (v < V) val = *(const uint4*)(w + (size_t)v * K + k);
-    *(uint4*)(wp + u * 8) = val;
+    const size_t dst = ((((size_t)vb * stride + offset) * KS + ks) * 2 + h) * 64 + lane;
+    *(uint4*)(wp + dst * 8) = val;
   }
 }
 
@@ -860,9 +864,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       for (int nt = 0; nt < NT; ++nt) {
         float t = ss[nt] + __shfl_xor(ss[nt], 16);
         t += __shfl_xor(t, 32);
-        const float rho = a.rms ? 1.0f / sqrtf(t / (float)K + 1e-5f) : 1.0f;
         const int m = 16 * nt + col;
         if (m >= a.M) continue;
+        const float rho = a.rho_in ? a.rho_in[m] : a.rms ? 1.0f / sqrtf(t / (float)K + 1e-5f) : 1.0f;
 #pragma unroll
         for (int vt = 0; vt < VT; ++vt) {
           const f32x4 cc = acc[vt][nt];
@@ -878,9 +882,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int nt = 0; nt < NT; ++nt) {
       float t = ss[nt] + __shfl_xor(ss[nt], 16);
       t += __shfl_xor(t, 32);
-      const float rho = a.rms ? 1.0f / sqrtf(t / (float)K + 1e-5f) : 1.0f;
       const int m = m0 + 16 * nt + col;
       if (m >= a.M) continue;
+      const float rho = a.rho_in ? a.rho_in[m] : a.rms ? 1.0f / sqrtf(t / (float)K + 1e-5f) : 1.0f;
 #pragma unroll
       for (int vt = 0; vt < VT; ++vt) {
         const int v = 16 * (vb0 + vt) + 4 * quad;
@@ -1021,7 +1025,8 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
     for (int o = 1; o < PIECES; o <<= 1) t += __shfl_xor(t, o);
     const int v = tid + NTH * j;
-    if (v < n_units && v % PIECES == 0) rho_s[v / PIECES] = a.rms ? 1.0f / sqrtf(t / (float)K + 1e-5f) : 1.0f;
+    if (v < n_units && v % PIECES == 0)
+      rho_s[v / PIECES] = a.rho_in ? a.rho_in[v / PIECES] : a.rms ? 1.0f / sqrtf(t / (float)K + 1e-5f) : 1.0f;
   }
   __syncthreads();
   if constexpr (FUSED) {
@@ -1376,6 +1381,240 @@ __global__ __launch_bounds__(256) void k_synth(SynthArgs a) {
   synth_fill<BF16>(a.v_new, row * a.kvdim, base[2], a.kvdim, a.value_scale);
 }
 
+// ------------------------------------------------------------ decoder stack
+
+constexpr int kGemmWaves = 8;  // waves per projection block (they split the K steps)
+constexpr int kGemmRing = 4;   // K steps in flight per wave
+
+// sum over the ss partials of row m, 8 lanes per row (lanes 8r .. 8r+7 of a
+// wave hold row r); every lane of the group returns the total
+__device__ __forceinline__ float row_ss8(const float* ss, int parts, int ld, int m, int j, bool valid) {
+  float t = 0.f;
+  if (valid)
+    for (int p = j; p < parts; p += 8) t += ss[(size_t)p * ld + m];
+  t += __shfl_xor(t, 1);
+  t += __shfl_xor(t, 2);
+  t += __shfl_xor(t, 4);
+  return t;
+}
+
+// Decoder projection for the rows of one decode step (M rows, looped in groups
+// of 16 NT): out[m][n] = rho_m sum_k x[m][k] W[n][k] on the matrix cores,
+// C^T[16 columns x 16 rows] += W[16 x 32] X^T[32 x 16] (v_mfma_f32_16x16x32_bf16).
+// A block owns CT consecutive 16-column tiles; its 8 waves split the K steps into
+// contiguous ranges, each wave streaming its slice of the packed W tiles
+// (contiguous 1 KiB loads, every byte read once) and of x (L2-resident) through
+// a kGemmRing-deep register ring. The waves' partial products are summed in LDS
+// in wave order (deterministic), then the epilogue applies rho and:
+//   kEpiQkv    RoPE on q and k (pairs (2i, 2i+1) at the sequence's position),
+//              q to the attention's query buffer, k and v into the paged cache;
+//   kEpiResid  h += out, then the next norm's input bf16(h * g) and the
+//              per-tile sums of h^2 its row scale is built from;
+//   kEpiSwiglu tiles alternate gate / up: act = bf16(silu(gate) * up).
+template <int NT, int CT, int EPI>
+__global__ __launch_bounds__(64 * kGemmWaves) void k_gemm_dec(GemmArgs a) {
+  constexpr int WPB = kGemmWaves, R = kGemmRing;
+  // the wave index (and so the K range and the ring's tail guards) must be
+  // scalar: a guard the compiler sees as divergent becomes an EXEC mask, and
+  // matrix-core instructions do not honour EXEC
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15, quad = lane >> 4;
+  const int tile0 = blockIdx.x * CT;
+  const int K = a.K, KS = K / 64;
+  const int per = (KS + WPB - 1) / WPB;
+  const int ks0 = min(wave * per, KS);
+  const int n = min(ks0 + per, KS) - ks0;
+  __shared__ f32x4 red[WPB][CT][NT][64];
+  __shared__ float rho_s[16 * NT];
+  const uint4* Wp = (const uint4*)a.w;
+  const uint4* wt[CT];
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct) wt[ct] = Wp + ((size_t)min(tile0 + ct, a.n_tiles - 1) * KS + ks0) * 128 + lane;
+
+  for (int m0 = 0; m0 < a.M; m0 += 16 * NT) {
+    f32x4 acc[CT][NT];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[ct][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const uint16_t* xrow[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      xrow[nt] = a.x + (size_t)min(m0 + 16 * nt + col, a.M - 1) * K + 64 * ks0 + 16 * quad;
+    struct Stage { uint4 w[CT][2]; uint4 x[NT][2]; };
+    Stage st[R];
+    // step i of the wave's range; past the end the last step again (a cache
+    // hit): the ring stays branch-free
+    auto load = [&](Stage& S, int i) __attribute__((always_inline)) {
+      i = min(i, n - 1);
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) {
+        S.w[ct][0] = wt[ct][(size_t)i * 128];
+        S.w[ct][1] = wt[ct][(size_t)i * 128 + 64];
+      }
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        S.x[nt][0] = *(const uint4*)(xrow[nt] + i * 64);
+        S.x[nt][1] = *(const uint4*)(xrow[nt] + i * 64 + 8);
+      }
+    };
+    auto mma = [&](const Stage& S) __attribute__((always_inline)) {
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          acc[ct][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[ct][0]), as_bf16x8(S.x[nt][0]),
+                                                                acc[ct][nt], 0, 0, 0);
+          acc[ct][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[ct][1]), as_bf16x8(S.x[nt][1]),
+                                                                acc[ct][nt], 0, 0, 0);
+        }
+    };
+    if (n > 0) {
+#pragma unroll
+      for (int j = 0; j < R; ++j) load(st[j], j);
+      for (int i = 0; i < n; i += R) {
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+          if (i + j < n) mma(st[j]);
+          load(st[j], i + j + R);
+        }
+      }
+    }
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) red[wave][ct][nt][lane] = acc[ct][nt];
+    if (a.ss_in) {  // row scales of this row group, 8 lanes per row
+      for (int t = threadIdx.x; t < 16 * NT * 8; t += 64 * WPB) {
+        const int r = t >> 3, m = m0 + r;
+        const float tot = row_ss8(a.ss_in, a.ss_parts, a.ld_ss, m, t & 7, m < a.M);
+        if ((t & 7) == 0) rho_s[r] = 1.0f / sqrtf(tot * a.inv_norm_dim + a.eps);
+      }
+    }
+    __syncthreads();
+
+    // epilogue: item (tile, row tile, lane) -> row m, columns n .. n+3
+    constexpr int PAIR = EPI == kEpiSwiglu ? 2 : 1;
+    constexpr int ITEMS = CT / PAIR * NT * 64;
+    for (int it = threadIdx.x; it < ITEMS; it += 64 * WPB) {
+      const int ln = it & 63, nt = (it >> 6) % NT, cp = (it >> 6) / NT;
+      const int r = 16 * nt + (ln & 15), m = m0 + r;
+      const bool valid = m < a.M;
+      f32x4 v = red[0][cp * PAIR][nt][ln];
+#pragma unroll
+      for (int w = 1; w < WPB; ++w) v += red[w][cp * PAIR][nt][ln];
+      if constexpr (EPI == kEpiResid) {
+        const int n0 = 16 * (tile0 + cp) + 4 * (ln >> 4);
+        float ss = 0.f;
+        if (valid) {
+          float* hp = a.h + (size_t)m * (16 * a.n_tiles) + n0;  // row stride: hidden = 16 * tiles
+          float4 hv = *(float4*)hp;
+          hv.x += v[0];
+          hv.y += v[1];
+          hv.z += v[2];
+          hv.w += v[3];
+          *(float4*)hp = hv;
+          const uint2 g = *(const uint2*)(a.g_next + n0);
+          uint2 pk;
+          pk.x = f2bf(hv.x * bf2f(g.x & 0xFFFFu)) | (f2bf(hv.y * bf2f(g.x >> 16)) << 16);
+          pk.y = f2bf(hv.z * bf2f(g.y & 0xFFFFu)) | (f2bf(hv.w * bf2f(g.y >> 16)) << 16);
+          *(uint2*)(a.a_out + (size_t)m * (16 * a.n_tiles) + n0) = pk;
+          ss = hv.x * hv.x + hv.y * hv.y + hv.z * hv.z + hv.w * hv.w;
+        }
+        ss += __shfl_xor(ss, 16);
+        ss += __shfl_xor(ss, 32);
+        if (valid && ln < 16) a.ss_out[(size_t)(tile0 + cp) * a.ld_ss + m] = ss;
+      } else if constexpr (EPI == kEpiSwiglu) {
+        if (valid) {
+          f32x4 u = red[0][cp * 2 + 1][nt][ln];
+#pragma unroll
+          for (int w = 1; w < WPB; ++w) u += red[w][cp * 2 + 1][nt][ln];
+          const float rho = a.ss_in ? rho_s[r] : 1.0f;
+          uint32_t o[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float g = v[q] * rho, up = u[q] * rho;
+            o[q] = f2bf(g / (1.0f + expf(-g)) * up);
+          }
+          const int f0 = 16 * (tile0 / 2 + cp) + 4 * (ln >> 4);
+          *(uint2*)(a.act + (size_t)m * a.F + f0) = make_uint2(o[0] | (o[1] << 16), o[2] | (o[3] << 16));
+        }
+      } else {  // kEpiQkv
+        if (valid) {
+          const float rho = a.ss_in ? rho_s[r] : 1.0f;
+          const int D = a.head_dim, qd = a.n_q_heads * D, kd = a.n_kv_heads * D;
+          const int n0 = 16 * (tile0 + cp) + 4 * (ln >> 4);
+          const int sec = n0 < qd ? 0 : n0 < qd + kd ? 1 : 2;
+          const int c0 = sec == 0 ? n0 : sec == 1 ? n0 - qd : n0 - qd - kd;
+          const int head = c0 / D, d = c0 % D;
+          const int pos = a.len0[m] + a.t;
+          float o[4] = {v[0] * rho, v[1] * rho, v[2] * rho, v[3] * rho};
+          if (sec < 2) {
+#pragma unroll
+            for (int pr = 0; pr < 2; ++pr) {
+              const int i = d / 2 + pr;
+              const double ang = (double)pos * exp2(-(2.0 * i / D) * a.log2_theta);
+              double sn, cs;
+              sincos(ang, &sn, &cs);
+              const float c = (float)cs, s_ = (float)sn;
+              const float x0 = o[2 * pr], x1 = o[2 * pr + 1];
+              o[2 * pr] = x0 * c - x1 * s_;
+              o[2 * pr + 1] = x0 * s_ + x1 * c;
+            }
+          }
+          uint32_t b[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) b[q] = f2bf(o[q]);
+          if (sec == 0) {
+            const size_t qo = (((size_t)m * a.n_layers + a.layer) * a.n_q_heads + head) * D + d;
+            *(uint2*)(a.q_out + qo) = make_uint2(b[0] | (b[1] << 16), b[2] | (b[3] << 16));
+          } else {
+            const int phys = a.page_table[(size_t)m * a.maxpps + pos / kPage];
+            const int slot = pos % kPage;
+            const size_t base = (((size_t)a.layer * a.max_pages + phys) * a.n_kv_heads + head) * kPage * D;
+            uint16_t* pool = sec == 1 ? a.kpool : a.vpool;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              pool[base + (sec == 1 ? kswz(slot, d + q) : vswz(slot, d + q))] = (uint16_t)b[q];
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// Token embedding of every sequence's new token (the query's token), the first
+// layer's norm input bf16(h * g) and the per-16-column sums of h^2.
+__global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
+  const int s = blockIdx.x;
+  const int tok = min(max(a.tokens[(size_t)a.seq_query[s] * a.tok_stride], 0), a.vocab - 1);
+  const uint16_t* e = a.embed + (size_t)tok * a.hidden;
+  for (int j = threadIdx.x; j < a.hidden / 4; j += 256) {
+    const uint2 ev = *(const uint2*)(e + 4 * j);
+    const uint2 g = *(const uint2*)(a.g + 4 * j);
+    const float h0 = bf2f(ev.x & 0xFFFFu), h1 = bf2f(ev.x >> 16), h2 = bf2f(ev.y & 0xFFFFu), h3 = bf2f(ev.y >> 16);
+    *(float4*)(a.h + (size_t)s * a.hidden + 4 * j) = make_float4(h0, h1, h2, h3);
+    uint2 pk;
+    pk.x = f2bf(h0 * bf2f(g.x & 0xFFFFu)) | (f2bf(h1 * bf2f(g.x >> 16)) << 16);
+    pk.y = f2bf(h2 * bf2f(g.y & 0xFFFFu)) | (f2bf(h3 * bf2f(g.y >> 16)) << 16);
+    *(uint2*)(a.a_out + (size_t)s * a.hidden + 4 * j) = pk;
+    float ss = h0 * h0 + h1 * h1 + h2 * h2 + h3 * h3;
+    ss += __shfl_xor(ss, 1);
+    ss += __shfl_xor(ss, 2);
+    if ((j & 3) == 0) a.ss_out[(size_t)(j / 4) * a.ld_ss + s] = ss;
+  }
+}
+
+// rho[m] = 1/sqrt(sum_p ss[p][m] * inv_dim + eps), 8 lanes per row.
+__global__ __launch_bounds__(256) void k_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps,
+                                             float* rho) {
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  const int m = t >> 3;
+  const float tot = row_ss8(ss, parts, ld, m, t & 7, m < M);
+  if ((t & 7) == 0 && m < M) rho[m] = 1.0f / sqrtf(tot * inv_dim + eps);
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------ launchers
@@ -1418,7 +1657,7 @@ hipError_t launch_load(const LoadArgs& a, int n_items, bool bf16, hipStream_t st
 }
 
 hipError_t launch_append(const AppendArgs& a, bool bf16, hipStream_t st, const Timing* tm) {
-  const int blocks = a.n_seqs * a.n_layers + a.n_seqs;
+  const int blocks = (a.k_new ? a.n_seqs * a.n_layers : 0) + a.n_seqs;  // no K/V rows given: planning only
   if (bf16) return go(k_append<true>, dim3(blocks), dim3(128), 0, st, t0(tm), t1(tm), a);
   return go(k_append<false>, dim3(blocks), dim3(128), 0, st, t0(tm), t1(tm), a);
 }
@@ -1451,8 +1690,46 @@ hipError_t launch_attn_combine(const AttnArgs& a, int head_dim, int max_splits, 
 
 hipError_t launch_pack_lm_head(const void* w, void* wp, int V, int K, bool bf16, hipStream_t st) {
   if (!bf16) return hipMemcpyAsync(wp, w, (size_t)V * K * 4, hipMemcpyDeviceToDevice, st);
-  k_pack_w_bf16<<<2048, 256, 0, st>>>((const uint16_t*)w, (uint16_t*)wp, V, K);
+  k_pack_w_bf16<<<2048, 256, 0, st>>>((const uint16_t*)w, (uint16_t*)wp, V, K, 1, 0);
   return hipGetLastError();
+}
+
+hipError_t launch_pack_tiles(const void* w, void* wp, int rows, int K, int stride, int offset, hipStream_t st) {
+  k_pack_w_bf16<<<2048, 256, 0, st>>>((const uint16_t*)w, (uint16_t*)wp, rows, K, stride, offset);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Timing* tm) {
+  if (a.K % 64 != 0 || a.M < 1) return hipErrorInvalidValue;
+  const int NT = a.M <= 16 ? 1 : a.M <= 32 ? 2 : 3;
+  const dim3 b(64 * kGemmWaves);
+  auto pick = [&](auto k1, auto k2, auto k3, int ct) {
+    const dim3 g((a.n_tiles + ct - 1) / ct);
+    return NT == 1 ? go(k1, g, b, 0, st, t0(tm), t1(tm), a)
+           : NT == 2 ? go(k2, g, b, 0, st, t0(tm), t1(tm), a)
+                     : go(k3, g, b, 0, st, t0(tm), t1(tm), a);
+  };
+  switch (epi) {
+    case kEpiQkv:
+      return pick(k_gemm_dec<1, 1, kEpiQkv>, k_gemm_dec<2, 1, kEpiQkv>, k_gemm_dec<3, 1, kEpiQkv>, 1);
+    case kEpiResid:
+      return pick(k_gemm_dec<1, 1, kEpiResid>, k_gemm_dec<2, 1, kEpiResid>, k_gemm_dec<3, 1, kEpiResid>, 1);
+    case kEpiSwiglu:
+      if (a.n_tiles % 2) return hipErrorInvalidValue;
+      return pick(k_gemm_dec<1, 2, kEpiSwiglu>, k_gemm_dec<2, 2, kEpiSwiglu>, k_gemm_dec<3, 2, kEpiSwiglu>, 2);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Timing* tm) {
+  if (a.hidden % 256 != 0) return hipErrorInvalidValue;
+  return go(k_embed, dim3(n_seqs), dim3(256), 0, st, t0(tm), t1(tm), a);
+}
+
+hipError_t launch_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps, float* rho,
+                      hipStream_t st) {
+  return go(k_rho, dim3((M * 8 + 255) / 256), dim3(256), 0, st, nullptr, nullptr, ss, parts, ld, M, inv_dim, eps,
+            rho);
 }
 
 int lmhead_fused_nblk(int M, int V) {

@@ -22,7 +22,7 @@ class PcedSession:
 
     def __init__(self, *, n_layers, n_q_heads, n_kv_heads, head_dim, vocab, dtype, max_queries,
                  max_seqs, max_pages, max_pages_per_seq, norm="rms", device="cuda", poison=False,
-                 max_attn_chunks=0, aggregation="max", beta_scalar=False):
+                 max_attn_chunks=0, aggregation="max", beta_scalar=False, ffn_dim=0, rope_theta=500000):
         torch = _torch()
         self.dtype = dtype
         self.device = device
@@ -33,7 +33,7 @@ class PcedSession:
                                     max_seqs=max_seqs, max_pages=max_pages,
                                     max_pages_per_seq=max_pages_per_seq, norm=norm,
                                     max_attn_chunks=max_attn_chunks, aggregation=aggregation,
-                                    beta_scalar=beta_scalar)
+                                    beta_scalar=beta_scalar, ffn_dim=ffn_dim, rope_theta=rope_theta)
         self.ctx = _lib.Context(self.cfg, device=device)
         pool = _lib.pced_pool_bytes(self.cfg)
         self.k_pool = torch.empty(pool, dtype=torch.uint8, device=device)
@@ -51,6 +51,29 @@ class PcedSession:
         torch = _torch()
         out = torch.empty(_lib.pced_lm_head_bytes(self.cfg), dtype=torch.uint8, device=self.device)
         _lib.pced_pack_lm_head(self.cfg, w, out)
+        return out
+
+    def pack_model(self, layer_tensors, embed, final_norm):
+        """Packed decoder-stack weights (device). ``layer_tensors(l)`` returns the 9
+        bf16 device tensors of layer l in pced_pack_model_layer order."""
+        torch = _torch()
+        out = torch.empty(_lib.pced_model_bytes(self.cfg), dtype=torch.uint8, device=self.device)
+        for l in range(self.geom["n_layers"]):
+            ts = layer_tensors(l)
+            _lib.pced_pack_model_layer(self.cfg, l, ts, out)
+            torch.cuda.current_stream().synchronize()  # the sources may be dropped after the copy
+            del ts
+        _lib.pced_pack_model_globals(self.cfg, embed, final_norm, out)
+        torch.cuda.current_stream().synchronize()
+        return out
+
+    def model_step(self, model, lm_head, in_tokens, want=("logits", "winner", "top1", "top2", "beta_used")):
+        torch = _torch()
+        tokens = torch.empty(self.B, dtype=torch.int32, device=self.device)
+        extra = self.out_buffers(want) if want else None
+        self.ctx.pced_model_step(model, lm_head, in_tokens, tokens, extra)
+        out = dict(extra or {})
+        out["tokens"] = tokens
         return out
 
     # ------------------------------------------------------------------ load
@@ -104,7 +127,7 @@ class PcedSession:
 
 def session_for_workload(wl, device="cuda", extra_tokens: Optional[int] = None, norm="rms",
                          load_now=True, max_queries=None, poison=False, max_attn_chunks=0, aggregation="max",
-                         beta_scalar=False):
+                         beta_scalar=False, ffn_dim=0, rope_theta=500000):
     """Build a session sized for a synthetic workload (duck-typed: any object with
     the attributes of ``pced_inputs.workloads.Workload``) and load its caches,
     materialised on ``device``."""
@@ -117,7 +140,7 @@ def session_for_workload(wl, device="cuda", extra_tokens: Optional[int] = None, 
                        max_queries=max_queries or wl.n_queries, max_seqs=wl.n_seqs,
                        max_pages=int(need.sum()), max_pages_per_seq=maxpps, norm=norm, device=device,
                        poison=poison, max_attn_chunks=max_attn_chunks, aggregation=aggregation,
-                       beta_scalar=beta_scalar)
+                       beta_scalar=beta_scalar, ffn_dim=ffn_dim, rope_theta=rope_theta)
     sess.workload_page_table = wl.page_table(extra, maxpps)
     if load_now:
         load_workload(sess, wl)

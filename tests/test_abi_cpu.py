@@ -215,3 +215,37 @@ def test_relevance_helper_errors():
     assert lib.pced_relevance(0, 0, a, None, out) == OK
     with pytest.raises(_lib.PcedError):
         _lib.pced_relevance("dense", np.array([np.nan], np.float32))
+
+
+def test_decoder_stack_config_and_sizes():
+    c = cfg(ffn_dim=512)
+    H, qd, kd, F = 512, 512, 128, 512
+    per_layer = sum((-(-b // 256)) * 256 for b in (H * 2, H * 2, (qd + 2 * kd) * H * 2, H * qd * 2,
+                                                   2 * F * H * 2, H * F * 2))
+    tail = sum((-(-b // 256)) * 256 for b in (1000 * H * 2, H * 2))
+    assert _lib.pced_model_bytes(c) == 2 * per_layer + tail
+    assert _lib.pced_workspace_bytes(c) > _lib.pced_workspace_bytes(cfg())   # decoder buffers
+    assert _lib.pced_model_bytes(cfg()) == 0                                  # no stack configured
+    for bad in (dict(ffn_dim=-64), dict(ffn_dim=100), dict(ffn_dim=512, rope_theta=1),
+                dict(ffn_dim=512, dtype="f32", n_q_heads=4, head_dim=16)):
+        assert _lib.pced_workspace_bytes(cfg(**bad)) == 0, bad
+        assert _lib.pced_model_bytes(cfg(**bad)) == 0, bad
+
+
+def test_decoder_stack_entry_points_validate_before_any_launch():
+    lib = _lib.load_library()
+    c = cfg(ffn_dim=512)
+    ts = (ctypes.c_void_p * 9)(*([1 << 40] * 9))
+    assert lib.pced_pack_model_layer(ctypes.byref(c), 2, ts, 1 << 41, None) == INVALID      # layer out of range
+    assert lib.pced_pack_model_layer(ctypes.byref(c), -1, ts, 1 << 41, None) == INVALID
+    assert lib.pced_pack_model_layer(ctypes.byref(c), 0, ts, None, None) == INVALID
+    ts[4] = None
+    assert lib.pced_pack_model_layer(ctypes.byref(c), 0, ts, 1 << 41, None) == INVALID
+    assert b"tensor 4" in lib.pced_last_error()
+    assert lib.pced_pack_model_layer(ctypes.byref(cfg()), 0, ts, 1 << 41, None) == INVALID  # ffn_dim == 0
+    assert lib.pced_pack_model_globals(ctypes.byref(c), None, 1, 1, None) == INVALID
+    fc = FakeCtx()   # ffn_dim == 0 context: nothing loaded, then no stack
+    assert lib.pced_model_step(fc.h, 1, 1, 1, 1, None, None) == STATE
+    assert lib.pced_model_prefill(fc.h, 1, 2, 1, None) == STATE
+    assert lib.pced_model_generate(fc.h, 1, 1, 2, 1, 1, None, None) == STATE
+    fc.close()
