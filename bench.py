@@ -53,6 +53,9 @@ def parse():
     p.add_argument("--generate", action="store_true",
                    help="also time pced_generate over the K steps, launched directly and as one replay of a "
                         "captured HIP graph")
+    p.add_argument("--model", action="store_true",
+                   help="also time K decode steps through the decoder stack (pced_model_generate: Llama-3-8B "
+                        "decoder, 32 layers, MLP 14336, random-init weights) on the same caches")
     p.add_argument("--copy-calibration", action="store_true",
                    help="after the timed steps, run one plain 256 MiB device copy (scale reference for "
                         "the FETCH_SIZE / WRITE_SIZE counters)")
@@ -197,6 +200,82 @@ def generate_timing(sess, wl, src, Wt, K, dev) -> dict:
             "graph_replay_ms": replays, "capture_s": capture_s, "tokens_match_direct": match}
 
 
+def kernel_table(prof, ms_total):
+    kernels = {}
+    for name, p in prof.items():
+        if p["launches"] == 0:
+            continue
+        avg_us = p["ms"] * 1e3 / p["launches"]
+        gbs = p["bytes"] / (p["ms"] * 1e-3) / 1e9 if p["ms"] > 0 else 0.0
+        kernels[name] = {"launches": p["launches"], "avg_us": avg_us, "GB/s": gbs, "hbm_frac": gbs / HBM_PEAK_GBS,
+                         "share_of_step": p["ms"] / ms_total}
+        if p["flops"] > 0:
+            tf = p["flops"] / (p["ms"] * 1e-3) / 1e12
+            kernels[name]["TFLOP/s"] = tf
+            kernels[name]["mfma_frac"] = tf / BF16_MFMA_PEAK_TFLOPS
+    return kernels
+
+
+def model_timing(wl, K, Wm, dev) -> dict:
+    """K decode steps through the decoder stack (pced_model_generate) on the
+    workload's caches: token embedding, 32 Llama-3-8B decoder layers (QKV +
+    RoPE + append, attention, O projection, SwiGLU MLP), final norm, LM head,
+    Eq. 2 / 3. Weights are random-init bf16 streams of the same shapes (no
+    trained checkpoint is involved; throughput does not depend on the values).
+    Timed like the main region: warm-up, reload, K steps between two
+    synchronisations, then the same K steps again with per-launch events."""
+    import torch
+
+    from paper_2601_08670_amd.session import load_workload, session_for_workload
+    from pced_inputs.model import LAYER_TENSORS, ModelSpec
+
+    g = wl.geom
+    spec = ModelSpec(g, ffn_dim=14336, rope_theta=500000.0, seed=wl.seed)
+    t0 = time.time()
+    sess = session_for_workload(wl, device=dev, extra_tokens=max(K, Wm) + 1, load_now=False,
+                                ffn_dim=spec.ffn_dim, rope_theta=int(spec.rope_theta))
+    src = load_workload(sess, wl)
+    model = sess.pack_model(lambda l: [spec.device(n, l, dev) for n in LAYER_TENSORS],
+                            spec.device("embed", 0, dev), spec.device("final_norm", 0, dev))
+    Wt = sess.pack_lm_head(wl.lm_head_device(dev))
+    first = torch.ones(sess.B, dtype=torch.int32, device=dev)
+    toks = torch.empty((sess.B, max(K, Wm)), dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    log(f"[bench] model setup {time.time() - t0:.1f}s (weights {model.numel() / 1e9:.2f} GB)")
+    sess.ctx.pced_model_generate(model, Wt, Wm, first, toks)
+    torch.cuda.synchronize()
+
+    def timed(with_events):
+        load_workload(sess, wl, src=src)
+        sess.ctx.pced_profile_enable(with_events)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(torch.cuda.current_stream())
+        sess.ctx.pced_model_generate(model, Wt, K, first, toks)
+        b.record(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        prof = sess.ctx.pced_profile_read()
+        sess.ctx.pced_profile_enable(False)
+        return a.elapsed_time(b), prof
+
+    ms_plain, _ = timed(False)
+    log(f"[bench] model: {K} steps {ms_plain / K:.3f} ms/step")
+    ms_ev, prof = timed(True)
+    log(f"[bench] model with per-launch events: {ms_ev / K:.3f} ms/step")
+    kernels = kernel_table(prof, ms_ev)
+    weight_bytes = float(model.numel())
+    del sess, model, Wt, src
+    torch.cuda.empty_cache()
+    return {"metric": "PCED decode steps/sec at N docs, through the decoder stack", "value": K / (ms_plain * 1e-3),
+            "unit": "steps/s", "ms_per_step": ms_plain / K, "ms_per_step_with_launch_events": ms_ev / K,
+            "steps": K, "warmup": Wm,
+            "model": {"layers": g.n_layers, "hidden": g.hidden, "ffn_dim": spec.ffn_dim, "q_heads": g.n_q_heads,
+                      "kv_heads": g.n_kv_heads, "head_dim": g.head_dim, "vocab": g.vocab,
+                      "rope_theta": spec.rope_theta, "weights": "random-init bf16",
+                      "weight_bytes": weight_bytes},
+            "kernels": kernels}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -278,6 +357,11 @@ def main():
                     "avg_launch_us": attn["avg_us"]}
 
     gen = generate_timing(sess, wl, src, Wt, K, dev) if args.generate else None
+    model = None
+    if args.model:
+        del sess, src, inputs
+        torch.cuda.empty_cache()
+        model = model_timing(wl, K, Wm, dev)
 
     if args.copy_calibration:
         n = 256 << 20
@@ -320,6 +404,8 @@ def main():
     }
     if gen is not None:
         out["generate"] = gen
+    if model is not None:
+        out["model_step"] = model
     print(json.dumps(out), flush=True)
 
 

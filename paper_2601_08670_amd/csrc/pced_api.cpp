@@ -78,7 +78,8 @@ struct Layout {
   size_t len0, page_table, seq_query, query_seq0, query_exp0, exp_seq, exp_query, prior, logw, beta_fixed,
       load_items, src_k, src_v, meta_end;
   size_t chunk_info, seg, nparts, work_pages, tick_fuse, tick_beta, prev_tok, beta, part_acc, part_ml, x, logits,
-      fuse_part, lse_part, jsd_part, agg_lse, syn_q, syn_k, syn_v, dec_h, dec_a, dec_act, dec_ss, dec_rho, total;
+      fuse_part, lse_part, jsd_part, agg_lse, syn_q, syn_k, syn_v, dec_h, dec_a, dec_act, dec_ss, dec_rho, dec_part,
+      total;
   int rows_pad, nblk_fuse, nchunk, max_work;
   size_t part_slots;
 };
@@ -139,6 +140,9 @@ Layout make_layout(const pced_config& c) {
   L.dec_act = take(dec * S * c.ffn_dim * 2);
   L.dec_ss = take(dec * (c.hidden / 16) * S * 4);
   L.dec_rho = take(dec * S * 4);
+  // K-slice partial sums of a projection: [slices][S][columns], columns <= max(QKV width, hidden)
+  const size_t proj_cols = std::max<size_t>((size_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim, c.hidden);
+  L.dec_part = take(dec * kProjMaxSplit * S * proj_cols * 4);
   L.total = o;
   return L;
 }
@@ -580,6 +584,12 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
   g.maxpps = cfg.max_pages_per_seq;
   g.t = c->t;
   g.log2_theta = std::log2((double)cfg.rope_theta);
+  g.part = c->at<float>(c->lay.dec_part);
+  // K slices per projection: about one block per compute unit (8-tile column groups)
+  auto slices = [&](int n_tiles, int K) {
+    const int groups = ceil_div(n_tiles, 8);
+    return std::max(1, std::min({kProjMaxSplit, K / 64, c->num_cus / groups}));
+  };
   const double F = cfg.ffn_dim;
   for (int l = 0; l < cfg.n_layers; ++l) {
     const char* lw = model + (size_t)l * ml.layer_bytes;
@@ -593,6 +603,7 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
       q.x = an;
       q.K = H;
       q.n_tiles = (qd + 2 * kd) / 16;
+      q.ksplit = slices(q.n_tiles, H);
       q.ss_in = ss;
       ProfScope ps(c, PCED_PROF_QKV, (double)(qd + 2 * kd) * H * 2 + (double)S * (H * 2 + (qd + 2 * kd) * 2),
                    2.0 * S * (qd + 2 * kd) * H);
@@ -614,6 +625,7 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
       o.x = c->at<uint16_t>(c->lay.x);
       o.K = qd;
       o.n_tiles = H / 16;
+      o.ksplit = slices(o.n_tiles, qd);
       o.g_next = (const uint16_t*)(lw + ml.mlp_norm);
       ProfScope ps(c, PCED_PROF_OPROJ, (double)H * qd * 2 + (double)S * (qd * 2 + H * 10),
                    2.0 * S * H * qd);
@@ -625,6 +637,7 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
       u.x = an;
       u.K = H;
       u.n_tiles = 2 * cfg.ffn_dim / 16;
+      u.ksplit = 1;
       u.ss_in = ss;
       ProfScope ps(c, PCED_PROF_GATEUP, 2.0 * F * H * 2 + (double)S * (H * 2 + F * 2), 4.0 * S * F * H);
       HIP_OK(launch_gemm(u, kEpiSwiglu, st, ps.timing()));
@@ -635,6 +648,7 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
       d.x = act;
       d.K = cfg.ffn_dim;
       d.n_tiles = H / 16;
+      d.ksplit = slices(d.n_tiles, cfg.ffn_dim);
       d.g_next = g_next;
       ProfScope ps(c, PCED_PROF_DOWN, F * H * 2 + (double)S * (F * 2 + H * 10), 2.0 * S * H * F);
       HIP_OK(launch_gemm(d, kEpiResid, st, ps.timing()));

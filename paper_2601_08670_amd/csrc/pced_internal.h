@@ -149,11 +149,14 @@ struct SynthArgs {
 // Decoder-stack projections of one decode step: out[m][n] = rho_m sum_k x[m][k] W[n][k]
 // for the M step rows, W packed in 16-row tiles (k_pack_w_bf16 layout), with an
 // epilogue per projection.
-enum GemmEpi { kEpiQkv = 0, kEpiResid = 1, kEpiSwiglu = 2 };
+enum GemmEpi { kEpiQkv = 0, kEpiResid = 1, kEpiSwiglu = 2, kEpiPartial = 3 };
+constexpr int kProjMaxSplit = 8;   // K slices of a projection (partial buffer sized for this many)
 struct GemmArgs {
   const void* w;            // packed tiles of this projection
   const uint16_t* x;        // [M][K] bf16 input rows
   int M, K, n_tiles;        // rows, inner dimension, 16-column output tiles
+  int ksplit;               // K slices (blocks per 8-tile column group); 1 for kEpiSwiglu
+  float* part;              // [ksplit][M][16 n_tiles] fp32 partial sums (kEpiQkv, kEpiResid)
   // row scale rho_m = 1/sqrt(sum_p ss_in[p][m] * inv_norm_dim + eps), or 1 without ss_in
   const float* ss_in;       // [ss_parts][ld_ss]
   int ss_parts, ld_ss;

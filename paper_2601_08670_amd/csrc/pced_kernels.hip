@@ -1383,8 +1383,8 @@ __global__ __launch_bounds__(256) void k_synth(SynthArgs a) {
 
 // ------------------------------------------------------------ decoder stack
 
-constexpr int kGemmWaves = 8;  // waves per projection block (they split the K steps)
-constexpr int kGemmRing = 4;   // K steps in flight per wave
+constexpr int kProjWaves = 8;  // waves per projection block, one 16-column tile each
+constexpr int kProjRing = 4;   // K steps in flight per wave
 
 // sum over the ss partials of row m, 8 lanes per row (lanes 8r .. 8r+7 of a
 // wave hold row r); every lane of the group returns the total
@@ -1399,59 +1399,53 @@ __device__ __forceinline__ float row_ss8(const float* ss, int parts, int ld, int
 }
 
 // Decoder projection for the rows of one decode step (M rows, looped in groups
-// of 16 NT): out[m][n] = rho_m sum_k x[m][k] W[n][k] on the matrix cores,
+// of 16 NT): out[m][n] = sum_k x[m][k] W[n][k] on the matrix cores,
 // C^T[16 columns x 16 rows] += W[16 x 32] X^T[32 x 16] (v_mfma_f32_16x16x32_bf16).
-// A block owns CT consecutive 16-column tiles; its 8 waves split the K steps into
-// contiguous ranges, each wave streaming its slice of the packed W tiles
-// (contiguous 1 KiB loads, every byte read once) and of x (L2-resident) through
-// a kGemmRing-deep register ring. The waves' partial products are summed in LDS
-// in wave order (deterministic), then the epilogue applies rho and:
-//   kEpiQkv    RoPE on q and k (pairs (2i, 2i+1) at the sequence's position),
-//              q to the attention's query buffer, k and v into the paged cache;
-//   kEpiResid  h += out, then the next norm's input bf16(h * g) and the
-//              per-tile sums of h^2 its row scale is built from;
-//   kEpiSwiglu tiles alternate gate / up: act = bf16(silu(gate) * up).
-template <int NT, int CT, int EPI>
-__global__ __launch_bounds__(64 * kGemmWaves) void k_gemm_dec(GemmArgs a) {
-  constexpr int WPB = kGemmWaves, R = kGemmRing;
-  // the wave index (and so the K range and the ring's tail guards) must be
-  // scalar: a guard the compiler sees as divergent becomes an EXEC mask, and
-  // matrix-core instructions do not honour EXEC
+// Block b covers column group b / ksplit (8 consecutive 16-column tiles, one per
+// wave) over K slice b % ksplit. Every wave streams its own packed W tile slice
+// (contiguous 1 KiB loads, each byte read once) through a kProjRing-deep
+// register ring; the 8 waves read the same x slice, so x comes from HBM/L2 once
+// per block and from L1 for the other waves: per block the x bytes are about a
+// quarter of the W bytes at 33 rows, where a block owning one tile over all of
+// K would read twice as much x as W.
+//   kEpiPartial  the block's fp32 partial sums go to part[split][m][n]
+//                (k_proj_reduce adds the slices in order and applies the epilogue);
+//   kEpiSwiglu   (one K slice) tiles alternate gate / up: with the row scale from
+//                the norm's sums of squares, act = bf16(silu(gate) * up).
+template <int NT, int EPI>
+__global__ __launch_bounds__(64 * kProjWaves) void k_proj(GemmArgs a) {
+  constexpr int WPB = kProjWaves, R = kProjRing;
+  // the wave index (and so the tile) is scalar; the ring's tail guards depend
+  // only on kernel arguments, so they are branches: matrix-core instructions do
+  // not honour EXEC, a guard turned into an EXEC mask would not stop them
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 15, quad = lane >> 4;
-  const int tile0 = blockIdx.x * CT;
+  const int grp = blockIdx.x / a.ksplit, split = blockIdx.x - grp * a.ksplit;
+  const int tile = grp * WPB + wave;
   const int K = a.K, KS = K / 64;
-  const int per = (KS + WPB - 1) / WPB;
-  const int ks0 = min(wave * per, KS);
-  const int n = min(ks0 + per, KS) - ks0;
-  __shared__ f32x4 red[WPB][CT][NT][64];
+  const int ks0 = split * KS / a.ksplit;
+  const int n = (split + 1) * KS / a.ksplit - ks0;
+  const int N = 16 * a.n_tiles;
+  const uint4* wt = (const uint4*)a.w + ((size_t)min(tile, a.n_tiles - 1) * KS + ks0) * 128 + lane;
   __shared__ float rho_s[16 * NT];
-  const uint4* Wp = (const uint4*)a.w;
-  const uint4* wt[CT];
-#pragma unroll
-  for (int ct = 0; ct < CT; ++ct) wt[ct] = Wp + ((size_t)min(tile0 + ct, a.n_tiles - 1) * KS + ks0) * 128 + lane;
+  __shared__ f32x4 xch[EPI == kEpiSwiglu ? WPB : 1][NT][64];
 
   for (int m0 = 0; m0 < a.M; m0 += 16 * NT) {
-    f32x4 acc[CT][NT];
+    f32x4 acc[NT];
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[ct][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     const uint16_t* xrow[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
       xrow[nt] = a.x + (size_t)min(m0 + 16 * nt + col, a.M - 1) * K + 64 * ks0 + 16 * quad;
-    struct Stage { uint4 w[CT][2]; uint4 x[NT][2]; };
+    struct Stage { uint4 w[2]; uint4 x[NT][2]; };
     Stage st[R];
-    // step i of the wave's range; past the end the last step again (a cache
-    // hit): the ring stays branch-free
+    // step i of the slice; past the end the last step again (a cache hit):
+    // the ring stays branch-free
     auto load = [&](Stage& S, int i) __attribute__((always_inline)) {
       i = min(i, n - 1);
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct) {
-        S.w[ct][0] = wt[ct][(size_t)i * 128];
-        S.w[ct][1] = wt[ct][(size_t)i * 128 + 64];
-      }
+      S.w[0] = wt[(size_t)i * 128];
+      S.w[1] = wt[(size_t)i * 128 + 64];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         S.x[nt][0] = *(const uint4*)(xrow[nt] + i * 64);
@@ -1460,14 +1454,10 @@ __global__ __launch_bounds__(64 * kGemmWaves) void k_gemm_dec(GemmArgs a) {
     };
     auto mma = [&](const Stage& S) __attribute__((always_inline)) {
 #pragma unroll
-      for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          acc[ct][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[ct][0]), as_bf16x8(S.x[nt][0]),
-                                                                acc[ct][nt], 0, 0, 0);
-          acc[ct][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[ct][1]), as_bf16x8(S.x[nt][1]),
-                                                                acc[ct][nt], 0, 0, 0);
-        }
+      for (int nt = 0; nt < NT; ++nt) {
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[0]), as_bf16x8(S.x[nt][0]), acc[nt], 0, 0, 0);
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[1]), as_bf16x8(S.x[nt][1]), acc[nt], 0, 0, 0);
+      }
     };
     if (n > 0) {
 #pragma unroll
@@ -1480,107 +1470,133 @@ __global__ __launch_bounds__(64 * kGemmWaves) void k_gemm_dec(GemmArgs a) {
         }
       }
     }
+    if constexpr (EPI == kEpiPartial) {
+      if (tile < a.n_tiles) {
+        float* dst = a.part + (size_t)split * a.M * N + 16 * tile + 4 * quad;
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) red[wave][ct][nt][lane] = acc[ct][nt];
-    if (a.ss_in) {  // row scales of this row group, 8 lanes per row
-      for (int t = threadIdx.x; t < 16 * NT * 8; t += 64 * WPB) {
-        const int r = t >> 3, m = m0 + r;
-        const float tot = row_ss8(a.ss_in, a.ss_parts, a.ld_ss, m, t & 7, m < a.M);
-        if ((t & 7) == 0) rho_s[r] = 1.0f / sqrtf(tot * a.inv_norm_dim + a.eps);
-      }
-    }
-    __syncthreads();
-
-    // epilogue: item (tile, row tile, lane) -> row m, columns n .. n+3
-    constexpr int PAIR = EPI == kEpiSwiglu ? 2 : 1;
-    constexpr int ITEMS = CT / PAIR * NT * 64;
-    for (int it = threadIdx.x; it < ITEMS; it += 64 * WPB) {
-      const int ln = it & 63, nt = (it >> 6) % NT, cp = (it >> 6) / NT;
-      const int r = 16 * nt + (ln & 15), m = m0 + r;
-      const bool valid = m < a.M;
-      f32x4 v = red[0][cp * PAIR][nt][ln];
-#pragma unroll
-      for (int w = 1; w < WPB; ++w) v += red[w][cp * PAIR][nt][ln];
-      if constexpr (EPI == kEpiResid) {
-        const int n0 = 16 * (tile0 + cp) + 4 * (ln >> 4);
-        float ss = 0.f;
-        if (valid) {
-          float* hp = a.h + (size_t)m * (16 * a.n_tiles) + n0;  // row stride: hidden = 16 * tiles
-          float4 hv = *(float4*)hp;
-          hv.x += v[0];
-          hv.y += v[1];
-          hv.z += v[2];
-          hv.w += v[3];
-          *(float4*)hp = hv;
-          const uint2 g = *(const uint2*)(a.g_next + n0);
-          uint2 pk;
-          pk.x = f2bf(hv.x * bf2f(g.x & 0xFFFFu)) | (f2bf(hv.y * bf2f(g.x >> 16)) << 16);
-          pk.y = f2bf(hv.z * bf2f(g.y & 0xFFFFu)) | (f2bf(hv.w * bf2f(g.y >> 16)) << 16);
-          *(uint2*)(a.a_out + (size_t)m * (16 * a.n_tiles) + n0) = pk;
-          ss = hv.x * hv.x + hv.y * hv.y + hv.z * hv.z + hv.w * hv.w;
+        for (int nt = 0; nt < NT; ++nt) {
+          const int m = m0 + 16 * nt + col;
+          if (m < a.M) *(float4*)(dst + (size_t)m * N) = make_float4(acc[nt][0], acc[nt][1], acc[nt][2], acc[nt][3]);
         }
-        ss += __shfl_xor(ss, 16);
-        ss += __shfl_xor(ss, 32);
-        if (valid && ln < 16) a.ss_out[(size_t)(tile0 + cp) * a.ld_ss + m] = ss;
-      } else if constexpr (EPI == kEpiSwiglu) {
-        if (valid) {
-          f32x4 u = red[0][cp * 2 + 1][nt][ln];
+      }
+    } else {  // kEpiSwiglu: wave 2j holds gate tile, wave 2j+1 the up tile of the same 16 columns
 #pragma unroll
-          for (int w = 1; w < WPB; ++w) u += red[w][cp * 2 + 1][nt][ln];
+      for (int nt = 0; nt < NT; ++nt) xch[wave][nt][lane] = acc[nt];
+      if (a.ss_in) {
+        for (int t = threadIdx.x; t < 16 * NT * 8; t += 64 * WPB) {
+          const int r = t >> 3, m = m0 + r;
+          const float tot = row_ss8(a.ss_in, a.ss_parts, a.ld_ss, m, t & 7, m < a.M);
+          if ((t & 7) == 0) rho_s[r] = 1.0f / sqrtf(tot * a.inv_norm_dim + a.eps);
+        }
+      }
+      __syncthreads();
+      for (int it = threadIdx.x; it < WPB / 2 * NT * 64; it += 64 * WPB) {
+        const int ln = it & 63, nt = (it >> 6) % NT, pr = (it >> 6) / NT;
+        const int r = 16 * nt + (ln & 15), m = m0 + r;
+        const int pair = grp * (WPB / 2) + pr;
+        if (m < a.M && 2 * pair < a.n_tiles) {
+          const f32x4 gv = xch[2 * pr][nt][ln], uv = xch[2 * pr + 1][nt][ln];
           const float rho = a.ss_in ? rho_s[r] : 1.0f;
           uint32_t o[4];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const float g = v[q] * rho, up = u[q] * rho;
+            const float g = gv[q] * rho, up = uv[q] * rho;
             o[q] = f2bf(g / (1.0f + expf(-g)) * up);
           }
-          const int f0 = 16 * (tile0 / 2 + cp) + 4 * (ln >> 4);
+          const int f0 = 16 * pair + 4 * (ln >> 4);
           *(uint2*)(a.act + (size_t)m * a.F + f0) = make_uint2(o[0] | (o[1] << 16), o[2] | (o[3] << 16));
         }
-      } else {  // kEpiQkv
-        if (valid) {
-          const float rho = a.ss_in ? rho_s[r] : 1.0f;
-          const int D = a.head_dim, qd = a.n_q_heads * D, kd = a.n_kv_heads * D;
-          const int n0 = 16 * (tile0 + cp) + 4 * (ln >> 4);
-          const int sec = n0 < qd ? 0 : n0 < qd + kd ? 1 : 2;
-          const int c0 = sec == 0 ? n0 : sec == 1 ? n0 - qd : n0 - qd - kd;
-          const int head = c0 / D, d = c0 % D;
-          const int pos = a.len0[m] + a.t;
-          float o[4] = {v[0] * rho, v[1] * rho, v[2] * rho, v[3] * rho};
-          if (sec < 2) {
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// Sum of a projection's K-slice partials (in slice order: deterministic), then
+// its epilogue. Block (x, y): row m = y, 4-column groups 256 x .. 256 x + 255.
+//   kEpiQkv    row scale from the norm's sums of squares; RoPE on q and k
+//              (pairs (2i, 2i+1) at the sequence's position); q to the
+//              attention's query buffer, k and v into the paged cache;
+//   kEpiResid  h += out, then the next norm's input bf16(h * g) and the
+//              per-16-column sums of h^2 its row scale is built from.
+template <int EPI>
+__global__ __launch_bounds__(256) void k_proj_reduce(GemmArgs a) {
+  const int m = blockIdx.y, N = 16 * a.n_tiles;
+  const int c4 = blockIdx.x * 256 + threadIdx.x;
+  const int n0 = 4 * c4;
+  const bool valid = n0 < N;
+  float rho = 1.0f;
+  if (EPI == kEpiQkv && a.ss_in) {
+    float t = 0.f;
+    for (int p = threadIdx.x; p < a.ss_parts; p += 256) t += a.ss_in[(size_t)p * a.ld_ss + m];
+    rho = 1.0f / sqrtf(block_reduce_sum(t) * a.inv_norm_dim + a.eps);
+  }
+  float o[4] = {0.f, 0.f, 0.f, 0.f};
+  if (valid) {
+    for (int sp = 0; sp < a.ksplit; ++sp) {
+      const float4 v = *(const float4*)(a.part + ((size_t)sp * a.M + m) * N + n0);
+      o[0] += v.x;
+      o[1] += v.y;
+      o[2] += v.z;
+      o[3] += v.w;
+    }
+  }
+  if constexpr (EPI == kEpiResid) {
+    float ss = 0.f;
+    if (valid) {
+      float* hp = a.h + (size_t)m * N + n0;  // residual row stride: hidden = N
+      float4 hv = *(float4*)hp;
+      hv.x += o[0];
+      hv.y += o[1];
+      hv.z += o[2];
+      hv.w += o[3];
+      *(float4*)hp = hv;
+      const uint2 g = *(const uint2*)(a.g_next + n0);
+      uint2 pk;
+      pk.x = f2bf(hv.x * bf2f(g.x & 0xFFFFu)) | (f2bf(hv.y * bf2f(g.x >> 16)) << 16);
+      pk.y = f2bf(hv.z * bf2f(g.y & 0xFFFFu)) | (f2bf(hv.w * bf2f(g.y >> 16)) << 16);
+      *(uint2*)(a.a_out + (size_t)m * N + n0) = pk;
+      ss = hv.x * hv.x + hv.y * hv.y + hv.z * hv.z + hv.w * hv.w;
+    }
+    ss += __shfl_xor(ss, 1);
+    ss += __shfl_xor(ss, 2);
+    if (valid && (c4 & 3) == 0) a.ss_out[(size_t)(n0 / 16) * a.ld_ss + m] = ss;
+  } else {  // kEpiQkv
+    if (!valid) return;
+    const int D = a.head_dim, qd = a.n_q_heads * D, kd = a.n_kv_heads * D;
+    const int sec = n0 < qd ? 0 : n0 < qd + kd ? 1 : 2;
+    const int c0 = sec == 0 ? n0 : sec == 1 ? n0 - qd : n0 - qd - kd;
+    const int head = c0 / D, d = c0 % D;
+    const int pos = a.len0[m] + a.t;
 #pragma unroll
-            for (int pr = 0; pr < 2; ++pr) {
-              const int i = d / 2 + pr;
-              const double ang = (double)pos * exp2(-(2.0 * i / D) * a.log2_theta);
-              double sn, cs;
-              sincos(ang, &sn, &cs);
-              const float c = (float)cs, s_ = (float)sn;
-              const float x0 = o[2 * pr], x1 = o[2 * pr + 1];
-              o[2 * pr] = x0 * c - x1 * s_;
-              o[2 * pr + 1] = x0 * s_ + x1 * c;
-            }
-          }
-          uint32_t b[4];
+    for (int q = 0; q < 4; ++q) o[q] *= rho;
+    if (sec < 2) {
 #pragma unroll
-          for (int q = 0; q < 4; ++q) b[q] = f2bf(o[q]);
-          if (sec == 0) {
-            const size_t qo = (((size_t)m * a.n_layers + a.layer) * a.n_q_heads + head) * D + d;
-            *(uint2*)(a.q_out + qo) = make_uint2(b[0] | (b[1] << 16), b[2] | (b[3] << 16));
-          } else {
-            const int phys = a.page_table[(size_t)m * a.maxpps + pos / kPage];
-            const int slot = pos % kPage;
-            const size_t base = (((size_t)a.layer * a.max_pages + phys) * a.n_kv_heads + head) * kPage * D;
-            uint16_t* pool = sec == 1 ? a.kpool : a.vpool;
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              pool[base + (sec == 1 ? kswz(slot, d + q) : vswz(slot, d + q))] = (uint16_t)b[q];
-          }
-        }
+      for (int pr = 0; pr < 2; ++pr) {
+        const int i = d / 2 + pr;
+        const double ang = (double)pos * exp2(-(2.0 * i / D) * a.log2_theta);
+        double sn, cs;
+        sincos(ang, &sn, &cs);
+        const float c = (float)cs, s_ = (float)sn;
+        const float x0 = o[2 * pr], x1 = o[2 * pr + 1];
+        o[2 * pr] = x0 * c - x1 * s_;
+        o[2 * pr + 1] = x0 * s_ + x1 * c;
       }
     }
-    __syncthreads();
+    uint32_t b[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) b[q] = f2bf(o[q]);
+    if (sec == 0) {
+      const size_t qo = (((size_t)m * a.n_layers + a.layer) * a.n_q_heads + head) * D + d;
+      *(uint2*)(a.q_out + qo) = make_uint2(b[0] | (b[1] << 16), b[2] | (b[3] << 16));
+    } else {
+      const int phys = a.page_table[(size_t)m * a.maxpps + pos / kPage];
+      const int slot = pos % kPage;
+      const size_t base = (((size_t)a.layer * a.max_pages + phys) * a.n_kv_heads + head) * kPage * D;
+      uint16_t* pool = sec == 1 ? a.kpool : a.vpool;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) pool[base + (sec == 1 ? kswz(slot, d + q) : vswz(slot, d + q))] = (uint16_t)b[q];
+    }
   }
 }
 
@@ -1700,25 +1716,24 @@ hipError_t launch_pack_tiles(const void* w, void* wp, int rows, int K, int strid
 }
 
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Timing* tm) {
-  if (a.K % 64 != 0 || a.M < 1) return hipErrorInvalidValue;
+  if (a.K % 64 != 0 || a.M < 1 || a.n_tiles < 1 || a.ksplit < 1 || a.ksplit > a.K / 64) return hipErrorInvalidValue;
   const int NT = a.M <= 16 ? 1 : a.M <= 32 ? 2 : 3;
-  const dim3 b(64 * kGemmWaves);
-  auto pick = [&](auto k1, auto k2, auto k3, int ct) {
-    const dim3 g((a.n_tiles + ct - 1) / ct);
-    return NT == 1 ? go(k1, g, b, 0, st, t0(tm), t1(tm), a)
-           : NT == 2 ? go(k2, g, b, 0, st, t0(tm), t1(tm), a)
-                     : go(k3, g, b, 0, st, t0(tm), t1(tm), a);
-  };
-  switch (epi) {
-    case kEpiQkv:
-      return pick(k_gemm_dec<1, 1, kEpiQkv>, k_gemm_dec<2, 1, kEpiQkv>, k_gemm_dec<3, 1, kEpiQkv>, 1);
-    case kEpiResid:
-      return pick(k_gemm_dec<1, 1, kEpiResid>, k_gemm_dec<2, 1, kEpiResid>, k_gemm_dec<3, 1, kEpiResid>, 1);
-    case kEpiSwiglu:
-      if (a.n_tiles % 2) return hipErrorInvalidValue;
-      return pick(k_gemm_dec<1, 2, kEpiSwiglu>, k_gemm_dec<2, 2, kEpiSwiglu>, k_gemm_dec<3, 2, kEpiSwiglu>, 2);
+  const dim3 b(64 * kProjWaves);
+  const dim3 g((a.n_tiles + kProjWaves - 1) / kProjWaves * a.ksplit);
+  if (epi == kEpiSwiglu) {
+    if (a.n_tiles % 2 || a.ksplit != 1) return hipErrorInvalidValue;
+    return NT == 1 ? go(k_proj<1, kEpiSwiglu>, g, b, 0, st, t0(tm), t1(tm), a)
+           : NT == 2 ? go(k_proj<2, kEpiSwiglu>, g, b, 0, st, t0(tm), t1(tm), a)
+                     : go(k_proj<3, kEpiSwiglu>, g, b, 0, st, t0(tm), t1(tm), a);
   }
-  return hipErrorInvalidValue;
+  if (epi != kEpiQkv && epi != kEpiResid) return hipErrorInvalidValue;
+  hipError_t e = NT == 1 ? go(k_proj<1, kEpiPartial>, g, b, 0, st, t0(tm), nullptr, a)
+                 : NT == 2 ? go(k_proj<2, kEpiPartial>, g, b, 0, st, t0(tm), nullptr, a)
+                           : go(k_proj<3, kEpiPartial>, g, b, 0, st, t0(tm), nullptr, a);
+  if (e != hipSuccess) return e;
+  const dim3 gr((4 * a.n_tiles + 255) / 256, a.M);
+  if (epi == kEpiQkv) return go(k_proj_reduce<kEpiQkv>, gr, dim3(256), 0, st, nullptr, t1(tm), a);
+  return go(k_proj_reduce<kEpiResid>, gr, dim3(256), 0, st, nullptr, t1(tm), a);
 }
 
 hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Timing* tm) {
