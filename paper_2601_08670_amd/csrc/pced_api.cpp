@@ -82,6 +82,7 @@ struct Layout {
       total;
   int rows_pad, nblk_fuse, nchunk, max_work;
   size_t part_slots;
+  size_t part_cols;  // slices x columns one row of the projection partial buffer holds
 };
 
 Layout make_layout(const pced_config& c) {
@@ -140,9 +141,11 @@ Layout make_layout(const pced_config& c) {
   L.dec_act = take(dec * S * c.ffn_dim * 2);
   L.dec_ss = take(dec * (c.hidden / 16) * S * 4);
   L.dec_rho = take(dec * S * 4);
-  // K-slice partial sums of a projection: [slices][S][columns], columns <= max(QKV width, hidden)
-  const size_t proj_cols = std::max<size_t>((size_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim, c.hidden);
-  L.dec_part = take(dec * kProjMaxSplit * S * proj_cols * 4);
+  // K-slice partial sums of a projection: [slices][S][columns]
+  L.part_cols = (size_t)kProjMaxSplit *
+                std::max<size_t>({(size_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim, (size_t)c.hidden,
+                                  (size_t)c.ffn_dim});
+  L.dec_part = take(dec * S * L.part_cols * 4);
   L.total = o;
   return L;
 }
@@ -586,9 +589,18 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
   g.log2_theta = std::log2((double)cfg.rope_theta);
   g.part = c->at<float>(c->lay.dec_part);
   // K slices per projection: about one block per compute unit (8-tile column groups)
+  // K slices per projection: about one block per compute unit, more where the
+  // staged x slice would not fit in LDS
+  const int stage_rows = std::min(S, S <= 16 ? 16 : S <= 32 ? 32 : 48);
   auto slices = [&](int n_tiles, int K) {
-    const int groups = ceil_div(n_tiles, 8);
-    return std::max(1, std::min({kProjMaxSplit, K / 64, c->num_cus / groups}));
+    const int groups = ceil_div(n_tiles, 8 * proj_tiles_per_wave(n_tiles));
+    int ks = std::max(1, std::min({kProjMaxSplit, K / 64, c->num_cus / groups}));
+    while (ks < std::min(kProjMaxSplit, K / 64) && proj_lds_bytes(stage_rows, K, ks) > kProjMaxLds) ++ks;
+    return ks;
+  };
+  auto fits = [&](const GemmArgs& p) {
+    return proj_lds_bytes(stage_rows, p.K, p.ksplit) <= kProjMaxLds &&
+           (size_t)p.ksplit * 16 * p.n_tiles <= c->lay.part_cols;
   };
   const double F = cfg.ffn_dim;
   for (int l = 0; l < cfg.n_layers; ++l) {
@@ -607,6 +619,7 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
       q.ss_in = ss;
       ProfScope ps(c, PCED_PROF_QKV, (double)(qd + 2 * kd) * H * 2 + (double)S * (H * 2 + (qd + 2 * kd) * 2),
                    2.0 * S * (qd + 2 * kd) * H);
+      if (!fits(q)) return fail(PCED_ERR_UNSUPPORTED, "QKV projection does not fit the partial buffer or LDS");
       HIP_OK(launch_gemm(q, kEpiQkv, st, ps.timing()));
     }
     at.layer = l;
@@ -629,6 +642,7 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
       o.g_next = (const uint16_t*)(lw + ml.mlp_norm);
       ProfScope ps(c, PCED_PROF_OPROJ, (double)H * qd * 2 + (double)S * (qd * 2 + H * 10),
                    2.0 * S * H * qd);
+      if (!fits(o)) return fail(PCED_ERR_UNSUPPORTED, "O projection does not fit the partial buffer or LDS");
       HIP_OK(launch_gemm(o, kEpiResid, st, ps.timing()));
     }
     {  // norm + gate/up + SwiGLU
@@ -637,9 +651,10 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
       u.x = an;
       u.K = H;
       u.n_tiles = 2 * cfg.ffn_dim / 16;
-      u.ksplit = 1;
+      u.ksplit = slices(u.n_tiles, H);
       u.ss_in = ss;
       ProfScope ps(c, PCED_PROF_GATEUP, 2.0 * F * H * 2 + (double)S * (H * 2 + F * 2), 4.0 * S * F * H);
+      if (!fits(u)) return fail(PCED_ERR_UNSUPPORTED, "gate/up projection does not fit the partial buffer or LDS");
       HIP_OK(launch_gemm(u, kEpiSwiglu, st, ps.timing()));
     }
     {  // down projection + residual; the next norm's input
@@ -651,6 +666,7 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
       d.ksplit = slices(d.n_tiles, cfg.ffn_dim);
       d.g_next = g_next;
       ProfScope ps(c, PCED_PROF_DOWN, F * H * 2 + (double)S * (F * 2 + H * 10), 2.0 * S * H * F);
+      if (!fits(d)) return fail(PCED_ERR_UNSUPPORTED, "down projection does not fit the partial buffer or LDS");
       HIP_OK(launch_gemm(d, kEpiResid, st, ps.timing()));
     }
   }

@@ -150,13 +150,14 @@ struct SynthArgs {
 // for the M step rows, W packed in 16-row tiles (k_pack_w_bf16 layout), with an
 // epilogue per projection.
 enum GemmEpi { kEpiQkv = 0, kEpiResid = 1, kEpiSwiglu = 2, kEpiPartial = 3 };
-constexpr int kProjMaxSplit = 8;   // K slices of a projection (partial buffer sized for this many)
+constexpr int kProjMaxSplit = 16;  // K slices of a projection (partial buffer sized for this many)
+constexpr size_t kProjMaxLds = 150 * 1024;  // staged x slice of a projection block
 struct GemmArgs {
   const void* w;            // packed tiles of this projection
   const uint16_t* x;        // [M][K] bf16 input rows
   int M, K, n_tiles;        // rows, inner dimension, 16-column output tiles
-  int ksplit;               // K slices (blocks per 8-tile column group); 1 for kEpiSwiglu
-  float* part;              // [ksplit][M][16 n_tiles] fp32 partial sums (kEpiQkv, kEpiResid)
+  int ksplit;               // K slices (blocks per column group)
+  float* part;              // [ksplit][M][16 n_tiles] fp32 partial sums
   // row scale rho_m = 1/sqrt(sum_p ss_in[p][m] * inv_norm_dim + eps), or 1 without ss_in
   const float* ss_in;       // [ss_parts][ld_ss]
   int ss_parts, ld_ss;
@@ -218,6 +219,8 @@ hipError_t launch_copy_rows(const void* src, void* dst, size_t nbytes, hipStream
 // pack a [rows][K] bf16 matrix into 16-row tiles, tile i going to slot i * stride + offset
 hipError_t launch_pack_tiles(const void* w, void* wp, int rows, int K, int stride, int offset, hipStream_t st);
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Timing* tm = nullptr);
+int proj_tiles_per_wave(int n_tiles);                // 16-column tiles per wave of a projection block
+size_t proj_lds_bytes(int rows, int K, int ksplit);  // LDS of a projection block
 hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Timing* tm = nullptr);
 // rho[m] = 1/sqrt(sum_p ss[p][m] * inv_dim + eps) for m < M
 hipError_t launch_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps, float* rho,

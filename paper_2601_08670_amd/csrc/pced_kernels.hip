@@ -1383,8 +1383,7 @@ __global__ __launch_bounds__(256) void k_synth(SynthArgs a) {
 
 // ------------------------------------------------------------ decoder stack
 
-constexpr int kProjWaves = 8;  // waves per projection block, one 16-column tile each
-constexpr int kProjRing = 4;   // K steps in flight per wave
+constexpr int kProjWaves = 8;  // waves per projection block
 
 // sum over the ss partials of row m, 8 lanes per row (lanes 8r .. 8r+7 of a
 // wave hold row r); every lane of the group returns the total
@@ -1398,138 +1397,149 @@ __device__ __forceinline__ float row_ss8(const float* ss, int parts, int ld, int
   return t;
 }
 
-// Decoder projection for the rows of one decode step (M rows, looped in groups
-// of 16 NT): out[m][n] = sum_k x[m][k] W[n][k] on the matrix cores,
-// C^T[16 columns x 16 rows] += W[16 x 32] X^T[32 x 16] (v_mfma_f32_16x16x32_bf16).
-// Block b covers column group b / ksplit (8 consecutive 16-column tiles, one per
-// wave) over K slice b % ksplit. Every wave streams its own packed W tile slice
-// (contiguous 1 KiB loads, each byte read once) through a kProjRing-deep
-// register ring; the 8 waves read the same x slice, so x comes from HBM/L2 once
-// per block and from L1 for the other waves: per block the x bytes are about a
-// quarter of the W bytes at 33 rows, where a block owning one tile over all of
-// K would read twice as much x as W.
-//   kEpiPartial  the block's fp32 partial sums go to part[split][m][n]
-//                (k_proj_reduce adds the slices in order and applies the epilogue);
-//   kEpiSwiglu   (one K slice) tiles alternate gate / up: with the row scale from
-//                the norm's sums of squares, act = bf16(silu(gate) * up).
-template <int NT, int EPI>
+// Decoder projection for the rows of one decode step (M rows, in groups of up
+// to 16 NT): K-slice partial sums part[split][m][n] = sum_{k in slice}
+// x[m][k] W[n][k] on the matrix cores, C^T[16 columns x 16 rows] += W[16 x 32]
+// X^T[32 x 16] (v_mfma_f32_16x16x32_bf16); k_proj_reduce adds the slices in
+// order and applies the projection's epilogue.
+// Block b covers column group b / ksplit (8 TPW consecutive 16-column tiles,
+// TPW per wave) over K slice b % ksplit. The block first stages its x slice
+// (rows x slice, row-major, rows padded by 16 bytes against bank conflicts) in
+// LDS with coalesced loads; each wave then streams only its packed W tiles
+// (contiguous 1 KiB loads, every byte read once) through an R-deep register ring
+// and reads its x operands from LDS, so the whole register ring holds W bytes
+// in flight. The barrier after staging waits on LDS only; it does not drain the
+// ring.
+template <int NT, int TPW>
 __global__ __launch_bounds__(64 * kProjWaves) void k_proj(GemmArgs a) {
-  constexpr int WPB = kProjWaves, R = kProjRing;
-  // the wave index (and so the tile) is scalar; the ring's tail guards depend
+  constexpr int WPB = kProjWaves, CT = WPB * TPW, R = TPW == 1 ? 8 : 5;
+  extern __shared__ __align__(16) uint16_t xs[];
+  // the wave index (and so the tiles) is scalar; the ring's tail guards depend
   // only on kernel arguments, so they are branches: matrix-core instructions do
   // not honour EXEC, a guard turned into an EXEC mask would not stop them
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 15, quad = lane >> 4;
   const int grp = blockIdx.x / a.ksplit, split = blockIdx.x - grp * a.ksplit;
-  const int tile = grp * WPB + wave;
   const int K = a.K, KS = K / 64;
   const int ks0 = split * KS / a.ksplit;
   const int n = (split + 1) * KS / a.ksplit - ks0;
+  const int LDX = 64 * n + 8;  // staged row length (elements)
   const int N = 16 * a.n_tiles;
-  const uint4* wt = (const uint4*)a.w + ((size_t)min(tile, a.n_tiles - 1) * KS + ks0) * 128 + lane;
-  __shared__ float rho_s[16 * NT];
-  __shared__ f32x4 xch[EPI == kEpiSwiglu ? WPB : 1][NT][64];
+  const uint4* wt[TPW];
+#pragma unroll
+  for (int tt = 0; tt < TPW; ++tt)
+    wt[tt] = (const uint4*)a.w + ((size_t)min(grp * CT + wave * TPW + tt, a.n_tiles - 1) * KS + ks0) * 128 + lane;
 
   for (int m0 = 0; m0 < a.M; m0 += 16 * NT) {
-    f32x4 acc[NT];
+    const int rows = min(16 * NT, a.M - m0);
+    f32x4 acc[TPW][NT];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const uint16_t* xrow[NT];
+    for (int tt = 0; tt < TPW; ++tt)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-      xrow[nt] = a.x + (size_t)min(m0 + 16 * nt + col, a.M - 1) * K + 64 * ks0 + 16 * quad;
-    struct Stage { uint4 w[2]; uint4 x[NT][2]; };
+      for (int nt = 0; nt < NT; ++nt) acc[tt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    struct Stage { uint4 w[TPW][2]; };
     Stage st[R];
-    // step i of the slice; past the end the last step again (a cache hit):
-    // the ring stays branch-free
     auto load = [&](Stage& S, int i) __attribute__((always_inline)) {
-      i = min(i, n - 1);
-      S.w[0] = wt[(size_t)i * 128];
-      S.w[1] = wt[(size_t)i * 128 + 64];
+      i = min(i, n - 1);  // past the end: the last step again (a cache hit), the ring stays branch-free
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        S.x[nt][0] = *(const uint4*)(xrow[nt] + i * 64);
-        S.x[nt][1] = *(const uint4*)(xrow[nt] + i * 64 + 8);
+      for (int tt = 0; tt < TPW; ++tt) {
+        S.w[tt][0] = wt[tt][(size_t)i * 128];
+        S.w[tt][1] = wt[tt][(size_t)i * 128 + 64];
       }
     };
-    auto mma = [&](const Stage& S) __attribute__((always_inline)) {
+    // x operand rows of this lane in LDS (rows past the group's end read the last row)
+    const uint16_t* xl[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) xl[nt] = xs + (size_t)min(16 * nt + col, rows - 1) * LDX + 16 * quad;
+    auto mma = [&](const Stage& S, int i) __attribute__((always_inline)) {
+      uint4 xv[NT][2];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[0]), as_bf16x8(S.x[nt][0]), acc[nt], 0, 0, 0);
-        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[1]), as_bf16x8(S.x[nt][1]), acc[nt], 0, 0, 0);
+        xv[nt][0] = *(const uint4*)(xl[nt] + 64 * i);
+        xv[nt][1] = *(const uint4*)(xl[nt] + 64 * i + 8);
       }
-    };
-    if (n > 0) {
 #pragma unroll
-      for (int j = 0; j < R; ++j) load(st[j], j);
-      for (int i = 0; i < n; i += R) {
+      for (int tt = 0; tt < TPW; ++tt)
 #pragma unroll
-        for (int j = 0; j < R; ++j) {
-          if (i + j < n) mma(st[j]);
-          load(st[j], i + j + R);
+        for (int nt = 0; nt < NT; ++nt) {
+          acc[tt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[tt][0]), as_bf16x8(xv[nt][0]),
+                                                                acc[tt][nt], 0, 0, 0);
+          acc[tt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[tt][1]), as_bf16x8(xv[nt][1]),
+                                                                acc[tt][nt], 0, 0, 0);
         }
+    };
+#pragma unroll
+    for (int j = 0; j < R; ++j) load(st[j], j);
+    // stage the x slice: units of 8 elements, consecutive threads along a row
+    const int upr = 8 * n;  // units per row
+    for (int u = threadIdx.x; u < rows * upr; u += 64 * WPB) {
+      const int r = u / upr, c = u - r * upr;
+      *(uint4*)(xs + (size_t)r * LDX + 8 * c) = *(const uint4*)(a.x + (size_t)(m0 + r) * K + 64 * ks0 + 8 * c);
+    }
+    __syncthreads();
+    for (int i = 0; i < n; i += R) {
+#pragma unroll
+      for (int j = 0; j < R; ++j) {
+        if (i + j < n) mma(st[j], i + j);
+        load(st[j], i + j + R);
       }
     }
-    if constexpr (EPI == kEpiPartial) {
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      const int tile = grp * CT + wave * TPW + tt;
       if (tile < a.n_tiles) {
         float* dst = a.part + (size_t)split * a.M * N + 16 * tile + 4 * quad;
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
           const int m = m0 + 16 * nt + col;
-          if (m < a.M) *(float4*)(dst + (size_t)m * N) = make_float4(acc[nt][0], acc[nt][1], acc[nt][2], acc[nt][3]);
+          if (m < a.M)
+            *(float4*)(dst + (size_t)m * N) = make_float4(acc[tt][nt][0], acc[tt][nt][1], acc[tt][nt][2], acc[tt][nt][3]);
         }
       }
-    } else {  // kEpiSwiglu: wave 2j holds gate tile, wave 2j+1 the up tile of the same 16 columns
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) xch[wave][nt][lane] = acc[nt];
-      if (a.ss_in) {
-        for (int t = threadIdx.x; t < 16 * NT * 8; t += 64 * WPB) {
-          const int r = t >> 3, m = m0 + r;
-          const float tot = row_ss8(a.ss_in, a.ss_parts, a.ld_ss, m, t & 7, m < a.M);
-          if ((t & 7) == 0) rho_s[r] = 1.0f / sqrtf(tot * a.inv_norm_dim + a.eps);
-        }
-      }
-      __syncthreads();
-      for (int it = threadIdx.x; it < WPB / 2 * NT * 64; it += 64 * WPB) {
-        const int ln = it & 63, nt = (it >> 6) % NT, pr = (it >> 6) / NT;
-        const int r = 16 * nt + (ln & 15), m = m0 + r;
-        const int pair = grp * (WPB / 2) + pr;
-        if (m < a.M && 2 * pair < a.n_tiles) {
-          const f32x4 gv = xch[2 * pr][nt][ln], uv = xch[2 * pr + 1][nt][ln];
-          const float rho = a.ss_in ? rho_s[r] : 1.0f;
-          uint32_t o[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float g = gv[q] * rho, up = uv[q] * rho;
-            o[q] = f2bf(g / (1.0f + expf(-g)) * up);
-          }
-          const int f0 = 16 * pair + 4 * (ln >> 4);
-          *(uint2*)(a.act + (size_t)m * a.F + f0) = make_uint2(o[0] | (o[1] << 16), o[2] | (o[3] << 16));
-        }
-      }
-      __syncthreads();
     }
+    __syncthreads();  // the next row group restages xs
   }
 }
 
 // Sum of a projection's K-slice partials (in slice order: deterministic), then
-// its epilogue. Block (x, y): row m = y, 4-column groups 256 x .. 256 x + 255.
+// its epilogue. Block (x, y): row m = y, 4-column output groups 256 x .. 256 x + 255.
 //   kEpiQkv    row scale from the norm's sums of squares; RoPE on q and k
 //              (pairs (2i, 2i+1) at the sequence's position); q to the
 //              attention's query buffer, k and v into the paged cache;
 //   kEpiResid  h += out, then the next norm's input bf16(h * g) and the
-//              per-16-column sums of h^2 its row scale is built from.
+//              per-16-column sums of h^2 its row scale is built from;
+//   kEpiSwiglu packed tiles alternate gate / up (16 columns each): with the row
+//              scale, act = bf16(silu(gate) * up) for the F MLP columns.
 template <int EPI>
 __global__ __launch_bounds__(256) void k_proj_reduce(GemmArgs a) {
   const int m = blockIdx.y, N = 16 * a.n_tiles;
   const int c4 = blockIdx.x * 256 + threadIdx.x;
   const int n0 = 4 * c4;
-  const bool valid = n0 < N;
+  const bool valid = n0 < (EPI == kEpiSwiglu ? N / 2 : N);
   float rho = 1.0f;
-  if (EPI == kEpiQkv && a.ss_in) {
+  if (EPI != kEpiResid && a.ss_in) {
     float t = 0.f;
     for (int p = threadIdx.x; p < a.ss_parts; p += 256) t += a.ss_in[(size_t)p * a.ld_ss + m];
     rho = 1.0f / sqrtf(block_reduce_sum(t) * a.inv_norm_dim + a.eps);
+  }
+  if constexpr (EPI == kEpiSwiglu) {
+    if (!valid) return;
+    const int ng = 32 * (n0 / 16) + n0 % 16;  // gate column in the interleaved tiles; up is 16 further
+    float g[4] = {0.f, 0.f, 0.f, 0.f}, u[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < a.ksplit; ++sp) {
+      const float* pr = a.part + ((size_t)sp * a.M + m) * N + ng;
+      const float4 gv = *(const float4*)pr, uv = *(const float4*)(pr + 16);
+      g[0] += gv.x; g[1] += gv.y; g[2] += gv.z; g[3] += gv.w;
+      u[0] += uv.x; u[1] += uv.y; u[2] += uv.z; u[3] += uv.w;
+    }
+    uint32_t o[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float gg = g[q] * rho, uu = u[q] * rho;
+      o[q] = f2bf(gg / (1.0f + expf(-gg)) * uu);
+    }
+    *(uint2*)(a.act + (size_t)m * a.F + n0) = make_uint2(o[0] | (o[1] << 16), o[2] | (o[3] << 16));
+    return;
   }
   float o[4] = {0.f, 0.f, 0.f, 0.f};
   if (valid) {
@@ -1715,25 +1725,40 @@ hipError_t launch_pack_tiles(const void* w, void* wp, int rows, int K, int strid
   return hipGetLastError();
 }
 
+int proj_tiles_per_wave(int n_tiles) { return n_tiles >= 1024 ? 2 : 1; }
+
+size_t proj_lds_bytes(int rows, int K, int ksplit) {
+  const int n = (K / 64 + ksplit - 1) / ksplit;  // longest slice
+  return (size_t)rows * (64 * n + 8) * 2;
+}
+
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Timing* tm) {
   if (a.K % 64 != 0 || a.M < 1 || a.n_tiles < 1 || a.ksplit < 1 || a.ksplit > a.K / 64) return hipErrorInvalidValue;
+  if (epi == kEpiSwiglu && a.n_tiles % 2) return hipErrorInvalidValue;
   const int NT = a.M <= 16 ? 1 : a.M <= 32 ? 2 : 3;
+  const int tpw = proj_tiles_per_wave(a.n_tiles);
+  const size_t lds = proj_lds_bytes(min(a.M, 16 * NT), a.K, a.ksplit);
+  if (lds > kProjMaxLds) return hipErrorInvalidValue;
   const dim3 b(64 * kProjWaves);
-  const dim3 g((a.n_tiles + kProjWaves - 1) / kProjWaves * a.ksplit);
-  if (epi == kEpiSwiglu) {
-    if (a.n_tiles % 2 || a.ksplit != 1) return hipErrorInvalidValue;
-    return NT == 1 ? go(k_proj<1, kEpiSwiglu>, g, b, 0, st, t0(tm), t1(tm), a)
-           : NT == 2 ? go(k_proj<2, kEpiSwiglu>, g, b, 0, st, t0(tm), t1(tm), a)
-                     : go(k_proj<3, kEpiSwiglu>, g, b, 0, st, t0(tm), t1(tm), a);
-  }
-  if (epi != kEpiQkv && epi != kEpiResid) return hipErrorInvalidValue;
-  hipError_t e = NT == 1 ? go(k_proj<1, kEpiPartial>, g, b, 0, st, t0(tm), nullptr, a)
-                 : NT == 2 ? go(k_proj<2, kEpiPartial>, g, b, 0, st, t0(tm), nullptr, a)
-                           : go(k_proj<3, kEpiPartial>, g, b, 0, st, t0(tm), nullptr, a);
+  const dim3 g((a.n_tiles + kProjWaves * tpw - 1) / (kProjWaves * tpw) * a.ksplit);
+  hipError_t e;
+  if (tpw == 1)
+    e = NT == 1 ? go(k_proj<1, 1>, g, b, lds, st, t0(tm), nullptr, a)
+        : NT == 2 ? go(k_proj<2, 1>, g, b, lds, st, t0(tm), nullptr, a)
+                  : go(k_proj<3, 1>, g, b, lds, st, t0(tm), nullptr, a);
+  else
+    e = NT == 1 ? go(k_proj<1, 2>, g, b, lds, st, t0(tm), nullptr, a)
+        : NT == 2 ? go(k_proj<2, 2>, g, b, lds, st, t0(tm), nullptr, a)
+                  : go(k_proj<3, 2>, g, b, lds, st, t0(tm), nullptr, a);
   if (e != hipSuccess) return e;
-  const dim3 gr((4 * a.n_tiles + 255) / 256, a.M);
-  if (epi == kEpiQkv) return go(k_proj_reduce<kEpiQkv>, gr, dim3(256), 0, st, nullptr, t1(tm), a);
-  return go(k_proj_reduce<kEpiResid>, gr, dim3(256), 0, st, nullptr, t1(tm), a);
+  const int outc = epi == kEpiSwiglu ? 8 * a.n_tiles : 16 * a.n_tiles;  // output columns
+  const dim3 gr((outc / 4 + 255) / 256, a.M);
+  switch (epi) {
+    case kEpiQkv: return go(k_proj_reduce<kEpiQkv>, gr, dim3(256), 0, st, nullptr, t1(tm), a);
+    case kEpiResid: return go(k_proj_reduce<kEpiResid>, gr, dim3(256), 0, st, nullptr, t1(tm), a);
+    case kEpiSwiglu: return go(k_proj_reduce<kEpiSwiglu>, gr, dim3(256), 0, st, nullptr, t1(tm), a);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Timing* tm) {
