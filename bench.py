@@ -232,7 +232,8 @@ def model_timing(wl, K, Wm, dev) -> dict:
     g = wl.geom
     spec = ModelSpec(g, ffn_dim=14336, rope_theta=500000.0, seed=wl.seed)
     t0 = time.time()
-    sess = session_for_workload(wl, device=dev, extra_tokens=max(K, Wm) + 1, load_now=False,
+    suffix = 64  # query-suffix tokens appended to every cache by the timed prefill
+    sess = session_for_workload(wl, device=dev, extra_tokens=max(K, Wm) + suffix + 1, load_now=False,
                                 ffn_dim=spec.ffn_dim, rope_theta=int(spec.rope_theta))
     src = load_workload(sess, wl)
     model = sess.pack_model(lambda l: [spec.device(n, l, dev) for n in LAYER_TENSORS],
@@ -263,12 +264,29 @@ def model_timing(wl, K, Wm, dev) -> dict:
     ms_ev, prof = timed(True)
     log(f"[bench] model with per-launch events: {ms_ev / K:.3f} ms/step")
     kernels = kernel_table(prof, ms_ev)
+
+    # query-suffix prefill: `suffix` tokens into every cache, chunked token-parallel
+    from pced_inputs.model import suffix_tokens
+    stoks = torch.from_numpy(suffix_tokens(wl.seed, sess.B, suffix, g.vocab)).to(dev)
+    prefill_ms = []
+    for _ in range(2):  # the first run warms up the chunk shapes
+        load_workload(sess, wl, src=src)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(torch.cuda.current_stream())
+        sess.ctx.pced_model_prefill(model, suffix, stoks)
+        b.record(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        prefill_ms.append(a.elapsed_time(b))
+    log(f"[bench] model prefill of {suffix} suffix tokens x {sess.S} sequences: {prefill_ms[-1]:.2f} ms")
     weight_bytes = float(model.numel())
     del sess, model, Wt, src
     torch.cuda.empty_cache()
     return {"metric": "PCED decode steps/sec at N docs, through the decoder stack", "value": K / (ms_plain * 1e-3),
             "unit": "steps/s", "ms_per_step": ms_plain / K, "ms_per_step_with_launch_events": ms_ev / K,
             "steps": K, "warmup": Wm,
+            "prefill": {"suffix_tokens": suffix, "sequences": int(wl.n_seqs), "ms": prefill_ms[-1],
+                        "tokens_per_s": suffix * wl.n_seqs / (prefill_ms[-1] * 1e-3)},
             "model": {"layers": g.n_layers, "hidden": g.hidden, "ffn_dim": spec.ffn_dim, "q_heads": g.n_q_heads,
                       "kv_heads": g.n_kv_heads, "head_dim": g.head_dim, "vocab": g.vocab,
                       "rope_theta": spec.rope_theta, "weights": "random-init bf16",

@@ -79,7 +79,10 @@ struct Layout {
       load_items, src_k, src_v, meta_end;
   size_t chunk_info, seg, nparts, work_pages, tick_fuse, tick_beta, prev_tok, beta, part_acc, part_ml, x, logits,
       fuse_part, lse_part, jsd_part, agg_lse, syn_q, syn_k, syn_v, dec_h, dec_a, dec_act, dec_ss, dec_rho, dec_part,
+      pf_len0, pf_pt, pf_tok, pf_nparts, pf_h, pf_a, pf_act, pf_ss, pf_q, pf_x, pf_part_acc, pf_part_ml, pf_proj,
       total;
+  int pf_rows;          // rows of one prefill chunk (sequences x suffix tokens)
+  size_t pf_proj_cols;  // slices x columns per row of the prefill projection partials
   int rows_pad, nblk_fuse, nchunk, max_work;
   size_t part_slots;
   size_t part_cols;  // slices x columns one row of the projection partial buffer holds
@@ -92,7 +95,11 @@ Layout make_layout(const pced_config& c) {
   L.rows_pad = ceil_div(c.max_seqs, kLmRowsPad) * kLmRowsPad;
   L.nblk_fuse = ceil_div(c.vocab, kFuseBlock);
   L.nchunk = ceil_div(c.vocab, kBetaChunk);
-  L.max_work = c.max_pages;  // every attention chunk holds at least one page
+  // every attention chunk holds at least one page: chunks <= pages in use (a
+  // prefill chunk's rows count their shared pages once per row)
+  L.max_work = c.max_pages;
+  if (c.ffn_dim > 0)
+    L.max_work = std::max<long>(L.max_work, (long)std::max(c.max_seqs, kPrefillRows) * c.max_pages_per_seq);
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes); return r; };
   // metadata block, uploaded by one copy at load
@@ -146,6 +153,23 @@ Layout make_layout(const pced_config& c) {
                 std::max<size_t>({(size_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim, (size_t)c.hidden,
                                   (size_t)c.ffn_dim});
   L.dec_part = take(dec * S * L.part_cols * 4);
+  // prefill chunk (ffn_dim > 0): up to pf_rows (sequence, suffix token) rows per pass
+  L.pf_rows = dec ? std::max(c.max_seqs, kPrefillRows) : 0;
+  const size_t PR = L.pf_rows;
+  L.pf_proj_cols = L.part_cols;
+  L.pf_len0 = take(PR * 4);
+  L.pf_pt = take(PR * c.max_pages_per_seq * 4);
+  L.pf_tok = take(PR * 4);
+  L.pf_nparts = take(PR * 4);
+  L.pf_h = take(PR * c.hidden * 4);
+  L.pf_a = take(PR * c.hidden * 2);
+  L.pf_act = take(PR * c.ffn_dim * 2);
+  L.pf_ss = take((c.hidden / 16) * PR * 4);
+  L.pf_q = take(PR * c.n_q_heads * c.head_dim * 2);
+  L.pf_x = take(PR * c.hidden * 2);
+  L.pf_part_acc = take(PR * c.n_kv_heads * kPrefillParts * G * c.head_dim * 4);
+  L.pf_part_ml = take(PR * c.n_kv_heads * kPrefillParts * G * 2 * 4);
+  L.pf_proj = take(PR * L.pf_proj_cols * 4);
   L.total = o;
   return L;
 }
@@ -259,10 +283,17 @@ void plan_stats(const std::vector<long>& pre, long P, long C, AttnPlan* out) {
 // wave starts in the first round and streams the same number of pages), at
 // least P/64 (one page id per lane), raised when a chunk would meet more
 // sequences than a wave can stage q rows for.
+AttnPlan plan_for_lengths(const pced_ctx* c, const std::vector<int>& lens);
+
 AttnPlan plan_attention(const pced_ctx* c) {
-  const int S = c->S;
+  return plan_for_lengths(c, std::vector<int>(c->len.begin(), c->len.end()));
+}
+
+// The same plan for rows of the given lengths (before the step's append).
+AttnPlan plan_for_lengths(const pced_ctx* c, const std::vector<int>& lens) {
+  const int S = (int)lens.size();
   std::vector<long> pre(S + 1, 0);
-  for (int s = 0; s < S; ++s) pre[s + 1] = pre[s] + ceil_div(c->len[s] + 1, kPage);
+  for (int s = 0; s < S; ++s) pre[s + 1] = pre[s] + ceil_div(lens[s] + 1, kPage);
   const long P = pre[S];
   long cap = std::max<long>(1, (long)c->num_cus * c->attn_waves_per_cu / c->cfg.n_kv_heads);
   if (c->cfg.max_attn_chunks > 0) cap = std::min<long>(cap, c->cfg.max_attn_chunks);
@@ -476,29 +507,62 @@ ModelLayout model_layout(const pced_config& c) {
   return m;
 }
 
-// Embedding plus every decoder layer for the new token of each sequence
-// (appending its K/V rows). in_tok: the queries' tokens, stride tok_stride.
-// Leaves the residual stream in dec_h and bf16(h * g_final) in dec_a.
-pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_tok, int tok_stride,
-                              float* attn_out, hipStream_t st) {
+// Rows of one pass through the decoder stack and the buffers they use. A decode
+// step has one row per sequence; a prefill chunk has one row per (sequence,
+// suffix token), each a virtual sequence that shares its base sequence's pages
+// and ends at its own token (so attention over it is causal by construction).
+struct FwdRows {
+  int M = 0;
+  std::vector<int> lens;             // host: length of each row's sequence before its append
+  const int32_t* len0 = nullptr;     // device [M]: the row's length minus the step counter t
+  const int32_t* page_table = nullptr;  // device [M][max_pages_per_seq]
+  int32_t* nparts = nullptr;         // device [M]
+  const int32_t* tok = nullptr;      // embedding token of row r: tok[tok_map[r] * tok_stride]
+  const int32_t* tok_map = nullptr;
+  int tok_stride = 1;
+  float* h = nullptr;
+  uint16_t* a = nullptr;
+  uint16_t* act = nullptr;
+  float* ss = nullptr;
+  int ld_ss = 0;
+  uint16_t* q = nullptr;             // attention queries: [M][L][Hq][D] (per_layer_q) or [M][Hq][D]
+  bool per_layer_q = true;
+  void* x = nullptr;                 // attention output [M][hidden]
+  float* part_acc = nullptr;
+  float* part_ml = nullptr;
+  size_t part_slots = 0;             // (row, kv-head, partial) slots of the attention partials
+  float* proj_part = nullptr;
+  size_t proj_cols = 0;              // slices x columns per row of the projection partials
+  float* attn_out = nullptr;
+};
+
+AttnPlan plan_for_lengths(const pced_ctx* c, const std::vector<int>& lens);
+
+// Embedding plus every decoder layer for the rows (appending their K/V rows).
+// Leaves the residual stream in rows.h and bf16(h * g_final) in rows.a.
+pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, hipStream_t st) {
   const pced_config& cfg = c->cfg;
   const ModelLayout ml = model_layout(cfg);
-  const int S = c->S, H = cfg.hidden, D = cfg.head_dim;
+  const int M = R.M, H = cfg.hidden, D = cfg.head_dim;
   const int qd = cfg.n_q_heads * D, kd = cfg.n_kv_heads * D;
-  const AttnPlan plan = plan_attention(c);
+  const AttnPlan plan = plan_for_lengths(c, R.lens);
   if (plan.chunks > c->lay.max_work) return fail(PCED_ERR_CAPACITY, "attention plan exceeds workspace");
+  if ((size_t)M * cfg.n_kv_heads * plan.max_parts > R.part_slots)
+    return fail(PCED_ERR_CAPACITY, "attention partial states exceed workspace");
+  // per-layer pool offset when the queries are not laid out per layer (the
+  // kernels then address layer 0 of the offset pools)
+  const size_t layer_elems = (size_t)cfg.max_pages * cfg.n_kv_heads * kPage * D;
 
-  // planning blocks of the append launch only: K/V rows come from the QKV epilogue
-  AppendArgs ap{};
+  AppendArgs ap{};  // planning blocks only: K/V rows come from the QKV epilogue
   ap.kpool = c->kpool;
   ap.vpool = c->vpool;
-  ap.len0 = c->at<int32_t>(c->lay.len0);
-  ap.page_table = c->at<int32_t>(c->lay.page_table);
+  ap.len0 = R.len0;
+  ap.page_table = R.page_table;
   ap.chunk_info = c->at<int2>(c->lay.chunk_info);
   ap.seg = c->at<int4>(c->lay.seg);
-  ap.nparts = c->at<int32_t>(c->lay.nparts);
+  ap.nparts = R.nparts;
   ap.work_pages = c->at<int32_t>(c->lay.work_pages);
-  ap.n_seqs = S;
+  ap.n_seqs = M;
   ap.n_layers = cfg.n_layers;
   ap.n_kv_heads = cfg.n_kv_heads;
   ap.head_dim = D;
@@ -511,45 +575,38 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
     ProfScope ps(c, PCED_PROF_APPEND, 0, 0);
     HIP_OK(launch_append(ap, true, st, ps.timing()));
   }
-
-  float* h = c->at<float>(c->lay.dec_h);
-  uint16_t* an = c->at<uint16_t>(c->lay.dec_a);
-  uint16_t* act = c->at<uint16_t>(c->lay.dec_act);
-  float* ss = c->at<float>(c->lay.dec_ss);
   {
     EmbedArgs e{};
     e.embed = (const uint16_t*)(model + ml.embed);
     e.g = (const uint16_t*)(model + ml.attn_norm);
-    e.tokens = in_tok;
-    e.seq_query = c->at<int32_t>(c->lay.seq_query);
-    e.h = h;
-    e.a_out = an;
-    e.ss_out = ss;
+    e.tokens = R.tok;
+    e.seq_query = R.tok_map;
+    e.h = R.h;
+    e.a_out = R.a;
+    e.ss_out = R.ss;
     e.hidden = H;
     e.vocab = cfg.vocab;
-    e.tok_stride = tok_stride;
-    e.ld_ss = cfg.max_seqs;
-    ProfScope ps(c, PCED_PROF_EMBED, (double)S * H * (2 + 4 + 2), 0);
-    HIP_OK(launch_embed(e, S, st, ps.timing()));
+    e.tok_stride = R.tok_stride;
+    e.ld_ss = R.ld_ss;
+    ProfScope ps(c, PCED_PROF_EMBED, (double)M * H * (2 + 4 + 2), 0);
+    HIP_OK(launch_embed(e, M, st, ps.timing()));
   }
 
   AttnArgs at{};
-  at.q = c->at<void>(c->lay.syn_q);
-  at.kpool = c->kpool;
-  at.vpool = c->vpool;
-  at.len0 = ap.len0;
-  at.page_table = ap.page_table;
+  at.q = R.q;
+  at.len0 = R.len0;
+  at.page_table = R.page_table;
   at.chunk_info = ap.chunk_info;
   at.seg = ap.seg;
-  at.nparts = ap.nparts;
+  at.nparts = R.nparts;
   at.work_pages = ap.work_pages;
-  at.part_acc = c->at<float>(c->lay.part_acc);
-  at.part_ml = c->at<float>(c->lay.part_ml);
-  at.x_out = c->at<void>(c->lay.x);
-  at.attn_out = attn_out;
+  at.part_acc = R.part_acc;
+  at.part_ml = R.part_ml;
+  at.x_out = R.x;
+  at.attn_out = R.per_layer_q ? R.attn_out : nullptr;
   at.hidden_out = nullptr;
-  at.n_seqs = S;
-  at.n_layers = cfg.n_layers;
+  at.n_seqs = M;
+  at.n_layers = R.per_layer_q ? cfg.n_layers : 1;
   at.n_q_heads = cfg.n_q_heads;
   at.n_kv_heads = cfg.n_kv_heads;
   at.group = c->G;
@@ -559,27 +616,25 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
   at.split_stride = plan.max_parts;
   at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
   double kv_tokens = 0;
-  for (int s = 0; s < S; ++s) kv_tokens += c->len[s] + 1;
-  const double attn_bytes = kv_tokens * 2.0 * kd * 2 + 2.0 * S * qd * 2;
+  for (int r = 0; r < M; ++r) kv_tokens += R.lens[r] + 1;
+  const double attn_bytes = kv_tokens * 2.0 * kd * 2 + 2.0 * M * qd * 2;
   const double attn_flops = kv_tokens * 4.0 * qd;
 
   GemmArgs g{};
-  g.M = S;
-  g.ld_ss = cfg.max_seqs;
+  g.M = M;
+  g.ld_ss = R.ld_ss;
   g.ss_parts = H / 16;
   g.inv_norm_dim = 1.0f / (float)H;
   g.eps = 1e-5f;
-  g.h = h;
-  g.a_out = an;
-  g.ss_out = ss;
-  g.act = act;
+  g.h = R.h;
+  g.a_out = R.a;
+  g.ss_out = R.ss;
+  g.act = R.act;
   g.F = cfg.ffn_dim;
-  g.q_out = c->at<uint16_t>(c->lay.syn_q);
-  g.kpool = (uint16_t*)c->kpool;
-  g.vpool = (uint16_t*)c->vpool;
-  g.len0 = ap.len0;
-  g.page_table = ap.page_table;
-  g.n_layers = cfg.n_layers;
+  g.q_out = R.q;
+  g.len0 = R.len0;
+  g.page_table = R.page_table;
+  g.n_layers = R.per_layer_q ? cfg.n_layers : 1;
   g.n_q_heads = cfg.n_q_heads;
   g.n_kv_heads = cfg.n_kv_heads;
   g.head_dim = D;
@@ -587,11 +642,10 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
   g.maxpps = cfg.max_pages_per_seq;
   g.t = c->t;
   g.log2_theta = std::log2((double)cfg.rope_theta);
-  g.part = c->at<float>(c->lay.dec_part);
-  // K slices per projection: about one block per compute unit (8-tile column groups)
+  g.part = R.proj_part;
   // K slices per projection: about one block per compute unit, more where the
   // staged x slice would not fit in LDS
-  const int stage_rows = std::min(S, S <= 16 ? 16 : S <= 32 ? 32 : 48);
+  const int stage_rows = std::min(M, M <= 16 ? 16 : M <= 32 ? 32 : 48);
   auto slices = [&](int n_tiles, int K) {
     const int groups = ceil_div(n_tiles, 8 * proj_tiles_per_wave(n_tiles));
     int ks = std::max(1, std::min({kProjMaxSplit, K / 64, c->num_cus / groups}));
@@ -599,8 +653,7 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
     return ks;
   };
   auto fits = [&](const GemmArgs& p) {
-    return proj_lds_bytes(stage_rows, p.K, p.ksplit) <= kProjMaxLds &&
-           (size_t)p.ksplit * 16 * p.n_tiles <= c->lay.part_cols;
+    return proj_lds_bytes(stage_rows, p.K, p.ksplit) <= kProjMaxLds && (size_t)p.ksplit * 16 * p.n_tiles <= R.proj_cols;
   };
   const double F = cfg.ffn_dim;
   for (int l = 0; l < cfg.n_layers; ++l) {
@@ -608,21 +661,33 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
     const uint16_t* g_next = (const uint16_t*)(l + 1 < cfg.n_layers ? model + (size_t)(l + 1) * ml.layer_bytes +
                                                                           ml.attn_norm
                                                                     : model + ml.final_norm);
-    g.layer = l;
+    uint16_t* kp = (uint16_t*)c->kpool;
+    uint16_t* vp = (uint16_t*)c->vpool;
+    int lq = l;
+    if (!R.per_layer_q) {
+      kp += (size_t)l * layer_elems;
+      vp += (size_t)l * layer_elems;
+      lq = 0;
+    }
+    g.layer = lq;
+    g.kpool = kp;
+    g.vpool = vp;
     {  // norm + QKV + RoPE + append
       GemmArgs q = g;
       q.w = lw + ml.qkv;
-      q.x = an;
+      q.x = R.a;
       q.K = H;
       q.n_tiles = (qd + 2 * kd) / 16;
       q.ksplit = slices(q.n_tiles, H);
-      q.ss_in = ss;
-      ProfScope ps(c, PCED_PROF_QKV, (double)(qd + 2 * kd) * H * 2 + (double)S * (H * 2 + (qd + 2 * kd) * 2),
-                   2.0 * S * (qd + 2 * kd) * H);
+      q.ss_in = R.ss;
+      ProfScope ps(c, PCED_PROF_QKV, (double)(qd + 2 * kd) * H * 2 + (double)M * (H * 2 + (qd + 2 * kd) * 2),
+                   2.0 * M * (qd + 2 * kd) * H);
       if (!fits(q)) return fail(PCED_ERR_UNSUPPORTED, "QKV projection does not fit the partial buffer or LDS");
       HIP_OK(launch_gemm(q, kEpiQkv, st, ps.timing()));
     }
-    at.layer = l;
+    at.layer = lq;
+    at.kpool = kp;
+    at.vpool = vp;
     at.is_last_layer = l == cfg.n_layers - 1;
     {
       ProfScope ps(c, PCED_PROF_ATTN, attn_bytes, attn_flops);
@@ -635,42 +700,116 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const int32_t* in_
     {  // O projection + residual; the MLP norm's input
       GemmArgs o = g;
       o.w = lw + ml.o;
-      o.x = c->at<uint16_t>(c->lay.x);
+      o.x = (const uint16_t*)R.x;
       o.K = qd;
       o.n_tiles = H / 16;
       o.ksplit = slices(o.n_tiles, qd);
       o.g_next = (const uint16_t*)(lw + ml.mlp_norm);
-      ProfScope ps(c, PCED_PROF_OPROJ, (double)H * qd * 2 + (double)S * (qd * 2 + H * 10),
-                   2.0 * S * H * qd);
+      ProfScope ps(c, PCED_PROF_OPROJ, (double)H * qd * 2 + (double)M * (qd * 2 + H * 10), 2.0 * M * H * qd);
       if (!fits(o)) return fail(PCED_ERR_UNSUPPORTED, "O projection does not fit the partial buffer or LDS");
       HIP_OK(launch_gemm(o, kEpiResid, st, ps.timing()));
     }
     {  // norm + gate/up + SwiGLU
       GemmArgs u = g;
       u.w = lw + ml.gu;
-      u.x = an;
+      u.x = R.a;
       u.K = H;
       u.n_tiles = 2 * cfg.ffn_dim / 16;
       u.ksplit = slices(u.n_tiles, H);
-      u.ss_in = ss;
-      ProfScope ps(c, PCED_PROF_GATEUP, 2.0 * F * H * 2 + (double)S * (H * 2 + F * 2), 4.0 * S * F * H);
+      u.ss_in = R.ss;
+      ProfScope ps(c, PCED_PROF_GATEUP, 2.0 * F * H * 2 + (double)M * (H * 2 + F * 2), 4.0 * M * F * H);
       if (!fits(u)) return fail(PCED_ERR_UNSUPPORTED, "gate/up projection does not fit the partial buffer or LDS");
       HIP_OK(launch_gemm(u, kEpiSwiglu, st, ps.timing()));
     }
     {  // down projection + residual; the next norm's input
       GemmArgs d = g;
       d.w = lw + ml.down;
-      d.x = act;
+      d.x = R.act;
       d.K = cfg.ffn_dim;
       d.n_tiles = H / 16;
       d.ksplit = slices(d.n_tiles, cfg.ffn_dim);
       d.g_next = g_next;
-      ProfScope ps(c, PCED_PROF_DOWN, F * H * 2 + (double)S * (F * 2 + H * 10), 2.0 * S * H * F);
+      ProfScope ps(c, PCED_PROF_DOWN, F * H * 2 + (double)M * (F * 2 + H * 10), 2.0 * M * H * F);
       if (!fits(d)) return fail(PCED_ERR_UNSUPPORTED, "down projection does not fit the partial buffer or LDS");
       HIP_OK(launch_gemm(d, kEpiResid, st, ps.timing()));
     }
   }
   return PCED_OK;
+}
+
+// The rows of a decode step: one per sequence.
+FwdRows decode_rows(pced_ctx* c, const int32_t* in_tok, float* attn_out) {
+  const pced_config& cfg = c->cfg;
+  FwdRows R;
+  R.M = c->S;
+  R.lens.assign(c->len.begin(), c->len.end());
+  R.len0 = c->at<int32_t>(c->lay.len0);
+  R.page_table = c->at<int32_t>(c->lay.page_table);
+  R.nparts = c->at<int32_t>(c->lay.nparts);
+  R.tok = in_tok;
+  R.tok_map = c->at<int32_t>(c->lay.seq_query);
+  R.tok_stride = 1;
+  R.h = c->at<float>(c->lay.dec_h);
+  R.a = c->at<uint16_t>(c->lay.dec_a);
+  R.act = c->at<uint16_t>(c->lay.dec_act);
+  R.ss = c->at<float>(c->lay.dec_ss);
+  R.ld_ss = cfg.max_seqs;
+  R.q = c->at<uint16_t>(c->lay.syn_q);
+  R.per_layer_q = true;
+  R.x = c->at<void>(c->lay.x);
+  R.part_acc = c->at<float>(c->lay.part_acc);
+  R.part_ml = c->at<float>(c->lay.part_ml);
+  R.part_slots = c->lay.part_slots;
+  R.proj_part = c->at<float>(c->lay.dec_part);
+  R.proj_cols = c->lay.part_cols;
+  R.attn_out = attn_out;
+  return R;
+}
+
+// One chunk of the query-suffix prefill: suffix tokens i0 .. i0+T-1 of every
+// query as S*T rows (row s*T + i: sequence s, token i0 + i, position len_s + i).
+pced_status run_prefill_chunk(pced_ctx* c, const char* model, const int32_t* tokens, int n_tokens, int i0, int T,
+                              hipStream_t st) {
+  const pced_config& cfg = c->cfg;
+  const int S = c->S, M = S * T;
+  PrefillMetaArgs pm{};
+  pm.len0 = c->at<int32_t>(c->lay.len0);
+  pm.page_table = c->at<int32_t>(c->lay.page_table);
+  pm.seq_query = c->at<int32_t>(c->lay.seq_query);
+  pm.len0_out = c->at<int32_t>(c->lay.pf_len0);
+  pm.page_table_out = c->at<int32_t>(c->lay.pf_pt);
+  pm.tok_map = c->at<int32_t>(c->lay.pf_tok);
+  pm.n_seqs = S;
+  pm.T = T;
+  pm.i0 = i0;
+  pm.n_tokens = n_tokens;
+  pm.maxpps = cfg.max_pages_per_seq;
+  HIP_OK(launch_prefill_meta(pm, st));
+  FwdRows R;
+  R.M = M;
+  R.lens.resize(M);
+  for (int s = 0; s < S; ++s)
+    for (int i = 0; i < T; ++i) R.lens[(size_t)s * T + i] = c->len[s] + i;
+  R.len0 = pm.len0_out;
+  R.page_table = pm.page_table_out;
+  R.nparts = c->at<int32_t>(c->lay.pf_nparts);
+  R.tok = tokens;
+  R.tok_map = pm.tok_map;
+  R.tok_stride = 1;
+  R.h = c->at<float>(c->lay.pf_h);
+  R.a = c->at<uint16_t>(c->lay.pf_a);
+  R.act = c->at<uint16_t>(c->lay.pf_act);
+  R.ss = c->at<float>(c->lay.pf_ss);
+  R.ld_ss = c->lay.pf_rows;
+  R.q = c->at<uint16_t>(c->lay.pf_q);
+  R.per_layer_q = false;
+  R.x = c->at<void>(c->lay.pf_x);
+  R.part_acc = c->at<float>(c->lay.pf_part_acc);
+  R.part_ml = c->at<float>(c->lay.pf_part_ml);
+  R.part_slots = (size_t)c->lay.pf_rows * cfg.n_kv_heads * kPrefillParts;
+  R.proj_part = c->at<float>(c->lay.pf_proj);
+  R.proj_cols = c->lay.pf_proj_cols;
+  return run_model_forward(c, model, R, st);
 }
 
 pced_status check_model(const pced_ctx* c, const void* model) {
@@ -686,7 +825,7 @@ pced_status run_model_step(pced_ctx* c, const void* model, const void* w, const 
                            int tok_stride, const pced_step_out* extra, hipStream_t st) {
   pced_status r = check_room(c, 1);
   if (r != PCED_OK) return r;
-  r = run_model_forward(c, (const char*)model, in_tok, 1, extra ? extra->attn_out : nullptr, st);
+  r = run_model_forward(c, (const char*)model, decode_rows(c, in_tok, extra ? extra->attn_out : nullptr), st);
   if (r != PCED_OK) return r;
   const pced_config& cfg = c->cfg;
   float* rho = c->at<float>(c->lay.dec_rho);
@@ -1125,11 +1264,14 @@ pced_status pced_model_prefill(pced_ctx* c, const void* model, int32_t n_tokens,
   if (n_tokens < 0) return fail(PCED_ERR_INVALID_ARG, "n_tokens < 0");
   r = check_room(c, n_tokens);
   if (r != PCED_OK) return r;
-  for (int i = 0; i < n_tokens; ++i) {
-    r = run_model_forward(c, (const char*)model, tokens + i, n_tokens, nullptr, st);
+  // chunks of T suffix tokens: S*T rows per pass through the stack
+  const int T = std::max(1, c->lay.pf_rows / c->S);
+  for (int i0 = 0; i0 < n_tokens; i0 += T) {
+    const int n = std::min(T, n_tokens - i0);
+    r = run_prefill_chunk(c, (const char*)model, tokens, n_tokens, i0, n, st);
     if (r != PCED_OK) return r;
-    for (int s = 0; s < c->S; ++s) c->len[s] += 1;
-    c->t += 1;
+    for (int s = 0; s < c->S; ++s) c->len[s] += n;
+    c->t += n;
   }
   return PCED_OK;
 }

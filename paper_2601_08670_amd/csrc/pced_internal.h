@@ -152,6 +152,8 @@ struct SynthArgs {
 enum GemmEpi { kEpiQkv = 0, kEpiResid = 1, kEpiSwiglu = 2, kEpiPartial = 3 };
 constexpr int kProjMaxSplit = 16;  // K slices of a projection (partial buffer sized for this many)
 constexpr size_t kProjMaxLds = 150 * 1024;  // staged x slice of a projection block
+constexpr int kPrefillRows = 256;  // (sequence, suffix token) rows of one prefill chunk, at least
+constexpr int kPrefillParts = 8;   // attention partial states per prefill row and kv-head
 struct GemmArgs {
   const void* w;            // packed tiles of this projection
   const uint16_t* x;        // [M][K] bf16 input rows
@@ -190,6 +192,17 @@ struct EmbedArgs {
   float* ss_out;            // [hidden/16][ld_ss]
   int hidden, vocab, tok_stride, ld_ss;
 };
+// Rows of one prefill chunk: row r = s*T + i is sequence s's suffix token i0 + i,
+// a virtual sequence over s's pages ending at position len_s + i.
+struct PrefillMetaArgs {
+  const int32_t* len0;      // [S]
+  const int32_t* page_table;// [S][maxpps]
+  const int32_t* seq_query; // [S]
+  int32_t* len0_out;        // [S*T] len0[s] + i
+  int32_t* page_table_out;  // [S*T][maxpps] copy of s's row
+  int32_t* tok_map;         // [S*T] index of the row's token in tokens [B][n_tokens]
+  int n_seqs, T, i0, n_tokens, maxpps;
+};
 // Optional timing events attached to the first / last dispatch of a launcher.
 struct Timing {
   hipEvent_t start = nullptr;
@@ -222,6 +235,7 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Tim
 int proj_tiles_per_wave(int n_tiles);                // 16-column tiles per wave of a projection block
 size_t proj_lds_bytes(int rows, int K, int ksplit);  // LDS of a projection block
 hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Timing* tm = nullptr);
+hipError_t launch_prefill_meta(const PrefillMetaArgs& a, hipStream_t st);
 // rho[m] = 1/sqrt(sum_p ss[p][m] * inv_dim + eps) for m < M
 hipError_t launch_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps, float* rho,
                       hipStream_t st);

@@ -1632,6 +1632,17 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
   }
 }
 
+// Metadata of a prefill chunk's rows (see PrefillMetaArgs): one block per row.
+__global__ __launch_bounds__(64) void k_prefill_meta(PrefillMetaArgs a) {
+  const int r = blockIdx.x, s = r / a.T, i = r - s * a.T;
+  if (threadIdx.x == 0) {
+    a.len0_out[r] = a.len0[s] + i;
+    a.tok_map[r] = a.seq_query[s] * a.n_tokens + a.i0 + i;
+  }
+  for (int p = threadIdx.x; p < a.maxpps; p += 64)
+    a.page_table_out[(size_t)r * a.maxpps + p] = a.page_table[(size_t)s * a.maxpps + p];
+}
+
 // rho[m] = 1/sqrt(sum_p ss[p][m] * inv_dim + eps), 8 lanes per row.
 __global__ __launch_bounds__(256) void k_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps,
                                              float* rho) {
@@ -1764,6 +1775,10 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Tim
 hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Timing* tm) {
   if (a.hidden % 256 != 0) return hipErrorInvalidValue;
   return go(k_embed, dim3(n_seqs), dim3(256), 0, st, t0(tm), t1(tm), a);
+}
+
+hipError_t launch_prefill_meta(const PrefillMetaArgs& a, hipStream_t st) {
+  return go(k_prefill_meta, dim3(a.n_seqs * a.T), dim3(64), 0, st, nullptr, nullptr, a);
 }
 
 hipError_t launch_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps, float* rho,
