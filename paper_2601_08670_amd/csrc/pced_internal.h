@@ -35,7 +35,7 @@ struct AttnArgs {
                             //  token end}, {partial index in s, partials of s, 0, 0}
   const int32_t* nparts;    // [S] partial states of each sequence (chunks it meets)
   const int32_t* work_pages;// [C][kMaxSplitPages] physical pages of each chunk
-  float* part_acc;          // [S*Hkv][split_stride][G][D] partial outputs
+  float* part_acc;          // [S*Hkv][split_stride][G][D] partial outputs (bf16 path: normalised, as bf16)
   float* part_ml;           // [S*Hkv][split_stride][G][2] (running max in log2 units, sum)
   void* x_out;              // [S][Hq*D] layer output, storage type
   float* attn_out;          // optional [S][L][Hq][D]

@@ -213,7 +213,9 @@ __device__ __forceinline__ void write_o4(const AttnArgs& a, int s, int head, int
 }
 
 // Merge of a sequence's split partial states, in split order:
-//   m* = max_j m_j,  o = sum_j acc_j 2^(m_j - m*) / sum_j l_j 2^(m_j - m*).
+//   m* = max_j m_j,  o = sum_j acc_j 2^(m_j - m*) / sum_j l_j 2^(m_j - m*),
+// with acc_j = l_j o_j for the bf16 path, whose partials hold the normalised
+// output o_j in bf16 (the fp32 path keeps acc_j in fp32).
 // One block per (sequence, kv-head); sequences that fit one split were written
 // directly by the attention kernel. Each thread owns 4 output dims of one head
 // and issues the loads of up to 16 splits at once (one memory round trip for
@@ -241,7 +243,12 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a, int D) {
         const size_t wj = w0 + min(j0 + u, stride - 1);
         mj[u] = a.part_ml[(wj * G + h) * 2];
         lj[u] = a.part_ml[(wj * G + h) * 2 + 1];
-        vj[u] = *(const float4*)(a.part_acc + (wj * G + h) * D + d);
+        if (BF16) {
+          const uint2 b = *(const uint2*)((const uint16_t*)a.part_acc + (wj * G + h) * D + d);
+          vj[u] = make_float4(bf2f(b.x & 0xFFFFu), bf2f(b.x >> 16), bf2f(b.y & 0xFFFFu), bf2f(b.y >> 16));
+        } else {
+          vj[u] = *(const float4*)(a.part_acc + (wj * G + h) * D + d);
+        }
       }
       if (nsplit <= 1) return;  // written directly by the attention kernel
       float mg = m_run;
@@ -254,8 +261,9 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a, int D) {
       for (int u = 0; u < J; ++u) {
         if (j0 + u < nsplit) {
           const float w = exp2f(mj[u] - mg);
+          const float wv = BF16 ? lj[u] * w : w;  // weight of the stored values
           den += lj[u] * w;
-          num.x += vj[u].x * w; num.y += vj[u].y * w; num.z += vj[u].z * w; num.w += vj[u].w * w;
+          num.x += vj[u].x * wv; num.y += vj[u].y * wv; num.z += vj[u].z * wv; num.w += vj[u].w * wv;
         }
       }
       m_run = mg;
@@ -359,9 +367,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
       }
       return;
     }
+    // partial state: the head's normalised output acc / l rounded to bf16 (a
+    // convex combination of V rows, so bf16 keeps its range) plus (m, l) in fp32
     const size_t w = (size_t)(s * Hkv + g) * a.split_stride + part;
-    float* dst = a.part_acc + w * G * D;
-    for (int e = 4 * lane; e < G * D; e += 256) *(float4*)(dst + e) = *(const float4*)(sa + e);
+    uint16_t* dst = (uint16_t*)a.part_acc + w * G * D;
+    for (int e = 8 * lane; e < G * D; e += 512) {
+      const float inv = 1.0f / sm[2 * (e / D) + 1];
+      const float4 v0 = *(const float4*)(sa + e), v1 = *(const float4*)(sa + e + 4);
+      uint4 pk;
+      pk.x = f2bf(v0.x * inv) | (f2bf(v0.y * inv) << 16);
+      pk.y = f2bf(v0.z * inv) | (f2bf(v0.w * inv) << 16);
+      pk.z = f2bf(v1.x * inv) | (f2bf(v1.y * inv) << 16);
+      pk.w = f2bf(v1.z * inv) | (f2bf(v1.w * inv) << 16);
+      *(uint4*)(dst + e) = pk;
+    }
     if (lane < 2 * G) a.part_ml[w * G * 2 + lane] = sm[lane];
   };
   auto reg_acc4 = [&](int j) __attribute__((always_inline)) {
