@@ -286,8 +286,8 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a, int D) {
 // alone, else a partial state for the merge kernel) and continues with the next
 // sequence's q, staged in LDS by the prologue, and a fresh softmax state; the
 // page stream itself does not stop at a switch.
-template <int D>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_attn_bf16(AttnArgs a) {
+template <int D, int RING>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 2 : 1, RING <= 4 ? 8 : 1))) void k_attn_bf16(AttnArgs a) {
   constexpr int NC = D / 32;
   constexpr int NJ = D / 16;
   // q rows of the chunk's later segments, [segment - 1][G][D]
@@ -482,22 +482,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
     }
   };
 
-  // four-page register ring: the refill of page i+3 (into the buffer of page
-  // i-1, already consumed) is issued before page i is consumed, so three pages
-  // are always in flight. The body is branch-free (a segment switch only touches
+  // RING-page register ring (4 at two waves per SIMD): the refill of page
+  // i+RING-1 (into the buffer of page i-1, already consumed) is issued before
+  // page i is consumed, so RING-1 pages are always in flight. The body is branch-free (a segment switch only touches
   // registers, LDS and stores) so that every iteration ends with the same loads
   // outstanding and the compiler's wait counts stay partial across the back
   // edge: pages past the chunk's end are the last page again and contribute
   // nothing (all their tokens are masked).
-  uint4 kA[NC], vA[NC], kB[NC], vB[NC], kC[NC], vC[NC], kD[NC], vD[NC];
-  // the prologue keeps its A, B, C issue order (the scheduler would otherwise
-  // reverse it, and the wait at the loop head then has to drain every load)
-  load_page(0, kA, vA);
-  __builtin_amdgcn_sched_barrier(0);
-  load_page(1, kB, vB);
-  __builtin_amdgcn_sched_barrier(0);
-  load_page(2, kC, vC);
-  __builtin_amdgcn_sched_barrier(0);
+  uint4 kr[RING][NC], vr[RING][NC];
+  // the prologue keeps its issue order (the scheduler would otherwise reverse
+  // it, and the wait at the loop head then has to drain every load)
+#pragma unroll
+  for (int j = 0; j < RING - 1; ++j) {
+    load_page(j, kr[j], vr[j]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
   // Later segments' q rows: 16-byte units u = ((k - 1) G + h) D/8 + d/8, spread
   // over lanes. Issued after the ring's first pages (loads complete in order, so
   // page 0 does not wait for them) and stored to LDS at the first switch.
@@ -518,15 +517,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
   stg1 = stage(1);
   stg2 = stage(2);
   stg3 = stage(3);
-  for (int i = 0; i < np; i += 4) {
-    load_page(i + 3, kD, vD);
-    process(i, kA, vA);
-    load_page(i + 4, kA, vA);
-    process(i + 1, kB, vB);
-    load_page(i + 5, kB, vB);
-    process(i + 2, kC, vC);
-    load_page(i + 6, kC, vC);
-    process(i + 3, kD, vD);
+  for (int i = 0; i < np; i += RING) {
+#pragma unroll
+    for (int j = 0; j < RING; ++j) {
+      load_page(i + j + RING - 1, kr[(j + RING - 1) % RING], vr[(j + RING - 1) % RING]);
+      process(i + j, kr[j], vr[j]);
+    }
   }
   // the saved segments, then the last one through slot 0 (LDS accesses of one
   // wave stay in order, so slot 0 is read out before it is overwritten)
@@ -1675,6 +1671,7 @@ __global__ __launch_bounds__(256) void k_rho(const float* ss, int parts, int ld,
 
 // ------------------------------------------------------------------ launchers
 
+
 namespace {
 // Launch, bracketed by the timing events (recorded on the launch stream) when given.
 template <typename Kern, typename... Args>
@@ -1720,8 +1717,8 @@ hipError_t launch_append(const AppendArgs& a, bool bf16, hipStream_t st, const T
 
 hipError_t launch_attn(const AttnArgs& a, int n_blocks, int head_dim, bool bf16, hipStream_t st, const Timing* tm) {
   if (bf16) {
-    if (head_dim == 128) return go(k_attn_bf16<128>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a);
-    if (head_dim == 64) return go(k_attn_bf16<64>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a);
+    if (head_dim == 128) return go(k_attn_bf16<128, 4>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a);
+    if (head_dim == 64) return go(k_attn_bf16<64, 4>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a);
     return hipErrorInvalidValue;
   }
   return go(k_attn_f32, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a, head_dim);
@@ -1730,8 +1727,8 @@ hipError_t launch_attn(const AttnArgs& a, int n_blocks, int head_dim, bool bf16,
 int attn_blocks_per_cu(int head_dim, bool bf16) {
   int n = 0;
   hipError_t e;
-  if (bf16 && head_dim == 128) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_bf16<128>, 64, 0);
-  else if (bf16) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_bf16<64>, 64, 0);
+  if (bf16 && head_dim == 128) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_bf16<128, 4>, 64, 0);
+  else if (bf16) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_bf16<64, 4>, 64, 0);
   else e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_f32, 64, 0);
   return (e == hipSuccess && n > 0) ? n : 8;
 }
