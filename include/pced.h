@@ -334,8 +334,10 @@ pced_status pced_pack_model_globals(const pced_config* cfg, const void* embed, c
 /*
  * Query-suffix prefill (paper, Section 3: the query is processed into every
  * expert's cache): appends tokens[b][0 .. n_tokens-1] to every sequence of
- * query b, one token position at a time through the whole stack (each token
- * attends to the cache and the suffix tokens before it). No logits.
+ * query b. The tokens go through the stack in chunks of up to
+ * max(256, max_seqs) / S tokens, all (sequence, token) rows of a chunk in one
+ * pass; each token attends to the cache and to the suffix tokens before it
+ * (causal). No logits.
  *   model   device, packed weights
  *   tokens  device int32 [B][n_tokens]; ids outside [0, V) are clamped
  * Errors: STATE (nothing loaded), CAPACITY (pages), INVALID_ARG, HIP.

@@ -149,7 +149,7 @@ struct SynthArgs {
 // Decoder-stack projections of one decode step: out[m][n] = rho_m sum_k x[m][k] W[n][k]
 // for the M step rows, W packed in 16-row tiles (k_pack_w_bf16 layout), with an
 // epilogue per projection.
-enum GemmEpi { kEpiQkv = 0, kEpiResid = 1, kEpiSwiglu = 2, kEpiPartial = 3 };
+enum GemmEpi { kEpiQkv = 0, kEpiResid = 1, kEpiSwiglu = 2 };
 constexpr int kProjMaxSplit = 16;  // K slices of a projection (partial buffer sized for this many)
 constexpr size_t kProjMaxLds = 150 * 1024;  // staged x slice of a projection block
 constexpr int kPrefillRows = 256;  // (sequence, suffix token) rows of one prefill chunk, at least
