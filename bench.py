@@ -11,10 +11,11 @@ LM head + (first step) dynamic beta + Eq. 2/3 fusion.
 Timing: W warm-up steps, then the caches are reloaded (lengths back to the
 preloaded ones) and exactly K steps are timed between two device
 synchronisations; inputs for every step are already resident in HBM. That
-region gives `value`. The same K steps are then run once more with every launch
-bracketed by HIP events on the launch stream (the events add a little time per
-launch, so they are kept out of `value`); per-kernel average durations and the
-roofline fractions come from that second region.
+region gives `value`. The same K steps are then run once more with HIP events
+attached to every kernel dispatch (start and stop timestamps of the kernel
+itself; recording them adds a little time per launch, so they are kept out of
+`value`); per-kernel average durations and the roofline fractions come from
+that second region.
 
 Prints one JSON line on stdout.
 """

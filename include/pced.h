@@ -368,8 +368,8 @@ pced_status pced_model_generate(pced_ctx* ctx, const void* model, const void* lm
                                 const int32_t* first_tokens, int32_t* tokens_out,
                                 const pced_step_out* last_extra, hipStream_t stream);
 
-/* Kernel timing with HIP events recorded around each launch on the launch
- * stream. Classes: */
+/* Kernel timing with HIP events attached to each kernel dispatch (start when
+ * the kernel begins, stop when it completes). Classes: */
 enum {
   PCED_PROF_APPEND = 0,  /* shared-history append and work planning */
   PCED_PROF_ATTN = 1,    /* decode attention, one launch per layer */

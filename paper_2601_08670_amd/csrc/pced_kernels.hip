@@ -12,6 +12,7 @@
 //     k = tokens 4*(l/16)..+3.
 //   f32 tiles are row-major [t][d].
 // Every wave load of a page is therefore a contiguous 1 KiB.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -1673,15 +1674,15 @@ __global__ __launch_bounds__(256) void k_rho(const float* ss, int parts, int ld,
 
 
 namespace {
-// Launch, bracketed by the timing events (recorded on the launch stream) when given.
+// Launch; timing events, when given, are attached to the dispatch itself
+// (start when the kernel begins, stop when it completes), so they measure the
+// kernel and not the queue around it.
 template <typename Kern, typename... Args>
 hipError_t go(Kern kernel, dim3 grid, dim3 block, size_t shm, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1,
               Args... args) {
-  if (ev0) (void)hipEventRecord(ev0, st);
-  hipLaunchKernelGGL(kernel, grid, block, shm, st, args...);
-  hipError_t e = hipGetLastError();
-  if (ev1) (void)hipEventRecord(ev1, st);
-  return e;
+  if (ev0 || ev1) hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)shm, st, ev0, ev1, 0u, args...);
+  else hipLaunchKernelGGL(kernel, grid, block, shm, st, args...);
+  return hipGetLastError();
 }
 hipEvent_t t0(const Timing* tm) { return tm ? tm->start : nullptr; }
 hipEvent_t t1(const Timing* tm) { return tm ? tm->stop : nullptr; }
