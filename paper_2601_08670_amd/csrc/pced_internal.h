@@ -16,6 +16,11 @@ constexpr int kLmRowsMTW = 9;      // many-row LM head: row tiles per wave (up t
 constexpr int kMaxSplitPages = 64; // pages per attention chunk (one page id per lane)
 constexpr int kMaxSeg = 8;         // sequences one attention chunk may span
 constexpr int kStageUnits = 4;     // 16-byte q units per lane staged in LDS for a chunk's later sequences
+// Packed LM-head tiles ordered [64-wide k step][16-row vocab block]: at every k
+// step the waves of a launch read adjacent tiles, so the weight stream sweeps W
+// as one front (the fastest HBM read pattern measured) instead of one region per
+// wave ([vocab block][k step], the order the decoder projections keep).
+constexpr bool kLmKMajor = true;
 
 // Per-step attention launch arguments (one launch per layer).
 struct AttnArgs {
@@ -87,6 +92,8 @@ struct LmArgs {
   float* fuse_part;
   int n_queries, fuse_nblk;
   const float* rho_in;      // optional [M] row scales used instead of rms (bf16 kernels)
+  size_t w_vb, w_ks;        // packed W: 16-byte units from one vocab block / 64-wide k step to the next
+                            // (set by launch_lmhead from kLmKMajor)
 };
 
 struct FuseArgs {

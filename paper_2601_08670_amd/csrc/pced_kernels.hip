@@ -753,15 +753,18 @@ __device__ void fuse_tile(const LmArgs& a, int v0, int blk, At at) {
 // ------------------------------------------------------------------- LM head
 
 // Packed LM-head layout (bf16). W [V][K] is re-laid once into 2 KiB tiles, one
-// per (16-row vocab block vb, 64-wide k step ks), tiles ordered [vb][ks]. Inside
+// per (16-row vocab block vb, 64-wide k step ks); tile (vb, ks) sits at tile
+// index vb * t_vb + ks * t_ks ([vb][ks]: t_vb = K/64, t_ks = 1; the LM head's
+// k-major order: t_vb = 1, t_ks = vocab blocks). Inside
 // a tile, half h (0, 1) and lane l = col + 16*quad hold the 8 elements
 // W[16*vb + col][64*ks + 16*quad + 8*h .. +7]: each half is exactly the A operand
 // of one v_mfma_f32_16x16x32_bf16, read as one contiguous 1 KiB wave load.
 // Rows past V are zero.
-// Row tile vb of the source goes to tile slot vb * stride + offset of wp (the
+// Row tile vb of the source goes to vocab block vb * stride + offset of wp (the
 // decoder projections interleave or concatenate several matrices this way).
 __global__ __launch_bounds__(256) void k_pack_w_bf16(const uint16_t* __restrict__ w, uint16_t* __restrict__ wp,
-                                                     int V, int K, int stride, int offset) {
+                                                     int V, int K, int stride, int offset, size_t t_vb,
+                                                     size_t t_ks) {
   const int KS = K / 64;
   const size_t n16 = (size_t)((V + 15) / 16) * KS * 2 * 64;  // 16-byte units of the packed matrix
   for (size_t u = blockIdx.x * (size_t)blockDim.x + threadIdx.x; u < n16; u += (size_t)gridDim.x * blockDim.x) {
@@ -775,7 +778,7 @@ __global__ __launch_bounds__(256) void k_pack_w_bf16(const uint16_t* __restrict_
     const int k = 64 * ks + 16 * (lane >> 4) + 8 * h;
     uint4 val = make_uint4(0u, 0u, 0u, 0u);
     if (v < V) val = *(const uint4*)(w + (size_t)v * K + k);
-    const size_t dst = ((((size_t)vb * stride + offset) * KS + ks) * 2 + h) * 64 + lane;
+    const size_t dst = ((((size_t)vb * stride + offset) * t_vb + ks * t_ks) * 2 + h) * 64 + lane;
     *(uint4*)(wp + dst * 8) = val;
   }
 }
@@ -810,7 +813,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const uint16_t* X = (const uint16_t*)a.x;
   const uint4* wt[VT];
 #pragma unroll
-  for (int vt = 0; vt < VT; ++vt) wt[vt] = Wp + (size_t)min(vb0 + vt, nvb - 1) * KS * 128 + lane;
+  for (int vt = 0; vt < VT; ++vt) wt[vt] = Wp + (size_t)min(vb0 + vt, nvb - 1) * a.w_vb + lane;
   for (int m0 = rg * 16 * NT; m0 < a.M; m0 += 16 * NT * R) {
     f32x4 acc[VT][NT];
     float ss[NT];
@@ -829,8 +832,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       ks = min(ks, KS - 1);  // past the end: the last step again (cache hit), keeps the ring branch-free
 #pragma unroll
       for (int vt = 0; vt < VT; ++vt) {
-        S.w[vt][0] = wt[vt][(size_t)ks * 128];
-        S.w[vt][1] = wt[vt][(size_t)ks * 128 + 64];
+        S.w[vt][0] = wt[vt][(size_t)ks * a.w_ks];
+        S.w[vt][1] = wt[vt][(size_t)ks * a.w_ks + 64];
       }
     };
     auto load_x = [&](XS& S, int ks) {
@@ -953,7 +956,7 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
   const uint16_t* X = (const uint16_t*)a.x;
   const uint4* wt[VTW];
 #pragma unroll
-  for (int vt = 0; vt < VTW; ++vt) wt[vt] = Wp + (size_t)min(vb0 + vt, nvb - 1) * (K / 64) * 128 + lane;
+  for (int vt = 0; vt < VTW; ++vt) wt[vt] = Wp + (size_t)min(vb0 + vt, nvb - 1) * a.w_vb + lane;
 
   // staging: thread unit v = tid + NTH j is row v / PIECES, 16-byte piece v % PIECES
   // of its stage slice (PIECES consecutive threads read one contiguous row piece);
@@ -987,8 +990,8 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
     for (int vt = 0; vt < VTW; ++vt)
 #pragma unroll
       for (int sb = 0; sb < KB; ++sb) {
-        S.w[vt][sb][0] = wt[vt][(size_t)(ks * KB + sb) * 128];
-        S.w[vt][sb][1] = wt[vt][(size_t)(ks * KB + sb) * 128 + 64];
+        S.w[vt][sb][0] = wt[vt][(size_t)(ks * KB + sb) * a.w_ks];
+        S.w[vt][sb][1] = wt[vt][(size_t)(ks * KB + sb) * a.w_ks + 64];
       }
   };
   f32x4 acc[VTW][MTW];
@@ -1744,12 +1747,14 @@ hipError_t launch_attn_combine(const AttnArgs& a, int head_dim, int max_splits, 
 
 hipError_t launch_pack_lm_head(const void* w, void* wp, int V, int K, bool bf16, hipStream_t st) {
   if (!bf16) return hipMemcpyAsync(wp, w, (size_t)V * K * 4, hipMemcpyDeviceToDevice, st);
-  k_pack_w_bf16<<<2048, 256, 0, st>>>((const uint16_t*)w, (uint16_t*)wp, V, K, 1, 0);
+  const size_t nvb = (size_t)(V + 15) / 16, ks = (size_t)K / 64;
+  k_pack_w_bf16<<<2048, 256, 0, st>>>((const uint16_t*)w, (uint16_t*)wp, V, K, 1, 0, kLmKMajor ? 1 : ks,
+                                      kLmKMajor ? nvb : 1);
   return hipGetLastError();
 }
 
 hipError_t launch_pack_tiles(const void* w, void* wp, int rows, int K, int stride, int offset, hipStream_t st) {
-  k_pack_w_bf16<<<2048, 256, 0, st>>>((const uint16_t*)w, (uint16_t*)wp, rows, K, stride, offset);
+  k_pack_w_bf16<<<2048, 256, 0, st>>>((const uint16_t*)w, (uint16_t*)wp, rows, K, stride, offset, (size_t)K / 64, 1);
   return hipGetLastError();
 }
 
@@ -1810,9 +1815,12 @@ int lmhead_fused_nblk(int M, int V) {
   return 0;
 }
 
-hipError_t launch_lmhead(const LmArgs& a, bool bf16, hipStream_t st, const Timing* tm) {
+hipError_t launch_lmhead(const LmArgs& a0, bool bf16, hipStream_t st, const Timing* tm) {
+  LmArgs a = a0;
   if (bf16) {
     const int nvb = (a.V + 15) / 16;
+    a.w_vb = kLmKMajor ? 128 : (size_t)(a.K / 64) * 128;
+    a.w_ks = kLmKMajor ? (size_t)nvb * 128 : 128;
     const bool fused = a.fuse_part != nullptr;
     if (fused && lmhead_fused_nblk(a.M, a.V) == 0) return hipErrorInvalidValue;
     if (a.M > kLmRowsPad && a.M <= 32 * kLmRowsMTW) {  // many rows: W streamed once for all of them
