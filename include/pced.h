@@ -211,8 +211,9 @@ typedef struct pced_step_out {
  *   lm_head    device                  LM-head weights packed by pced_pack_lm_head
  *   tokens_out device [B]              chosen token y_t per query
  *   extra      optional outputs, may be NULL
- * All in the storage type except the fp32 outputs. Errors: STATE (nothing
- * loaded), CAPACITY (a sequence has no page for the new token), INVALID_ARG, HIP.
+ * All in the storage type except the fp32 outputs; q, k_new and v_new must be
+ * 16-byte aligned. Errors: STATE (nothing loaded), CAPACITY (a sequence has no
+ * page for the new token), INVALID_ARG (NULL, misaligned), HIP.
  */
 pced_status pced_step(pced_ctx* ctx, const void* q, const void* k_new, const void* v_new,
                       const void* lm_head, int32_t* tokens_out, const pced_step_out* extra,

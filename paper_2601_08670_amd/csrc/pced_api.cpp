@@ -1161,6 +1161,9 @@ pced_status pced_step(pced_ctx* c, const void* q, const void* k_new, const void*
   pced_status r = check_ctx(c, true);
   if (r != PCED_OK) return r;
   if (!q || !k_new || !v_new || !lm_head || !tokens_out) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  // the kernels read q, k_new and v_new in 16-byte units
+  if (((uintptr_t)q | (uintptr_t)k_new | (uintptr_t)v_new) % 16)
+    return fail(PCED_ERR_INVALID_ARG, "q, k_new and v_new must be 16-byte aligned");
   return run_step(c, q, k_new, v_new, lm_head, tokens_out, 1, extra, st);
 }
 

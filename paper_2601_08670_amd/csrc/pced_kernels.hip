@@ -121,11 +121,18 @@ __global__ __launch_bounds__(128) void k_append(AppendArgs a) {
     const int s = blockIdx.x - n_app;
     const long P = a.total_pages, C = a.n_chunks;
     auto pages_of = [&](int r) { return (a.len0[r] + a.t + 1 + kPage - 1) / kPage; };
-    // first global page of this sequence: sum over earlier sequences
+    // first global page of this sequence: sum over earlier sequences; the page
+    // counts of the kMaxSeg sequences just before s also go to LDS for the walk
+    // back below (one round of loads instead of a chain of dependent ones)
     __shared__ int red[2];
+    __shared__ int back[kMaxSeg];
     __shared__ int k_first;
     int part = 0;
-    for (int r = threadIdx.x; r < s; r += blockDim.x) part += pages_of(r);
+    for (int r = threadIdx.x; r < s; r += blockDim.x) {
+      const int p = pages_of(r);
+      part += p;
+      if (r >= s - kMaxSeg) back[r - (s - kMaxSeg)] = p;
+    }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) part += __shfl_xor(part, o);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = part;
@@ -140,9 +147,9 @@ __global__ __launch_bounds__(128) void k_append(AppendArgs a) {
       const long b0 = chunk_lo(c0, P, C);
       long end = pre;
       int k = 0;
-      for (int r = s - 1; r >= 0 && end > b0 && k < kMaxSeg; --r) {
+      for (int r = s - 1; r >= 0 && end > b0 && k < kMaxSeg; --r) {  // r >= s - kMaxSeg
         ++k;
-        end -= pages_of(r);
+        end -= back[r - (s - kMaxSeg)];
       }
       k_first = k;
     }
@@ -174,15 +181,27 @@ __global__ __launch_bounds__(128) void k_append(AppendArgs a) {
   const size_t tile = (size_t)kPage * D;
   const size_t tile0 = ((size_t)l * a.max_pages + phys) * Hkv;
   const size_t src0 = ((size_t)s * L + l) * Hkv * D;
-  for (int idx = threadIdx.x; idx < Hkv * D; idx += blockDim.x) {
-    const int g = idx / D, d = idx % D;
+  // VEC consecutive dims per thread (bf16: 8, D being 64 or 128; f32: 4, D a
+  // multiple of 4): one load per tensor, then the stores (a loop of
+  // load-then-store would wait for every load in turn). In a bf16 K tile the 8
+  // dims of one token are contiguous; in a V tile they are 8 elements apart.
+  constexpr int VEC = BF16 ? 8 : 4;
+  for (int i0 = VEC * threadIdx.x; i0 < Hkv * D; i0 += VEC * blockDim.x) {
+    const int g = i0 / D, d0 = i0 % D;
     const size_t base = (tile0 + g) * tile;
     if (BF16) {
-      ((uint16_t*)a.kpool)[base + kswz(slot, d)] = ((const uint16_t*)a.k_new)[src0 + idx];
-      ((uint16_t*)a.vpool)[base + vswz(slot, d)] = ((const uint16_t*)a.v_new)[src0 + idx];
+      const uint4 kv = *(const uint4*)((const uint16_t*)a.k_new + src0 + i0);
+      const uint4 vv = *(const uint4*)((const uint16_t*)a.v_new + src0 + i0);
+      *(uint4*)((uint16_t*)a.kpool + base + kswz(slot, d0)) = kv;
+      uint16_t* vt = (uint16_t*)a.vpool + base;
+      const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) vt[vswz(slot, d0 + e)] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
     } else {
-      ((float*)a.kpool)[base + (size_t)slot * D + d] = ((const float*)a.k_new)[src0 + idx];
-      ((float*)a.vpool)[base + (size_t)slot * D + d] = ((const float*)a.v_new)[src0 + idx];
+      const float4 kv = *(const float4*)((const float*)a.k_new + src0 + i0);
+      const float4 vv = *(const float4*)((const float*)a.v_new + src0 + i0);
+      *(float4*)((float*)a.kpool + base + (size_t)slot * D + d0) = kv;
+      *(float4*)((float*)a.vpool + base + (size_t)slot * D + d0) = vv;
     }
   }
 }

@@ -429,3 +429,23 @@ def test_capacity_error_leaves_state_unchanged():
         sess.step(*wl.step_inputs_device(1, DEV), Wt)
     assert ei.value.status == 2 and "no page" in str(ei.value)
     assert sess.lengths() == before
+
+
+def test_misaligned_step_inputs_rejected_before_any_launch():
+    from paper_2601_08670_amd._lib import PcedError
+    geom = W.Geometry(1, 4, 1, 64, 256, 300, "bf16")
+    wl = W.custom(geom, [1], [16], 15, 2, seed=2)
+    sess = _session(wl)
+    Wt = sess.pack_lm_head(wl.lm_head_device(DEV))
+    q, kn, vn = wl.step_inputs_device(0, DEV)
+    raw = torch.empty(q.numel() * 2 + 16, dtype=torch.uint8, device=DEV)
+    q_off = raw[2:2 + q.numel() * 2]          # same bytes, 2-byte aligned only
+    q_off.copy_(q.contiguous().view(torch.uint8).reshape(-1))
+    before = sess.lengths()
+    with pytest.raises(PcedError) as ei:
+        sess.step(q_off, kn, vn, Wt)
+    assert ei.value.status == 1 and "aligned" in str(ei.value)
+    assert sess.lengths() == before
+    sess.step(q, kn, vn, Wt)                   # the aligned call still works
+    torch.cuda.synchronize()
+    assert sess.lengths() == [x + 1 for x in before]
