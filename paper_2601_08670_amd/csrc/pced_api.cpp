@@ -1234,14 +1234,15 @@ pced_status pced_pack_model_layer(const pced_config* cfg, int32_t layer, const v
   HIP_OK(hipMemcpyAsync(lw + ml.attn_norm, tensors[0], (size_t)H * 2, hipMemcpyDeviceToDevice, st));
   HIP_OK(hipMemcpyAsync(lw + ml.mlp_norm, tensors[5], (size_t)H * 2, hipMemcpyDeviceToDevice, st));
   // QKV: q tiles, then k tiles, then v tiles (all row counts are multiples of 16)
-  HIP_OK(launch_pack_tiles(tensors[1], lw + ml.qkv, qd, H, 1, 0, st));
-  HIP_OK(launch_pack_tiles(tensors[2], lw + ml.qkv, kd, H, 1, qd / 16, st));
-  HIP_OK(launch_pack_tiles(tensors[3], lw + ml.qkv, kd, H, 1, (qd + kd) / 16, st));
-  HIP_OK(launch_pack_tiles(tensors[4], lw + ml.o, H, qd, 1, 0, st));
+  const int qkv_tiles = (qd + 2 * kd) / 16;
+  HIP_OK(launch_pack_tiles(tensors[1], lw + ml.qkv, qd, H, 1, 0, qkv_tiles, st));
+  HIP_OK(launch_pack_tiles(tensors[2], lw + ml.qkv, kd, H, 1, qd / 16, qkv_tiles, st));
+  HIP_OK(launch_pack_tiles(tensors[3], lw + ml.qkv, kd, H, 1, (qd + kd) / 16, qkv_tiles, st));
+  HIP_OK(launch_pack_tiles(tensors[4], lw + ml.o, H, qd, 1, 0, H / 16, st));
   // gate and up tiles alternate, so a block owning tiles 2j, 2j+1 has both halves of 16 MLP columns
-  HIP_OK(launch_pack_tiles(tensors[6], lw + ml.gu, F, H, 2, 0, st));
-  HIP_OK(launch_pack_tiles(tensors[7], lw + ml.gu, F, H, 2, 1, st));
-  HIP_OK(launch_pack_tiles(tensors[8], lw + ml.down, H, F, 1, 0, st));
+  HIP_OK(launch_pack_tiles(tensors[6], lw + ml.gu, F, H, 2, 0, 2 * F / 16, st));
+  HIP_OK(launch_pack_tiles(tensors[7], lw + ml.gu, F, H, 2, 1, 2 * F / 16, st));
+  HIP_OK(launch_pack_tiles(tensors[8], lw + ml.down, H, F, 1, 0, H / 16, st));
   return PCED_OK;
 }
 

@@ -19,8 +19,12 @@ constexpr int kStageUnits = 4;     // 16-byte q units per lane staged in LDS for
 // Packed LM-head tiles ordered [64-wide k step][16-row vocab block]: at every k
 // step the waves of a launch read adjacent tiles, so the weight stream sweeps W
 // as one front (the fastest HBM read pattern measured) instead of one region per
-// wave ([vocab block][k step], the order the decoder projections keep).
+// wave ([vocab block][k step]).
 constexpr bool kLmKMajor = true;
+// The decoder projections' packed matrices in the same k-step-major order:
+// [64-wide k step][16-column tile], so the blocks working on one K slice read
+// adjacent tiles at every step.
+constexpr bool kProjKMajor = true;
 
 // Per-step attention launch arguments (one launch per layer).
 struct AttnArgs {
@@ -237,7 +241,8 @@ int lmhead_fused_nblk(int M, int V);
 hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st, const Timing* tm = nullptr);
 hipError_t launch_copy_rows(const void* src, void* dst, size_t nbytes, hipStream_t st);
 // pack a [rows][K] bf16 matrix into 16-row tiles, tile i going to slot i * stride + offset
-hipError_t launch_pack_tiles(const void* w, void* wp, int rows, int K, int stride, int offset, hipStream_t st);
+hipError_t launch_pack_tiles(const void* w, void* wp, int rows, int K, int stride, int offset, int n_tiles,
+                             hipStream_t st);
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Timing* tm = nullptr);
 int proj_tiles_per_wave(int n_tiles);                // 16-column tiles per wave of a projection block
 size_t proj_lds_bytes(int rows, int K, int ksplit);  // LDS of a projection block

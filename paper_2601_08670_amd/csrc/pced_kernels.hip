@@ -1463,10 +1463,13 @@ __global__ __launch_bounds__(64 * kProjWaves) void k_proj(GemmArgs a) {
   const int n = (split + 1) * KS / a.ksplit - ks0;
   const int LDX = 64 * n + 8;  // staged row length (elements)
   const int N = 16 * a.n_tiles;
+  // packed W: tile (t, ks) at (t * t_vb + ks * t_ks) * 128 16-byte units
+  const size_t t_vb = kProjKMajor ? 1 : KS, t_ks = kProjKMajor ? (size_t)a.n_tiles : 1;
   const uint4* wt[TPW];
 #pragma unroll
   for (int tt = 0; tt < TPW; ++tt)
-    wt[tt] = (const uint4*)a.w + ((size_t)min(grp * CT + wave * TPW + tt, a.n_tiles - 1) * KS + ks0) * 128 + lane;
+    wt[tt] = (const uint4*)a.w + ((size_t)min(grp * CT + wave * TPW + tt, a.n_tiles - 1) * t_vb + ks0 * t_ks) * 128 +
+             lane;
 
   for (int m0 = 0; m0 < a.M; m0 += 16 * NT) {
     const int rows = min(16 * NT, a.M - m0);
@@ -1481,8 +1484,8 @@ __global__ __launch_bounds__(64 * kProjWaves) void k_proj(GemmArgs a) {
       i = min(i, n - 1);  // past the end: the last step again (a cache hit), the ring stays branch-free
 #pragma unroll
       for (int tt = 0; tt < TPW; ++tt) {
-        S.w[tt][0] = wt[tt][(size_t)i * 128];
-        S.w[tt][1] = wt[tt][(size_t)i * 128 + 64];
+        S.w[tt][0] = wt[tt][(size_t)i * t_ks * 128];
+        S.w[tt][1] = wt[tt][(size_t)i * t_ks * 128 + 64];
       }
     };
     // x operand rows of this lane in LDS (rows past the group's end read the last row)
@@ -1772,8 +1775,10 @@ hipError_t launch_pack_lm_head(const void* w, void* wp, int V, int K, bool bf16,
   return hipGetLastError();
 }
 
-hipError_t launch_pack_tiles(const void* w, void* wp, int rows, int K, int stride, int offset, hipStream_t st) {
-  k_pack_w_bf16<<<2048, 256, 0, st>>>((const uint16_t*)w, (uint16_t*)wp, rows, K, stride, offset, (size_t)K / 64, 1);
+hipError_t launch_pack_tiles(const void* w, void* wp, int rows, int K, int stride, int offset, int n_tiles,
+                             hipStream_t st) {
+  k_pack_w_bf16<<<2048, 256, 0, st>>>((const uint16_t*)w, (uint16_t*)wp, rows, K, stride, offset,
+                                      kProjKMajor ? 1 : (size_t)K / 64, kProjKMajor ? (size_t)n_tiles : 1);
   return hipGetLastError();
 }
 
