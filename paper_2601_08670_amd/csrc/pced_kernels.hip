@@ -47,6 +47,16 @@ __device__ __forceinline__ int vswz(int t, int d) {
   return (((j >> 1) * 64 + (d & 15) + 16 * (t >> 2)) * 2 + (j & 1)) * 4 + (t & 3);
 }
 
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte load with the non-temporal hint, for data read once per step (KV
+// pages, LM-head and projection weights): it streams through the caches
+// without displacing what is reused (partial states, outputs, q and x rows).
+__device__ __forceinline__ uint4 ld_stream(const uint4* p) {
+  const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // ------------------------------------------------------------------ utilities
 
 __global__ void k_fill_i32(int32_t* p, int32_t v, size_t n) {
@@ -354,8 +364,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
     const size_t t0 = (lay + (size_t)phys * Hkv) * tile16;
 #pragma unroll
     for (int cc = 0; cc < NC; ++cc) {
-      kb[cc] = kp[t0 + cc * 64 + lane];
-      vb[cc] = vp[t0 + cc * 64 + lane];
+      kb[cc] = ld_stream(&kp[t0 + cc * 64 + lane]);
+      vb[cc] = ld_stream(&vp[t0 + cc * 64 + lane]);
     }
   };
 
@@ -851,8 +861,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       ks = min(ks, KS - 1);  // past the end: the last step again (cache hit), keeps the ring branch-free
 #pragma unroll
       for (int vt = 0; vt < VT; ++vt) {
-        S.w[vt][0] = wt[vt][(size_t)ks * a.w_ks];
-        S.w[vt][1] = wt[vt][(size_t)ks * a.w_ks + 64];
+        S.w[vt][0] = ld_stream(&wt[vt][(size_t)ks * a.w_ks]);
+        S.w[vt][1] = ld_stream(&wt[vt][(size_t)ks * a.w_ks + 64]);
       }
     };
     auto load_x = [&](XS& S, int ks) {
@@ -1009,8 +1019,8 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
     for (int vt = 0; vt < VTW; ++vt)
 #pragma unroll
       for (int sb = 0; sb < KB; ++sb) {
-        S.w[vt][sb][0] = wt[vt][(size_t)(ks * KB + sb) * a.w_ks];
-        S.w[vt][sb][1] = wt[vt][(size_t)(ks * KB + sb) * a.w_ks + 64];
+        S.w[vt][sb][0] = ld_stream(&wt[vt][(size_t)(ks * KB + sb) * a.w_ks]);
+        S.w[vt][sb][1] = ld_stream(&wt[vt][(size_t)(ks * KB + sb) * a.w_ks + 64]);
       }
   };
   f32x4 acc[VTW][MTW];
@@ -1484,8 +1494,8 @@ __global__ __launch_bounds__(64 * kProjWaves) void k_proj(GemmArgs a) {
       i = min(i, n - 1);  // past the end: the last step again (a cache hit), the ring stays branch-free
 #pragma unroll
       for (int tt = 0; tt < TPW; ++tt) {
-        S.w[tt][0] = wt[tt][(size_t)i * t_ks * 128];
-        S.w[tt][1] = wt[tt][(size_t)i * t_ks * 128 + 64];
+        S.w[tt][0] = ld_stream(&wt[tt][(size_t)i * t_ks * 128]);
+        S.w[tt][1] = ld_stream(&wt[tt][(size_t)i * t_ks * 128 + 64]);
       }
     };
     // x operand rows of this lane in LDS (rows past the group's end read the last row)
