@@ -357,10 +357,14 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
   const size_t lay = (size_t)a.layer * a.max_pages * Hkv + g;
   constexpr size_t tile16 = (size_t)kPage * D / 8;  // tile size in 16-byte units
 
-  // Loads are issued unconditionally (past the end: the last page again, an L2
-  // hit) so that the wait before each page's use leaves the next page in flight.
+  // Loads are issued unconditionally so that the wait before each page's use
+  // leaves the next page in flight. Past the chunk's end they read physical page
+  // 0 of the layer and kv-head, one tile that every wave's extra loads share, so
+  // they stay cache hits although the page loads carry the streaming hint (the
+  // chunk's own last page again missed the caches: +20 MB per launch); all of
+  // their tokens are masked.
   auto load_page = [&](int i, uint4 (&kb)[NC], uint4 (&vb)[NC]) {
-    const int phys = __builtin_amdgcn_readlane(my_pid, min(i, np - 1));
+    const int phys = i < np ? __builtin_amdgcn_readlane(my_pid, min(i, 63)) : 0;
     const size_t t0 = (lay + (size_t)phys * Hkv) * tile16;
 #pragma unroll
     for (int cc = 0; cc < NC; ++cc) {
@@ -517,8 +521,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
   // page i is consumed, so RING-1 pages are always in flight. The body is branch-free (a segment switch only touches
   // registers, LDS and stores) so that every iteration ends with the same loads
   // outstanding and the compiler's wait counts stay partial across the back
-  // edge: pages past the chunk's end are the last page again and contribute
-  // nothing (all their tokens are masked).
+  // edge: pages past the chunk's end (the shared page 0, see load_page)
+  // contribute nothing (all their tokens are masked).
   uint4 kr[RING][NC], vr[RING][NC];
   // the prologue keeps its issue order (the scheduler would otherwise reverse
   // it, and the wait at the loop head then has to drain every load)
