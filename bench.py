@@ -15,7 +15,11 @@ region gives `value`. The same K steps are then run once more with HIP events
 attached to every kernel dispatch (start and stop timestamps of the kernel
 itself; recording them adds a little time per launch, so they are kept out of
 `value`); per-kernel average durations and the roofline fractions come from
-that second region.
+that second region. In `kernels`, "fuse" is Eq. 2 / Eq. 3 over materialised
+logits (the first step, which also computes beta), "fuse_merge" the per-query
+merge after the LM head's fused Eq. 2 epilogue (every later step);
+`fuse_standalone` times pced_fuse on its own over logits of the workload's
+shape.
 
 Prints one JSON line on stdout.
 """
@@ -201,6 +205,33 @@ def generate_timing(sess, wl, src, Wt, K, dev) -> dict:
             "graph_replay_ms": replays, "capture_s": capture_s, "tokens_match_direct": match}
 
 
+def fuse_standalone(sess, wl, Wt, dev, reps: int = 50) -> dict:
+    """Eq. 2 and Eq. 3 as a stand-alone stage (pced_fuse) over materialised
+    logits of the workload's shape: the form the first step uses (the later
+    steps run it inside the LM head's epilogue). The logits come from the LM
+    head over the last layer's query rows as stand-in hidden states; beta is the
+    one the timed steps froze. Timed with the dispatch-attached events."""
+    import torch
+    g = wl.geom
+    S = sess.S
+    x = wl.step_inputs_device(0, dev)[0][:, -1].reshape(S, g.hidden).contiguous()
+    logits = torch.empty((S, g.vocab), dtype=torch.float32, device=dev)
+    tokens = torch.empty(sess.B, dtype=torch.int32, device=dev)
+    sess.ctx.pced_lmhead(x, S, Wt, logits)
+    sess.ctx.pced_fuse(logits, 0, tokens)
+    torch.cuda.synchronize()
+    sess.ctx.pced_profile_enable(True)
+    for _ in range(reps):
+        sess.ctx.pced_fuse(logits, 0, tokens)
+    torch.cuda.synchronize()
+    p = sess.ctx.pced_profile_read()["fuse"]
+    sess.ctx.pced_profile_enable(False)
+    us = p["ms"] * 1e3 / p["launches"]
+    gbs = p["bytes"] / (p["ms"] * 1e-3) / 1e9
+    return {"launches": p["launches"], "avg_us": us, "bytes_per_launch": p["bytes"] / p["launches"], "GB/s": gbs,
+            "hbm_frac": gbs / HBM_PEAK_GBS, "kernels": "k_fuse + k_fuse_final"}
+
+
 def kernel_table(prof, ms_total):
     kernels = {}
     for name, p in prof.items():
@@ -375,6 +406,9 @@ def main():
                     "bytes_per_launch": prof["attn"]["bytes"] / prof["attn"]["launches"],
                     "avg_launch_us": attn["avg_us"]}
 
+    fuse_sa = fuse_standalone(sess, wl, Wt, dev)
+    log(f"[bench] pced_fuse stand-alone over materialised logits: {fuse_sa['avg_us']:.2f} us, "
+        f"{fuse_sa['GB/s']:.0f} GB/s")
     gen = generate_timing(sess, wl, src, Wt, K, dev) if args.generate else None
     model = None
     if args.model:
@@ -419,6 +453,7 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": roofline,
         "kernels": kernels,
+        "fuse_standalone": fuse_sa,
         "cpu_baseline": cpu,
     }
     if gen is not None:

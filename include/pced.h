@@ -384,7 +384,11 @@ enum {
   PCED_PROF_OPROJ = 9,   /* decoder stack: O projection + residual  */
   PCED_PROF_GATEUP = 10, /* decoder stack: norm + gate/up + SwiGLU  */
   PCED_PROF_DOWN = 11,   /* decoder stack: down projection + residual */
-  PCED_PROF_NCLASS = 12
+  PCED_PROF_FUSE_MERGE = 12, /* per-query merge of the slice candidates left
+                                by the LM head's fused Eq. 2 epilogue (steps
+                                after the first); PCED_PROF_FUSE is Eq. 2 + 3
+                                over materialised logits                    */
+  PCED_PROF_NCLASS = 13
 };
 typedef struct pced_profile {
   int64_t launches[PCED_PROF_NCLASS];

@@ -18,7 +18,7 @@ PCED_F32, PCED_BF16 = 0, 1
 PCED_NORM_NONE, PCED_NORM_RMS = 0, 1
 STATUS = {0: "OK", 1: "INVALID_ARG", 2: "CAPACITY", 3: "HIP", 4: "UNSUPPORTED", 5: "STATE"}
 PROF_CLASSES = ("append", "attn", "lmhead", "beta", "fuse", "synth", "combine", "embed", "qkv", "oproj",
-                "gateup", "down")
+                "gateup", "down", "fuse_merge")
 
 EXPORTED = ("pced_pool_bytes", "pced_lm_head_bytes", "pced_pack_lm_head", "pced_workspace_bytes", "pced_create", "pced_destroy", "pced_last_error",
             "pced_load_caches", "pced_step", "pced_generate", "pced_lmhead", "pced_fuse",
@@ -51,8 +51,8 @@ class pced_synth(ctypes.Structure):
 
 
 class pced_profile(ctypes.Structure):
-    _fields_ = [("launches", ctypes.c_int64 * 12), ("total_ms", ctypes.c_double * 12),
-                ("bytes", ctypes.c_double * 12), ("flops", ctypes.c_double * 12)]
+    _fields_ = [("launches", ctypes.c_int64 * 13), ("total_ms", ctypes.c_double * 13),
+                ("bytes", ctypes.c_double * 13), ("flops", ctypes.c_double * 13)]
 
 
 _lib = None

@@ -406,7 +406,7 @@ pced_status run_fuse_final(pced_ctx* c, int nblk, int32_t* tokens_out, int tok_s
                            hipStream_t st) {
   FuseArgs f = fuse_args(c, nullptr, tokens_out, tok_stride, extra, nblk);
   {
-    ProfScope ps(c, PCED_PROF_FUSE, (double)c->B * nblk * 5 * 4, 0);
+    ProfScope ps(c, PCED_PROF_FUSE_MERGE, (double)c->B * nblk * 5 * 4, 0);
     HIP_OK(launch_fuse_final(f, c->B, st, ps.timing()));
   }
   return copy_beta_used(c, extra, st);

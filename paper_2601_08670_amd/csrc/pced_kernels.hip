@@ -1164,13 +1164,14 @@ __global__ __launch_bounds__(kFuseBlock) void k_fuse(FuseArgs a) {
     const float sa = colp[(size_t)s0 * a.V];
     float best = kNegInf;
     int bk = 0;
-    // experts in batches of 16 independent loads, so their latencies overlap
-    for (int kb = 1; kb <= N; kb += 16) {
-      float x[16];
+    // experts in batches of 32 independent loads (one memory round trip for up
+    // to 32 documents), so their latencies overlap
+    for (int kb = 1; kb <= N; kb += 32) {
+      float x[32];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) x[j] = (kb + j <= N) ? colp[(size_t)(s0 + kb + j) * a.V] : 0.f;
+      for (int j = 0; j < 32; ++j) x[j] = (kb + j <= N) ? colp[(size_t)(s0 + kb + j) * a.V] : 0.f;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
+      for (int j = 0; j < 32; ++j) {
         const int k = kb + j;
         if (k > N) continue;
         const float beta = a.beta[e0 + k - 1];
