@@ -125,10 +125,13 @@ Layout make_layout(const pced_config& c) {
   L.tick_beta = take(S * 4);
   L.prev_tok = take(B * 4);
   L.beta = take(S * 4);
-  // split partials: [S*Hkv][stride][G][D] with stride <= pages per sequence
+  // split partials: [S*Hkv][stride][G][D] with stride <= pages per sequence.
+  // The decode step alternates two sets by layer parity (bf16: both fit the
+  // fp32-sized accumulator buffer), so that a layer's attention launch can merge
+  // the previous layer's partials while writing its own.
   L.part_slots = (size_t)c.max_seqs * c.n_kv_heads * c.max_pages_per_seq;
   L.part_acc = take(L.part_slots * G * c.head_dim * 4);
-  L.part_ml = take(L.part_slots * G * 2 * 4);
+  L.part_ml = take(2 * L.part_slots * G * 2 * 4);
   L.x = take((size_t)L.rows_pad * c.hidden * es);
   L.logits = take(S * c.vocab * 4);
   // per-slice candidates: k_fuse uses 256-column slices, the fused LM-head epilogue 128-column ones
@@ -910,18 +913,37 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
   const double attn_bytes = kv_tokens * 2.0 * cfg.n_kv_heads * cfg.head_dim * es +
                             2.0 * c->S * cfg.n_q_heads * cfg.head_dim * es;
   const double attn_flops = kv_tokens * 4.0 * cfg.n_q_heads * cfg.head_dim;
+  // Sequences that span several chunks need a merge of their partial states.
+  // bf16: layer l's partials go to set l % 2 and the attention launch of layer
+  // l + 1 merges them (one launch per layer instead of two); only the last
+  // layer's merge is a launch of its own.
+  const bool split = plan.max_parts > 1;
+  const bool fold = split && c->bf16;
+  const size_t acc_set = c->lay.part_slots * c->G * cfg.head_dim / 2;  // floats per bf16 set
+  const size_t ml_set = c->lay.part_slots * c->G * 2;
+  float* acc0 = at.part_acc;
+  float* ml0 = at.part_ml;
   for (int l = 0; l < cfg.n_layers; ++l) {
     at.layer = l;
     at.is_last_layer = l == cfg.n_layers - 1;
+    const int set = fold ? l & 1 : 0;
+    at.part_acc = acc0 + set * acc_set;
+    at.part_ml = ml0 + set * ml_set;
+    const bool merge_prev = fold && l > 0;
+    at.mrg_acc = merge_prev ? (const uint16_t*)(acc0 + (set ^ 1) * acc_set) : nullptr;
+    at.mrg_ml = merge_prev ? ml0 + (set ^ 1) * ml_set : nullptr;
+    at.mrg_layer = l - 1;
     {
       ProfScope ps(c, PCED_PROF_ATTN, attn_bytes, attn_flops);
       HIP_OK(launch_attn(at, plan.chunks * cfg.n_kv_heads, cfg.head_dim, c->bf16, st, ps.timing()));
     }
-    if (plan.max_parts > 1) {  // some sequence spans more than one chunk
+    if (split && (!fold || l == cfg.n_layers - 1)) {
       ProfScope ps(c, PCED_PROF_COMBINE, 0, 0);
       HIP_OK(launch_attn_combine(at, cfg.head_dim, plan.max_parts, c->bf16, st, ps.timing()));
     }
   }
+  at.mrg_acc = nullptr;
+  at.mrg_ml = nullptr;
 
   const pced_status r = run_head(c, at.x_out, nullptr, w, tokens_out, tok_stride, extra, st);
   if (r != PCED_OK) return r;

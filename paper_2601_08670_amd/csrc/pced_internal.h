@@ -49,6 +49,12 @@ struct AttnArgs {
   void* x_out;              // [S][Hq*D] layer output, storage type
   float* attn_out;          // optional [S][L][Hq][D]
   float* hidden_out;        // optional [S][Hq*D] (last layer only)
+  // bf16 decode attention only, optional: the previous layer's partial states
+  // (same plan, [S*Hkv][split_stride][G][D] bf16 and [S*Hkv][split_stride][G][2]),
+  // merged by this launch into x_out (and attn_out at layer mrg_layer)
+  const uint16_t* mrg_acc;
+  const float* mrg_ml;
+  int mrg_layer;
   int n_seqs, n_layers, layer, n_q_heads, n_kv_heads, group;
   int max_pages, maxpps, t, split_stride, is_last_layer;
   float scale_log2;         // log2(e) / sqrt(D)

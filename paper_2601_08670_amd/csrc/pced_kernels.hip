@@ -245,20 +245,118 @@ __device__ __forceinline__ void write_o4(const AttnArgs& a, int s, int head, int
 // Merge of a sequence's split partial states, in split order:
 //   m* = max_j m_j,  o = sum_j acc_j 2^(m_j - m*) / sum_j l_j 2^(m_j - m*),
 // with acc_j = l_j o_j for the bf16 path, whose partials hold the normalised
-// output o_j in bf16 (the fp32 path keeps acc_j in fp32).
-// One block per (sequence, kv-head); sequences that fit one split were written
-// directly by the attention kernel. Each thread owns 4 output dims of one head
-// and issues the loads of up to 16 splits at once (one memory round trip for
-// the usual split counts), merging further groups of 16 online. Slots past the
-// split count are read but never used (no arithmetic touches them).
-template <bool BF16>
-__global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a, int D) {
+// output o_j in bf16 (the fp32 path keeps acc_j in fp32). Sequences that fit
+// one split were written directly by the attention kernel.
+//
+// bf16: one wave per (sequence, kv-head). Each lane owns 8 consecutive output
+// dims (one 16-byte unit of a partial, so a split's [G][D] slot is one
+// contiguous wave load) and issues the loads of 16 splits at once; lane
+// t = 16 h + j loads (m, l) of head h, split j, and the 16 lanes of a head
+// reduce the maximum and publish (l_j, 2^(m_j - m*)) through LDS. Every lane
+// then sums its splits in split order. Further groups of 16 splits merge
+// online. Slots past the split count are read but never used.
+__global__ __launch_bounds__(64) void k_attn_combine_bf16(AttnArgs a, int D) {
+  constexpr int J = 16;
+  constexpr int NU = kMaxGroup * 128 / 512;  // 16-byte units per lane at most (G D <= kMaxGroup * 128)
+  constexpr int NML = kMaxGroup * J / 64;    // (m, l) entries per lane at most
+  __shared__ float2 wl[kMaxGroup * J];
+  __shared__ float mg_sh[kMaxGroup];
+  const int lane = threadIdx.x;
+  const int s = blockIdx.x / a.n_kv_heads, g = blockIdx.x % a.n_kv_heads;
+  const int G = a.group, stride = a.split_stride;
+  const int units = G * D / 8;  // 16-byte units of one partial slot
+  const size_t w0 = (size_t)blockIdx.x * stride;
+  const uint4* pa = (const uint4*)a.part_acc;
+  const int nsplit = a.nparts[s];
+  float num[NU][8], den[NU], m_run[NU], m_own[NML];
+#pragma unroll
+  for (int k = 0; k < NU; ++k) {
+    den[k] = 0.f;
+    m_run[k] = kNegInf;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) num[k][e] = 0.f;
+  }
+#pragma unroll
+  for (int i = 0; i < NML; ++i) m_own[i] = kNegInf;
+  for (int j0 = 0; j0 < max(nsplit, 1); j0 += J) {
+    float2 ml[NML];
+#pragma unroll
+    for (int i = 0; i < NML; ++i) {
+      const int t = lane + 64 * i;
+      if (t < G * J) {
+        const size_t wj = w0 + min(j0 + (t & (J - 1)), stride - 1);
+        ml[i] = *(const float2*)(a.part_ml + (wj * G + t / J) * 2);
+      }
+    }
+    uint4 v[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) v[j] = pa[(w0 + min(j0 + j, stride - 1)) * units + min(lane, units - 1)];
+    if (nsplit <= 1) return;  // written directly by the attention kernel
+    __syncthreads();  // the previous group's weights have been read
+#pragma unroll
+    for (int i = 0; i < NML; ++i) {
+      const int t = lane + 64 * i;
+      if (t < G * J) {  // whole 16-lane groups (G J is a multiple of 16)
+        const int jj = t & (J - 1);
+        const bool valid = j0 + jj < nsplit;
+        const float mj = valid ? ml[i].x : kNegInf;
+        float mg = mj;
+#pragma unroll
+        for (int o = J / 2; o >= 1; o >>= 1) mg = fmaxf(mg, __shfl_xor(mg, o));
+        mg = fmaxf(mg, m_own[i]);
+        m_own[i] = mg;
+        wl[t] = make_float2(ml[i].y, valid ? exp2f(mj - mg) : 0.f);
+        if (jj == 0) mg_sh[t / J] = mg;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < NU; ++k) {
+      const int u = lane + 64 * k;
+      if (u >= units) break;
+      if (k > 0) {
+#pragma unroll
+        for (int j = 0; j < J; ++j) v[j] = pa[(w0 + min(j0 + j, stride - 1)) * units + u];
+      }
+      const int h = 8 * u / D;
+      const float mg = mg_sh[h];
+      const float r = exp2f(m_run[k] - mg);
+      den[k] *= r;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) num[k][e] *= r;
+      m_run[k] = mg;
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        if (j0 + j < nsplit) {
+          const float2 lw = wl[h * J + j];
+          const float wv = lw.x * lw.y;  // weight of the stored (normalised) values
+          den[k] = fmaf(lw.x, lw.y, den[k]);
+          const uint32_t b[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            num[k][e] = fmaf(bf2f((b[e >> 1] >> (16 * (e & 1))) & 0xFFFFu), wv, num[k][e]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < NU; ++k) {
+    const int u = lane + 64 * k;
+    if (u >= units) break;
+    const int h = 8 * u / D, d = 8 * u % D;
+    const float inv = 1.0f / den[k];
+    write_o4<true>(a, s, g * G + h, d, D, make_float4(num[k][0] * inv, num[k][1] * inv, num[k][2] * inv, num[k][3] * inv));
+    write_o4<true>(a, s, g * G + h, d + 4, D, make_float4(num[k][4] * inv, num[k][5] * inv, num[k][6] * inv, num[k][7] * inv));
+  }
+}
+
+// fp32: one block per (sequence, kv-head); each thread owns 4 output dims of
+// one head and issues the loads of up to 16 splits at once, merging further
+// groups of 16 online.
+__global__ __launch_bounds__(128) void k_attn_combine_f32(AttnArgs a, int D) {
   constexpr int J = 16;
   const int s = blockIdx.x / a.n_kv_heads, g = blockIdx.x % a.n_kv_heads;
   const int G = a.group, stride = a.split_stride;
-  // partial slots of (s, g) are contiguous, so their loads do not wait for the
-  // split count: the first J are read at once (clamped inside the slot range)
-  // together with the sequence length
   const size_t w0 = (size_t)blockIdx.x * stride;
   const int nsplit = a.nparts[s];
   for (int idx = threadIdx.x; idx < G * D / 4; idx += blockDim.x) {
@@ -273,12 +371,7 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a, int D) {
         const size_t wj = w0 + min(j0 + u, stride - 1);
         mj[u] = a.part_ml[(wj * G + h) * 2];
         lj[u] = a.part_ml[(wj * G + h) * 2 + 1];
-        if (BF16) {
-          const uint2 b = *(const uint2*)((const uint16_t*)a.part_acc + (wj * G + h) * D + d);
-          vj[u] = make_float4(bf2f(b.x & 0xFFFFu), bf2f(b.x >> 16), bf2f(b.y & 0xFFFFu), bf2f(b.y >> 16));
-        } else {
-          vj[u] = *(const float4*)(a.part_acc + (wj * G + h) * D + d);
-        }
+        vj[u] = *(const float4*)(a.part_acc + (wj * G + h) * D + d);
       }
       if (nsplit <= 1) return;  // written directly by the attention kernel
       float mg = m_run;
@@ -291,15 +384,15 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a, int D) {
       for (int u = 0; u < J; ++u) {
         if (j0 + u < nsplit) {
           const float w = exp2f(mj[u] - mg);
-          const float wv = BF16 ? lj[u] * w : w;  // weight of the stored values
-          den += lj[u] * w;
-          num.x += vj[u].x * wv; num.y += vj[u].y * wv; num.z += vj[u].z * wv; num.w += vj[u].w * wv;
+          den = fmaf(lj[u], w, den);
+          num.x = fmaf(vj[u].x, w, num.x); num.y = fmaf(vj[u].y, w, num.y);
+          num.z = fmaf(vj[u].z, w, num.z); num.w = fmaf(vj[u].w, w, num.w);
         }
       }
       m_run = mg;
     }
     const float inv = 1.0f / den;
-    write_o4<BF16>(a, s, g * G + h, d, D, make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv));
+    write_o4<false>(a, s, g * G + h, d, D, make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv));
   }
 }
 
@@ -330,6 +423,37 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
   const int col = lane & 15, quad = lane >> 4;
   const int G = a.group, Hkv = a.n_kv_heads;
   const int c = blockIdx.x / Hkv, g = blockIdx.x % Hkv;
+  // Merge of the previous layer's split sequences (when a.mrg_acc is set): item
+  // (sequence, kv-head, q-head) it = blockIdx.x (+ gridDim.x ...), lanes
+  // 0 .. D/4 - 1 owning 4 output dims each. The first item's loads are issued
+  // before anything else, so they arrive with the first pages; the merge itself
+  // runs just before the page loop (see mrg_run).
+  const int n_mrg = a.mrg_acc ? a.n_seqs * Hkv * G : 0;
+  int m_s = 0, m_g = 0, m_h = 0, m_n = 0;
+  size_t m_w0 = 0;
+  uint2 mv[16];
+  float2 mml = make_float2(0.f, 0.f);
+  auto mrg_item = [&](int it) __attribute__((always_inline)) {
+    m_s = it / (Hkv * G);
+    m_g = (it / G) % Hkv;
+    m_h = it % G;
+    m_w0 = (size_t)(m_s * Hkv + m_g) * a.split_stride;
+    m_n = a.nparts[m_s];
+  };
+  // splits j0 .. j0 + 15 (clamped inside the slot range; slots past the count
+  // are read but never used): lane j % 16 holds (m, l) of split j0 + j % 16
+  auto mrg_load = [&](int j0) __attribute__((always_inline)) {
+    const int last = a.split_stride - 1;
+    mml = *(const float2*)(a.mrg_ml + ((m_w0 + min(j0 + (lane & 15), last)) * G + m_h) * 2);
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      mv[j] = *(const uint2*)(a.mrg_acc + ((m_w0 + min(j0 + j, last)) * G + m_h) * D + 4 * min(lane, D / 4 - 1));
+  };
+  if ((int)blockIdx.x < n_mrg) {
+    mrg_item(blockIdx.x);
+    mrg_load(0);
+  }
+
   const int2 ci = a.chunk_info[c];
   const int nseg = ci.x, np = ci.y;  // 1 .. kMaxSeg segments, 1 .. kMaxSplitPages pages
   // the chunk's physical page ids and segment descriptors, lane k holding entry
@@ -551,6 +675,59 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
   stg1 = stage(1);
   stg2 = stage(2);
   stg3 = stage(3);
+  // The merge, in the arithmetic of k_attn_combine_bf16: groups of 16 splits
+  // merged online, each group's splits summed in split order.
+  if ((int)blockIdx.x < n_mrg) {
+    for (int it = blockIdx.x; it < n_mrg; it += gridDim.x) {
+      if (it != (int)blockIdx.x) {
+        mrg_item(it);
+        mrg_load(0);
+      }
+      if (m_n <= 1) continue;  // written directly by the previous launch
+      float m_run = kNegInf, den = 0.f;
+      float num[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int j0 = 0; j0 < m_n; j0 += 16) {
+        if (j0 > 0) mrg_load(j0);
+        const bool valid = j0 + (lane & 15) < m_n;
+        const float mj = valid ? mml.x : kNegInf;
+        float mg = mj;
+#pragma unroll
+        for (int o = 8; o >= 1; o >>= 1) mg = fmaxf(mg, __shfl_xor(mg, o));
+        mg = fmaxf(mg, m_run);
+        const float wj = valid ? exp2f(mj - mg) : 0.f;
+        const float r = exp2f(m_run - mg);
+        den *= r;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) num[e] *= r;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          if (j0 + j < m_n) {
+            const float lj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mml.y), j));
+            const float w = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wj), j));
+            const float wv = lj * w;  // weight of the stored (normalised) values
+            den = fmaf(lj, w, den);
+            num[0] = fmaf(bf2f(mv[j].x & 0xFFFFu), wv, num[0]);
+            num[1] = fmaf(bf2f(mv[j].x >> 16), wv, num[1]);
+            num[2] = fmaf(bf2f(mv[j].y & 0xFFFFu), wv, num[2]);
+            num[3] = fmaf(bf2f(mv[j].y >> 16), wv, num[3]);
+          }
+        }
+        m_run = mg;
+      }
+      if (lane < D / 4) {  // the layer output (never the last layer's: no hidden_out)
+        const float inv = 1.0f / den;
+        const float4 o = make_float4(num[0] * inv, num[1] * inv, num[2] * inv, num[3] * inv);
+        const size_t row = (size_t)m_s * a.n_q_heads + m_g * G + m_h;
+        if (a.attn_out)
+          *(float4*)(a.attn_out + ((row + (size_t)m_s * (a.n_layers - 1) * a.n_q_heads +
+                                    (size_t)a.mrg_layer * a.n_q_heads) * D + 4 * lane)) = o;
+        uint2 pk;
+        pk.x = f2bf(o.x) | (f2bf(o.y) << 16);
+        pk.y = f2bf(o.z) | (f2bf(o.w) << 16);
+        *(uint2*)((uint16_t*)a.x_out + row * D + 4 * lane) = pk;
+      }
+    }
+  }
   for (int i = 0; i < np; i += RING) {
 #pragma unroll
     for (int j = 0; j < RING; ++j) {
@@ -1778,8 +1955,8 @@ hipError_t launch_attn_combine(const AttnArgs& a, int head_dim, int max_splits, 
                                const Timing* tm) {
   const int blocks = a.n_seqs * a.n_kv_heads;
   (void)max_splits;
-  if (bf16) return go(k_attn_combine<true>, dim3(blocks), dim3(128), 0, st, t0(tm), t1(tm), a, head_dim);
-  return go(k_attn_combine<false>, dim3(blocks), dim3(128), 0, st, t0(tm), t1(tm), a, head_dim);
+  if (bf16) return go(k_attn_combine_bf16, dim3(blocks), dim3(64), 0, st, t0(tm), t1(tm), a, head_dim);
+  return go(k_attn_combine_f32, dim3(blocks), dim3(128), 0, st, t0(tm), t1(tm), a, head_dim);
 }
 
 hipError_t launch_pack_lm_head(const void* w, void* wp, int V, int K, bool bf16, hipStream_t st) {
