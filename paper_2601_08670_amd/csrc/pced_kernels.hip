@@ -242,112 +242,143 @@ __device__ __forceinline__ void write_o4(const AttnArgs& a, int s, int head, int
   }
 }
 
-// Merge of a sequence's split partial states, in split order:
+// Merge of a sequence's split partial states:
 //   m* = max_j m_j,  o = sum_j acc_j 2^(m_j - m*) / sum_j l_j 2^(m_j - m*),
 // with acc_j = l_j o_j for the bf16 path, whose partials hold the normalised
 // output o_j in bf16 (the fp32 path keeps acc_j in fp32). Sequences that fit
 // one split were written directly by the attention kernel.
 //
-// bf16: one wave per (sequence, kv-head). Each lane owns 8 consecutive output
-// dims (one 16-byte unit of a partial, so a split's [G][D] slot is one
-// contiguous wave load) and issues the loads of 16 splits at once; lane
-// t = 16 h + j loads (m, l) of head h, split j, and the 16 lanes of a head
-// reduce the maximum and publish (l_j, 2^(m_j - m*)) through LDS. Every lane
-// then sums its splits in split order. Further groups of 16 splits merge
-// online. Slots past the split count are read but never used.
-__global__ __launch_bounds__(64) void k_attn_combine_bf16(AttnArgs a, int D) {
-  constexpr int J = 16;
-  constexpr int NU = kMaxGroup * 128 / 512;  // 16-byte units per lane at most (G D <= kMaxGroup * 128)
-  constexpr int NML = kMaxGroup * J / 64;    // (m, l) entries per lane at most
-  __shared__ float2 wl[kMaxGroup * J];
-  __shared__ float mg_sh[kMaxGroup];
+// bf16: one wave per item (sequence, kv-head, q-head), in the merge kernel and
+// in the prologue of the next layer's attention launch alike, through the
+// functions below (same operations in the same order: bit-identical results).
+// Splits go in groups of 16, merged online. Within a group, lane l loads 8
+// dims (16 bytes) of split 4 i + l / (D/8) in load i (D = 128: 4 splits per
+// load), and lane l % 16 holds (m, l) of split l % 16; a lane sums its splits in
+// order, then the lane groups are added by a butterfly (every group ends with
+// the same bits). Slots past the split count are read but never used.
+template <int D>
+struct MergeShape {
+  static constexpr int LPS = D / 8;     // lanes per split
+  static constexpr int SPI = 64 / LPS;  // splits per load
+  static constexpr int NI = 16 / SPI;   // loads per group of 16 splits
+};
+
+template <int D>
+struct MergeRegs {
+  uint4 v[MergeShape<D>::NI];
+  float2 ml;
+};
+
+template <int D>
+__device__ __forceinline__ void merge_load(MergeRegs<D>& R, const uint16_t* acc, const float* ml, size_t w0,
+                                           int stride, int G, int h, int j0, int lane) {
+  using M = MergeShape<D>;
+  const int last = stride - 1;
+  R.ml = *(const float2*)(ml + ((w0 + min(j0 + (lane & 15), last)) * G + h) * 2);
+#pragma unroll
+  for (int i = 0; i < M::NI; ++i) {
+    const int j = j0 + i * M::SPI + lane / M::LPS;
+    R.v[i] = *(const uint4*)(acc + ((w0 + min(j, last)) * G + h) * D + 8 * (lane % M::LPS));
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void merge_group(const MergeRegs<D>& R, int j0, int n, int lane, float& m_run,
+                                            float& den, float (&num)[8]) {
+#pragma clang fp contract(off)
+  using M = MergeShape<D>;
+  const bool valid = j0 + (lane & 15) < n;
+  const float mj = valid ? R.ml.x : kNegInf;
+  float mg = mj;
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) mg = fmaxf(mg, __shfl_xor(mg, o));
+  mg = fmaxf(mg, m_run);  // uniform: every 16-lane group holds all 16 splits
+  const float wj = valid ? exp2f(mj - mg) : 0.f;
+  const float r = exp2f(m_run - mg);
+  den *= r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) num[e] *= r;
+  m_run = mg;
+#pragma unroll
+  for (int i = 0; i < M::NI; ++i) {
+    const int jj = i * M::SPI + lane / M::LPS;
+    const float lj = __shfl(R.ml.y, jj), w = __shfl(wj, jj);
+    if (j0 + jj < n) {
+      const float wv = lj * w;  // weight of the stored (normalised) values
+      den = fmaf(lj, w, den);
+      const uint32_t b[4] = {R.v[i].x, R.v[i].y, R.v[i].z, R.v[i].w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) num[e] = fmaf(bf2f((b[e >> 1] >> (16 * (e & 1))) & 0xFFFFu), wv, num[e]);
+    }
+  }
+}
+
+// Sum over the lane groups and store: x_out (bf16), attn_out at `layer` and,
+// for the last layer, hidden_out (fp32 of the stored x).
+template <int D>
+__device__ __forceinline__ void merge_store(const AttnArgs& a, int s, int head, int layer, bool last_layer,
+                                            int lane, float den, float (&num)[8]) {
+#pragma clang fp contract(off)
+  using M = MergeShape<D>;
+#pragma unroll
+  for (int o = M::LPS; o < 64; o <<= 1) {
+    den += __shfl_xor(den, o);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) num[e] += __shfl_xor(num[e], o);
+  }
+  if (lane >= M::LPS) return;
+  const float inv = 1.0f / den;
+  float o[8];
+  uint32_t b[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    o[e] = num[e] * inv;
+    b[e] = f2bf(o[e]);
+  }
+  const int d = 8 * lane;
+  const size_t row = (size_t)s * a.n_q_heads + head;
+  *(uint4*)((uint16_t*)a.x_out + row * D + d) =
+      make_uint4(b[0] | (b[1] << 16), b[2] | (b[3] << 16), b[4] | (b[5] << 16), b[6] | (b[7] << 16));
+  if (a.attn_out) {
+    float* p = a.attn_out + (((size_t)s * a.n_layers + layer) * a.n_q_heads + head) * D + d;
+    *(float4*)p = make_float4(o[0], o[1], o[2], o[3]);
+    *(float4*)(p + 4) = make_float4(o[4], o[5], o[6], o[7]);
+  }
+  if (last_layer && a.hidden_out) {
+    float* p = a.hidden_out + row * D + d;
+    *(float4*)p = make_float4(bf2f(b[0]), bf2f(b[1]), bf2f(b[2]), bf2f(b[3]));
+    *(float4*)(p + 4) = make_float4(bf2f(b[4]), bf2f(b[5]), bf2f(b[6]), bf2f(b[7]));
+  }
+}
+
+// The whole merge of item `it` whose first group is already in R.
+template <int D>
+__device__ __forceinline__ void merge_item(const AttnArgs& a, MergeRegs<D>& R, const uint16_t* acc,
+                                           const float* ml, int s, int g, int h, int n, int layer,
+                                           bool last_layer, int lane) {
+  if (n <= 1) return;  // written directly by the attention kernel
+  const size_t w0 = (size_t)(s * a.n_kv_heads + g) * a.split_stride;
+  float m_run = kNegInf, den = 0.f;
+  float num[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int j0 = 0; j0 < n; j0 += 16) {
+    if (j0 > 0) merge_load<D>(R, acc, ml, w0, a.split_stride, a.group, h, j0, lane);
+    merge_group<D>(R, j0, n, lane, m_run, den, num);
+  }
+  merge_store<D>(a, s, g * a.group + h, layer, last_layer, lane, den, num);
+}
+
+// The merge as a launch of its own: one wave per item.
+template <int D>
+__global__ __launch_bounds__(64) void k_attn_combine_bf16(AttnArgs a) {
   const int lane = threadIdx.x;
-  const int s = blockIdx.x / a.n_kv_heads, g = blockIdx.x % a.n_kv_heads;
-  const int G = a.group, stride = a.split_stride;
-  const int units = G * D / 8;  // 16-byte units of one partial slot
-  const size_t w0 = (size_t)blockIdx.x * stride;
-  const uint4* pa = (const uint4*)a.part_acc;
-  const int nsplit = a.nparts[s];
-  float num[NU][8], den[NU], m_run[NU], m_own[NML];
-#pragma unroll
-  for (int k = 0; k < NU; ++k) {
-    den[k] = 0.f;
-    m_run[k] = kNegInf;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) num[k][e] = 0.f;
-  }
-#pragma unroll
-  for (int i = 0; i < NML; ++i) m_own[i] = kNegInf;
-  for (int j0 = 0; j0 < max(nsplit, 1); j0 += J) {
-    float2 ml[NML];
-#pragma unroll
-    for (int i = 0; i < NML; ++i) {
-      const int t = lane + 64 * i;
-      if (t < G * J) {
-        const size_t wj = w0 + min(j0 + (t & (J - 1)), stride - 1);
-        ml[i] = *(const float2*)(a.part_ml + (wj * G + t / J) * 2);
-      }
-    }
-    uint4 v[J];
-#pragma unroll
-    for (int j = 0; j < J; ++j) v[j] = pa[(w0 + min(j0 + j, stride - 1)) * units + min(lane, units - 1)];
-    if (nsplit <= 1) return;  // written directly by the attention kernel
-    __syncthreads();  // the previous group's weights have been read
-#pragma unroll
-    for (int i = 0; i < NML; ++i) {
-      const int t = lane + 64 * i;
-      if (t < G * J) {  // whole 16-lane groups (G J is a multiple of 16)
-        const int jj = t & (J - 1);
-        const bool valid = j0 + jj < nsplit;
-        const float mj = valid ? ml[i].x : kNegInf;
-        float mg = mj;
-#pragma unroll
-        for (int o = J / 2; o >= 1; o >>= 1) mg = fmaxf(mg, __shfl_xor(mg, o));
-        mg = fmaxf(mg, m_own[i]);
-        m_own[i] = mg;
-        wl[t] = make_float2(ml[i].y, valid ? exp2f(mj - mg) : 0.f);
-        if (jj == 0) mg_sh[t / J] = mg;
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < NU; ++k) {
-      const int u = lane + 64 * k;
-      if (u >= units) break;
-      if (k > 0) {
-#pragma unroll
-        for (int j = 0; j < J; ++j) v[j] = pa[(w0 + min(j0 + j, stride - 1)) * units + u];
-      }
-      const int h = 8 * u / D;
-      const float mg = mg_sh[h];
-      const float r = exp2f(m_run[k] - mg);
-      den[k] *= r;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) num[k][e] *= r;
-      m_run[k] = mg;
-#pragma unroll
-      for (int j = 0; j < J; ++j) {
-        if (j0 + j < nsplit) {
-          const float2 lw = wl[h * J + j];
-          const float wv = lw.x * lw.y;  // weight of the stored (normalised) values
-          den[k] = fmaf(lw.x, lw.y, den[k]);
-          const uint32_t b[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            num[k][e] = fmaf(bf2f((b[e >> 1] >> (16 * (e & 1))) & 0xFFFFu), wv, num[k][e]);
-        }
-      }
-    }
-  }
-#pragma unroll
-  for (int k = 0; k < NU; ++k) {
-    const int u = lane + 64 * k;
-    if (u >= units) break;
-    const int h = 8 * u / D, d = 8 * u % D;
-    const float inv = 1.0f / den[k];
-    write_o4<true>(a, s, g * G + h, d, D, make_float4(num[k][0] * inv, num[k][1] * inv, num[k][2] * inv, num[k][3] * inv));
-    write_o4<true>(a, s, g * G + h, d + 4, D, make_float4(num[k][4] * inv, num[k][5] * inv, num[k][6] * inv, num[k][7] * inv));
-  }
+  const int G = a.group, Hkv = a.n_kv_heads;
+  const int it = blockIdx.x;
+  const int s = it / (Hkv * G), g = (it / G) % Hkv, h = it % G;
+  const int n = a.nparts[s];
+  const uint16_t* acc = (const uint16_t*)a.part_acc;
+  MergeRegs<D> R;
+  merge_load<D>(R, acc, a.part_ml, (size_t)(s * Hkv + g) * a.split_stride, a.split_stride, G, h, 0, lane);
+  merge_item<D>(a, R, acc, a.part_ml, s, g, h, n, a.layer, a.is_last_layer != 0, lane);
 }
 
 // fp32: one block per (sequence, kv-head); each thread owns 4 output dims of
@@ -423,36 +454,22 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
   const int col = lane & 15, quad = lane >> 4;
   const int G = a.group, Hkv = a.n_kv_heads;
   const int c = blockIdx.x / Hkv, g = blockIdx.x % Hkv;
-  // Merge of the previous layer's split sequences (when a.mrg_acc is set): item
-  // (sequence, kv-head, q-head) it = blockIdx.x (+ gridDim.x ...), lanes
-  // 0 .. D/4 - 1 owning 4 output dims each. The first item's loads are issued
-  // before anything else, so they arrive with the first pages; the merge itself
-  // runs just before the page loop (see mrg_run).
+  // Merge of the previous layer's split sequences (when a.mrg_acc is set):
+  // items (sequence, kv-head, q-head) it = blockIdx.x, + gridDim.x, ... The
+  // first item's loads are issued before anything else, so they arrive with
+  // the first pages; the merge itself runs just before the page loop.
   const int n_mrg = a.mrg_acc ? a.n_seqs * Hkv * G : 0;
+  MergeRegs<D> mr;
   int m_s = 0, m_g = 0, m_h = 0, m_n = 0;
-  size_t m_w0 = 0;
-  uint2 mv[16];
-  float2 mml = make_float2(0.f, 0.f);
   auto mrg_item = [&](int it) __attribute__((always_inline)) {
     m_s = it / (Hkv * G);
     m_g = (it / G) % Hkv;
     m_h = it % G;
-    m_w0 = (size_t)(m_s * Hkv + m_g) * a.split_stride;
     m_n = a.nparts[m_s];
+    merge_load<D>(mr, a.mrg_acc, a.mrg_ml, (size_t)(m_s * Hkv + m_g) * a.split_stride, a.split_stride, G, m_h, 0,
+                  lane);
   };
-  // splits j0 .. j0 + 15 (clamped inside the slot range; slots past the count
-  // are read but never used): lane j % 16 holds (m, l) of split j0 + j % 16
-  auto mrg_load = [&](int j0) __attribute__((always_inline)) {
-    const int last = a.split_stride - 1;
-    mml = *(const float2*)(a.mrg_ml + ((m_w0 + min(j0 + (lane & 15), last)) * G + m_h) * 2);
-#pragma unroll
-    for (int j = 0; j < 16; ++j)
-      mv[j] = *(const uint2*)(a.mrg_acc + ((m_w0 + min(j0 + j, last)) * G + m_h) * D + 4 * min(lane, D / 4 - 1));
-  };
-  if ((int)blockIdx.x < n_mrg) {
-    mrg_item(blockIdx.x);
-    mrg_load(0);
-  }
+  if ((int)blockIdx.x < n_mrg) mrg_item(blockIdx.x);
 
   const int2 ci = a.chunk_info[c];
   const int nseg = ci.x, np = ci.y;  // 1 .. kMaxSeg segments, 1 .. kMaxSplitPages pages
@@ -675,58 +692,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
   stg1 = stage(1);
   stg2 = stage(2);
   stg3 = stage(3);
-  // The merge, in the arithmetic of k_attn_combine_bf16: groups of 16 splits
-  // merged online, each group's splits summed in split order.
-  if ((int)blockIdx.x < n_mrg) {
-    for (int it = blockIdx.x; it < n_mrg; it += gridDim.x) {
-      if (it != (int)blockIdx.x) {
-        mrg_item(it);
-        mrg_load(0);
-      }
-      if (m_n <= 1) continue;  // written directly by the previous launch
-      float m_run = kNegInf, den = 0.f;
-      float num[4] = {0.f, 0.f, 0.f, 0.f};
-      for (int j0 = 0; j0 < m_n; j0 += 16) {
-        if (j0 > 0) mrg_load(j0);
-        const bool valid = j0 + (lane & 15) < m_n;
-        const float mj = valid ? mml.x : kNegInf;
-        float mg = mj;
-#pragma unroll
-        for (int o = 8; o >= 1; o >>= 1) mg = fmaxf(mg, __shfl_xor(mg, o));
-        mg = fmaxf(mg, m_run);
-        const float wj = valid ? exp2f(mj - mg) : 0.f;
-        const float r = exp2f(m_run - mg);
-        den *= r;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) num[e] *= r;
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          if (j0 + j < m_n) {
-            const float lj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mml.y), j));
-            const float w = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wj), j));
-            const float wv = lj * w;  // weight of the stored (normalised) values
-            den = fmaf(lj, w, den);
-            num[0] = fmaf(bf2f(mv[j].x & 0xFFFFu), wv, num[0]);
-            num[1] = fmaf(bf2f(mv[j].x >> 16), wv, num[1]);
-            num[2] = fmaf(bf2f(mv[j].y & 0xFFFFu), wv, num[2]);
-            num[3] = fmaf(bf2f(mv[j].y >> 16), wv, num[3]);
-          }
-        }
-        m_run = mg;
-      }
-      if (lane < D / 4) {  // the layer output (never the last layer's: no hidden_out)
-        const float inv = 1.0f / den;
-        const float4 o = make_float4(num[0] * inv, num[1] * inv, num[2] * inv, num[3] * inv);
-        const size_t row = (size_t)m_s * a.n_q_heads + m_g * G + m_h;
-        if (a.attn_out)
-          *(float4*)(a.attn_out + ((row + (size_t)m_s * (a.n_layers - 1) * a.n_q_heads +
-                                    (size_t)a.mrg_layer * a.n_q_heads) * D + 4 * lane)) = o;
-        uint2 pk;
-        pk.x = f2bf(o.x) | (f2bf(o.y) << 16);
-        pk.y = f2bf(o.z) | (f2bf(o.w) << 16);
-        *(uint2*)((uint16_t*)a.x_out + row * D + 4 * lane) = pk;
-      }
-    }
+  for (int it = blockIdx.x; it < n_mrg; it += gridDim.x) {
+    if (it != (int)blockIdx.x) mrg_item(it);
+    merge_item<D>(a, mr, a.mrg_acc, a.mrg_ml, m_s, m_g, m_h, m_n, a.mrg_layer, false, lane);
   }
   for (int i = 0; i < np; i += RING) {
 #pragma unroll
@@ -1955,7 +1923,12 @@ hipError_t launch_attn_combine(const AttnArgs& a, int head_dim, int max_splits, 
                                const Timing* tm) {
   const int blocks = a.n_seqs * a.n_kv_heads;
   (void)max_splits;
-  if (bf16) return go(k_attn_combine_bf16, dim3(blocks), dim3(64), 0, st, t0(tm), t1(tm), a, head_dim);
+  if (bf16) {
+    const int items = blocks * a.group;
+    if (head_dim == 128) return go(k_attn_combine_bf16<128>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a);
+    if (head_dim == 64) return go(k_attn_combine_bf16<64>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a);
+    return hipErrorInvalidValue;
+  }
   return go(k_attn_combine_f32, dim3(blocks), dim3(128), 0, st, t0(tm), t1(tm), a, head_dim);
 }
 
