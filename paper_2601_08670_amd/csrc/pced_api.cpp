@@ -610,6 +610,7 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
   at.hidden_out = nullptr;
   at.n_seqs = M;
   at.n_layers = R.per_layer_q ? cfg.n_layers : 1;
+  at.kv_reread = R.per_layer_q ? 0 : 1;  // prefill: the virtual rows of a sequence share its pages
   at.n_q_heads = cfg.n_q_heads;
   at.n_kv_heads = cfg.n_kv_heads;
   at.group = c->G;

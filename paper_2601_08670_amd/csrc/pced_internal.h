@@ -57,6 +57,7 @@ struct AttnArgs {
   int mrg_layer;
   int n_seqs, n_layers, layer, n_q_heads, n_kv_heads, group;
   int max_pages, maxpps, t, split_stride, is_last_layer;
+  int kv_reread;            // pages are read by several rows of the launch (prefill): plain loads
   float scale_log2;         // log2(e) / sqrt(D)
 };
 

@@ -49,12 +49,20 @@ __device__ __forceinline__ int vswz(int t, int d) {
 
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
-// 16-byte load with the non-temporal hint, for data read once per step (KV
-// pages, LM-head and projection weights): it streams through the caches
-// without displacing what is reused (partial states, outputs, q and x rows).
-__device__ __forceinline__ uint4 ld_stream(const uint4* p) {
-  const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
-  return make_uint4(v.x, v.y, v.z, v.w);
+// 16-byte load of data a launch reads once (KV pages, LM-head and projection
+// weights in a decode step): with STREAM it carries the non-temporal hint and
+// streams through the caches without displacing what is reused (partial
+// states, outputs, q and x rows). Launches that read the same bytes several
+// times (the prefill's row groups and virtual rows, the LM head's row groups)
+// use plain loads, so that the repeats hit the caches.
+template <bool STREAM>
+__device__ __forceinline__ uint4 ld_w(const uint4* p) {
+  if constexpr (STREAM) {
+    const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
+    return make_uint4(v.x, v.y, v.z, v.w);
+  } else {
+    return *p;
+  }
 }
 
 // ------------------------------------------------------------------ utilities
@@ -440,7 +448,7 @@ __global__ __launch_bounds__(128) void k_attn_combine_f32(AttnArgs a, int D) {
 // alone, else a partial state for the merge kernel) and continues with the next
 // sequence's q, staged in LDS by the prologue, and a fresh softmax state; the
 // page stream itself does not stop at a switch.
-template <int D, int RING>
+template <int D, int RING, bool STREAM>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 2 : 1, RING <= 4 ? 8 : 1))) void k_attn_bf16(AttnArgs a) {
   constexpr int NC = D / 32;
   constexpr int NJ = D / 16;
@@ -509,8 +517,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
     const size_t t0 = (lay + (size_t)phys * Hkv) * tile16;
 #pragma unroll
     for (int cc = 0; cc < NC; ++cc) {
-      kb[cc] = ld_stream(&kp[t0 + cc * 64 + lane]);
-      vb[cc] = ld_stream(&vp[t0 + cc * 64 + lane]);
+      kb[cc] = ld_w<STREAM>(&kp[t0 + cc * 64 + lane]);
+      vb[cc] = ld_w<STREAM>(&vp[t0 + cc * 64 + lane]);
     }
   };
 
@@ -968,7 +976,7 @@ __global__ __launch_bounds__(256) void k_pack_w_bf16(const uint16_t* __restrict_
 // register ring (two 64-wide k steps in flight); the x operands (a few hundred
 // KiB, L2-resident) are loaded one step ahead.
 // rho (the RMS scale) is accumulated from the same x operands.
-template <int VT, int NT, bool FUSED>
+template <int VT, int NT, bool FUSED, bool STREAM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_lmhead_bf16(LmArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, quad = lane >> 4;
@@ -1010,8 +1018,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       ks = min(ks, KS - 1);  // past the end: the last step again (cache hit), keeps the ring branch-free
 #pragma unroll
       for (int vt = 0; vt < VT; ++vt) {
-        S.w[vt][0] = ld_stream(&wt[vt][(size_t)ks * a.w_ks]);
-        S.w[vt][1] = ld_stream(&wt[vt][(size_t)ks * a.w_ks + 64]);
+        S.w[vt][0] = ld_w<STREAM>(&wt[vt][(size_t)ks * a.w_ks]);
+        S.w[vt][1] = ld_w<STREAM>(&wt[vt][(size_t)ks * a.w_ks + 64]);
       }
     };
     auto load_x = [&](XS& S, int ks) {
@@ -1168,8 +1176,8 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
     for (int vt = 0; vt < VTW; ++vt)
 #pragma unroll
       for (int sb = 0; sb < KB; ++sb) {
-        S.w[vt][sb][0] = ld_stream(&wt[vt][(size_t)(ks * KB + sb) * a.w_ks]);
-        S.w[vt][sb][1] = ld_stream(&wt[vt][(size_t)(ks * KB + sb) * a.w_ks + 64]);
+        S.w[vt][sb][0] = ld_w<true>(&wt[vt][(size_t)(ks * KB + sb) * a.w_ks]);
+        S.w[vt][sb][1] = ld_w<true>(&wt[vt][(size_t)(ks * KB + sb) * a.w_ks + 64]);
       }
   };
   f32x4 acc[VTW][MTW];
@@ -1608,7 +1616,7 @@ __device__ __forceinline__ float row_ss8(const float* ss, int parts, int ld, int
 // and reads its x operands from LDS, so the whole register ring holds W bytes
 // in flight. The barrier after staging waits on LDS only; it does not drain the
 // ring.
-template <int NT, int TPW>
+template <int NT, int TPW, bool STREAM>
 __global__ __launch_bounds__(64 * kProjWaves) void k_proj(GemmArgs a) {
   constexpr int WPB = kProjWaves, CT = WPB * TPW, R = TPW == 1 ? 8 : 5;
   extern __shared__ __align__(16) uint16_t xs[];
@@ -1644,8 +1652,8 @@ __global__ __launch_bounds__(64 * kProjWaves) void k_proj(GemmArgs a) {
       i = min(i, n - 1);  // past the end: the last step again (a cache hit), the ring stays branch-free
 #pragma unroll
       for (int tt = 0; tt < TPW; ++tt) {
-        S.w[tt][0] = ld_stream(&wt[tt][(size_t)i * t_ks * 128]);
-        S.w[tt][1] = ld_stream(&wt[tt][(size_t)i * t_ks * 128 + 64]);
+        S.w[tt][0] = ld_w<STREAM>(&wt[tt][(size_t)i * t_ks * 128]);
+        S.w[tt][1] = ld_w<STREAM>(&wt[tt][(size_t)i * t_ks * 128 + 64]);
       }
     };
     // x operand rows of this lane in LDS (rows past the group's end read the last row)
@@ -1903,8 +1911,13 @@ hipError_t launch_append(const AppendArgs& a, bool bf16, hipStream_t st, const T
 
 hipError_t launch_attn(const AttnArgs& a, int n_blocks, int head_dim, bool bf16, hipStream_t st, const Timing* tm) {
   if (bf16) {
-    if (head_dim == 128) return go(k_attn_bf16<128, 4>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a);
-    if (head_dim == 64) return go(k_attn_bf16<64, 4>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a);
+    const bool s = !a.kv_reread;
+    if (head_dim == 128)
+      return s ? go(k_attn_bf16<128, 4, true>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a)
+               : go(k_attn_bf16<128, 4, false>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a);
+    if (head_dim == 64)
+      return s ? go(k_attn_bf16<64, 4, true>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a)
+               : go(k_attn_bf16<64, 4, false>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a);
     return hipErrorInvalidValue;
   }
   return go(k_attn_f32, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a, head_dim);
@@ -1913,8 +1926,8 @@ hipError_t launch_attn(const AttnArgs& a, int n_blocks, int head_dim, bool bf16,
 int attn_blocks_per_cu(int head_dim, bool bf16) {
   int n = 0;
   hipError_t e;
-  if (bf16 && head_dim == 128) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_bf16<128, 4>, 64, 0);
-  else if (bf16) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_bf16<64, 4>, 64, 0);
+  if (bf16 && head_dim == 128) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_bf16<128, 4, true>, 64, 0);
+  else if (bf16) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_bf16<64, 4, true>, 64, 0);
   else e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_f32, 64, 0);
   return (e == hipSuccess && n > 0) ? n : 8;
 }
@@ -1964,14 +1977,17 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Tim
   const dim3 b(64 * kProjWaves);
   const dim3 g((a.n_tiles + kProjWaves * tpw - 1) / (kProjWaves * tpw) * a.ksplit);
   hipError_t e;
-  if (tpw == 1)
-    e = NT == 1 ? go(k_proj<1, 1>, g, b, lds, st, t0(tm), nullptr, a)
-        : NT == 2 ? go(k_proj<2, 1>, g, b, lds, st, t0(tm), nullptr, a)
-                  : go(k_proj<3, 1>, g, b, lds, st, t0(tm), nullptr, a);
+  if (a.M > 16 * NT)  // several row groups: each re-reads the block's W tiles, plain loads
+    e = tpw == 1 ? go(k_proj<3, 1, false>, g, b, lds, st, t0(tm), nullptr, a)
+                 : go(k_proj<3, 2, false>, g, b, lds, st, t0(tm), nullptr, a);
+  else if (tpw == 1)
+    e = NT == 1 ? go(k_proj<1, 1, true>, g, b, lds, st, t0(tm), nullptr, a)
+        : NT == 2 ? go(k_proj<2, 1, true>, g, b, lds, st, t0(tm), nullptr, a)
+                  : go(k_proj<3, 1, true>, g, b, lds, st, t0(tm), nullptr, a);
   else
-    e = NT == 1 ? go(k_proj<1, 2>, g, b, lds, st, t0(tm), nullptr, a)
-        : NT == 2 ? go(k_proj<2, 2>, g, b, lds, st, t0(tm), nullptr, a)
-                  : go(k_proj<3, 2>, g, b, lds, st, t0(tm), nullptr, a);
+    e = NT == 1 ? go(k_proj<1, 2, true>, g, b, lds, st, t0(tm), nullptr, a)
+        : NT == 2 ? go(k_proj<2, 2, true>, g, b, lds, st, t0(tm), nullptr, a)
+                  : go(k_proj<3, 2, true>, g, b, lds, st, t0(tm), nullptr, a);
   if (e != hipSuccess) return e;
   const int outc = epi == kEpiSwiglu ? 8 * a.n_tiles : 16 * a.n_tiles;  // output columns
   const dim3 gr((outc / 4 + 255) / 256, a.M);
@@ -2027,8 +2043,12 @@ hipError_t launch_lmhead(const LmArgs& a0, bool bf16, hipStream_t st, const Timi
     LmArgs b = a;
     b.row_groups = (a.M + 16 * NT - 1) / (16 * NT);
     const int blocks = b.row_groups > 1 ? (chunks + 7) / 8 * 8 * b.row_groups : chunks;
-    if (fused) return go(k_lmhead_bf16<VT, NT, true>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), b);
-    return go(k_lmhead_bf16<VT, NT, false>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), b);
+    // row groups > 1 share each W tile through the XCD's L2: plain loads
+    if (b.row_groups > 1)
+      return fused ? go(k_lmhead_bf16<VT, NT, true, false>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), b)
+                   : go(k_lmhead_bf16<VT, NT, false, false>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), b);
+    return fused ? go(k_lmhead_bf16<VT, NT, true, true>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), b)
+                 : go(k_lmhead_bf16<VT, NT, false, true>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), b);
   }
   return go(k_lmhead_f32, dim3((a.V + 255) / 256), dim3(256), 0, st, t0(tm), t1(tm), a);
 }
