@@ -1127,8 +1127,13 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
   constexpr int UNITS = SUB * KB;        // ... of one stage
   constexpr int UPT = (UNITS + NTH - 1) / NTH;
   constexpr int PIECES = 8 * KB;         // 16-byte pieces of a row's stage slice
-  // unit (k step sb, tile, half h, lane l) at sb*SUB + tile*128 + 64 h + l
-  __shared__ __align__(16) uint4 xs[2][UNITS];
+  // Row-major stage slice, rows padded by one 16-byte unit (odd stride): the
+  // coalesced staging stores (consecutive pieces of a row) and the B-operand
+  // reads (16 rows x 4 pieces per wave load) both spread over all banks. (The
+  // slice in B-operand order made each wave's stores hit the same banks 8 to
+  // 16 times over: bank conflicts took 70% of the LDS cycles.)
+  constexpr int RS = PIECES + 1;
+  __shared__ __align__(16) uint4 xs[2][MT * 16 * RS];
   __shared__ float rho_s[MT * 16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int col = lane & 15, quad = lane >> 4;
@@ -1149,9 +1154,9 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
   // unit j of a thread is NTH / PIECES rows below unit 0
   static_assert(NTH % (16 * PIECES) == 0, "whole tiles per staging round");
   constexpr int ROWS_J = NTH / PIECES;
-  const int row0 = tid / PIECES, pc = tid % PIECES, sb0 = pc >> 3, c8 = pc & 7;
+  const int row0 = tid / PIECES, pc = tid % PIECES;
   const uint16_t* xsrc = X + (size_t)row0 * K + 8 * pc;
-  const int xdst = sb0 * SUB + (row0 >> 4) * 128 + 64 * (c8 & 1) + 16 * (c8 >> 1) + (row0 & 15);
+  const int xdst = row0 * RS + pc;
   float ss[UPT];
 #pragma unroll
   for (int j = 0; j < UPT; ++j) ss[j] = 0.f;
@@ -1165,7 +1170,7 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
     for (int j = 0; j < UPT; ++j)
       if (tid + NTH * j < n_units) {
-        xs[buf][xdst + j * (ROWS_J / 16) * 128] = xr[j];
+        xs[buf][xdst + j * ROWS_J * RS] = xr[j];
         ss[j] += sumsq8(as_bf16x8(xr[j]));
       }
   };
@@ -1192,8 +1197,10 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
       for (int i = 0; i < MTW; ++i) {
         const int t = 2 * i + rh;
         if (t < nt) {
-          const bf16x8 b0 = as_bf16x8(xs[buf][sb * SUB + t * 128 + lane]);
-          const bf16x8 b1 = as_bf16x8(xs[buf][sb * SUB + t * 128 + 64 + lane]);
+          // lane (col, quad): row 16 t + col, elements 64 sb + 16 quad + 8 h .. + 7
+          const uint4* xp = &xs[buf][(16 * t + col) * RS + 8 * sb + 2 * quad];
+          const bf16x8 b0 = as_bf16x8(xp[0]);
+          const bf16x8 b1 = as_bf16x8(xp[1]);
 #pragma unroll
           for (int vt = 0; vt < VTW; ++vt) {
             acc[vt][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(A.w[vt][sb][0]), b0, acc[vt][i], 0, 0, 0);
@@ -1238,7 +1245,7 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
     // logits tile of the block in the (now free) x buffers: rows x 128 columns,
     // float4 groups XOR-swizzled by row against bank conflicts; then Eq. 2 per column
     constexpr int NC = WPB / 2 * VTW * 16;  // columns of the block
-    static_assert(NC == 128 && 2 * UNITS * 4 >= 32 * MTW * NC, "tile fits the x buffers");
+    static_assert(NC == 128 && 2 * (MT * 16 * RS) * 4 >= 32 * MTW * NC, "tile fits the x buffers");
     float* tile = (float*)&xs[0][0];
     auto at = [&](int m, int j) { return tile[m * NC + ((((j >> 2) ^ (m & 31)) << 2) | (j & 3))]; };
 #pragma unroll
