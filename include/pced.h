@@ -373,12 +373,15 @@ pced_status pced_model_generate(pced_ctx* ctx, const void* model, const void* lm
  * the kernel begins, stop when it completes). Classes: */
 enum {
   PCED_PROF_APPEND = 0,  /* shared-history append and work planning */
-  PCED_PROF_ATTN = 1,    /* decode attention, one launch per layer */
+  PCED_PROF_ATTN = 1,    /* decode attention, one launch per layer (bf16
+                            pced_step: each launch after the first also
+                            merges the previous layer's split partials) */
   PCED_PROF_LMHEAD = 2,  /* LM head                                */
   PCED_PROF_BETA = 3,    /* dynamic beta (first step only)         */
   PCED_PROF_FUSE = 4,    /* Eq. 2 + Eq. 3                          */
   PCED_PROF_SYNTH = 5,   /* pced_generate's input synthesis        */
-  PCED_PROF_COMBINE = 6, /* merge of split attention partials      */
+  PCED_PROF_COMBINE = 6, /* merge of split attention partials as a launch
+                            of its own (bf16 pced_step: last layer only) */
   PCED_PROF_EMBED = 7,   /* decoder stack: token embedding          */
   PCED_PROF_QKV = 8,     /* decoder stack: norm + QKV + RoPE + append */
   PCED_PROF_OPROJ = 9,   /* decoder stack: O projection + residual  */
