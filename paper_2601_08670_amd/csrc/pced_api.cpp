@@ -157,7 +157,8 @@ Layout make_layout(const pced_config& c) {
                                   (size_t)c.ffn_dim});
   L.dec_part = take(dec * S * L.part_cols * 4);
   // prefill chunk (ffn_dim > 0): up to pf_rows (sequence, suffix token) rows per pass
-  L.pf_rows = dec ? std::max(c.max_seqs, kPrefillRows) : 0;
+  // (a multiple of 16 rows: the many-row projection path reads whole 16-row tiles)
+  L.pf_rows = dec ? (int)ceil_div(std::max(c.max_seqs, kPrefillRows), 16) * 16 : 0;
   const size_t PR = L.pf_rows;
   L.pf_proj_cols = L.part_cols;
   L.pf_len0 = take(PR * 4);
@@ -646,6 +647,7 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
   g.maxpps = cfg.max_pages_per_seq;
   g.t = c->t;
   g.log2_theta = std::log2((double)cfg.rope_theta);
+  g.num_cus = c->num_cus;
   g.part = R.proj_part;
   // K slices per projection: about one block per compute unit, more where the
   // staged x slice would not fit in LDS

@@ -199,6 +199,7 @@ struct GemmArgs {
   const int32_t* page_table;
   int layer, n_layers, n_q_heads, n_kv_heads, head_dim, max_pages, maxpps, t;
   double log2_theta;
+  int num_cus;              // compute units of the device (choice of the many-row path)
 };
 struct EmbedArgs {
   const uint16_t* embed;    // [V][hidden]

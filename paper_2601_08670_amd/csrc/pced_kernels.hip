@@ -1155,6 +1155,7 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
   static_assert(NTH % (16 * PIECES) == 0, "whole tiles per staging round");
   constexpr int ROWS_J = NTH / PIECES;
   const int row0 = tid / PIECES, pc = tid % PIECES;
+  // (x holds whole 16-row tiles: the callers' row buffers are padded to them)
   const uint16_t* xsrc = X + (size_t)row0 * K + 8 * pc;
   const int xdst = row0 * RS + pc;
   float ss[UPT];
@@ -1975,8 +1976,40 @@ size_t proj_lds_bytes(int rows, int K, int ksplit) {
 }
 
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Timing* tm) {
-  if (a.K % 64 != 0 || a.M < 1 || a.n_tiles < 1 || a.ksplit < 1 || a.ksplit > a.K / 64) return hipErrorInvalidValue;
+  if (a.K % 64 != 0 || a.M < 1 || a.n_tiles < 1) return hipErrorInvalidValue;
   if (epi == kEpiSwiglu && a.n_tiles % 2) return hipErrorInvalidValue;
+  if (a.M > kLmRowsPad && a.M <= 32 * kLmRowsMTW && a.K % 256 == 0 && kProjKMajor == kLmKMajor &&
+      a.n_tiles / 8 >= a.num_cus / 2) {
+    // 49..288 rows (the prefill's chunks) of a wide projection (gate/up: a
+    // 128-column block for at least every other compute unit): the many-row
+    // LM-head kernel reads W once for all rows (the split-K kernel re-reads it
+    // per 48-row group) and writes the plain products as a single K slice; the
+    // reduce applies the epilogue (the norm's row scale included). Narrower
+    // projections would leave most compute units idle and keep split-K.
+    LmArgs l{};
+    l.x = a.x;
+    l.w = a.w;
+    l.logits = a.part;
+    l.M = a.M;
+    l.V = 16 * a.n_tiles;
+    l.K = a.K;
+    l.rms = 0;
+    l.row_groups = 1;
+    const Timing start{tm ? tm->start : nullptr, nullptr};
+    const hipError_t e = launch_lmhead(l, true, st, tm ? &start : nullptr);
+    if (e != hipSuccess) return e;
+    GemmArgs r = a;
+    r.ksplit = 1;
+    const int outc = epi == kEpiSwiglu ? 8 * a.n_tiles : 16 * a.n_tiles;
+    const dim3 gr((outc / 4 + 255) / 256, a.M);
+    switch (epi) {
+      case kEpiQkv: return go(k_proj_reduce<kEpiQkv>, gr, dim3(256), 0, st, nullptr, t1(tm), r);
+      case kEpiResid: return go(k_proj_reduce<kEpiResid>, gr, dim3(256), 0, st, nullptr, t1(tm), r);
+      case kEpiSwiglu: return go(k_proj_reduce<kEpiSwiglu>, gr, dim3(256), 0, st, nullptr, t1(tm), r);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  if (a.ksplit < 1 || a.ksplit > a.K / 64) return hipErrorInvalidValue;
   const int NT = a.M <= 16 ? 1 : a.M <= 32 ? 2 : 3;
   const int tpw = proj_tiles_per_wave(a.n_tiles);
   const size_t lds = proj_lds_bytes(min(a.M, 16 * NT), a.K, a.ksplit);
