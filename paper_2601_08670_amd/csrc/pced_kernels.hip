@@ -1727,12 +1727,46 @@ __global__ __launch_bounds__(64 * kProjWaves) void k_proj(GemmArgs a) {
 //              per-16-column sums of h^2 its row scale is built from;
 //   kEpiSwiglu packed tiles alternate gate / up (16 columns each): with the row
 //              scale, act = bf16(silu(gate) * up) for the F MLP columns.
-template <int EPI>
+// KMAX >= ksplit: every slice's load is issued before any is used (slots past
+// ksplit re-read the last slice, so the count is fixed and branch-free), then
+// the slices are added in order; a runtime loop of load-then-add paid one
+// memory round trip per slice.
+template <int EPI, int KMAX>
 __global__ __launch_bounds__(256) void k_proj_reduce(GemmArgs a) {
   const int m = blockIdx.y, N = 16 * a.n_tiles;
   const int c4 = blockIdx.x * 256 + threadIdx.x;
   const int n0 = 4 * c4;
-  const bool valid = n0 < (EPI == kEpiSwiglu ? N / 2 : N);
+  const int ncols = EPI == kEpiSwiglu ? N / 2 : N;
+  const bool valid = n0 < ncols;
+  const int nc = valid ? n0 : ncols - 4;  // in-range column for the loads of threads past the end
+  const int last = a.ksplit - 1;
+  auto slice = [&](int sp) __attribute__((always_inline)) {
+    return a.part + ((size_t)min(sp, last) * a.M + m) * N;
+  };
+  float4 pv[KMAX], uv[EPI == kEpiSwiglu ? KMAX : 1];
+  if constexpr (EPI == kEpiSwiglu) {
+    const int ng = 32 * (nc / 16) + nc % 16;  // gate column in the interleaved tiles; up is 16 further
+#pragma unroll
+    for (int sp = 0; sp < KMAX; ++sp) {
+      pv[sp] = *(const float4*)(slice(sp) + ng);
+      uv[sp] = *(const float4*)(slice(sp) + ng + 16);
+    }
+  } else {
+#pragma unroll
+    for (int sp = 0; sp < KMAX; ++sp) pv[sp] = *(const float4*)(slice(sp) + nc);
+  }
+  // the epilogue's own inputs, in the same round trip: the residual row and the
+  // next norm's weights, or the row's position and the page of its new K/V row
+  float4 h_in = make_float4(0.f, 0.f, 0.f, 0.f);
+  uint2 g_in = make_uint2(0u, 0u);
+  int pos = 0, phys = 0;
+  if constexpr (EPI == kEpiResid) {
+    h_in = *(const float4*)(a.h + (size_t)m * N + nc);  // residual row stride: hidden = N
+    g_in = *(const uint2*)(a.g_next + nc);
+  } else if constexpr (EPI == kEpiQkv) {
+    pos = a.len0[m] + a.t;
+    phys = a.page_table[(size_t)m * a.maxpps + pos / kPage];
+  }
   float rho = 1.0f;
   if (EPI != kEpiResid && a.ss_in) {
     float t = 0.f;
@@ -1741,13 +1775,14 @@ __global__ __launch_bounds__(256) void k_proj_reduce(GemmArgs a) {
   }
   if constexpr (EPI == kEpiSwiglu) {
     if (!valid) return;
-    const int ng = 32 * (n0 / 16) + n0 % 16;  // gate column in the interleaved tiles; up is 16 further
     float g[4] = {0.f, 0.f, 0.f, 0.f}, u[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int sp = 0; sp < a.ksplit; ++sp) {
-      const float* pr = a.part + ((size_t)sp * a.M + m) * N + ng;
-      const float4 gv = *(const float4*)pr, uv = *(const float4*)(pr + 16);
-      g[0] += gv.x; g[1] += gv.y; g[2] += gv.z; g[3] += gv.w;
-      u[0] += uv.x; u[1] += uv.y; u[2] += uv.z; u[3] += uv.w;
+#pragma unroll
+    for (int sp = 0; sp < KMAX; ++sp) {
+      if (sp < a.ksplit) {
+        const float4 gv = pv[sp], u4 = uv[sp];
+        g[0] += gv.x; g[1] += gv.y; g[2] += gv.z; g[3] += gv.w;
+        u[0] += u4.x; u[1] += u4.y; u[2] += u4.z; u[3] += u4.w;
+      }
     }
     uint32_t o[4];
 #pragma unroll
@@ -1759,9 +1794,10 @@ __global__ __launch_bounds__(256) void k_proj_reduce(GemmArgs a) {
     return;
   }
   float o[4] = {0.f, 0.f, 0.f, 0.f};
-  if (valid) {
-    for (int sp = 0; sp < a.ksplit; ++sp) {
-      const float4 v = *(const float4*)(a.part + ((size_t)sp * a.M + m) * N + n0);
+#pragma unroll
+  for (int sp = 0; sp < KMAX; ++sp) {
+    if (sp < a.ksplit) {
+      const float4 v = pv[sp];
       o[0] += v.x;
       o[1] += v.y;
       o[2] += v.z;
@@ -1771,14 +1807,14 @@ __global__ __launch_bounds__(256) void k_proj_reduce(GemmArgs a) {
   if constexpr (EPI == kEpiResid) {
     float ss = 0.f;
     if (valid) {
-      float* hp = a.h + (size_t)m * N + n0;  // residual row stride: hidden = N
-      float4 hv = *(float4*)hp;
+      float* hp = a.h + (size_t)m * N + n0;
+      float4 hv = h_in;
       hv.x += o[0];
       hv.y += o[1];
       hv.z += o[2];
       hv.w += o[3];
       *(float4*)hp = hv;
-      const uint2 g = *(const uint2*)(a.g_next + n0);
+      const uint2 g = g_in;
       uint2 pk;
       pk.x = f2bf(hv.x * bf2f(g.x & 0xFFFFu)) | (f2bf(hv.y * bf2f(g.x >> 16)) << 16);
       pk.y = f2bf(hv.z * bf2f(g.y & 0xFFFFu)) | (f2bf(hv.w * bf2f(g.y >> 16)) << 16);
@@ -1794,7 +1830,6 @@ __global__ __launch_bounds__(256) void k_proj_reduce(GemmArgs a) {
     const int sec = n0 < qd ? 0 : n0 < qd + kd ? 1 : 2;
     const int c0 = sec == 0 ? n0 : sec == 1 ? n0 - qd : n0 - qd - kd;
     const int head = c0 / D, d = c0 % D;
-    const int pos = a.len0[m] + a.t;
 #pragma unroll
     for (int q = 0; q < 4; ++q) o[q] *= rho;
     if (sec < 2) {
@@ -1817,7 +1852,6 @@ __global__ __launch_bounds__(256) void k_proj_reduce(GemmArgs a) {
       const size_t qo = (((size_t)m * a.n_layers + a.layer) * a.n_q_heads + head) * D + d;
       *(uint2*)(a.q_out + qo) = make_uint2(b[0] | (b[1] << 16), b[2] | (b[3] << 16));
     } else {
-      const int phys = a.page_table[(size_t)m * a.maxpps + pos / kPage];
       const int slot = pos % kPage;
       const size_t base = (((size_t)a.layer * a.max_pages + phys) * a.n_kv_heads + head) * kPage * D;
       uint16_t* pool = sec == 1 ? a.kpool : a.vpool;
@@ -1975,6 +2009,31 @@ size_t proj_lds_bytes(int rows, int K, int ksplit) {
   return (size_t)rows * (64 * n + 8) * 2;
 }
 
+namespace {
+// the K-slice sum and epilogue of a projection (ksplit <= kProjMaxSplit)
+template <int EPI>
+hipError_t launch_reduce_epi(const GemmArgs& a, dim3 g, hipStream_t st, hipEvent_t ev1) {
+  const dim3 b(256);
+  static_assert(kProjMaxSplit == 16, "slice-count instantiations below");
+  if (a.ksplit <= 1) return go(k_proj_reduce<EPI, 1>, g, b, 0, st, nullptr, ev1, a);
+  if (a.ksplit <= 2) return go(k_proj_reduce<EPI, 2>, g, b, 0, st, nullptr, ev1, a);
+  if (a.ksplit <= 4) return go(k_proj_reduce<EPI, 4>, g, b, 0, st, nullptr, ev1, a);
+  if (a.ksplit <= 8) return go(k_proj_reduce<EPI, 8>, g, b, 0, st, nullptr, ev1, a);
+  return go(k_proj_reduce<EPI, 16>, g, b, 0, st, nullptr, ev1, a);
+}
+hipError_t launch_reduce(const GemmArgs& a, GemmEpi epi, hipStream_t st, hipEvent_t ev1) {
+  if (a.ksplit < 1 || a.ksplit > kProjMaxSplit) return hipErrorInvalidValue;
+  const int outc = epi == kEpiSwiglu ? 8 * a.n_tiles : 16 * a.n_tiles;  // output columns
+  const dim3 g((outc / 4 + 255) / 256, a.M);
+  switch (epi) {
+    case kEpiQkv: return launch_reduce_epi<kEpiQkv>(a, g, st, ev1);
+    case kEpiResid: return launch_reduce_epi<kEpiResid>(a, g, st, ev1);
+    case kEpiSwiglu: return launch_reduce_epi<kEpiSwiglu>(a, g, st, ev1);
+    default: return hipErrorInvalidValue;
+  }
+}
+}  // namespace
+
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Timing* tm) {
   if (a.K % 64 != 0 || a.M < 1 || a.n_tiles < 1) return hipErrorInvalidValue;
   if (epi == kEpiSwiglu && a.n_tiles % 2) return hipErrorInvalidValue;
@@ -2000,14 +2059,7 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Tim
     if (e != hipSuccess) return e;
     GemmArgs r = a;
     r.ksplit = 1;
-    const int outc = epi == kEpiSwiglu ? 8 * a.n_tiles : 16 * a.n_tiles;
-    const dim3 gr((outc / 4 + 255) / 256, a.M);
-    switch (epi) {
-      case kEpiQkv: return go(k_proj_reduce<kEpiQkv>, gr, dim3(256), 0, st, nullptr, t1(tm), r);
-      case kEpiResid: return go(k_proj_reduce<kEpiResid>, gr, dim3(256), 0, st, nullptr, t1(tm), r);
-      case kEpiSwiglu: return go(k_proj_reduce<kEpiSwiglu>, gr, dim3(256), 0, st, nullptr, t1(tm), r);
-      default: return hipErrorInvalidValue;
-    }
+    return launch_reduce(r, epi, st, t1(tm));
   }
   if (a.ksplit < 1 || a.ksplit > a.K / 64) return hipErrorInvalidValue;
   const int NT = a.M <= 16 ? 1 : a.M <= 32 ? 2 : 3;
@@ -2029,14 +2081,7 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Tim
         : NT == 2 ? go(k_proj<2, 2, true>, g, b, lds, st, t0(tm), nullptr, a)
                   : go(k_proj<3, 2, true>, g, b, lds, st, t0(tm), nullptr, a);
   if (e != hipSuccess) return e;
-  const int outc = epi == kEpiSwiglu ? 8 * a.n_tiles : 16 * a.n_tiles;  // output columns
-  const dim3 gr((outc / 4 + 255) / 256, a.M);
-  switch (epi) {
-    case kEpiQkv: return go(k_proj_reduce<kEpiQkv>, gr, dim3(256), 0, st, nullptr, t1(tm), a);
-    case kEpiResid: return go(k_proj_reduce<kEpiResid>, gr, dim3(256), 0, st, nullptr, t1(tm), a);
-    case kEpiSwiglu: return go(k_proj_reduce<kEpiSwiglu>, gr, dim3(256), 0, st, nullptr, t1(tm), a);
-    default: return hipErrorInvalidValue;
-  }
+  return launch_reduce(a, epi, st, t1(tm));
 }
 
 hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Timing* tm) {
