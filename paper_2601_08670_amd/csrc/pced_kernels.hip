@@ -1011,7 +1011,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     }
     const uint16_t* xrow[NT];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) xrow[nt] = X + (size_t)(m0 + 16 * nt + col) * K + 16 * quad;
+    // rows past M (padding of the last tile, never stored) read row M - 1: the
+    // same lines as that row, not 15 more per step
+    for (int nt = 0; nt < NT; ++nt) xrow[nt] = X + (size_t)min(m0 + 16 * nt + col, a.M - 1) * K + 16 * quad;
     struct WS { uint4 w[VT][2]; };
     struct XS { uint4 x[NT][2]; };
     auto load_w = [&](WS& S, int ks) {
