@@ -1956,8 +1956,11 @@ hipError_t launch_append(const AppendArgs& a, bool bf16, hipStream_t st, const T
 hipError_t launch_attn(const AttnArgs& a, int n_blocks, int head_dim, bool bf16, hipStream_t st, const Timing* tm) {
   if (bf16) {
     const bool s = !a.kv_reread;
+    // decode at head dim 128: a 3-page ring (two pages in flight) measured
+    // faster than 4 pages (33.7 against 34.2 us at 33 caches x 32 layers): fewer
+    // loads past each chunk's end for the same two waves per SIMD
     if (head_dim == 128)
-      return s ? go(k_attn_bf16<128, 4, true>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a)
+      return s ? go(k_attn_bf16<128, 3, true>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a)
                : go(k_attn_bf16<128, 4, false>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a);
     if (head_dim == 64)
       return s ? go(k_attn_bf16<64, 4, true>, dim3(n_blocks), dim3(64), 0, st, t0(tm), t1(tm), a)
@@ -1970,7 +1973,7 @@ hipError_t launch_attn(const AttnArgs& a, int n_blocks, int head_dim, bool bf16,
 int attn_blocks_per_cu(int head_dim, bool bf16) {
   int n = 0;
   hipError_t e;
-  if (bf16 && head_dim == 128) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_bf16<128, 4, true>, 64, 0);
+  if (bf16 && head_dim == 128) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_bf16<128, 3, true>, 64, 0);
   else if (bf16) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_bf16<64, 4, true>, 64, 0);
   else e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_attn_f32, 64, 0);
   return (e == hipSuccess && n > 0) ? n : 8;
