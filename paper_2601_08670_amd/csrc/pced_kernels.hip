@@ -199,27 +199,62 @@ __global__ __launch_bounds__(128) void k_append(AppendArgs a) {
   const size_t tile = (size_t)kPage * D;
   const size_t tile0 = ((size_t)l * a.max_pages + phys) * Hkv;
   const size_t src0 = ((size_t)s * L + l) * Hkv * D;
-  // VEC consecutive dims per thread (bf16: 8, D being 64 or 128; f32: 4, D a
-  // multiple of 4): one load per tensor, then the stores (a loop of
-  // load-then-store would wait for every load in turn). In a bf16 K tile the 8
-  // dims of one token are contiguous; in a V tile they are 8 elements apart.
-  constexpr int VEC = BF16 ? 8 : 4;
-  for (int i0 = VEC * threadIdx.x; i0 < Hkv * D; i0 += VEC * blockDim.x) {
-    const int g = i0 / D, d0 = i0 % D;
-    const size_t base = (tile0 + g) * tile;
-    if (BF16) {
-      const uint4 kv = *(const uint4*)((const uint16_t*)a.k_new + src0 + i0);
-      const uint4 vv = *(const uint4*)((const uint16_t*)a.v_new + src0 + i0);
-      *(uint4*)((uint16_t*)a.kpool + base + kswz(slot, d0)) = kv;
-      uint16_t* vt = (uint16_t*)a.vpool + base;
-      const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+  if constexpr (BF16) {
+    // Only whole 32-byte sectors are written: a store that fills part of a
+    // sector leaves a partly valid line behind, and merging it with memory
+    // later slows the attention launches that read the page. The sector is
+    // read back and only this slot's bytes change, so the neighbouring slots
+    // keep what they hold.
+    // The stores carry the non-temporal hint: the rows go out to memory during
+    // this launch instead of staying dirty in the caches, where the next
+    // attention launches, streaming every page of the layer, would pay for
+    // their write-back. D is 64 or 128.
+    const uint16_t* kn = (const uint16_t*)a.k_new + src0;
+    const uint16_t* vn = (const uint16_t*)a.v_new + src0;
+    // K: 8 dims of one token are 16 contiguous bytes, and a sector holds them
+    // for the token pair (slot & ~1, slot | 1)
+    const bool odd = slot & 1;
+    for (int i0 = 8 * threadIdx.x; i0 < Hkv * D; i0 += 8 * blockDim.x) {
+      const int g = i0 / D, d0 = i0 % D;
+      uint4* sec = (uint4*)((uint16_t*)a.kpool + (tile0 + g) * tile + kswz(slot & ~1, d0));
+      const uint4 kv = *(const uint4*)(kn + i0);
+      const uint4 other = sec[odd ? 0 : 1];
+      const uint4 lo = odd ? other : kv, hi = odd ? kv : other;
+      __builtin_nontemporal_store(u32x4{lo.x, lo.y, lo.z, lo.w}, (u32x4*)sec);
+      __builtin_nontemporal_store(u32x4{hi.x, hi.y, hi.z, hi.w}, (u32x4*)sec + 1);
+    }
+    // V: the 4 tokens of a slot group share each 8-byte unit of one dim, and
+    // the 16 units of dims d0 .. d0+7 and d0+16 .. d0+23 (d0 = 32 jj + 8 h)
+    // are 128 contiguous bytes: unit 2 i holds dim d0 + i, unit 2 i + 1 dim
+    // d0 + 16 + i. A thread owns one such run.
+    const int q4 = slot & 3, sh = 16 * (q4 & 1);
+    for (int v = threadIdx.x; v < Hkv * D / 16; v += blockDim.x) {
+      const int g = v / (D / 16), r = v % (D / 16);
+      const int d0 = 32 * (r >> 1) + 8 * (r & 1);
+      uint4* run = (uint4*)((uint16_t*)a.vpool + (tile0 + g) * tile + vswz(slot & ~3, d0));
+      const uint4 va = *(const uint4*)(vn + g * D + d0), vb = *(const uint4*)(vn + g * D + d0 + 16);
+      uint4 cur[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) vt[vswz(slot, d0 + e)] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
-    } else {
+      for (int k = 0; k < 8; ++k) cur[k] = run[k];
+      const uint32_t wa[4] = {va.x, va.y, va.z, va.w}, wb[4] = {vb.x, vb.y, vb.z, vb.w};
+      auto put = [&](uint32_t& w, uint32_t e) { w = (w & ~(0xFFFFu << sh)) | ((e & 0xFFFFu) << sh); };
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const uint32_t e0 = wa[k >> 1] >> (16 * (k & 1)), e1 = wb[k >> 1] >> (16 * (k & 1));
+        if (q4 < 2) { put(cur[k].x, e0); put(cur[k].z, e1); }
+        else { put(cur[k].y, e0); put(cur[k].w, e1); }
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) __builtin_nontemporal_store(u32x4{cur[k].x, cur[k].y, cur[k].z, cur[k].w}, (u32x4*)run + k);
+    }
+  } else {
+    // row-major fp32 tiles: a token's row is whole lines
+    for (int i0 = 4 * threadIdx.x; i0 < Hkv * D; i0 += 4 * blockDim.x) {
+      const size_t base = (tile0 + i0 / D) * tile + (size_t)slot * D + i0 % D;
       const float4 kv = *(const float4*)((const float*)a.k_new + src0 + i0);
       const float4 vv = *(const float4*)((const float*)a.v_new + src0 + i0);
-      *(float4*)((float*)a.kpool + base + (size_t)slot * D + d0) = kv;
-      *(float4*)((float*)a.vpool + base + (size_t)slot * D + d0) = vv;
+      *(float4*)((float*)a.kpool + base) = kv;
+      *(float4*)((float*)a.vpool + base) = vv;
     }
   }
 }
