@@ -29,9 +29,10 @@
  *   - Device memory is owned by the caller: KV pools, workspace, weights, inputs
  *     and outputs. The library never allocates or frees device memory. It owns
  *     only the host-side context.
- *   - Work is enqueued on the caller's stream and never synchronised; outputs
- *     are valid once the caller synchronises that stream. A NULL stream is the
- *     default stream.
+ *   - Work is enqueued on the caller's stream and not synchronised (the one
+ *     exception: pced_load_caches waits for its copies of caches held in host
+ *     memory); outputs are valid once the caller synchronises that stream. A
+ *     NULL stream is the default stream.
  *   - Every argument and capacity check runs on the host before anything is
  *     enqueued. On any non-OK status nothing was enqueued and the context is
  *     unchanged; pced_last_error() returns a description (thread-local).
@@ -161,9 +162,18 @@ const char* pced_last_error(void);
  *   n_experts       host [B]: N_b >= 1 documents of query b
  *   cache_len       host [S]: preloaded tokens of each sequence (>= 1), in order
  *                   query 0: amateur, expert 1..N_0; query 1: amateur, ...
- *   src_k, src_v    host arrays [S] of DEVICE pointers, each to a contiguous
- *                   [L][cache_len[s]][Hkv][D] tensor of the storage type; they must
- *                   stay valid until the stream has executed this call
+ *   src_k, src_v    host arrays [S] of pointers, each to a contiguous
+ *                   [L][cache_len[s]][Hkv][D] tensor of the storage type, in
+ *                   device memory or in host memory (told apart per pointer by
+ *                   hipPointerGetAttributes; pinned host memory counts as host).
+ *                   Device sources are copied by a kernel on `stream` and must
+ *                   stay valid until the stream has executed this call. Host
+ *                   sources cross to the device during the call: the library
+ *                   re-lays each host sequence into the pool's page layout in
+ *                   host memory and copies it with hipMemcpyAsync on `stream`,
+ *                   waiting for those copies before it returns (the one
+ *                   synchronisation in the library), so host buffers may be
+ *                   freed as soon as the call returns
  *   k_pool, v_pool  device, pced_pool_bytes(cfg) each, caller-owned; this call
  *                   writes the caches into them and later steps append to them
  *   page_table      host [S][max_pages_per_seq] physical page ids (>= 0,
@@ -200,6 +210,15 @@ typedef struct pced_step_out {
   float* beta_used;       /* [sum N_b] beta_k used by this step                    */
   float* hidden;          /* [S][hidden] fp32 copy of the stored hidden state x;
                              pced_model_*: the final residual stream h        */
+  /* Per-layer values of the decoder stack (pced_model_step / _generate only;
+   * ignored by pced_step), for layer-by-layer checks against a reference: */
+  float* resid_trace;     /* [L][2][S][hidden] fp32 residual stream entering
+                             layer l's attention block (index 0) and its MLP
+                             block (index 1)                                 */
+  uint16_t* qkv_trace;    /* [L][S][Hq*D + 2*Hkv*D] bf16 q, k, v of layer l
+                             after RoPE, as attended and as appended         */
+  uint16_t* act_trace;    /* [L][S][ffn_dim] bf16 MLP activation
+                             silu(gate) * up of layer l                      */
 } pced_step_out;
 
 /*
@@ -260,6 +279,20 @@ pced_status pced_lmhead(pced_ctx* ctx, const void* x, int32_t n_rows, const void
  */
 pced_status pced_fuse(pced_ctx* ctx, const float* logits, int32_t refresh_beta,
                       int32_t* tokens_out, const pced_step_out* extra, hipStream_t stream);
+
+/*
+ * Copy tokens [start, start + count) of sequence `seq` (load order), layer
+ * `layer`, out of the KV pool into k_out / v_out: device, contiguous
+ * [count][Hkv][D] of the storage type, caller-owned (the layout of
+ * pced_load_caches' sources). Reads what the loaded caches and every append so
+ * far hold, e.g. to export a cache or to inspect the rows a step appended
+ * (Section 3: the chosen token joins every expert's cache). count == 0 is a
+ * no-op. Asynchronous on `stream`. Errors: STATE (nothing loaded), INVALID_ARG
+ * (NULL output, seq or layer out of range, a token range beyond the
+ * sequence's current length), HIP.
+ */
+pced_status pced_read_cache(pced_ctx* ctx, int32_t seq, int32_t layer, int32_t start, int32_t count,
+                            void* k_out, void* v_out, hipStream_t stream);
 
 /* Host mirror of the current cache length of every sequence: out [S]. */
 pced_status pced_get_lengths(const pced_ctx* ctx, int32_t* out, int32_t capacity);

@@ -117,53 +117,95 @@ class ModelOracle:
     def lengths(self):
         return [self.K[s][0].shape[0] for s in range(self.S)]
 
-    def layer(self, l: int, h: np.ndarray):
-        """One decoder layer for the new token of every sequence; appends its K/V
-        rows. Returns (h after the layer, attention output [S, Hq, D])."""
-        S, Hq, Hkv, D = self.S, self.Hq, self.Hkv, self.D
-        w = lambda n: self.weight(n, l)  # noqa: E731
-        g_attn, g_mlp = w("attn_norm"), w("mlp_norm")
-        q = normed_product(h, g_attn, w("wq")).reshape(S, Hq, D)
-        k = normed_product(h, g_attn, w("wk")).reshape(S, Hkv, D)
-        v = normed_product(h, g_attn, w("wv")).reshape(S, Hkv, D)
-        o = np.empty((S, Hq, D))
-        for s in range(S):
-            pos = self.K[s][l].shape[0]
-            qs = round_to_bf16(rope(q[s], pos, self.theta))
-            ks = round_to_bf16(rope(k[s], pos, self.theta))
-            vs = round_to_bf16(v[s])
-            self.K[s][l] = np.concatenate([self.K[s][l], ks[None]], axis=0)
-            self.Vc[s][l] = np.concatenate([self.Vc[s][l], vs[None]], axis=0)
-            o[s] = attention(qs, self.K[s][l], self.Vc[s][l])
-        h = h + round_to_bf16(o.reshape(S, Hq * D)) @ w("wo").T
-        gate = normed_product(h, g_mlp, w("w_gate"))
-        up = normed_product(h, g_mlp, w("w_up"))
-        act = round_to_bf16(silu(gate) * up)
-        h = h + act @ w("w_down").T
-        return h, o
+    # ---- the stages of one decoder layer (each takes its inputs explicitly, so a
+    # test can feed any stage the values another implementation produced)
 
-    def forward(self, in_tokens: np.ndarray):
+    def qkv(self, l: int, h: np.ndarray, positions) -> tuple:
+        """Layer l's q [S, Hq, D], k, v [S, Hkv, D] for residual rows h at the given
+        positions: normalised products, RoPE on q and k, all rounded to bf16."""
+        S, Hq, Hkv, D = h.shape[0], self.Hq, self.Hkv, self.D
+        g = self.weight("attn_norm", l)
+        q = normed_product(h, g, self.weight("wq", l)).reshape(S, Hq, D)
+        k = normed_product(h, g, self.weight("wk", l)).reshape(S, Hkv, D)
+        v = normed_product(h, g, self.weight("wv", l)).reshape(S, Hkv, D)
+        qs = np.empty_like(q)
+        ks = np.empty_like(k)
+        for s in range(S):
+            qs[s] = round_to_bf16(rope(q[s], positions[s], self.theta))
+            ks[s] = round_to_bf16(rope(k[s], positions[s], self.theta))
+        return qs, ks, round_to_bf16(v)
+
+    def o_residual(self, l: int, h: np.ndarray, o: np.ndarray) -> np.ndarray:
+        """h + bf16(o) Wo^T for the attention output o [S, Hq*D] (or [S, Hq, D])."""
+        return h + round_to_bf16(o.reshape(h.shape[0], self.Hq * self.D)) @ self.weight("wo", l).T
+
+    def mlp_act(self, l: int, h: np.ndarray) -> np.ndarray:
+        """bf16(silu(b Wg^T) * (b Wu^T)) with b the MLP norm's product of h."""
+        g = self.weight("mlp_norm", l)
+        gate = normed_product(h, g, self.weight("w_gate", l))
+        up = normed_product(h, g, self.weight("w_up", l))
+        return round_to_bf16(silu(gate) * up)
+
+    def down_residual(self, l: int, h: np.ndarray, act: np.ndarray) -> np.ndarray:
+        """h + act Wd^T."""
+        return h + act @ self.weight("w_down", l).T
+
+    def logits_of(self, h: np.ndarray) -> np.ndarray:
+        """Final norm and LM head: RMSNorm(h) g_final W_lm^T."""
+        return normed_product(h, self.final_norm, self.lm_head)
+
+    def append_rows(self, l: int, k: np.ndarray, v: np.ndarray):
+        """Append one K/V row per sequence (decoded values [S, Hkv, D]) to layer l."""
+        for s in range(self.S):
+            self.K[s][l] = np.concatenate([self.K[s][l], k[s][None]], axis=0)
+            self.Vc[s][l] = np.concatenate([self.Vc[s][l], v[s][None]], axis=0)
+
+    def attend(self, l: int, q: np.ndarray) -> np.ndarray:
+        """Every sequence's attention over its layer-l cache: [S, Hq, D]."""
+        return np.stack([attention(q[s], self.K[s][l], self.Vc[s][l]) for s in range(self.S)])
+
+    def layer(self, l: int, h: np.ndarray, kv_rows: Optional[Callable] = None):
+        """One decoder layer for the new token of every sequence; appends its K/V
+        rows. ``kv_rows(l)``, if given, returns the rows [S, Hkv, D] to append in
+        place of the layer's own (a cache taught by another implementation).
+        Returns (h after the layer, attention output [S, Hq, D], own (q, k, v))."""
+        pos = [self.K[s][l].shape[0] for s in range(self.S)]
+        q, k, v = self.qkv(l, h, pos)
+        ka, va = (k, v) if kv_rows is None else kv_rows(l)
+        self.append_rows(l, ka, va)
+        o = self.attend(l, q)
+        h = self.o_residual(l, h, o)
+        h = self.down_residual(l, h, self.mlp_act(l, h))
+        return h, o, (q, k, v)
+
+    def forward(self, in_tokens: np.ndarray, kv_rows: Optional[Callable] = None):
         """Embed each query's token into all its sequences and run every layer.
-        Returns (final residual stream h [S, hidden], {layer: attention output})."""
+        Returns (final residual stream h [S, hidden], {layer: attention output},
+        {layer: own (q, k, v)})."""
         toks = np.asarray(in_tokens)[self.seq_query]
         h = decode_stored(self._embed(toks), "bf16")
-        attn = {}
+        attn, own = {}, {}
         for l in range(self.L):
-            h, attn[l] = self.layer(l, h)
-        return h, attn
+            h, attn[l], own[l] = self.layer(l, h, kv_rows)
+        return h, attn, own
 
-    def prefill(self, tokens: np.ndarray):
+    def prefill(self, tokens: np.ndarray, kv_rows: Optional[Callable] = None):
         """Append the query-suffix tokens [B][n] to every sequence of each query,
-        one token at a time (causal by construction); no logits."""
+        one token at a time (causal by construction); no logits. ``kv_rows(i, l)``
+        optionally supplies suffix token i's rows at layer l (see ``layer``).
+        Returns {(i, l): own (q, k, v)}."""
         tokens = np.asarray(tokens)
+        own = {}
         for i in range(tokens.shape[1]):
-            self.forward(tokens[:, i])
+            rows = None if kv_rows is None else (lambda l, i=i: kv_rows(i, l))
+            _, _, o = self.forward(tokens[:, i], rows)
+            for l, x in o.items():
+                own[(i, l)] = x
+        return own
 
-    def step(self, in_tokens: np.ndarray) -> StepResult:
-        """One decode step: append the queries' previous tokens, logits of every
-        sequence, dynamic beta at the first step, Eq. 2 / Eq. 3 per query."""
-        h, attn = self.forward(in_tokens)
-        logits = normed_product(h, self.final_norm, self.lm_head)
+    def select(self, logits: np.ndarray) -> StepResult:
+        """Dynamic beta at the first call (frozen afterwards) and Eq. 2 / Eq. 3 per
+        query over the logits of every sequence."""
         if self.fixed_beta is not None:
             beta = self.fixed_beta
         else:
@@ -182,7 +224,15 @@ class ModelOracle:
         return StepResult(
             tokens=np.array([x.token for x in sels]), winners=np.array([x.winner for x in sels]),
             top1=np.array([x.top1 for x in sels]), top2=np.array([x.top2 for x in sels]),
-            beta=np.array(beta, copy=True), logits=logits, hidden=h, attn=attn)
+            beta=np.array(beta, copy=True), logits=logits, hidden=None, attn={})
+
+    def step(self, in_tokens: np.ndarray) -> StepResult:
+        """One decode step: append the queries' previous tokens, logits of every
+        sequence, dynamic beta at the first step, Eq. 2 / Eq. 3 per query."""
+        h, attn, _ = self.forward(in_tokens)
+        r = self.select(self.logits_of(h))
+        r.hidden, r.attn = h, attn
+        return r
 
 
 def causal_block_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, n_new: int) -> np.ndarray:

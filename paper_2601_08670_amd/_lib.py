@@ -24,7 +24,7 @@ EXPORTED = ("pced_pool_bytes", "pced_lm_head_bytes", "pced_pack_lm_head", "pced_
             "pced_load_caches", "pced_step", "pced_generate", "pced_lmhead", "pced_fuse",
             "pced_get_lengths", "pced_profile_enable", "pced_profile_read", "pced_relevance",
             "pced_model_bytes", "pced_pack_model_layer", "pced_pack_model_globals", "pced_model_prefill",
-            "pced_model_step", "pced_model_generate")
+            "pced_model_step", "pced_model_generate", "pced_read_cache")
 
 
 class PcedError(RuntimeError):
@@ -43,7 +43,10 @@ class pced_config(ctypes.Structure):
 class pced_step_out(ctypes.Structure):
     _fields_ = [("attn_out", ctypes.c_void_p), ("logits", ctypes.c_void_p), ("winner", ctypes.c_void_p),
                 ("top1", ctypes.c_void_p), ("top2", ctypes.c_void_p), ("beta_used", ctypes.c_void_p),
-                ("hidden", ctypes.c_void_p)]
+                ("hidden", ctypes.c_void_p), ("resid_trace", ctypes.c_void_p), ("qkv_trace", ctypes.c_void_p),
+                ("act_trace", ctypes.c_void_p)]
+
+STEP_OUT_FIELDS = tuple(n for n, _ in pced_step_out._fields_)
 
 
 class pced_synth(ctypes.Structure):
@@ -91,6 +94,7 @@ def load_library() -> ctypes.CDLL:
         "pced_model_prefill": (I, [P, P, I, P, V]),
         "pced_model_step": (I, [P, P, P, P, P, ctypes.POINTER(pced_step_out), V]),
         "pced_model_generate": (I, [P, P, P, I, P, P, ctypes.POINTER(pced_step_out), V]),
+        "pced_read_cache": (I, [P, I, I, I, I, P, P, V]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -194,7 +198,10 @@ def _step_out(extra: Optional[dict]):
     if not extra:
         return None
     so = pced_step_out()
-    for name in ("attn_out", "logits", "winner", "top1", "top2", "beta_used", "hidden"):
+    unknown = set(extra) - set(STEP_OUT_FIELDS)
+    if unknown:
+        raise ValueError(f"unknown step outputs {sorted(unknown)}")
+    for name in STEP_OUT_FIELDS:
         t = extra.get(name)
         setattr(so, name, None if t is None else t.data_ptr())
     return ctypes.byref(so), so
@@ -285,6 +292,10 @@ class Context:
         _check(self.lib.pced_model_generate(self.handle, model.data_ptr(), lm_head.data_ptr(), int(n_steps),
                                             first_tokens.data_ptr(), tokens_out.data_ptr(), so[0] if so else None,
                                             _stream(stream)))
+
+    def pced_read_cache(self, seq, layer, start, count, k_out, v_out, stream=None):
+        _check(self.lib.pced_read_cache(self.handle, int(seq), int(layer), int(start), int(count), k_out.data_ptr(),
+                                        v_out.data_ptr(), _stream(stream)))
 
     def pced_get_lengths(self, n_seqs):
         out = (ctypes.c_int32 * n_seqs)()

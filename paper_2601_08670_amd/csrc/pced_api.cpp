@@ -77,7 +77,7 @@ bool cfg_valid(const pced_config* c, std::string* why) {
 struct Layout {
   size_t len0, page_table, seq_query, query_seq0, query_exp0, exp_seq, exp_query, prior, logw, beta_fixed,
       load_items, src_k, src_v, meta_end;
-  size_t chunk_info, seg, nparts, work_pages, tick_fuse, tick_beta, prev_tok, beta, part_acc, part_ml, x, logits,
+  size_t chunk_info, seg, nparts, work_pages, prev_tok, beta, part_acc, part_ml, x, logits,
       fuse_part, lse_part, jsd_part, agg_lse, syn_q, syn_k, syn_v, dec_h, dec_a, dec_act, dec_ss, dec_rho, dec_part,
       pf_len0, pf_pt, pf_tok, pf_nparts, pf_h, pf_a, pf_act, pf_ss, pf_q, pf_x, pf_part_acc, pf_part_ml, pf_proj,
       total;
@@ -121,8 +121,6 @@ Layout make_layout(const pced_config& c) {
   L.seg = take((size_t)L.max_work * kMaxSeg * 2 * 16);
   L.nparts = take(S * 4);
   L.work_pages = take((size_t)L.max_work * kMaxSplitPages * 4);
-  L.tick_fuse = take(B * 4);
-  L.tick_beta = take(S * 4);
   L.prev_tok = take(B * 4);
   L.beta = take(S * 4);
   // split partials: [S*Hkv][stride][G][D] with stride <= pages per sequence.
@@ -314,6 +312,78 @@ AttnPlan plan_for_lengths(const pced_ctx* c, const std::vector<int>& lens) {
   return plan;
 }
 
+// Device memory a kernel can read directly; anything else (pageable or pinned
+// host memory) takes the host path of pced_load_caches.
+bool is_device_memory(const void* p) {
+  hipPointerAttribute_t attr{};
+  if (hipPointerGetAttributes(&attr, p) != hipSuccess) {
+    (void)hipGetLastError();  // unregistered host memory: clear the sticky error
+    return false;
+  }
+  return attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeManaged || attr.isManaged;
+}
+
+// Host path of pced_load_caches: sequence s's cache, held in host memory as
+// [L][len][Hkv][D], re-laid on the host into the pool's tiles of each of its
+// pages (slots past len zero) and copied into the pool with one hipMemcpyAsync
+// per run of consecutive physical pages. The staging image is reused once the
+// copies out of it have completed (hence the stream synchronisations).
+struct HostLoader {
+  const pced_config& cfg;
+  hipStream_t st;
+  size_t es, tile_elems, page_bytes;  // page_bytes: all kv-heads of one page and layer
+  std::vector<char> img;
+  size_t used = 0;
+  HostLoader(const pced_config& c, hipStream_t s)
+      : cfg(c), st(s), es(c.dtype == PCED_BF16 ? 2 : 4), tile_elems((size_t)kPage * c.head_dim),
+        page_bytes((size_t)c.n_kv_heads * kPage * c.head_dim * (c.dtype == PCED_BF16 ? 2 : 4)) {}
+
+  pced_status flush() {
+    if (used) HIP_OK(hipStreamSynchronize(st));
+    used = 0;
+    return PCED_OK;
+  }
+
+  // one (sequence, layer, K or V) image and its copies
+  pced_status put(const void* src, int len, int layer, const int32_t* pt, bool is_v, void* pool) {
+    const int D = cfg.head_dim, Hkv = cfg.n_kv_heads, np = ceil_div(len, kPage);
+    const size_t bytes = (size_t)np * page_bytes;
+    if (used + bytes > img.size()) {
+      pced_status r = flush();
+      if (r != PCED_OK) return r;
+      if (bytes > img.size()) img.resize(std::max(bytes, (size_t)64 << 20));
+    }
+    char* dst = img.data() + used;
+    const bool bf16 = cfg.dtype == PCED_BF16;
+    for (int p = 0; p < np; ++p)
+      for (int g = 0; g < Hkv; ++g) {
+        char* tile = dst + ((size_t)p * Hkv + g) * tile_elems * es;
+        for (int t = 0; t < kPage; ++t) {
+          const int tok = p * kPage + t;
+          const size_t row = (((size_t)layer * len + tok) * Hkv + g) * D;
+          for (int d = 0; d < D; ++d) {
+            if (bf16) {
+              const uint16_t v = tok < len ? ((const uint16_t*)src)[row + d] : 0;
+              ((uint16_t*)tile)[is_v ? vswz(t, d) : kswz(t, d)] = v;
+            } else {
+              ((float*)tile)[(size_t)t * D + d] = tok < len ? ((const float*)src)[row + d] : 0.f;
+            }
+          }
+        }
+      }
+    const size_t layer_off = (size_t)layer * cfg.max_pages * page_bytes;
+    for (int p0 = 0; p0 < np;) {
+      int p1 = p0 + 1;
+      while (p1 < np && pt[p1] == pt[p1 - 1] + 1) ++p1;
+      HIP_OK(hipMemcpyAsync((char*)pool + layer_off + (size_t)pt[p0] * page_bytes, dst + (size_t)p0 * page_bytes,
+                            (size_t)(p1 - p0) * page_bytes, hipMemcpyHostToDevice, st));
+      p0 = p1;
+    }
+    used += bytes;
+    return PCED_OK;
+  }
+};
+
 pced_status check_ctx(const pced_ctx* c, bool need_loaded) {
   if (!c) return fail(PCED_ERR_INVALID_ARG, "ctx is NULL");
   if (need_loaded && !c->loaded) return fail(PCED_ERR_STATE, "no batch loaded (call pced_load_caches first)");
@@ -329,7 +399,6 @@ FuseArgs fuse_args(pced_ctx* c, const float* logits, int32_t* tokens_out, int to
   f.beta = c->at<float>(c->lay.beta);
   f.prior = c->at<float>(c->lay.prior);
   f.part = c->at<float>(c->lay.fuse_part);
-  f.tickets = c->at<int32_t>(c->lay.tick_fuse);
   f.tokens_out = tokens_out;
   f.prev_tok = c->at<int32_t>(c->lay.prev_tok);
   f.winner = extra ? extra->winner : nullptr;
@@ -360,7 +429,6 @@ pced_status run_fuse(pced_ctx* c, const float* logits, bool refresh_beta, int32_
     b.exp_query = c->at<int32_t>(c->lay.exp_query);
     b.lse_part = c->at<float>(c->lay.lse_part);
     b.jsd_part = c->at<float>(c->lay.jsd_part);
-    b.tickets = c->at<int32_t>(c->lay.tick_beta);
     b.beta = c->at<float>(c->lay.beta);
     b.V = cfg.vocab;
     b.nchunk = c->lay.nchunk;
@@ -538,6 +606,10 @@ struct FwdRows {
   float* proj_part = nullptr;
   size_t proj_cols = 0;              // slices x columns per row of the projection partials
   float* attn_out = nullptr;
+  // optional per-layer traces (decode rows only; see pced_step_out)
+  float* resid_trace = nullptr;
+  uint16_t* qkv_trace = nullptr;
+  uint16_t* act_trace = nullptr;
 };
 
 AttnPlan plan_for_lengths(const pced_ctx* c, const std::vector<int>& lens);
@@ -595,6 +667,13 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
     ProfScope ps(c, PCED_PROF_EMBED, (double)M * H * (2 + 4 + 2), 0);
     HIP_OK(launch_embed(e, M, st, ps.timing()));
   }
+  const size_t h_bytes = (size_t)M * H * 4;
+  auto trace_h = [&](int l, int j) -> pced_status {  // residual stream entering layer l's block j
+    if (R.resid_trace)
+      HIP_OK(hipMemcpyAsync(R.resid_trace + ((size_t)l * 2 + j) * M * H, R.h, h_bytes, hipMemcpyDeviceToDevice, st));
+    return PCED_OK;
+  };
+  if (trace_h(0, 0) != PCED_OK) return PCED_ERR_HIP;
 
   AttnArgs at{};
   at.q = R.q;
@@ -686,6 +765,7 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
       q.n_tiles = (qd + 2 * kd) / 16;
       q.ksplit = slices(q.n_tiles, H);
       q.ss_in = R.ss;
+      q.qkv_trace = R.qkv_trace ? R.qkv_trace + (size_t)l * M * (qd + 2 * kd) : nullptr;
       ProfScope ps(c, PCED_PROF_QKV, (double)(qd + 2 * kd) * H * 2 + (double)M * (H * 2 + (qd + 2 * kd) * 2),
                    2.0 * M * (qd + 2 * kd) * H);
       if (!fits(q)) return fail(PCED_ERR_UNSUPPORTED, "QKV projection does not fit the partial buffer or LDS");
@@ -715,6 +795,7 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
       if (!fits(o)) return fail(PCED_ERR_UNSUPPORTED, "O projection does not fit the partial buffer or LDS");
       HIP_OK(launch_gemm(o, kEpiResid, st, ps.timing()));
     }
+    if (trace_h(l, 1) != PCED_OK) return PCED_ERR_HIP;
     {  // norm + gate/up + SwiGLU
       GemmArgs u = g;
       u.w = lw + ml.gu;
@@ -727,6 +808,9 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
       if (!fits(u)) return fail(PCED_ERR_UNSUPPORTED, "gate/up projection does not fit the partial buffer or LDS");
       HIP_OK(launch_gemm(u, kEpiSwiglu, st, ps.timing()));
     }
+    if (R.act_trace)
+      HIP_OK(hipMemcpyAsync(R.act_trace + (size_t)l * M * cfg.ffn_dim, R.act, (size_t)M * cfg.ffn_dim * 2,
+                            hipMemcpyDeviceToDevice, st));
     {  // down projection + residual; the next norm's input
       GemmArgs d = g;
       d.w = lw + ml.down;
@@ -739,12 +823,13 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
       if (!fits(d)) return fail(PCED_ERR_UNSUPPORTED, "down projection does not fit the partial buffer or LDS");
       HIP_OK(launch_gemm(d, kEpiResid, st, ps.timing()));
     }
+    if (l + 1 < cfg.n_layers && trace_h(l + 1, 0) != PCED_OK) return PCED_ERR_HIP;
   }
   return PCED_OK;
 }
 
 // The rows of a decode step: one per sequence.
-FwdRows decode_rows(pced_ctx* c, const int32_t* in_tok, float* attn_out) {
+FwdRows decode_rows(pced_ctx* c, const int32_t* in_tok, const pced_step_out* extra) {
   const pced_config& cfg = c->cfg;
   FwdRows R;
   R.M = c->S;
@@ -768,7 +853,12 @@ FwdRows decode_rows(pced_ctx* c, const int32_t* in_tok, float* attn_out) {
   R.part_slots = c->lay.part_slots;
   R.proj_part = c->at<float>(c->lay.dec_part);
   R.proj_cols = c->lay.part_cols;
-  R.attn_out = attn_out;
+  if (extra) {
+    R.attn_out = extra->attn_out;
+    R.resid_trace = extra->resid_trace;
+    R.qkv_trace = extra->qkv_trace;
+    R.act_trace = extra->act_trace;
+  }
   return R;
 }
 
@@ -831,7 +921,7 @@ pced_status run_model_step(pced_ctx* c, const void* model, const void* w, const 
                            int tok_stride, const pced_step_out* extra, hipStream_t st) {
   pced_status r = check_room(c, 1);
   if (r != PCED_OK) return r;
-  r = run_model_forward(c, (const char*)model, decode_rows(c, in_tok, extra ? extra->attn_out : nullptr), st);
+  r = run_model_forward(c, (const char*)model, decode_rows(c, in_tok, extra), st);
   if (r != PCED_OK) return r;
   const pced_config& cfg = c->cfg;
   float* rho = c->at<float>(c->lay.dec_rho);
@@ -1042,6 +1132,13 @@ pced_status pced_load_caches(pced_ctx* c, int32_t n_queries, const int32_t* n_ex
     if (cache_len[s] < 1) return fail(PCED_ERR_INVALID_ARG, "cache_len[%ld] = %d < 1", s, cache_len[s]);
     if (!src_k[s] || !src_v[s]) return fail(PCED_ERR_INVALID_ARG, "source pointer of sequence %ld is NULL", s);
   }
+  std::vector<char> on_host(S, 0);
+  for (long s = 0; s < S; ++s) {
+    const bool dk = is_device_memory(src_k[s]), dv = is_device_memory(src_v[s]);
+    if (dk != dv)
+      return fail(PCED_ERR_INVALID_ARG, "sequence %ld: src_k and src_v must both be device or both host memory", s);
+    on_host[s] = !dk;
+  }
   for (long e = 0; e < NE; ++e) {
     if (!std::isfinite(relevance[e])) return fail(PCED_ERR_INVALID_ARG, "relevance[%ld] is not finite", e);
     if (beta && !std::isfinite(beta[e])) return fail(PCED_ERR_INVALID_ARG, "beta[%ld] is not finite", e);
@@ -1132,7 +1229,8 @@ pced_status pced_load_caches(pced_ctx* c, int32_t n_queries, const int32_t* n_ex
     }
   }
   for (long s = 0; s < S; ++s)
-    for (int p = 0; p < ceil_div(cache_len[s], kPage); ++p) { items.push_back((int32_t)s); items.push_back(p); }
+    if (!on_host[s])
+      for (int p = 0; p < ceil_div(cache_len[s], kPage); ++p) { items.push_back((int32_t)s); items.push_back(p); }
   put(L.seq_query, seq_query.data(), S * 4);
   put(L.query_seq0, c->seq_off.data(), (n_queries + 1) * 4);
   put(L.query_exp0, c->exp_off.data(), (n_queries + 1) * 4);
@@ -1149,8 +1247,6 @@ pced_status pced_load_caches(pced_ctx* c, int32_t n_queries, const int32_t* n_ex
   HIP_OK(hipMemcpyAsync(c->ws, c->staging.data(), L.meta_end, hipMemcpyHostToDevice, st));
 
   // per-batch device state
-  HIP_OK(launch_fill_i32(c->at<int32_t>(L.tick_fuse), 0, cfg.max_queries, st));
-  HIP_OK(launch_fill_i32(c->at<int32_t>(L.tick_beta), 0, cfg.max_seqs, st));
   HIP_OK(launch_fill_i32(c->at<int32_t>(L.prev_tok), -1, cfg.max_queries, st));
   HIP_OK(launch_zero_bytes(c->at<void>(L.x), (size_t)L.rows_pad * cfg.hidden * esize_of(cfg), st));
   HIP_OK(hipMemcpyAsync(c->at<float>(L.beta), c->at<float>(L.beta_fixed), (size_t)NE * 4,
@@ -1169,7 +1265,20 @@ pced_status pced_load_caches(pced_ctx* c, int32_t n_queries, const int32_t* n_ex
   la.head_dim = cfg.head_dim;
   la.max_pages = cfg.max_pages;
   la.maxpps = P;
-  HIP_OK(launch_load(la, (int)(items.size() / 2), c->bf16, st));
+  if (!items.empty()) HIP_OK(launch_load(la, (int)(items.size() / 2), c->bf16, st));
+  {
+    HostLoader hl(cfg, st);
+    for (long s = 0; s < S; ++s) {
+      if (!on_host[s]) continue;
+      for (int l = 0; l < cfg.n_layers; ++l) {
+        r = hl.put(src_k[s], cache_len[s], l, &pt[s * P], false, k_pool);
+        if (r == PCED_OK) r = hl.put(src_v[s], cache_len[s], l, &pt[s * P], true, v_pool);
+        if (r != PCED_OK) return r;
+      }
+    }
+    r = hl.flush();
+    if (r != PCED_OK) return r;
+  }
 
   c->kpool = k_pool;
   c->vpool = v_pool;
@@ -1377,6 +1486,37 @@ pced_status pced_relevance(int32_t mode, int32_t n, const float* retrieval, cons
     }
     relevance[k] = (float)r;
   }
+  return PCED_OK;
+}
+
+pced_status pced_read_cache(pced_ctx* c, int32_t seq, int32_t layer, int32_t start, int32_t count, void* k_out,
+                            void* v_out, hipStream_t st) {
+  pced_status r = check_ctx(c, true);
+  if (r != PCED_OK) return r;
+  if (!k_out || !v_out) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  if (seq < 0 || seq >= c->S) return fail(PCED_ERR_INVALID_ARG, "seq %d not in [0, %d)", seq, c->S);
+  if (layer < 0 || layer >= c->cfg.n_layers)
+    return fail(PCED_ERR_INVALID_ARG, "layer %d not in [0, %d)", layer, c->cfg.n_layers);
+  if (start < 0 || count < 0 || (long)start + count > c->len[seq])
+    return fail(PCED_ERR_INVALID_ARG, "tokens [%d, %ld) beyond the %d of sequence %d", start, (long)start + count,
+                c->len[seq], seq);
+  if (count == 0) return PCED_OK;
+  ReadCacheArgs a{};
+  a.kpool = c->kpool;
+  a.vpool = c->vpool;
+  a.page_table = c->at<int32_t>(c->lay.page_table);
+  a.k_out = k_out;
+  a.v_out = v_out;
+  a.seq = seq;
+  a.layer = layer;
+  a.start = start;
+  a.count = count;
+  a.n_kv_heads = c->cfg.n_kv_heads;
+  a.head_dim = c->cfg.head_dim;
+  a.max_pages = c->cfg.max_pages;
+  a.maxpps = c->cfg.max_pages_per_seq;
+  a.bf16 = c->bf16;
+  HIP_OK(launch_read_cache(a, st));
   return PCED_OK;
 }
 

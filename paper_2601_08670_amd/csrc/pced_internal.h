@@ -26,6 +26,19 @@ constexpr bool kLmKMajor = true;
 // adjacent tiles at every step.
 constexpr bool kProjKMajor = true;
 
+// Element offsets inside a bf16 KV tile (16 tokens x head_dim; see pced.h, pool
+// layout): every matrix-core operand of the attention is one contiguous 16-byte
+// load per lane. K token t, dim d: the A operand of the 16x16x32 q.k product;
+// V: the A operand of the 16x16x16 V^T.P^T product. Used by the kernels and by
+// the host-side loading of caches held in host memory.
+__host__ __device__ inline int kswz(int t, int d) {
+  return ((d >> 5) * 64 + t + 16 * ((d & 31) >> 3)) * 8 + (d & 7);
+}
+__host__ __device__ inline int vswz(int t, int d) {
+  const int j = d >> 4;
+  return (((j >> 1) * 64 + (d & 15) + 16 * (t >> 2)) * 2 + (j & 1)) * 4 + (t & 3);
+}
+
 // Per-step attention launch arguments (one launch per layer).
 struct AttnArgs {
   const void* q;            // [S][L][Hq][D]
@@ -114,7 +127,6 @@ struct FuseArgs {
   const float* beta;        // [sum N]
   const float* prior;       // [sum N] gamma * ln(clip(r)) rounded to fp32
   float* part;              // [B][nblk][5]
-  int32_t* tickets;         // [B]
   int32_t* tokens_out;      // [B] with stride
   int32_t* prev_tok;        // [B]
   int32_t* winner;          // optional [B]
@@ -147,7 +159,6 @@ struct BetaArgs {
   const int32_t* exp_query; // [sum N] query of each expert slot
   float* lse_part;          // [S][nchunk][2]
   float* jsd_part;          // [sum N][nchunk]
-  int32_t* tickets;         // [sum N]
   float* beta;              // [sum N]
   const int32_t* query_exp0;// [B+1] (scalar mode)
   int V, nchunk;
@@ -193,6 +204,7 @@ struct GemmArgs {
   // kEpiQkv: columns [0, Hq*D) q, then k, then v; RoPE at pos = len0[m] + t;
   // q to q_out, k / v into the paged pool at that position
   uint16_t* q_out;          // [S][L][Hq][D]
+  uint16_t* qkv_trace;      // optional [M][Hq*D + 2 Hkv*D]: q, k, v after RoPE as stored (parity tracing)
   uint16_t* kpool;
   uint16_t* vpool;
   const int32_t* len0;
@@ -222,6 +234,16 @@ struct PrefillMetaArgs {
   int32_t* tok_map;         // [S*T] index of the row's token in tokens [B][n_tokens]
   int n_seqs, T, i0, n_tokens, maxpps;
 };
+// Copy of tokens [start, start + count) of one sequence and layer out of the pool.
+struct ReadCacheArgs {
+  const void* kpool;
+  const void* vpool;
+  const int32_t* page_table;  // device [S][maxpps]
+  void* k_out;                // [count][Hkv][D]
+  void* v_out;
+  int seq, layer, start, count, n_kv_heads, head_dim, max_pages, maxpps, bf16;
+};
+
 // Optional timing events attached to the first / last dispatch of a launcher.
 struct Timing {
   hipEvent_t start = nullptr;
@@ -257,6 +279,7 @@ size_t proj_lds_bytes(int rows, int K, int ksplit);  // LDS of a projection bloc
 hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Timing* tm = nullptr);
 hipError_t launch_prefill_meta(const PrefillMetaArgs& a, hipStream_t st);
 // rho[m] = 1/sqrt(sum_p ss[p][m] * inv_dim + eps) for m < M
+hipError_t launch_read_cache(const ReadCacheArgs& a, hipStream_t st);
 hipError_t launch_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps, float* rho,
                       hipStream_t st);
 

@@ -39,13 +39,6 @@ __device__ __forceinline__ uint32_t f2bf(float f) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-__device__ __forceinline__ int kswz(int t, int d) {
-  return ((d >> 5) * 64 + t + 16 * ((d & 31) >> 3)) * 8 + (d & 7);
-}
-__device__ __forceinline__ int vswz(int t, int d) {
-  const int j = d >> 4;
-  return (((j >> 1) * 64 + (d & 15) + 16 * (t >> 2)) * 2 + (j & 1)) * 4 + (t & 3);
-}
 
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
@@ -1885,6 +1878,8 @@ __global__ __launch_bounds__(256) void k_proj_reduce(GemmArgs a) {
     uint32_t b[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) b[q] = f2bf(o[q]);
+    if (a.qkv_trace)
+      *(uint2*)(a.qkv_trace + (size_t)m * (qd + 2 * kd) + n0) = make_uint2(b[0] | (b[1] << 16), b[2] | (b[3] << 16));
     if (sec == 0) {
       const size_t qo = (((size_t)m * a.n_layers + a.layer) * a.n_q_heads + head) * D + d;
       *(uint2*)(a.q_out + qo) = make_uint2(b[0] | (b[1] << 16), b[2] | (b[3] << 16));
@@ -1929,6 +1924,26 @@ __global__ __launch_bounds__(64) void k_prefill_meta(PrefillMetaArgs a) {
   }
   for (int p = threadIdx.x; p < a.maxpps; p += 64)
     a.page_table_out[(size_t)r * a.maxpps + p] = a.page_table[(size_t)s * a.maxpps + p];
+}
+
+// Tokens [start, start + count) of one sequence and layer out of the paged pool
+// into contiguous [count][Hkv][D] rows: one block per (token, kv-head), one
+// thread per dimension.
+__global__ __launch_bounds__(128) void k_read_cache(ReadCacheArgs a) {
+  const int i = blockIdx.x, g = blockIdx.y, d = threadIdx.x;
+  if (d >= a.head_dim) return;
+  const int tok = a.start + i, D = a.head_dim;
+  const int phys = a.page_table[(size_t)a.seq * a.maxpps + tok / kPage];
+  const int t = tok % kPage;
+  const size_t base = (((size_t)a.layer * a.max_pages + phys) * a.n_kv_heads + g) * kPage * D;
+  const size_t o = ((size_t)i * a.n_kv_heads + g) * D + d;
+  if (a.bf16) {
+    ((uint16_t*)a.k_out)[o] = ((const uint16_t*)a.kpool)[base + kswz(t, d)];
+    ((uint16_t*)a.v_out)[o] = ((const uint16_t*)a.vpool)[base + vswz(t, d)];
+  } else {
+    ((float*)a.k_out)[o] = ((const float*)a.kpool)[base + (size_t)t * D + d];
+    ((float*)a.v_out)[o] = ((const float*)a.vpool)[base + (size_t)t * D + d];
+  }
 }
 
 // rho[m] = 1/sqrt(sum_p ss[p][m] * inv_dim + eps), 8 lanes per row.
@@ -2131,6 +2146,10 @@ hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Ti
 
 hipError_t launch_prefill_meta(const PrefillMetaArgs& a, hipStream_t st) {
   return go(k_prefill_meta, dim3(a.n_seqs * a.T), dim3(64), 0, st, nullptr, nullptr, a);
+}
+
+hipError_t launch_read_cache(const ReadCacheArgs& a, hipStream_t st) {
+  return go(k_read_cache, dim3(a.count, a.n_kv_heads), dim3(128), 0, st, nullptr, nullptr, a);
 }
 
 hipError_t launch_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps, float* rho,

@@ -28,6 +28,7 @@ class PcedSession:
         self.device = device
         self.geom = dict(n_layers=n_layers, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads,
                          head_dim=head_dim, vocab=vocab)
+        self.ffn_dim = ffn_dim
         self.cfg = _lib.make_config(n_layers=n_layers, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads,
                                     head_dim=head_dim, vocab=vocab, dtype=dtype, max_queries=max_queries,
                                     max_seqs=max_seqs, max_pages=max_pages,
@@ -101,6 +102,12 @@ class PcedSession:
             "beta_used": ((self.NE,), f32),
             "hidden": ((self.S, g["n_q_heads"] * g["head_dim"]), f32),
         }
+        if self.ffn_dim:
+            L, H, D = g["n_layers"], g["n_q_heads"] * g["head_dim"], g["head_dim"]
+            qkv = (g["n_q_heads"] + 2 * g["n_kv_heads"]) * D
+            shapes["resid_trace"] = ((L, 2, self.S, H), f32)
+            shapes["qkv_trace"] = ((L, self.S, qkv), torch.int16)
+            shapes["act_trace"] = ((L, self.S, self.ffn_dim), torch.int16)
         return {k: torch.empty(shapes[k][0], dtype=shapes[k][1], device=self.device) for k in want}
 
     def step(self, q, k_new, v_new, lm_head, want=("logits", "winner", "top1", "top2", "beta_used")):
@@ -123,6 +130,17 @@ class PcedSession:
 
     def lengths(self):
         return self.ctx.pced_get_lengths(self.S)
+
+    def read_cache(self, seq, layer, start, count):
+        """(k, v) rows [count][Hkv][D] of one sequence and layer, read out of the
+        pool (int16 bf16 bits or float32), on the session's device."""
+        torch = _torch()
+        g = self.geom
+        dt = torch.int16 if self.dtype == "bf16" else torch.float32
+        k = torch.empty((count, g["n_kv_heads"], g["head_dim"]), dtype=dt, device=self.device)
+        v = torch.empty_like(k)
+        self.ctx.pced_read_cache(seq, layer, start, count, k, v)
+        return k, v
 
 
 def session_for_workload(wl, device="cuda", extra_tokens: Optional[int] = None, norm="rms",

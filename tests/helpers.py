@@ -49,6 +49,42 @@ def make_oracle(wl: W.Workload, layers=None, seqs=None, norm="rms") -> O.Oracle:
                     relevance=wl.relevance, gamma=wl.gamma, beta=wl.beta, norm=norm)
 
 
+def beta_tol(logits, ref_logits, wl) -> np.ndarray:
+    """Per-expert bound on |beta_gpu - beta_ref| from the logits' errors. beta_k =
+    JSD(softmax s_k || softmax s_0) in bits; the gradient of the JSD with respect
+    to either logit row has L1 norm at most sum_v p(v) |log2(p(v)/m(v))| <=
+    1 + 1/(e ln 2) < 1.6 (p/m <= 2 above the mixture m; x log2(1/x) <= 1/(e ln 2)
+    below it), so to first order |d beta_k| <= 1.6 (e_k + e_0), e_r = max_v
+    |d s_r(v)|. Floor 1e-4 for the fp32 sums over the vocabulary. ``wl``: any
+    object with ``n_experts`` and ``seq_offsets`` of the rows' queries."""
+    e = np.abs(np.asarray(logits, np.float64) - ref_logits).max(axis=1)
+    tol = []
+    for b, n in enumerate(wl.n_experts):
+        r0 = wl.seq_offsets[b]
+        tol += [max(1e-4, 1.6 * (e[r0 + k] + e[r0])) for k in range(1, n + 1)]
+    return np.array(tol)
+
+
+def score_tol(logits, ref_logits, wl, beta_gpu, beta_ref, top1_ref) -> np.ndarray:
+    """Per-query bound on |top_gpu - top_ref| for the fused scores of Eq. 2. A
+    score (1 + b) s_k - b s_0 + c moves by at most (1 + 2 b) e with e the query's
+    max logit error, plus |d b| |s_k - s_0| from the difference in beta, plus
+    the fp32 evaluation of Eq. 2 (a few ulp of the score, taken as 1e-5 of it);
+    top-1 and top-2 are maxima of such scores, so they move by at most as much."""
+    lg = np.asarray(logits, np.float64)
+    out = []
+    e0 = 0
+    for b, n in enumerate(wl.n_experts):
+        r0, r1 = wl.seq_offsets[b], wl.seq_offsets[b + 1]
+        e = float(np.abs(lg[r0:r1] - ref_logits[r0:r1]).max())
+        bb = np.asarray(beta_ref[e0:e0 + n], np.float64)
+        db = float(np.abs(np.asarray(beta_gpu[e0:e0 + n], np.float64) - bb).max())
+        spread = float(np.abs(ref_logits[r0 + 1:r1] - ref_logits[r0][None, :]).max())
+        out.append((1 + 2 * float(bb.max())) * e + db * spread + 1e-5 * max(1.0, abs(float(top1_ref[b]))))
+        e0 += n
+    return np.array(out)
+
+
 def fused_best(logits_query, relevance, gamma, beta):
     """S(v) = max over experts of Eq. 2 (oracle, float64)."""
     return O.contrastive_scores(logits_query, beta, O.prior_term(relevance, gamma)).max(axis=0)

@@ -249,3 +249,24 @@ def test_decoder_stack_entry_points_validate_before_any_launch():
     assert lib.pced_model_prefill(fc.h, 1, 2, 1, None) == STATE
     assert lib.pced_model_generate(fc.h, 1, 1, 2, 1, 1, None, None) == STATE
     fc.close()
+
+
+def _struct_fields(name):
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    body = re.search(r"typedef struct %s \{(.*?)\} %s;" % (name, name), text, flags=re.S).group(1)
+    return re.findall(r"\b(\w+)\s*;", body)
+
+
+def test_struct_layouts_match_the_binding():
+    # the ctypes mirrors must list the header's members in the header's order
+    assert _struct_fields("pced_config") == [n for n, _ in _lib.pced_config._fields_]
+    assert _struct_fields("pced_step_out") == [n for n, _ in _lib.pced_step_out._fields_]
+    assert _struct_fields("pced_synth") == [n for n, _ in _lib.pced_synth._fields_]
+
+
+def test_read_cache_validation_before_any_launch():
+    fc = FakeCtx()
+    lib = fc.lib
+    assert lib.pced_read_cache(fc.h, 0, 0, 0, 1, 1 << 40, 1 << 41, None) == STATE
+    assert lib.pced_read_cache(None, 0, 0, 0, 1, 1 << 40, 1 << 41, None) == INVALID
+    fc.close()

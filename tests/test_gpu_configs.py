@@ -7,7 +7,7 @@ import pytest
 from oracle import pced_oracle as O
 from oracle import synth as osynth
 from pced_inputs import workloads as W
-from tests.helpers import REL_TOL, check_tokens, lm_head_host, rel_err_rows
+from tests.helpers import REL_TOL, beta_tol, check_tokens, lm_head_host, rel_err_rows, score_tol
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -24,18 +24,29 @@ def _session(wl, **kw):
     return session_for_workload(wl, device=DEV, **kw)
 
 
-def _oracle_for_queries(wl, queries):
-    """Oracle restricted to some queries (queries are independent of each other)."""
+def _oracle_for_queries(wl, queries, cache_layers=None):
+    """Oracle restricted to some queries (queries are independent of each other).
+    Cache rows of the layers in ``cache_layers`` (all if None) are generated once
+    and kept; the others are generated again at every step that evaluates them."""
     off = wl.seq_offsets
     seqs = [s for b in queries for s in range(off[b], off[b + 1])]
     eoff = np.concatenate([[0], np.cumsum(wl.n_experts)])
     rel = np.concatenate([wl.relevance[eoff[b]:eoff[b + 1]] for b in queries])
     beta = None if wl.beta is None else np.concatenate([wl.beta[eoff[b]:eoff[b + 1]] for b in queries])
     g = wl.geom
+    kept = {}
+
+    def cache(kind, s, l):
+        if cache_layers is not None and l not in cache_layers:
+            return (wl.kcache_host if kind == "k" else wl.vcache_host)(seqs[s], l)
+        if (kind, s, l) not in kept:
+            kept[(kind, s, l)] = (wl.kcache_host if kind == "k" else wl.vcache_host)(seqs[s], l)
+        return kept[(kind, s, l)]
+
     orc = O.Oracle(n_layers=g.n_layers, n_q_heads=g.n_q_heads, n_kv_heads=g.n_kv_heads, head_dim=g.head_dim,
                    vocab=g.vocab, dtype=g.dtype, n_experts=[wl.n_experts[b] for b in queries],
-                   cache_k=lambda s, l: wl.kcache_host(seqs[s], l),
-                   cache_v=lambda s, l: wl.vcache_host(seqs[s], l), relevance=rel, gamma=wl.gamma, beta=beta)
+                   cache_k=lambda s, l: cache("k", s, l), cache_v=lambda s, l: cache("v", s, l),
+                   relevance=rel, gamma=wl.gamma, beta=beta)
     return orc, seqs
 
 
@@ -49,21 +60,6 @@ class _SubWorkload:
         eoff = np.concatenate([[0], np.cumsum(wl.n_experts)])
         self.relevance = np.concatenate([wl.relevance[eoff[b]:eoff[b + 1]] for b in queries])
         self.gamma = wl.gamma
-
-
-def _beta_tol(logits, ref_logits, sub):
-    """Per-expert bound on |beta_gpu - beta_ref| from the logits' errors. beta_k =
-    JSD(softmax s_k || softmax s_0) in bits; the gradient of the JSD with respect
-    to either logit row has L1 norm at most sum_v p(v) |log2(p(v)/m(v))| <=
-    1 + 1/(e ln 2) < 1.6 (p/m <= 2 above the mixture m; x log2(1/x) <= 1/(e ln 2)
-    below it), so to first order |d beta_k| <= 1.6 (e_k + e_0), e_r = max_v
-    |d s_r(v)|. Floor 1e-4 for the fp32 sums over the vocabulary."""
-    e = np.abs(np.asarray(logits, np.float64) - ref_logits).max(axis=1)
-    tol = []
-    for b, n in enumerate(sub.n_experts):
-        r0 = sub.seq_offsets[b]
-        tol += [max(1e-4, 1.6 * (e[r0 + k] + e[r0])) for k in range(1, n + 1)]
-    return np.array(tol)
 
 
 def _check_queries(wl, queries, steps, attn_layers=None, sess=None):
@@ -93,7 +89,7 @@ def _check_queries(wl, queries, steps, attn_layers=None, sess=None):
         err = rel_err_rows(lg, ref.logits)
         assert err <= tol, f"step {t}: logits rel err {err}"
         d_beta = np.abs(_np(out["beta_used"])[eidx].astype(np.float64) - ref.beta)
-        bt = _beta_tol(lg, ref.logits, sub)
+        bt = beta_tol(lg, ref.logits, sub)
         assert (d_beta <= bt).all(), f"step {t}: beta off by {d_beta} (bounds {bt})"
         toks = _np(out["tokens"])[queries]
         exempt += check_tokens(toks, ref.logits, sub, ref.beta, ref.tokens, ref.gaps)
@@ -101,6 +97,64 @@ def _check_queries(wl, queries, steps, attn_layers=None, sess=None):
         for i in range(len(queries)):
             if toks[i] == ref.tokens[i] and ref.gaps[i] > 1e-3:
                 assert win[i] == ref.winners[i]
+    return exempt
+
+
+def _check_timed_path(wl, queries, steps, all_layers_at=(), attn_layers=None):
+    """The path bench.py times, against the oracle. Two sessions run the same
+    steps: A requests the logits (the materialised path: logits, attention and
+    beta are compared with the oracle, and A's logit errors bound the scores), B
+    requests none (the timed path: from the second step on, with beta frozen,
+    Eq. 2 and the slice argmax run in the LM head's epilogue and the logits are
+    never written). B's tokens, winners and top-1 / top-2 scores must equal A's
+    bit for bit and meet the oracle's under the token contract and the score
+    bound of ``score_tol``. The oracle evaluates ``attn_layers`` (plus the last)
+    at every step and all layers at the steps in ``all_layers_at``."""
+    sa, sb = _session(wl), _session(wl)
+    g = wl.geom
+    Wt = sa.pack_lm_head(wl.lm_head_device(DEV))
+    Wh = lm_head_host(wl.seed, g.vocab, g.hidden, g.dtype)
+    keep = sorted(set(attn_layers or []) | {g.n_layers - 1})
+    orc, seqs = _oracle_for_queries(wl, queries, cache_layers=set(keep))
+    sub = _SubWorkload(wl, queries)
+    tol = REL_TOL[g.dtype]
+    eoff = np.concatenate([[0], np.cumsum(wl.n_experts)])
+    eidx = np.concatenate([np.arange(eoff[b], eoff[b + 1]) for b in queries])
+    exempt = 0
+    for t in range(steps):
+        q, kn, vn = wl.step_inputs_device(t, DEV)
+        oa = sa.step(q, kn, vn, Wt, want=("logits", "attn_out", "winner", "top1", "top2", "beta_used"))
+        ob = sb.step(q, kn, vn, Wt, want=("winner", "top1", "top2", "beta_used"))
+        torch.cuda.synchronize()
+        for k in ("tokens", "winner", "top1", "top2", "beta_used"):
+            assert np.array_equal(_np(oa[k]).view(np.uint8), _np(ob[k]).view(np.uint8)), (t, k)
+        del q, kn, vn
+        qh, kh, vh = wl.step_inputs_host(t)
+        layers = None if t in all_layers_at else keep
+        ref = orc.step(qh[seqs], kh[seqs], vh[seqs], Wh, attn_layers=layers)
+        del qh, kh, vh
+        a = _np(oa["attn_out"])[seqs]
+        for l, ra in ref.attn.items():
+            err = rel_err_rows(a[:, l].reshape(-1, g.head_dim), ra.reshape(-1, g.head_dim))
+            assert err <= tol, f"step {t} layer {l}: attention rel err {err}"
+        print(f"step {t}: attention compared on {len(ref.attn)} layers")
+        lg = _np(oa["logits"])[seqs]
+        err = rel_err_rows(lg, ref.logits)
+        assert err <= tol, f"step {t}: logits rel err {err}"
+        beta_gpu = _np(ob["beta_used"])[eidx].astype(np.float64)
+        bt = beta_tol(lg, ref.logits, sub)
+        assert (np.abs(beta_gpu - ref.beta) <= bt).all(), f"step {t}: beta off (bounds {bt})"
+        toks = _np(ob["tokens"])[queries]
+        exempt += check_tokens(toks, ref.logits, sub, ref.beta, ref.tokens, ref.gaps)
+        win = _np(ob["winner"])[queries]
+        st = score_tol(lg, ref.logits, sub, beta_gpu, ref.beta, ref.top1)
+        top1, top2 = _np(ob["top1"])[queries], _np(ob["top2"])[queries]
+        for i in range(len(queries)):
+            if toks[i] == ref.tokens[i]:
+                assert abs(float(top1[i]) - ref.top1[i]) <= st[i], (t, i, top1[i], ref.top1[i], st[i])
+                assert abs(float(top2[i]) - ref.top2[i]) <= st[i], (t, i, top2[i], ref.top2[i], st[i])
+                if ref.gaps[i] > 1e-3:
+                    assert win[i] == ref.winners[i], (t, i)
     return exempt
 
 
@@ -127,6 +181,26 @@ def test_config5_sixteen_queries_paged_sampled_queries():
     wl = W.config5()
     assert wl.shuffle_pages
     _check_queries(wl, [0, 9, 15], steps=2)
+
+
+def test_config3_timed_path_three_steps_all_layers_once():
+    # the benchmark's workload: dynamic beta at step 0, frozen and fused into the
+    # LM head's epilogue at steps 1 and 2; all 32 layers compared at step 1
+    wl = W.config3()
+    _check_timed_path(wl, [0], steps=3, all_layers_at=(1,), attn_layers=[0])
+
+
+def test_config5_timed_path_all_queries_three_steps():
+    # 16 queries x 17 sequences (272 rows: the many-row LM head and its fused
+    # epilogue from step 1), scattered pages
+    wl = W.config5()
+    _check_timed_path(wl, list(range(16)), steps=3)
+
+
+def test_config4_timed_path_two_steps():
+    wl = W.config4()
+    wl.steps = 2
+    _check_timed_path(wl, [0], steps=2)
 
 
 def test_config1_steps_cross_page_boundaries():
