@@ -270,6 +270,24 @@ pced_status pced_lmhead(pced_ctx* ctx, const void* x, int32_t n_rows, const void
                         float* logits, hipStream_t stream);
 
 /*
+ * Allocation-free form of pced_lmhead, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc. It needs no context and no workspace: the padded copy of x
+ * that pced_lmhead stages in the context's workspace goes to a library-owned
+ * device array of 4 MiB, one per GPU, held until the process ends. Same
+ * arguments and results as pced_lmhead (cfg gives the shapes, dtype and norm;
+ * lm_head packed by pced_pack_lm_head; x device [n_rows][hidden]; logits device
+ * [n_rows][V] fp32); calls no allocating routine.
+ * Limit: ceil(n_rows / 16) * 16 * hidden * sizeof(storage) <= 4 MiB (512 rows
+ * at hidden 4096 in bf16), else CAPACITY. Every call on a GPU shares that GPU's
+ * array: calls that overlap on one GPU (several streams or threads) race, so
+ * order them, e.g. on one stream. Asynchronous on `stream`.
+ * Errors: INVALID_ARG (invalid cfg, NULL, n_rows < 1), CAPACITY, HIP.
+ */
+pced_status pced_lmhead_noalloc(const pced_config* cfg, const void* x, int32_t n_rows, const void* lm_head,
+                                float* logits, hipStream_t stream);
+
+/*
  * Stage entry: Eq. 2 and Eq. 3 on given logits for the loaded batch.
  *   logits        device [S][V] fp32, rows in load order
  *   refresh_beta  with dynamic beta: nonzero recomputes beta from these logits

@@ -24,7 +24,7 @@ EXPORTED = ("pced_pool_bytes", "pced_lm_head_bytes", "pced_pack_lm_head", "pced_
             "pced_load_caches", "pced_step", "pced_generate", "pced_lmhead", "pced_fuse",
             "pced_get_lengths", "pced_profile_enable", "pced_profile_read", "pced_relevance",
             "pced_model_bytes", "pced_pack_model_layer", "pced_pack_model_globals", "pced_model_prefill",
-            "pced_model_step", "pced_model_generate", "pced_read_cache")
+            "pced_model_step", "pced_model_generate", "pced_read_cache", "pced_lmhead_noalloc")
 
 
 class PcedError(RuntimeError):
@@ -95,6 +95,7 @@ def load_library() -> ctypes.CDLL:
         "pced_model_step": (I, [P, P, P, P, P, ctypes.POINTER(pced_step_out), V]),
         "pced_model_generate": (I, [P, P, P, I, P, P, ctypes.POINTER(pced_step_out), V]),
         "pced_read_cache": (I, [P, I, I, I, I, P, P, V]),
+        "pced_lmhead_noalloc": (I, [ctypes.POINTER(pced_config), P, I, P, P, V]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -137,6 +138,12 @@ def pced_lm_head_bytes(cfg: pced_config) -> int:
 def pced_pack_lm_head(cfg: pced_config, w, w_packed, stream=None):
     """Re-lay row-major [V][hidden] LM-head weights into the packed form the steps read."""
     _check(load_library().pced_pack_lm_head(ctypes.byref(cfg), w.data_ptr(), w_packed.data_ptr(), _stream(stream)))
+
+
+def pced_lmhead_noalloc(cfg: pced_config, x, n_rows, lm_head, logits, stream=None):
+    """Logits of n_rows hidden states with no context and no caller workspace."""
+    _check(load_library().pced_lmhead_noalloc(ctypes.byref(cfg), x.data_ptr(), int(n_rows), lm_head.data_ptr(),
+                                              logits.data_ptr(), _stream(stream)))
 
 
 def pced_model_bytes(cfg: pced_config) -> int:

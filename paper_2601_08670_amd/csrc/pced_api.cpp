@@ -1454,6 +1454,35 @@ pced_status pced_lmhead(pced_ctx* c, const void* x, int32_t n_rows, const void* 
   return run_lmhead(c, xw, n_rows, lm_head, logits, st);
 }
 
+pced_status pced_lmhead_noalloc(const pced_config* cfg, const void* x, int32_t n_rows, const void* lm_head,
+                                float* logits, hipStream_t st) {
+  std::string why;
+  if (!cfg_valid(cfg, &why)) return fail(PCED_ERR_INVALID_ARG, "invalid config: %s", why.c_str());
+  if (!x || !lm_head || !logits) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  if (n_rows < 1) return fail(PCED_ERR_INVALID_ARG, "n_rows %d < 1", n_rows);
+  // the kernels read whole 16-row tiles of x: stage the rows, padded with zero rows
+  const size_t row_bytes = (size_t)cfg->hidden * esize_of(*cfg);
+  const size_t rows = (size_t)ceil_div(n_rows, 16) * 16;
+  if (rows * row_bytes > kNoAllocScratchBytes)
+    return fail(PCED_ERR_CAPACITY, "%d rows of %zu bytes need %zu bytes of scratch > the %zu available", n_rows,
+                row_bytes, rows * row_bytes, kNoAllocScratchBytes);
+  void* scratch = nullptr;
+  HIP_OK(noalloc_scratch(&scratch));
+  char* xs = (char*)scratch;
+  HIP_OK(launch_copy_rows(x, xs, (size_t)n_rows * row_bytes, st));
+  HIP_OK(launch_zero_bytes(xs + (size_t)n_rows * row_bytes, (rows - n_rows) * row_bytes, st));
+  LmArgs a{};
+  a.x = xs;
+  a.w = lm_head;
+  a.logits = logits;
+  a.M = n_rows;
+  a.V = cfg->vocab;
+  a.K = cfg->hidden;
+  a.rms = cfg->norm == PCED_NORM_RMS;
+  HIP_OK(launch_lmhead(a, cfg->dtype == PCED_BF16, st));
+  return PCED_OK;
+}
+
 pced_status pced_fuse(pced_ctx* c, const float* logits, int32_t refresh_beta, int32_t* tokens_out,
                       const pced_step_out* extra, hipStream_t st) {
   pced_status r = check_ctx(c, true);

@@ -280,6 +280,10 @@ hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Ti
 hipError_t launch_prefill_meta(const PrefillMetaArgs& a, hipStream_t st);
 // rho[m] = 1/sqrt(sum_p ss[p][m] * inv_dim + eps) for m < M
 hipError_t launch_read_cache(const ReadCacheArgs& a, hipStream_t st);
+// The allocation-free entry point's scratch: a library-owned device array of
+// kNoAllocScratchBytes per GPU; out = its address on the current device.
+constexpr size_t kNoAllocScratchBytes = (size_t)4 << 20;
+hipError_t noalloc_scratch(void** out);
 hipError_t launch_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps, float* rho,
                       hipStream_t st);
 

@@ -17,6 +17,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "pced_internal.h"
 
 namespace pced {
@@ -2235,6 +2237,38 @@ hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st, const Ti
 
 hipError_t launch_copy_rows(const void* src, void* dst, size_t nbytes, hipStream_t st) {
   return hipMemcpyAsync(dst, src, nbytes, hipMemcpyDeviceToDevice, st);
+}
+
+// ------------------------------------------------- allocation-free scratch
+
+// Device scratch of the allocation-free entry point (pced_lmhead_noalloc): a
+// library-owned array instead of caller workspace, one copy per GPU the library
+// runs on, held until the process ends. In host code its name is only a
+// host-side stand-in: kernels and copies get the device address that
+// hipGetSymbolAddress returns for the current device (kept per device).
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t noalloc_scratch(void** out) {
+  *out = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {  // first use on this device, with the device current
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace pced

@@ -270,3 +270,14 @@ def test_read_cache_validation_before_any_launch():
     assert lib.pced_read_cache(fc.h, 0, 0, 0, 1, 1 << 40, 1 << 41, None) == STATE
     assert lib.pced_read_cache(None, 0, 0, 0, 1, 1 << 40, 1 << 41, None) == INVALID
     fc.close()
+
+
+def test_lmhead_noalloc_validation_before_any_launch():
+    lib = _lib.load_library()
+    c = cfg(n_q_heads=32, n_kv_heads=8, head_dim=128)            # hidden 4096, bf16: 8 KiB per row
+    assert lib.pced_lmhead_noalloc(None, 1, 1, 1, 1, None) == INVALID
+    assert lib.pced_lmhead_noalloc(ctypes.byref(cfg(n_kv_heads=3)), 1, 1, 1, 1, None) == INVALID
+    assert lib.pced_lmhead_noalloc(ctypes.byref(c), None, 1, 1, 1, None) == INVALID
+    assert lib.pced_lmhead_noalloc(ctypes.byref(c), 1, 0, 1, 1, None) == INVALID
+    assert lib.pced_lmhead_noalloc(ctypes.byref(c), 1, 513, 1, 1, None) == CAPACITY
+    assert b"scratch" in lib.pced_last_error()
