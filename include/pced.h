@@ -429,7 +429,8 @@ enum {
                             merges the previous layer's split partials) */
   PCED_PROF_LMHEAD = 2,  /* LM head                                */
   PCED_PROF_BETA = 3,    /* dynamic beta (first step only)         */
-  PCED_PROF_FUSE = 4,    /* Eq. 2 + Eq. 3                          */
+  PCED_PROF_FUSE = 4,    /* Eq. 2 + Eq. 3 over materialised logits:
+                            the slice pass (k_fuse)               */
   PCED_PROF_SYNTH = 5,   /* pced_generate's input synthesis        */
   PCED_PROF_COMBINE = 6, /* merge of split attention partials as a launch
                             of its own (bf16 pced_step: last layer only) */
@@ -438,10 +439,10 @@ enum {
   PCED_PROF_OPROJ = 9,   /* decoder stack: O projection + residual  */
   PCED_PROF_GATEUP = 10, /* decoder stack: norm + gate/up + SwiGLU  */
   PCED_PROF_DOWN = 11,   /* decoder stack: down projection + residual */
-  PCED_PROF_FUSE_MERGE = 12, /* per-query merge of the slice candidates left
-                                by the LM head's fused Eq. 2 epilogue (steps
-                                after the first); PCED_PROF_FUSE is Eq. 2 + 3
-                                over materialised logits                    */
+  PCED_PROF_FUSE_MERGE = 12, /* per-query merge of the slice candidates
+                                (k_fuse_final): after the LM head's fused
+                                Eq. 2 epilogue (steps after the first) or
+                                after the slice pass of PCED_PROF_FUSE     */
   PCED_PROF_NCLASS = 13
 };
 typedef struct pced_profile {

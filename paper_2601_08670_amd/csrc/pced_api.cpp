@@ -83,7 +83,7 @@ struct Layout {
       total;
   int pf_rows;          // rows of one prefill chunk (sequences x suffix tokens)
   size_t pf_proj_cols;  // slices x columns per row of the prefill projection partials
-  int rows_pad, nblk_fuse, nchunk, max_work;
+  int rows_pad, nblk_fuse, nblk_agg, nchunk, max_work;
   size_t part_slots;
   size_t part_cols;  // slices x columns one row of the projection partial buffer holds
 };
@@ -93,7 +93,8 @@ Layout make_layout(const pced_config& c) {
   const size_t S = c.max_seqs, B = c.max_queries, es = esize_of(c);
   const int G = c.n_q_heads / c.n_kv_heads;
   L.rows_pad = ceil_div(c.max_seqs, kLmRowsPad) * kLmRowsPad;
-  L.nblk_fuse = ceil_div(c.vocab, kFuseBlock);
+  L.nblk_fuse = ceil_div(c.vocab, 512);  // at most: the stand-alone fuse's slices are 512 or 1024 tokens
+  L.nblk_agg = ceil_div(c.vocab, kFuseBlock);
   L.nchunk = ceil_div(c.vocab, kBetaChunk);
   // every attention chunk holds at least one page: chunks <= pages in use (a
   // prefill chunk's rows count their shared pages once per row)
@@ -406,6 +407,11 @@ FuseArgs fuse_args(pced_ctx* c, const float* logits, int32_t* tokens_out, int to
   f.top2 = extra ? extra->top2 : nullptr;
   f.V = c->cfg.vocab;
   f.nblk = nblk;
+  f.max_n = c->n_experts.empty() ? 0 : *std::max_element(c->n_experts.begin(), c->n_experts.end());
+  for (int b = 0; b <= std::min(c->B, kFuseInlineQueries); ++b) {
+    f.inl_seq0[b] = c->seq_off[b];
+    f.inl_exp0[b] = c->exp_off[b];
+  }
   f.tok_stride = tok_stride;
   return f;
 }
@@ -438,7 +444,9 @@ pced_status run_fuse(pced_ctx* c, const float* logits, bool refresh_beta, int32_
     if (cfg.beta_scalar) HIP_OK(launch_beta_mean(b, c->B, st));
     c->beta_frozen = true;
   }
-  FuseArgs f = fuse_args(c, logits, tokens_out, tok_stride, extra, c->lay.nblk_fuse);
+  FuseArgs f = fuse_args(c, logits, tokens_out, tok_stride, extra,
+                         cfg.aggregation != PCED_AGG_MAX ? c->lay.nblk_agg
+                                                         : ceil_div(cfg.vocab, fuse_slice(cfg.vocab, c->B, c->num_cus)));
   if (cfg.aggregation != PCED_AGG_MAX) {
     AggArgs g{};
     g.logits = logits;
@@ -453,7 +461,7 @@ pced_status run_fuse(pced_ctx* c, const float* logits, bool refresh_beta, int32_
     g.part = f.part;
     g.V = cfg.vocab;
     g.nchunk = c->lay.nchunk;
-    g.nblk = c->lay.nblk_fuse;
+    g.nblk = c->lay.nblk_agg;
     g.product = cfg.aggregation == PCED_AGG_POE;
     {
       ProfScope ps(c, PCED_PROF_FUSE, 2.0 * (c->NE + c->S) * cfg.vocab * 4, 0);
@@ -467,7 +475,8 @@ pced_status run_fuse(pced_ctx* c, const float* logits, bool refresh_beta, int32_
   }
   {
     ProfScope ps(c, PCED_PROF_FUSE, (double)c->S * cfg.vocab * 4, 0);
-    HIP_OK(launch_fuse(f, c->B, st, ps.timing()));
+    ProfScope pm(c, PCED_PROF_FUSE_MERGE, (double)c->B * f.nblk * 5 * 4, 0);
+    HIP_OK(launch_fuse(f, c->B, st, ps.timing(), pm.timing()));
   }
   return copy_beta_used(c, extra, st);
 }

@@ -9,7 +9,8 @@ namespace pced {
 
 constexpr int kPage = 16;          // tokens per KV page (= MFMA M/K tile edge)
 constexpr int kMaxGroup = 16;      // q-heads per kv-head (MFMA N edge)
-constexpr int kFuseBlock = 256;    // vocab entries per fuse work-group
+constexpr int kFuseBlock = 256;    // threads of the fuse work-groups
+constexpr int kFuseInlineQueries = 32;  // queries whose row offsets the fuse gets in its kernel arguments
 constexpr int kBetaChunk = 4096;   // vocab entries per beta work-group
 constexpr int kLmRowsPad = 48;     // hidden-state rows are padded to a multiple of this
 constexpr int kLmRowsMTW = 9;      // many-row LM head: row tiles per wave (up to 32 * 9 = 288 rows at once)
@@ -133,6 +134,9 @@ struct FuseArgs {
   float* top1;              // optional [B]
   float* top2;              // optional [B]
   int V, nblk, tok_stride;
+  int max_n;                // most experts of any query (load batch of the stand-alone fuse)
+  int32_t inl_seq0[kFuseInlineQueries + 1];  // query_seq0 / query_exp0 of the first queries
+  int32_t inl_exp0[kFuseInlineQueries + 1];
 };
 
 // MoE / PoE aggregation (the alternatives to Eq. 3's max): per-expert
@@ -261,7 +265,11 @@ hipError_t launch_attn_combine(const AttnArgs& a, int head_dim, int max_splits, 
 hipError_t launch_pack_lm_head(const void* w, void* wp, int V, int K, bool bf16, hipStream_t st);
 hipError_t launch_lmhead(const LmArgs& a, bool bf16, hipStream_t st, const Timing* tm = nullptr);
 hipError_t launch_beta(const BetaArgs& a, int n_seqs, int n_exp, hipStream_t st, const Timing* tm = nullptr);
-hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st, const Timing* tm = nullptr);
+// k_fuse (timed by tm) then the per-query merge k_fuse_final (timed by tm_merge)
+hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st, const Timing* tm = nullptr,
+                       const Timing* tm_merge = nullptr);
+// vocabulary tokens per work-group of the stand-alone fuse (1024, or 512 for few queries)
+int fuse_slice(int V, int n_queries, int num_cus);
 hipError_t launch_beta_mean(const BetaArgs& a, int n_queries, hipStream_t st);
 hipError_t launch_agg(const AggArgs& a, int n_exp, int n_queries, hipStream_t st, const Timing* tm = nullptr);
 // the final per-query merge alone (after an LM head with the fused epilogue)

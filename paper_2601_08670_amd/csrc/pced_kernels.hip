@@ -1339,49 +1339,146 @@ __global__ __launch_bounds__(256) void k_lmhead_f32(LmArgs a) {
 
 // ---------------------------------------------------------- Eq. 2 and Eq. 3
 
-// One block per (query, 256-token vocab slice). Per token v:
+// Eq. 2 and the best two tokens of one SW-token vocabulary slice per block
+// (SW = 1024, or 512 when 1024-token slices would leave compute units idle).
+// Per token v:
 //   s_hat_k(v) = ((1 + beta_k) s_k(v) - beta_k s_0(v)) + gamma ln r_k     (Eq. 2)
 // evaluated in float32 in exactly that order without fused multiply-adds,
-// S(v) = max over experts 1..N (lowest k on ties), then the block's best and
-// second-best tokens, merged per query by k_fuse_final.
-__global__ __launch_bounds__(kFuseBlock) void k_fuse(FuseArgs a) {
+// S(v) = max over experts 1..N (lowest k on ties). A block of 4 waves owns
+// SW consecutive tokens; wave w takes the experts of its quarter of 1..N and
+// reads their rows in 4 SW-byte runs: lane l holds tokens 4l + 256i .. +3 (i < SW/256),
+// one 16-byte load each (VEC: rows 16-byte aligned, V % 4 == 0; otherwise
+// 4-byte loads), so every wave load is a contiguous 1 KiB of a row and a batch
+// of NB rows keeps 4 NB loads in flight before any arithmetic (rows past the
+// quarter re-read its last row and are masked by selects). The waves' per-token
+// maxima meet in LDS and are combined in wave order (ties keep the lower k),
+// then each wave takes 256 of the tokens, the lanes' candidates are merged by
+// shuffles and the waves' by LDS; the slice's best two tokens go to
+// part[b][slice] for k_fuse_final. (A single launch, the last block merging the
+// slices behind an agent-scope release/acquire counter, measured 2x slower at
+// one query and 7x at sixteen: the release writes back the L2 of every wave's
+// compute unit.)
+template <bool VEC>
+__device__ __forceinline__ float4 load_tok4(const float* row, int v0, int V) {
+  if constexpr (VEC) {
+    return *(const float4*)(row + min(v0, V - 4));
+  } else {
+    return make_float4(row[min(v0, V - 1)], row[min(v0 + 1, V - 1)], row[min(v0 + 2, V - 1)],
+                       row[min(v0 + 3, V - 1)]);
+  }
+}
+
+__device__ __forceinline__ void fuse_write_outputs(const FuseArgs& a, int b, const Top2& r) {
+  a.tokens_out[(size_t)b * a.tok_stride] = r.i1;
+  a.prev_tok[b] = r.i1;
+  if (a.winner) a.winner[b] = r.k1;
+  if (a.top1) a.top1[b] = r.v1;
+  if (a.top2) a.top2[b] = r.v2;
+}
+
+__device__ __forceinline__ Top2 wave_top2(Top2 c) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) c = merge(c, shfl_top2(c, o));
+  return c;
+}
+
+template <bool VEC, int NB, int SW>
+__global__ __launch_bounds__(256) void k_fuse(FuseArgs a) {
 #pragma clang fp contract(off)
-  const int b = blockIdx.y;
-  const int s0 = a.query_seq0[b];
-  const int N = a.query_seq0[b + 1] - s0 - 1;
-  const int e0 = a.query_exp0[b];
-  const int v = blockIdx.x * kFuseBlock + threadIdx.x;
-  Top2 c{kNegInf, 0x7FFFFFFF, 0, kNegInf, 0x7FFFFFFF};
-  if (v < a.V) {
-    const float* colp = a.logits + v;
-    const float sa = colp[(size_t)s0 * a.V];
-    float best = kNegInf;
-    int bk = 0;
-    // experts in batches of 32 independent loads (one memory round trip for up
-    // to 32 documents), so their latencies overlap
-    for (int kb = 1; kb <= N; kb += 32) {
-      float x[32];
+  constexpr int RI = SW / 256;  // 16-byte loads per lane and row
+  __shared__ float sbest[4][SW];
+  __shared__ int sk[4][SW];
+  __shared__ Top2 swave[4];
+  const int b = blockIdx.y, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // the first queries' row offsets travel in the kernel arguments (no dependent load)
+  const bool inl = b < kFuseInlineQueries;
+  const int s0 = inl ? a.inl_seq0[b] : a.query_seq0[b];
+  const int N = (inl ? a.inl_seq0[b + 1] : a.query_seq0[b + 1]) - s0 - 1;
+  const int e0 = inl ? a.inl_exp0[b] : a.query_exp0[b];
+  const int per = (N + 3) / 4;                       // experts per wave
+  const int k_lo = 1 + wave * per, k_hi = min(N, k_lo + per - 1);
+  const int vb = blockIdx.x * SW;
+  const float* L0 = a.logits + (size_t)s0 * a.V;
+  float sa[4 * RI], best[4 * RI];
+  int bk[4 * RI];
 #pragma unroll
-      for (int j = 0; j < 32; ++j) x[j] = (kb + j <= N) ? colp[(size_t)(s0 + kb + j) * a.V] : 0.f;
+  for (int i = 0; i < RI; ++i) {
+    const float4 t = load_tok4<VEC>(L0, vb + 256 * i + 4 * lane, a.V);
+    sa[4 * i] = t.x; sa[4 * i + 1] = t.y; sa[4 * i + 2] = t.z; sa[4 * i + 3] = t.w;
+  }
 #pragma unroll
-      for (int j = 0; j < 32; ++j) {
-        const int k = kb + j;
-        if (k > N) continue;
-        const float beta = a.beta[e0 + k - 1];
-        const float coef = 1.0f + beta;
-        const float t1 = coef * x[j];
-        const float t2 = beta * sa;
-        const float val = (t1 - t2) + a.prior[e0 + k - 1];
-        if (val > best) { best = val; bk = k; }
+  for (int u = 0; u < 4 * RI; ++u) { best[u] = kNegInf; bk[u] = 0; }
+  for (int kb = k_lo; kb <= k_hi; kb += NB) {
+    float4 x[NB][RI];
+    float cb[NB], cp[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const float* row = L0 + (size_t)min(kb + j, k_hi) * a.V;
+#pragma unroll
+      for (int i = 0; i < RI; ++i) x[j][i] = load_tok4<VEC>(row, vb + 256 * i + 4 * lane, a.V);
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int e = e0 + min(kb + j, k_hi) - 1;
+      cb[j] = a.beta[e];
+      cp[j] = a.prior[e];
+    }
+    __builtin_amdgcn_sched_barrier(0);  // all of the batch's loads go out before the arithmetic
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int k = kb + j;
+      const bool ok = k <= k_hi;
+      const float beta = cb[j], pr = cp[j];
+      const float coef = 1.0f + beta;
+#pragma unroll
+      for (int i = 0; i < RI; ++i) {
+        const float xs[4] = {x[j][i].x, x[j][i].y, x[j][i].z, x[j][i].w};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int u = 4 * i + c;
+          const float t1 = coef * xs[c];
+          const float t2 = beta * sa[u];
+          const float val = (t1 - t2) + pr;
+          const bool up = ok && val > best[u];
+          best[u] = up ? val : best[u];
+          bk[u] = up ? k : bk[u];
+        }
       }
     }
-    c.v1 = best; c.i1 = v; c.k1 = bk;
   }
-  c = block_top2<kFuseBlock / 64>(c);
+  // per-token maxima of the four expert ranges, combined in wave order
+#pragma unroll
+  for (int i = 0; i < RI; ++i)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      sbest[wave][256 * i + 4 * lane + c] = best[4 * i + c];
+      sk[wave][256 * i + 4 * lane + c] = bk[4 * i + c];
+    }
+  __syncthreads();
+  Top2 cand{kNegInf, 0x7FFFFFFF, 0, kNegInf, 0x7FFFFFFF};
+#pragma unroll
+  for (int c = 0; c < SW / 256; ++c) {  // wave w finishes tokens w SW/4 .. (w + 1) SW/4 - 1
+    const int t = SW / 4 * wave + (SW / 256) * lane + c;
+    float v = sbest[0][t];
+    int k = sk[0][t];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      const float vw = sbest[w][t];
+      if (vw > v) { v = vw; k = sk[w][t]; }
+    }
+    if (vb + t < a.V) cand = merge(cand, Top2{v, vb + t, k, kNegInf, 0x7FFFFFFF});
+  }
+  cand = wave_top2(cand);
+  if (lane == 0) swave[wave] = cand;
+  __syncthreads();
   if (threadIdx.x == 0) {
+    Top2 r = swave[0];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) r = merge(r, swave[w]);
     float* p = a.part + ((size_t)b * a.nblk + blockIdx.x) * 5;
-    p[0] = c.v1; p[1] = __int_as_float(c.i1); p[2] = __int_as_float(c.k1);
-    p[3] = c.v2; p[4] = __int_as_float(c.i2);
+    p[0] = r.v1; p[1] = __int_as_float(r.i1); p[2] = __int_as_float(r.k1);
+    p[3] = r.v2; p[4] = __int_as_float(r.i2);
   }
 }
 
@@ -1396,13 +1493,7 @@ __global__ __launch_bounds__(kFuseBlock) void k_fuse_final(FuseArgs a) {
     r = merge(r, x);
   }
   r = block_top2<kFuseBlock / 64>(r);
-  if (threadIdx.x == 0) {
-    a.tokens_out[(size_t)b * a.tok_stride] = r.i1;
-    a.prev_tok[b] = r.i1;
-    if (a.winner) a.winner[b] = r.k1;
-    if (a.top1) a.top1[b] = r.v1;
-    if (a.top2) a.top2[b] = r.v2;
-  }
+  if (threadIdx.x == 0) fuse_write_outputs(a, b, r);
 }
 
 // ---------------------------------------------------------------- dynamic beta
@@ -2207,10 +2298,29 @@ hipError_t launch_beta(const BetaArgs& a, int n_seqs, int n_exp, hipStream_t st,
   return go(k_beta_final, dim3((n_exp + 255) / 256), dim3(256), 0, st, nullptr, t1(tm), a, n_exp);
 }
 
-hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st, const Timing* tm) {
-  hipError_t e = go(k_fuse, dim3(a.nblk, n_queries), dim3(kFuseBlock), 0, st, t0(tm), nullptr, a);
+int fuse_slice(int V, int n_queries, int num_cus) {
+  // 1024-token slices unless that leaves fewer work-groups than compute units
+  return (long)((V + 1023) / 1024) * n_queries >= num_cus ? 1024 : 512;
+}
+
+template <int SW>
+hipError_t launch_fuse_sw(const FuseArgs& a, dim3 g, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+  const bool vec = a.V % 4 == 0 && a.V >= 4;
+  // rows per load batch: a wave's quarter of the experts in one batch up to 16 or 32 experts
+  if ((a.max_n + 3) / 4 <= 4)
+    return vec ? go(k_fuse<true, 4, SW>, g, dim3(256), 0, st, e0, e1, a)
+               : go(k_fuse<false, 4, SW>, g, dim3(256), 0, st, e0, e1, a);
+  return vec ? go(k_fuse<true, 8, SW>, g, dim3(256), 0, st, e0, e1, a)
+             : go(k_fuse<false, 8, SW>, g, dim3(256), 0, st, e0, e1, a);
+}
+
+hipError_t launch_fuse(const FuseArgs& a, int n_queries, hipStream_t st, const Timing* tm, const Timing* tm_merge) {
+  // a.nblk: slices of fuse_slice() tokens
+  const int sw = (a.V + a.nblk - 1) / a.nblk > 512 ? 1024 : 512;
+  const dim3 g(a.nblk, n_queries);
+  hipError_t e = sw == 1024 ? launch_fuse_sw<1024>(a, g, st, t0(tm), t1(tm)) : launch_fuse_sw<512>(a, g, st, t0(tm), t1(tm));
   if (e != hipSuccess) return e;
-  return go(k_fuse_final, dim3(n_queries), dim3(kFuseBlock), 0, st, nullptr, t1(tm), a);
+  return go(k_fuse_final, dim3(n_queries), dim3(kFuseBlock), 0, st, t0(tm_merge), t1(tm_merge), a);
 }
 
 hipError_t launch_beta_mean(const BetaArgs& a, int n_queries, hipStream_t st) {
