@@ -78,7 +78,7 @@ struct Layout {
   size_t len0, page_table, seq_query, query_seq0, query_exp0, exp_seq, exp_query, prior, logw, beta_fixed,
       load_items, src_k, src_v, meta_end;
   size_t chunk_info, seg, nparts, work_pages, prev_tok, beta, part_acc, part_ml, x, logits,
-      fuse_part, lse_part, jsd_part, agg_lse, syn_q, syn_k, syn_v, dec_h, dec_a, dec_act, dec_ss, dec_rho, dec_part,
+      rho, x_packed, fuse_part, lse_part, jsd_part, agg_lse, syn_q, syn_k, syn_v, dec_h, dec_a, dec_act, dec_ss, dec_rho, dec_part,
       pf_len0, pf_pt, pf_tok, pf_nparts, pf_h, pf_a, pf_act, pf_ss, pf_q, pf_x, pf_part_acc, pf_part_ml, pf_proj,
       total;
   int pf_rows;          // rows of one prefill chunk (sequences x suffix tokens)
@@ -133,6 +133,10 @@ Layout make_layout(const pced_config& c) {
   L.part_ml = take(2 * L.part_slots * G * 2 * 4);
   L.x = take((size_t)L.rows_pad * c.hidden * es);
   L.logits = take(S * c.vocab * 4);
+  L.rho = take((size_t)L.rows_pad * 4);
+  // the many-row LM head's operand-ordered copy of x (bf16, more than 48 rows)
+  const bool wide = c.dtype == PCED_BF16 && c.max_seqs > kLmRowsPad;
+  L.x_packed = take(wide ? (size_t)kLmWideMaxRows * c.hidden * 2 : 0);
   // per-slice candidates: k_fuse uses 256-column slices, the fused LM-head epilogue 128-column ones
   L.fuse_part = take(B * (size_t)ceil_div(c.vocab, 128) * 5 * 4);
   L.lse_part = take(S * L.nchunk * 2 * 4);
@@ -507,6 +511,8 @@ pced_status run_lmhead(pced_ctx* c, const void* x, int M, const void* w, float* 
   a.K = cfg.hidden;
   a.rms = cfg.norm == PCED_NORM_RMS;
   a.rho_in = rho_in;
+  a.rho_buf = c->at<float>(c->lay.rho);
+  a.x_packed = cfg.max_seqs > kLmRowsPad && c->bf16 ? c->at<void>(c->lay.x_packed) : nullptr;
   if (fuse_nblk > 0) {
     a.query_seq0 = c->at<int32_t>(c->lay.query_seq0);
     a.query_exp0 = c->at<int32_t>(c->lay.query_exp0);
@@ -1469,25 +1475,40 @@ pced_status pced_lmhead_noalloc(const pced_config* cfg, const void* x, int32_t n
   if (!cfg_valid(cfg, &why)) return fail(PCED_ERR_INVALID_ARG, "invalid config: %s", why.c_str());
   if (!x || !lm_head || !logits) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
   if (n_rows < 1) return fail(PCED_ERR_INVALID_ARG, "n_rows %d < 1", n_rows);
-  // the kernels read whole 16-row tiles of x: stage the rows, padded with zero rows
   const size_t row_bytes = (size_t)cfg->hidden * esize_of(*cfg);
-  const size_t rows = (size_t)ceil_div(n_rows, 16) * 16;
-  if (rows * row_bytes > kNoAllocScratchBytes)
-    return fail(PCED_ERR_CAPACITY, "%d rows of %zu bytes need %zu bytes of scratch > the %zu available", n_rows,
-                row_bytes, rows * row_bytes, kNoAllocScratchBytes);
-  void* scratch = nullptr;
-  HIP_OK(noalloc_scratch(&scratch));
-  char* xs = (char*)scratch;
-  HIP_OK(launch_copy_rows(x, xs, (size_t)n_rows * row_bytes, st));
-  HIP_OK(launch_zero_bytes(xs + (size_t)n_rows * row_bytes, (rows - n_rows) * row_bytes, st));
+  const int wide = cfg->dtype == PCED_BF16 ? lmhead_wide_tiles(n_rows, cfg->vocab, cfg->hidden) : 0;
   LmArgs a{};
-  a.x = xs;
   a.w = lm_head;
   a.logits = logits;
   a.M = n_rows;
   a.V = cfg->vocab;
   a.K = cfg->hidden;
   a.rms = cfg->norm == PCED_NORM_RMS;
+  if (wide) {
+    // the many-row kernel reads only rows < n_rows of x (through its packed
+    // copy, which holds the padding): scratch = packed x, then the row scales
+    const size_t packed = (size_t)wide * 32 * row_bytes;
+    if (packed + (size_t)n_rows * 4 > kNoAllocScratchBytes)
+      return fail(PCED_ERR_CAPACITY, "%d rows need %zu bytes of scratch > the %zu available", n_rows,
+                  packed + (size_t)n_rows * 4, kNoAllocScratchBytes);
+    void* scratch = nullptr;
+    HIP_OK(noalloc_scratch(&scratch));
+    a.x = x;
+    a.x_packed = scratch;
+    a.rho_buf = (float*)((char*)scratch + packed);
+  } else {
+    // the other kernels read whole 16-row tiles of x: stage the rows, padded with zero rows
+    const size_t rows = (size_t)ceil_div(n_rows, 16) * 16;
+    if (rows * row_bytes > kNoAllocScratchBytes)
+      return fail(PCED_ERR_CAPACITY, "%d rows of %zu bytes need %zu bytes of scratch > the %zu available", n_rows,
+                  row_bytes, rows * row_bytes, kNoAllocScratchBytes);
+    void* scratch = nullptr;
+    HIP_OK(noalloc_scratch(&scratch));
+    char* xs = (char*)scratch;
+    HIP_OK(launch_copy_rows(x, xs, (size_t)n_rows * row_bytes, st));
+    HIP_OK(launch_zero_bytes(xs + (size_t)n_rows * row_bytes, (rows - n_rows) * row_bytes, st));
+    a.x = xs;
+  }
   HIP_OK(launch_lmhead(a, cfg->dtype == PCED_BF16, st));
   return PCED_OK;
 }

@@ -117,6 +117,9 @@ struct LmArgs {
   float* fuse_part;
   int n_queries, fuse_nblk;
   const float* rho_in;      // optional [M] row scales used instead of rms (bf16 kernels)
+  float* rho_buf;           // optional [M] scratch: the many-row kernel computes the row scales there first
+  void* x_packed;           // optional scratch of ceil(M/16)*16*K bf16 (rounded up to the kernel's tile
+                            // count): the many-row kernel's operand-ordered copy of x
   size_t w_vb, w_ks;        // packed W: 16-byte units from one vocab block / 64-wide k step to the next
                             // (set by launch_lmhead from kLmKMajor)
 };
@@ -276,6 +279,10 @@ hipError_t launch_agg(const AggArgs& a, int n_exp, int n_queries, hipStream_t st
 hipError_t launch_fuse_final(const FuseArgs& a, int n_queries, hipStream_t st, const Timing* tm = nullptr);
 // vocabulary slices (blocks) of the fused LM-head epilogue for M rows, or 0 if M rows cannot be fused
 int lmhead_fused_nblk(int M, int V);
+// 32-row tiles of the many-row LM head for M rows of a bf16 LM head (its packed
+// x then holds that many tiles, zero past M), or 0 if another kernel runs
+int lmhead_wide_tiles(int M, int V, int K);
+constexpr int kLmWideMaxRows = 288;  // rows of the largest many-row tile count
 hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st, const Timing* tm = nullptr);
 hipError_t launch_copy_rows(const void* src, void* dst, size_t nbytes, hipStream_t st);
 // pack a [rows][K] bf16 matrix into 16-row tiles, tile i going to slot i * stride + offset

@@ -18,6 +18,7 @@
 #include <stdint.h>
 
 #include <mutex>
+#include <type_traits>
 
 #include "pced_internal.h"
 
@@ -1320,6 +1321,252 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
   }
 }
 
+// s_waitcnt that waits for the vector-memory counter only (vmcnt <= N); the
+// expcnt / lgkmcnt fields are left at their "no wait" maxima.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt has 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+
+// The many-row LM head's B operands, laid out in advance: x [M][K] bf16
+// (row-major) into xp [K/64][MTP][2][64] 16-byte units, unit (ks, t, h, lane)
+// holding x[16t + lane%16][64ks + 16(lane/16) + 8h .. +7], so that each
+// (64-wide k step, 16-row tile, half) operand is one contiguous 1 KiB; rows
+// M .. 16 MTP - 1 are zero. Also rho[m] = 1/sqrt(mean(x[m]^2) + 1e-5) (or 1
+// without RMS) from the same reads. One wave per row, 16-byte loads.
+__global__ __launch_bounds__(256) void k_pack_x(const uint16_t* __restrict__ x, int M, int K, int MTP, int rms,
+                                                uint4* __restrict__ xp, float* __restrict__ rho) {
+  const int m = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (m >= 16 * MTP) return;
+  const int t = m >> 4, col = m & 15;
+  float ss = 0.f;
+  for (int k = 8 * lane; k < K; k += 512) {
+    const uint4 v = m < M ? *(const uint4*)(x + (size_t)m * K + k) : make_uint4(0u, 0u, 0u, 0u);
+    ss += sumsq8(as_bf16x8(v));
+    const int ks = k >> 6, kk = k & 63, quad = kk >> 4, h = (kk >> 3) & 1;
+    xp[(((size_t)ks * MTP + t) * 2 + h) * 64 + col + 16 * quad] = v;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
+  if (lane == 0 && m < M) rho[m] = rms ? 1.0f / sqrtf(ss / (float)K + 1e-5f) : 1.0f;
+}
+
+// LM head for 49..288 rows with W read once: logits[m][v] = rho_m sum_k x[m][k] W[v][k]
+// (x packed by k_pack_x, rho precomputed) on the matrix cores,
+// C^T[16 vocab x 16 rows] += W[16 x 32] X^T[32 x 16] (v_mfma_f32_16x16x32_bf16).
+// A block of 8 waves (two per SIMD) owns 256 vocabulary rows: wave w serves
+// vocab group w / 2 (64 rows, four 16-row tiles) for row half w % 2 (MTH
+// 16-row tiles), so each B operand read from LDS feeds four products (acc:
+// 4 x MTH x 4 registers). The hidden dimension is walked in 32-wide half steps;
+// per half step h every wave
+//   1. (even h) loads its share of x for the next 64-wide step (the packed x
+//      holds each (k step, row tile, half) B operand as one contiguous 1 KiB;
+//      the block's 2 MTP operands are shared by the 8 waves) into registers,
+//      then its four W operands of half step h + 2 into a 3-slot register ring;
+//   2. runs the MTH x 4 products of half step h, each tile's B operand read
+//      from LDS stage (h / 2) % 2 two tiles ahead of its products;
+//   3. (odd h) waits for its x only (vector loads retire in order and x was
+//      issued before the W still in flight), writes it to the other LDS stage
+//      and meets the other waves at a barrier.
+// Scheduling barriers pin this order (left alone, the compiler sinks the W
+// loads next to their use). The two waves of a vocab group load the same W
+// bytes with plain loads: the second is a cache hit. FUSED: Eq. 2 and the
+// slice argmax in the epilogue, in two halves of 128 columns through the
+// (then free) LDS buffers.
+template <int N>
+__device__ __forceinline__ void wait_lgkmcnt() {
+  static_assert(N >= 0 && N < 16, "lgkmcnt has 4 bits");
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (N << 8));
+}
+
+template <int MTH, bool FUSED>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_lmhead_wide_bf16(LmArgs a) {
+  constexpr int MTP = 2 * MTH;           // 16-row tiles of the packed x
+  constexpr int XB = (2 * MTP + 7) / 8;  // x operand loads per wave and step
+  // two x stages (the ring) and two more arrays: room for the fused epilogue's tile
+  __shared__ __align__(16) uint4 xs0[2 * MTP][64];
+  __shared__ __align__(16) uint4 xs1[2 * MTP][64];
+  __shared__ __align__(16) uint4 xs2[2 * MTP][64];
+  __shared__ __align__(16) uint4 xs3[2 * MTP][64];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 1, rh = wave & 1;  // vocab group (64 rows) and row half of this wave
+  const int col = lane & 15, quad = lane >> 4;
+  const int K = a.K, KS = K / 64, H = 2 * KS;
+  const int nvb = (a.V + 15) / 16;
+  const int vb0 = blockIdx.x * 16 + 4 * grp;  // this wave's first 16-row vocab block (of 4)
+  // Buffer loads: a uniform descriptor per operand, one 32-bit vector offset per
+  // lane and the step's advance in a scalar offset (few registers per load).
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc((void*)a.w, 0, 0x7FFFFFFF, 0x00020000);
+  uint32_t w_t[4];
+#pragma unroll
+  for (int vt = 0; vt < 4; ++vt) w_t[vt] = (uint32_t)min(vb0 + vt, nvb - 1) * (uint32_t)a.w_vb * 16u;
+  const uint32_t w_ks = (uint32_t)a.w_ks * 16u;
+  const uint32_t lane16 = 16u * lane;
+  const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, 0x7FFFFFFF, 0x00020000);
+  const uint32_t x_ks = (uint32_t)MTP * 2048u;  // bytes of one k step of the packed x
+  uint32_t xoff[XB];
+  int xblk[XB];
+#pragma unroll
+  for (int i = 0; i < XB; ++i) {
+    int j = wave + 8 * i;
+    if (j >= 2 * MTP) j -= 2 * MTP;
+    xblk[i] = j;
+    xoff[i] = (uint32_t)j * 1024u + lane16;
+  }
+  u32x4 xr[XB];
+  auto load_x = [&](int ks) __attribute__((always_inline)) {
+    ks = min(ks, KS - 1);
+#pragma unroll
+    for (int i = 0; i < XB; ++i) xr[i] = __builtin_amdgcn_raw_buffer_load_b128(xrs, xoff[i], (uint32_t)ks * x_ks, 0);
+  };
+  auto store_x = [&](auto stage_c) __attribute__((always_inline)) {
+    uint4(*dst)[64] = decltype(stage_c)::value == 0 ? xs0 : xs1;
+#pragma unroll
+    for (int i = 0; i < XB; ++i) dst[xblk[i]][lane] = __builtin_bit_cast(uint4, xr[i]);
+  };
+  // W in half steps (32 of the hidden dimension): 4 vocab tiles each, a 3-slot
+  // ring loaded two half steps ahead. The two waves of a vocab group load the
+  // same bytes; plain loads, so that the second is a cache hit.
+  u32x4 wr[3][4];
+  auto load_w = [&](auto slot_c, int h) __attribute__((always_inline)) {
+    constexpr int SL = decltype(slot_c)::value;
+    h = min(h, H - 1);  // past the end: the last half step again (cache hits)
+    const uint32_t so = (uint32_t)(h >> 1) * w_ks + (uint32_t)(h & 1) * 1024u;
+#pragma unroll
+    for (int vt = 0; vt < 4; ++vt)
+      wr[SL][vt] = __builtin_amdgcn_raw_buffer_load_b128(wrs, lane16, so + w_t[vt], 0);
+  };
+  f32x4 acc[4][MTH];
+#pragma unroll
+  for (int t = 0; t < MTH; ++t)
+#pragma unroll
+    for (int vt = 0; vt < 4; ++vt) acc[vt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // half step h: W slot h % 3, LDS stage (h / 2) % 2, half h % 2 of the step's 64
+  auto half = [&](auto slot_c, auto stage_c, auto hf_c, int h) __attribute__((always_inline)) {
+    constexpr int SL = decltype(slot_c)::value, ST = decltype(stage_c)::value, HF = decltype(hf_c)::value;
+    if constexpr (HF == 0) load_x((h >> 1) + 1);
+    load_w(std::integral_constant<int, (SL + 2) % 3>{}, h + 2);
+    __builtin_amdgcn_sched_barrier(0);  // this step's loads are issued before its products
+    uint4(*src)[64] = ST == 0 ? xs0 : xs1;
+    const int r0 = 2 * rh * MTH + HF;  // B operand of tile t: src[r0 + 2 t]
+    bf16x8 b[3];
+    b[0] = as_bf16x8(src[r0][lane]);
+    if constexpr (MTH > 1) b[1] = as_bf16x8(src[r0 + 2][lane]);
+#pragma unroll
+    for (int t = 0; t < MTH; ++t) {
+      if (t + 2 < MTH) b[(t + 2) % 3] = as_bf16x8(src[r0 + 2 * (t + 2)][lane]);  // two tiles ahead
+#pragma unroll
+      for (int vt = 0; vt < 4; ++vt)
+        acc[vt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wr[SL][vt]), b[t % 3],
+                                                              acc[vt][t], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (HF == 1) {
+      wait_vmcnt<8>();  // this wave's x of the next step (the W of the next two half steps may stay in flight)
+      store_x(std::integral_constant<int, 1 - ST>{});
+      wait_lgkmcnt<0>();
+      __builtin_amdgcn_s_barrier();  // every wave's x of the next step is in LDS; stage ST is free
+    }
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  // prologue: x of step 0 to LDS, W of half steps 0 and 1 in flight
+  load_x(0);
+  load_w(I0{}, 0);
+  load_w(I1{}, 1);
+  wait_vmcnt<8>();
+  store_x(I0{});
+  wait_lgkmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  // W slot h % 3 and stage (h / 2) % 2 repeat every 12 half steps
+  int h = 0;
+  for (; h + 12 <= H; h += 12) {
+    half(I0{}, I0{}, I0{}, h);
+    half(I1{}, I0{}, I1{}, h + 1);
+    half(I2{}, I1{}, I0{}, h + 2);
+    half(I0{}, I1{}, I1{}, h + 3);
+    half(I1{}, I0{}, I0{}, h + 4);
+    half(I2{}, I0{}, I1{}, h + 5);
+    half(I0{}, I1{}, I0{}, h + 6);
+    half(I1{}, I1{}, I1{}, h + 7);
+    half(I2{}, I0{}, I0{}, h + 8);
+    half(I0{}, I0{}, I1{}, h + 9);
+    half(I1{}, I1{}, I0{}, h + 10);
+    half(I2{}, I1{}, I1{}, h + 11);
+  }
+  // the remaining H % 12 half steps, whole steps (uniform branches)
+  if (h < H) { half(I0{}, I0{}, I0{}, h); half(I1{}, I0{}, I1{}, h + 1); }
+  if (h + 2 < H) { half(I2{}, I1{}, I0{}, h + 2); half(I0{}, I1{}, I1{}, h + 3); }
+  if (h + 4 < H) { half(I1{}, I0{}, I0{}, h + 4); half(I2{}, I0{}, I1{}, h + 5); }
+  if (h + 6 < H) { half(I0{}, I1{}, I0{}, h + 6); half(I1{}, I1{}, I1{}, h + 7); }
+  if (h + 8 < H) { half(I2{}, I0{}, I0{}, h + 8); half(I0{}, I0{}, I1{}, h + 9); }
+  wait_vmcnt<0>();  // the ring's loads past the end have landed
+  const int M = a.M;
+  if constexpr (FUSED) {
+    // two halves of 128 columns: waves 4h .. 4h + 3 (vocab groups 2h, 2h + 1) write
+    // their tiles (rows x 128, float4 groups XOR-swizzled by row against bank
+    // conflicts; rows spread over the four LDS arrays, 4 MTP rows each), all waves fuse
+    constexpr int NC = 128, RPS = 4 * MTP;
+    static_assert(2 * MTP * 64 * 16 == RPS * NC * 4, "an LDS array holds 4 MTP tile rows");
+    auto tile_row = [&](int m) -> float* {
+      const int q = m / RPS;
+      float* base = q == 0 ? (float*)&xs0[0][0] : q == 1 ? (float*)&xs1[0][0] : q == 2 ? (float*)&xs2[0][0]
+                                                                                   : (float*)&xs3[0][0];
+      return base + (m % RPS) * NC;
+    };
+    auto at = [&](int m, int j) { return tile_row(m)[((((j >> 2) ^ (m & 31)) << 2) | (j & 3))]; };
+    __syncthreads();  // every wave is done with the x stages
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if ((wave >> 2) == h) {
+#pragma unroll
+        for (int t = 0; t < MTH; ++t) {
+          const int m = 16 * (rh * MTH + t) + col;
+          if (m >= M) continue;
+          const float rho = a.rho_in[m];
+          float* row = tile_row(m);
+#pragma unroll
+          for (int vt = 0; vt < 4; ++vt) {
+            const f32x4 cc = acc[vt][t];
+            const int c4 = 16 * (grp & 1) + 4 * vt + quad;
+            *(float4*)(row + ((c4 ^ (m & 31)) << 2)) = make_float4(cc[0] * rho, cc[1] * rho, cc[2] * rho, cc[3] * rho);
+          }
+        }
+      }
+      __syncthreads();
+      fuse_tile<8, NC>(a, blockIdx.x * 256 + NC * h, 2 * blockIdx.x + h, at);
+      __syncthreads();
+    }
+    return;
+  }
+#pragma unroll
+  for (int t = 0; t < MTH; ++t) {
+    const int m = 16 * (rh * MTH + t) + col;
+    if (m >= M) continue;
+    const float rho = a.rho_in[m];
+#pragma unroll
+    for (int vt = 0; vt < 4; ++vt) {
+      if (vb0 + vt >= nvb) continue;
+      const int v = 16 * (vb0 + vt) + 4 * quad;
+      float* out = a.logits + (size_t)m * a.V + v;
+      const f32x4 cc = acc[vt][t];
+      if (v + 3 < a.V && (a.V & 3) == 0) {
+        *(float4*)out = make_float4(cc[0] * rho, cc[1] * rho, cc[2] * rho, cc[3] * rho);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (v + r < a.V) out[r] = cc[r] * rho;
+      }
+    }
+  }
+}
+
 // fp32 LM head for small validation shapes: one thread per vocab row.
 __global__ __launch_bounds__(256) void k_lmhead_f32(LmArgs a) {
   const int v = blockIdx.x * blockDim.x + threadIdx.x;
@@ -2251,6 +2498,13 @@ hipError_t launch_rho(const float* ss, int parts, int ld, int M, float inv_dim, 
             rho);
 }
 
+int lmhead_wide_tiles(int M, int V, int K) {
+  if (M <= kLmRowsPad || M > kLmWideMaxRows || K % 256 != 0) return 0;
+  if ((size_t)((V + 15) / 16) * 16 * K * 2 >= 0x7FFFFFFFull) return 0;  // 32-bit buffer offsets into W
+  const int mt = (M + 15) / 16;
+  return mt <= 8 ? 4 : mt <= 12 ? 6 : 9;  // the instantiated tile counts per row half
+}
+
 int lmhead_fused_nblk(int M, int V) {
   if (M <= kLmRowsPad) return (V + 255) / 256;         // 48-row kernel: 256 columns per block
   if (M <= 32 * kLmRowsMTW) return (V + 127) / 128;    // many-row kernel: 128 columns per block
@@ -2265,6 +2519,23 @@ hipError_t launch_lmhead(const LmArgs& a0, bool bf16, hipStream_t st, const Timi
     a.w_ks = kLmKMajor ? (size_t)nvb * 128 : 128;
     const bool fused = a.fuse_part != nullptr;
     if (fused && lmhead_fused_nblk(a.M, a.V) == 0) return hipErrorInvalidValue;
+    const int mtk = lmhead_wide_tiles(a.M, a.V, a.K);
+    if (mtk > 0 && a.x_packed && a.rho_buf) {
+      // many rows: W streamed once for all of them; x packed into operand order
+      // (and the row scales) first
+      hipError_t e = go(k_pack_x, dim3((32 * mtk + 3) / 4), dim3(256), 0, st, t0(tm), nullptr, (const uint16_t*)a.x,
+                        a.M, a.K, 2 * mtk, a.rms, (uint4*)a.x_packed, a.rho_buf);
+      if (e != hipSuccess) return e;
+      if (!a.rho_in) a.rho_in = a.rho_buf;
+      a.x = a.x_packed;
+      const dim3 g((nvb + 15) / 16), b(512);
+#define PCED_WIDE(MT)                                                                                        \
+  if (mtk == MT)                                                                                             \
+    return fused ? go(k_lmhead_wide_bf16<MT, true>, g, b, 0, st, nullptr, t1(tm), a)                         \
+                 : go(k_lmhead_wide_bf16<MT, false>, g, b, 0, st, nullptr, t1(tm), a);
+      PCED_WIDE(4) PCED_WIDE(6) PCED_WIDE(9)
+#undef PCED_WIDE
+    }
     if (a.M > kLmRowsPad && a.M <= 32 * kLmRowsMTW) {  // many rows: W streamed once for all of them
       constexpr int VTW = 2, WPB = 8;
       const int blocks = (nvb + WPB / 2 * VTW - 1) / (WPB / 2 * VTW);
