@@ -62,8 +62,8 @@ def parse():
                    help="also time K decode steps through the decoder stack (pced_model_generate: Llama-3-8B "
                         "decoder, 32 layers, MLP 14336, random-init weights) on the same caches")
     p.add_argument("--copy-calibration", action="store_true",
-                   help="after the timed steps, run one plain 256 MiB device copy (scale reference for "
-                        "the FETCH_SIZE / WRITE_SIZE counters)")
+                   help="after the timed steps, run one plain 256 MiB device copy and one 256 MiB streaming "
+                        "read (scale references for the FETCH_SIZE / WRITE_SIZE counters)")
     return p.parse_args()
 
 
@@ -73,11 +73,10 @@ def kernel_source_sha256() -> str:
     return hashlib.sha256(open(path, "rb").read()).hexdigest()
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per decode-attention launch from the committed counter summary
-    (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known size), or None if
-    there is none for this workload or the kernels changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.md")
+def committed_profile(name: str):
+    """The `- key: value` lines of a committed profiles/ summary, or None if there
+    is none or it was taken on other kernel sources than these."""
+    path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
     vals = {}
@@ -87,10 +86,46 @@ def measured_traffic(workload: str):
             vals[k.strip("` ")] = v.strip("` ")
     if vals.get("kernel source sha256") != kernel_source_sha256():
         return None
+    return vals
+
+
+def profile_number(vals, key: str):
     try:
-        return float(vals["pced_decode_attn HBM bytes per launch"])
+        return float(vals[key]) if vals else None
     except (KeyError, ValueError):
         return None
+
+
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, scaled by reads and a copy of known size), or None
+    if there is none for this workload or the kernels changed since it was taken."""
+    return profile_number(committed_profile(f"hbm_traffic_{workload}.md"), f"{kernel} HBM bytes per launch")
+
+
+def stream_read_bandwidth(dev, nbytes: int = 1 << 30, reps: int = 5) -> dict:
+    """Best of `reps` streaming reads of `nbytes` through pced_stream_read (the
+    decode kernels' non-temporal 16-byte loads, a plain grid-stride loop): a
+    reference read of known size, not a ceiling (the tuned decode kernels stream
+    faster than this simple loop)."""
+    import torch
+
+    from paper_2601_08670_amd import _lib
+    src = torch.ones(nbytes // 4, dtype=torch.int32, device=dev)
+    out = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    best = None
+    for _ in range(reps + 1):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        _lib.pced_stream_read(src, nbytes, out)
+        b.record(stream)
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b)
+        best = ms if best is None else min(best, ms)
+    del src, out
+    return {"bytes": nbytes, "best_ms": best, "GB/s": nbytes / (best * 1e-3) / 1e9,
+            "note": "simple grid-stride read, event-timed (launch overhead included); not a ceiling"}
 
 
 def cpu_baseline(wl, n_layers_sample: int, vocab_sample: int) -> dict:
@@ -412,14 +447,36 @@ def main():
                 tf = p["flops"] / (p["ms"] * 1e-3) / 1e12
                 kernels[name]["TFLOP/s"] = tf
                 kernels[name]["mfma_frac"] = tf / BF16_MFMA_PEAK_TFLOPS
+    rooflines = {}
     attn = kernels.get("attn")
-    roofline = None
     if attn:
-        roofline = {"bound": "hbm", "achieved": attn["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": attn["GB/s"] / HBM_PEAK_GBS, "traffic": measured_traffic(wl.name),
-                    "kernel": "pced_decode_attn",
-                    "bytes_per_launch": prof["attn"]["bytes"] / prof["attn"]["launches"],
-                    "avg_launch_us": attn["avg_us"]}
+        rooflines["pced_decode_attn"] = {
+            "bound": "hbm", "achieved": attn["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": attn["GB/s"] / HBM_PEAK_GBS, "traffic": measured_traffic(wl.name, "pced_decode_attn"),
+            "kernel": "pced_decode_attn", "bytes_per_launch": prof["attn"]["bytes"] / prof["attn"]["launches"],
+            "avg_launch_us": attn["avg_us"], "share_of_step": attn["share_of_step"]}
+    lm = kernels.get("lmhead")
+    if lm and "TFLOP/s" in lm:
+        # the bound is whichever floor is higher: W's bytes at the HBM peak or the
+        # flops at the bf16 matrix-core peak (below 312 rows, HBM)
+        mfma = committed_profile(f"mfma_{wl.name}.md")
+        flops = prof["lmhead"]["flops"] / prof["lmhead"]["launches"]
+        nbytes = prof["lmhead"]["bytes"] / prof["lmhead"]["launches"]
+        hbm_bound = nbytes / (HBM_PEAK_GBS * 1e9) >= flops / (BF16_MFMA_PEAK_TFLOPS * 1e12)
+        rooflines["pced_lmhead"] = {
+            "bound": "hbm" if hbm_bound else "mfma",
+            "achieved": lm["GB/s"] if hbm_bound else lm["TFLOP/s"],
+            "peak": HBM_PEAK_GBS if hbm_bound else BF16_MFMA_PEAK_TFLOPS,
+            "unit": "GB/s" if hbm_bound else "TFLOP/s",
+            "frac": lm["hbm_frac"] if hbm_bound else lm["mfma_frac"],
+            "traffic": measured_traffic(wl.name, "pced_lmhead"), "kernel": "pced_lmhead",
+            "rows": int(sess.S), "bytes_per_launch": nbytes, "flops_per_launch": flops,
+            "hbm_frac": lm["hbm_frac"], "mfma_frac": lm["mfma_frac"],
+            "avg_launch_us": lm["avg_us"], "share_of_step": lm["share_of_step"],
+            "mfma_util_counter": profile_number(mfma, "pced_lmhead MfmaUtil percent"),
+            "mfma_flops_counter_per_launch": profile_number(mfma, "pced_lmhead MFMA flops per launch")}
+    # the dominant kernel of the step is the roofline line's subject
+    roofline = max(rooflines.values(), key=lambda r: r["share_of_step"]) if rooflines else None
 
     fuse_sa = fuse_standalone(sess, wl, Wt, dev)
     log(f"[bench] pced_fuse stand-alone over materialised logits: warm {fuse_sa['avg_us']:.2f} us, "
@@ -431,15 +488,20 @@ def main():
         torch.cuda.empty_cache()
         model = model_timing(wl, K, Wm, dev)
 
+    stream_read = stream_read_bandwidth(dev)
+    log(f"[bench] streaming read of {stream_read['bytes'] >> 20} MiB: {stream_read['GB/s']:.0f} GB/s")
     if args.copy_calibration:
+        from paper_2601_08670_amd import _lib
         n = 256 << 20
         src = torch.ones(n // 4, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
+        out = torch.zeros(1, dtype=torch.int32, device=dev)
         torch.cuda.synchronize()
-        dst.copy_(src)
+        dst.copy_(src)  # plain loads and stores
+        _lib.pced_stream_read(src, n, out)  # non-temporal loads only
         torch.cuda.synchronize()
-        del src, dst
-        log("[bench] calibration copy of 256 MiB done")
+        del src, dst, out
+        log("[bench] calibration copy and streaming read of 256 MiB done")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -467,6 +529,8 @@ def main():
                    "generated_tokens": K, "beta": "dynamic" if wl.beta is None else "fixed",
                    "parallelism": "single GPU"},
         "roofline": roofline,
+        "rooflines": rooflines,
+        "hbm_stream_read": stream_read,
         "kernels": kernels,
         "fuse_standalone": fuse_sa,
         "cpu_baseline": cpu,

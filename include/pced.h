@@ -315,6 +315,20 @@ pced_status pced_read_cache(pced_ctx* ctx, int32_t seq, int32_t layer, int32_t s
 /* Host mirror of the current cache length of every sequence: out [S]. */
 pced_status pced_get_lengths(const pced_ctx* ctx, int32_t* out, int32_t capacity);
 
+/*
+ * Diagnostic, not a step of the method: *xor_out = the XOR of every 32-bit word
+ * of the `bytes` bytes at src, read once with the non-temporal 16-byte loads
+ * the decode kernels stream KV pages and weights with. A streaming read of
+ * known size, for calibrating memory-traffic counters (FETCH_SIZE) and for
+ * checking a device's streaming bandwidth. src: device, 16-byte aligned,
+ * bytes a multiple of 16 and within src's allocation (may be NULL when bytes
+ * is 0); xor_out: device, one uint32 (written 0 for bytes == 0). Asynchronous
+ * on `stream`.
+ * Errors: INVALID_ARG (NULL, misaligned, not device memory, past the
+ * allocation), HIP.
+ */
+pced_status pced_stream_read(const void* src, size_t bytes, uint32_t* xor_out, hipStream_t stream);
+
 /* Retrieval score modes (paper, Appendix B: normalisation per scoring mode). */
 typedef enum pced_score_mode {
   PCED_SCORE_DENSE = 0,    /* cosine similarity in [-1, 1]: r = clip((s + 1) / 2, 0, 1 - eps)     */

@@ -24,7 +24,8 @@ EXPORTED = ("pced_pool_bytes", "pced_lm_head_bytes", "pced_pack_lm_head", "pced_
             "pced_load_caches", "pced_step", "pced_generate", "pced_lmhead", "pced_fuse",
             "pced_get_lengths", "pced_profile_enable", "pced_profile_read", "pced_relevance",
             "pced_model_bytes", "pced_pack_model_layer", "pced_pack_model_globals", "pced_model_prefill",
-            "pced_model_step", "pced_model_generate", "pced_read_cache", "pced_lmhead_noalloc")
+            "pced_model_step", "pced_model_generate", "pced_read_cache", "pced_lmhead_noalloc",
+            "pced_stream_read")
 
 
 class PcedError(RuntimeError):
@@ -96,6 +97,7 @@ def load_library() -> ctypes.CDLL:
         "pced_model_generate": (I, [P, P, P, I, P, P, ctypes.POINTER(pced_step_out), V]),
         "pced_read_cache": (I, [P, I, I, I, I, P, P, V]),
         "pced_lmhead_noalloc": (I, [ctypes.POINTER(pced_config), P, I, P, P, V]),
+        "pced_stream_read": (I, [P, ctypes.c_size_t, P, V]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -144,6 +146,11 @@ def pced_lmhead_noalloc(cfg: pced_config, x, n_rows, lm_head, logits, stream=Non
     """Logits of n_rows hidden states with no context and no caller workspace."""
     _check(load_library().pced_lmhead_noalloc(ctypes.byref(cfg), x.data_ptr(), int(n_rows), lm_head.data_ptr(),
                                               logits.data_ptr(), _stream(stream)))
+
+
+def pced_stream_read(src, nbytes, xor_out, stream=None):
+    """XOR of the 32-bit words of nbytes of src (device), read with streaming loads."""
+    _check(load_library().pced_stream_read(src.data_ptr(), int(nbytes), xor_out.data_ptr(), _stream(stream)))
 
 
 def pced_model_bytes(cfg: pced_config) -> int:

@@ -1523,6 +1523,32 @@ pced_status pced_fuse(pced_ctx* c, const float* logits, int32_t refresh_beta, in
   return run_fuse(c, logits, refresh_beta != 0, tokens_out, 1, extra, st);
 }
 
+pced_status pced_stream_read(const void* src, size_t bytes, uint32_t* xor_out, hipStream_t st) {
+  if (!xor_out || (!src && bytes > 0)) return fail(PCED_ERR_INVALID_ARG, "NULL argument");
+  if ((uintptr_t)src % 16 != 0 || bytes % 16 != 0)
+    return fail(PCED_ERR_INVALID_ARG, "src must be 16-byte aligned and bytes a multiple of 16 (bytes = %zu)", bytes);
+  if ((uintptr_t)xor_out % 4 != 0) return fail(PCED_ERR_INVALID_ARG, "xor_out is not 4-byte aligned");
+  if (!is_device_memory(xor_out) || (bytes > 0 && !is_device_memory(src)))
+    return fail(PCED_ERR_INVALID_ARG, "src and xor_out must be device memory");
+  int dev = 0, cus = 0;
+  HIP_OK(hipGetDevice(&dev));
+  HIP_OK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  if (bytes == 0) {
+    HIP_OK(launch_stream_read(nullptr, 0, xor_out, cus, st));
+    return PCED_OK;
+  }
+  hipDeviceptr_t base = nullptr;
+  size_t size = 0;
+  if (hipMemGetAddressRange(&base, &size, (hipDeviceptr_t)src) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(PCED_ERR_INVALID_ARG, "src is not inside a device allocation");
+  }
+  if ((const char*)src + bytes > (const char*)base + size)
+    return fail(PCED_ERR_INVALID_ARG, "%zu bytes from src run past the end of its allocation", bytes);
+  HIP_OK(launch_stream_read(src, bytes, xor_out, cus, st));
+  return PCED_OK;
+}
+
 pced_status pced_relevance(int32_t mode, int32_t n, const float* retrieval, const float* reranker_logits,
                            float* relevance) {
   if (!retrieval || !relevance) return fail(PCED_ERR_INVALID_ARG, "NULL argument");

@@ -285,6 +285,7 @@ int lmhead_wide_tiles(int M, int V, int K);
 constexpr int kLmWideMaxRows = 288;  // rows of the largest many-row tile count
 hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st, const Timing* tm = nullptr);
 hipError_t launch_copy_rows(const void* src, void* dst, size_t nbytes, hipStream_t st);
+hipError_t launch_stream_read(const void* src, size_t nbytes, uint32_t* xor_out, int num_cus, hipStream_t st);
 // pack a [rows][K] bf16 matrix into 16-row tiles, tile i going to slot i * stride + offset
 hipError_t launch_pack_tiles(const void* w, void* wp, int rows, int K, int stride, int offset, int n_tiles,
                              hipStream_t st);

@@ -1026,11 +1026,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int nvb = (a.V + 15) / 16;
   if (!FUSED && vb0 >= nvb) return;  // (fused: every wave reaches the block's barriers)
   const int K = a.K, KS = K / 64;
-  const uint4* Wp = (const uint4*)a.w;
   const uint16_t* X = (const uint16_t*)a.x;
-  const uint4* wt[VT];
+  // W tile addresses: a wave-uniform 64-bit base (scalar registers) plus the
+  // lane's 16 bytes, so the ring's loads cost no per-lane pointer registers
+  const char* Wb = (const char*)a.w;
+  const uint32_t lane16 = 16u * lane;
+  size_t wvb[VT];
 #pragma unroll
-  for (int vt = 0; vt < VT; ++vt) wt[vt] = Wp + (size_t)min(vb0 + vt, nvb - 1) * a.w_vb + lane;
+  for (int vt = 0; vt < VT; ++vt)
+    wvb[vt] = (size_t)__builtin_amdgcn_readfirstlane(min(vb0 + vt, nvb - 1)) * a.w_vb * 16;
   for (int m0 = rg * 16 * NT; m0 < a.M; m0 += 16 * NT * R) {
     f32x4 acc[VT][NT];
     float ss[NT];
@@ -1049,10 +1053,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     struct XS { uint4 x[NT][2]; };
     auto load_w = [&](WS& S, int ks) {
       ks = min(ks, KS - 1);  // past the end: the last step again (cache hit), keeps the ring branch-free
+      const size_t kso = (size_t)ks * a.w_ks * 16;
 #pragma unroll
       for (int vt = 0; vt < VT; ++vt) {
-        S.w[vt][0] = ld_w<STREAM>(&wt[vt][(size_t)ks * a.w_ks]);
-        S.w[vt][1] = ld_w<STREAM>(&wt[vt][(size_t)ks * a.w_ks + 64]);
+        const char* base = Wb + wvb[vt] + kso;
+        S.w[vt][0] = ld_w<STREAM>((const uint4*)(base + lane16));
+        S.w[vt][1] = ld_w<STREAM>((const uint4*)(base + 1024 + lane16));
       }
     };
     auto load_x = [&](XS& S, int ks) {
@@ -1114,7 +1120,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
       __syncthreads();
       fuse_tile<4, 64 * VT>(a, chunk * 256, chunk, [&](int m, int j) { return tile[m * LD + j]; });
-      continue;
+      return;  // fused: at most 16 NT rows, a single row group
     }
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -2286,6 +2292,30 @@ __global__ __launch_bounds__(128) void k_read_cache(ReadCacheArgs a) {
   }
 }
 
+// XOR of every 32-bit word of n16 16-byte units, read with the decode kernels'
+// streaming loads: eight loads in flight per lane, grid-stride, one wave-level
+// fold and one vector atomic per wave.
+__global__ __launch_bounds__(256) void k_stream_read(const uint4* __restrict__ p, size_t n16, uint32_t* out) {
+  constexpr int U = 8;
+  const size_t stride = (size_t)gridDim.x * 256;
+  uint32_t x = 0u;
+  size_t i = blockIdx.x * (size_t)256 + threadIdx.x;
+  for (; i + (U - 1) * stride < n16; i += U * stride) {
+    uint4 v[U];
+#pragma unroll
+    for (int j = 0; j < U; ++j) v[j] = ld_w<true>(p + i + j * stride);
+#pragma unroll
+    for (int j = 0; j < U; ++j) x ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
+  }
+  for (; i < n16; i += stride) {
+    const uint4 v = ld_w<true>(p + i);
+    x ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x ^= (uint32_t)__shfl_xor((int)x, o);
+  if ((threadIdx.x & 63) == 0) atomicXor(out, x);
+}
+
 // rho[m] = 1/sqrt(sum_p ss[p][m] * inv_dim + eps), 8 lanes per row.
 __global__ __launch_bounds__(256) void k_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps,
                                              float* rho) {
@@ -2547,6 +2577,7 @@ hipError_t launch_lmhead(const LmArgs& a0, bool bf16, hipStream_t st, const Timi
     // up to 48 rows, or beyond the many-row kernel: 48-row groups, the groups of
     // one vocab chunk together on one XCD so that W comes from HBM once
     constexpr int VT = 4, NT = 3;
+    if (fused && a.M > 16 * NT) return hipErrorInvalidValue;  // the fused epilogue covers one row group
     const int chunks = (nvb + 4 * VT - 1) / (4 * VT);
     LmArgs b = a;
     b.row_groups = (a.M + 16 * NT - 1) / (16 * NT);
@@ -2614,6 +2645,15 @@ hipError_t launch_synth(const SynthArgs& a, int n_seqs, hipStream_t st, const Ti
   const int blocks = n_seqs * a.n_layers;
   if (a.bf16) return go(k_synth<true>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), a);
   return go(k_synth<false>, dim3(blocks), dim3(256), 0, st, t0(tm), t1(tm), a);
+}
+
+hipError_t launch_stream_read(const void* src, size_t nbytes, uint32_t* xor_out, int num_cus, hipStream_t st) {
+  hipError_t e = go(k_zero_u32, dim3(1), dim3(64), 0, st, nullptr, nullptr, xor_out, (size_t)1);
+  if (e != hipSuccess || nbytes == 0) return e;
+  const size_t n16 = nbytes / 16;
+  const size_t want = (n16 + 2047) / 2048;  // eight 16-byte loads per lane
+  const unsigned blocks = (unsigned)std::max<size_t>(1, std::min<size_t>(want, (size_t)num_cus * 8));
+  return go(k_stream_read, dim3(blocks), dim3(256), 0, st, nullptr, nullptr, (const uint4*)src, n16, xor_out);
 }
 
 hipError_t launch_copy_rows(const void* src, void* dst, size_t nbytes, hipStream_t st) {

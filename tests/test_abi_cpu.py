@@ -281,3 +281,18 @@ def test_lmhead_noalloc_validation_before_any_launch():
     assert lib.pced_lmhead_noalloc(ctypes.byref(c), 1, 0, 1, 1, None) == INVALID
     assert lib.pced_lmhead_noalloc(ctypes.byref(c), 1, 513, 1, 1, None) == CAPACITY
     assert b"scratch" in lib.pced_last_error()
+
+
+def test_stream_read_validation_before_any_launch():
+    lib = _lib.load_library()
+    host = (ctypes.c_uint32 * 64)()
+    out = (ctypes.c_uint32 * 1)()
+    base = ctypes.addressof(host)
+    base16 = (base + 15) // 16 * 16
+    assert lib.pced_stream_read(None, 16, ctypes.addressof(out), None) == INVALID
+    assert lib.pced_stream_read(base16, 0, ctypes.addressof(out), None) == INVALID       # host output
+    assert lib.pced_stream_read(base16, 16, None, None) == INVALID
+    assert lib.pced_stream_read(base16 + 4, 16, ctypes.addressof(out), None) == INVALID   # misaligned
+    assert lib.pced_stream_read(base16, 24, ctypes.addressof(out), None) == INVALID       # not whole units
+    assert lib.pced_stream_read(base16, 16, ctypes.addressof(out), None) == INVALID       # host memory
+    assert b"device memory" in lib.pced_last_error()

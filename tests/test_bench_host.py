@@ -38,11 +38,12 @@ def test_traffic_is_reported_only_for_the_kernels_it_was_measured_on(monkeypatch
     rec = _recorded(WORKLOAD)
     value = float(rec["pced_decode_attn HBM bytes per launch"])
     assert 1e8 < value < 1e9   # one layer's K/V pages of the 33 caches plus split states, in bytes
-    assert b.measured_traffic("no-such-workload") is None
+    assert b.measured_traffic("no-such-workload", "pced_decode_attn") is None
     monkeypatch.setattr(b, "kernel_source_sha256", lambda: rec["kernel source sha256"])
-    assert b.measured_traffic(WORKLOAD) == value
+    assert b.measured_traffic(WORKLOAD, "pced_decode_attn") == value
+    assert b.measured_traffic(WORKLOAD, "no_such_kernel") is None
     monkeypatch.setattr(b, "kernel_source_sha256", lambda: "0" * 64)
-    assert b.measured_traffic(WORKLOAD) is None
+    assert b.measured_traffic(WORKLOAD, "pced_decode_attn") is None
 
 
 def test_kernel_source_hash_is_of_the_kernel_file():
