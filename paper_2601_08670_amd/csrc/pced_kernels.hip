@@ -967,6 +967,69 @@ __device__ void fuse_tile(const LmArgs& a, int v0, int blk, At at) {
   }
 }
 
+// Eq. 2 and the best two tokens per query over a block's logits tile (the
+// many-row LM head's fused epilogue), with the queries' row and expert offsets
+// (qs, qe), beta (cb) and prior (pr) already in LDS: the block's threads form
+// groups of tpq lanes inside a wave (tpq a power of two, 2..64), one query per
+// group at a time; a lane takes every tpq-th of the NC columns (vocabulary ids
+// v0 + j, row m of column j read through at(m, j)) and keeps the best two
+// tokens over them, and the group merges its lanes with shuffles, so no block
+// barrier is needed per query. The arithmetic is k_fuse's, in the same order
+// and without contraction, so the result is bit-identical to materialising the
+// logits and fusing them afterwards. Writes fuse_part[b][blk] for every query b.
+template <int NW, int NC, typename At>
+__device__ void fuse_tile_groups(const LmArgs& a, int v0, int blk, At at, int tpq, const int* qs, const int* qe,
+                                 const float* cb, const float* pr) {
+#pragma clang fp contract(off)
+  const int groups = 64 * NW / tpq, g = threadIdx.x / tpq, c = threadIdx.x % tpq;
+  for (int b = g; b < a.n_queries; b += groups) {
+    const int s0 = qs[b];
+    const int N = qs[b + 1] - s0 - 1;
+    const int e0 = qe[b];
+    Top2 cand{kNegInf, 0x7FFFFFFF, 0, kNegInf, 0x7FFFFFFF};
+    for (int j = c; j < NC; j += tpq) {
+      const int v = v0 + j;
+      if (v >= a.V) break;
+      const float sa = at(s0, j);
+      float best = kNegInf;
+      int bk = 0;
+      for (int kb = 1; kb <= N; kb += 8) {
+        float x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = (kb + u <= N) ? at(s0 + kb + u, j) : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int k = kb + u;
+          if (k > N) continue;
+          const float beta = cb[e0 + k - 1];
+          const float coef = 1.0f + beta;
+          const float t1 = coef * x[u];
+          const float t2 = beta * sa;
+          const float val = (t1 - t2) + pr[e0 + k - 1];
+          if (val > best) { best = val; bk = k; }
+        }
+      }
+      cand = merge(cand, Top2{best, v, bk, kNegInf, 0x7FFFFFFF});
+    }
+    for (int o = tpq >> 1; o >= 1; o >>= 1) cand = merge(cand, shfl_top2(cand, o));
+    if (c == 0) {
+      float* p = a.fuse_part + ((size_t)b * a.fuse_nblk + blk) * 5;
+      p[0] = cand.v1; p[1] = __int_as_float(cand.i1); p[2] = __int_as_float(cand.k1);
+      p[3] = cand.v2; p[4] = __int_as_float(cand.i2);
+    }
+  }
+}
+
+// What the many-row LM head's fused epilogue reads besides its tile, staged in
+// LDS at the start of the launch (an empty struct without the epilogue).
+template <bool FUSED>
+struct WideEpi {
+  float rho[kLmWideMaxRows], beta[kLmWideMaxRows], prior[kLmWideMaxRows];
+  int qs[kLmWideMaxRows / 2 + 1], qe[kLmWideMaxRows / 2 + 1];
+};
+template <>
+struct WideEpi<false> {};
+
 // ------------------------------------------------------------------- LM head
 
 // Packed LM-head layout (bf16). W [V][K] is re-laid once into 2 KiB tiles, one
@@ -1393,11 +1456,11 @@ template <int MTH, bool FUSED>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_lmhead_wide_bf16(LmArgs a) {
   constexpr int MTP = 2 * MTH;           // 16-row tiles of the packed x
   constexpr int XB = (2 * MTP + 7) / 8;  // x operand loads per wave and step
-  // two x stages (the ring) and two more arrays: room for the fused epilogue's tile
-  __shared__ __align__(16) uint4 xs0[2 * MTP][64];
-  __shared__ __align__(16) uint4 xs1[2 * MTP][64];
-  __shared__ __align__(16) uint4 xs2[2 * MTP][64];
-  __shared__ __align__(16) uint4 xs3[2 * MTP][64];
+  // two x stages (the ring) and two more: room for the fused epilogue's tile
+  __shared__ __align__(16) uint4 xsb[4][2 * MTP][64];
+  __shared__ WideEpi<FUSED> epi;
+  uint4(*xs0)[64] = xsb[0];
+  uint4(*xs1)[64] = xsb[1];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 1, rh = wave & 1;  // vocab group (64 rows) and row half of this wave
@@ -1482,10 +1545,36 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
+  // the fused epilogue's row scales, beta, prior and query offsets: loaded first,
+  // written to LDS once the prologue's loads are in flight
+  float e_rho = 0.f, e_beta = 0.f, e_prior = 0.f;
+  int e_qs = 0, e_qe = 0;
+  if constexpr (FUSED) {
+    if (tid < a.M) e_rho = a.rho_in[tid];
+    if (tid < a.M - a.n_queries) {  // experts: every query has one amateur row
+      e_beta = a.beta[tid];
+      e_prior = a.prior[tid];
+    }
+    if (tid <= a.n_queries) {
+      e_qs = a.query_seq0[tid];
+      e_qe = a.query_exp0[tid];
+    }
+  }
   // prologue: x of step 0 to LDS, W of half steps 0 and 1 in flight
   load_x(0);
   load_w(I0{}, 0);
   load_w(I1{}, 1);
+  if constexpr (FUSED) {
+    if (tid < a.M) epi.rho[tid] = e_rho;
+    if (tid < a.M - a.n_queries) {  // experts: every query has one amateur row
+      epi.beta[tid] = e_beta;
+      epi.prior[tid] = e_prior;
+    }
+    if (tid <= a.n_queries) {
+      epi.qs[tid] = e_qs;
+      epi.qe[tid] = e_qe;
+    }
+  }
   wait_vmcnt<8>();
   store_x(I0{});
   wait_lgkmcnt<0>();
@@ -1516,17 +1605,15 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int M = a.M;
   if constexpr (FUSED) {
     // two halves of 128 columns: waves 4h .. 4h + 3 (vocab groups 2h, 2h + 1) write
-    // their tiles (rows x 128, float4 groups XOR-swizzled by row against bank
-    // conflicts; rows spread over the four LDS arrays, 4 MTP rows each), all waves fuse
-    constexpr int NC = 128, RPS = 4 * MTP;
-    static_assert(2 * MTP * 64 * 16 == RPS * NC * 4, "an LDS array holds 4 MTP tile rows");
-    auto tile_row = [&](int m) -> float* {
-      const int q = m / RPS;
-      float* base = q == 0 ? (float*)&xs0[0][0] : q == 1 ? (float*)&xs1[0][0] : q == 2 ? (float*)&xs2[0][0]
-                                                                                   : (float*)&xs3[0][0];
-      return base + (m % RPS) * NC;
-    };
-    auto at = [&](int m, int j) { return tile_row(m)[((((j >> 2) ^ (m & 31)) << 2) | (j & 3))]; };
+    // their tiles (rows x 128 floats over the four stages, float4 groups
+    // XOR-swizzled by row against bank conflicts), then all waves fuse; one
+    // query per group of tpq lanes (64 lanes per query up to 8 queries, 2 at 144)
+    constexpr int NC = 128;
+    static_assert(4 * 2 * MTP * 64 * 16 >= 16 * MTP * NC * 4, "the stages hold every tile row");
+    float* tile = (float*)&xsb[0][0][0];
+    auto at = [&](int m, int j) { return tile[m * NC + ((((j >> 2) ^ (m & 31)) << 2) | (j & 3))]; };
+    int tpq = 64;
+    while (tpq > 2 && (512 / tpq) < a.n_queries) tpq >>= 1;
     __syncthreads();  // every wave is done with the x stages
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -1535,8 +1622,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         for (int t = 0; t < MTH; ++t) {
           const int m = 16 * (rh * MTH + t) + col;
           if (m >= M) continue;
-          const float rho = a.rho_in[m];
-          float* row = tile_row(m);
+          const float rho = epi.rho[m];
+          float* row = tile + m * NC;
 #pragma unroll
           for (int vt = 0; vt < 4; ++vt) {
             const f32x4 cc = acc[vt][t];
@@ -1546,8 +1633,9 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         }
       }
       __syncthreads();
-      fuse_tile<8, NC>(a, blockIdx.x * 256 + NC * h, 2 * blockIdx.x + h, at);
-      __syncthreads();
+      fuse_tile_groups<8, NC>(a, blockIdx.x * 256 + NC * h, 2 * blockIdx.x + h, at, tpq, epi.qs, epi.qe, epi.beta,
+                              epi.prior);
+      if (h == 0) __syncthreads();  // before the second half's tile overwrites the first
     }
     return;
   }

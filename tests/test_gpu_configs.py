@@ -347,6 +347,11 @@ FUSED = [
      list(range(3, 183, 3)), 5, 2, "fixed"),
     ("llama-heads-vocab-tail-dynamic-beta", W.Geometry(1, 32, 8, 128, 4096, 4103, "bf16"), [6],
      [100, 7, 64, 300, 16, 45], 64, 3, None),
+    # 8 or more queries in the many-row kernel: one query per group of lanes
+    ("many-row-12-queries-fixed-beta", W.Geometry(1, 8, 2, 64, 512, 1003, "bf16"),
+     [1, 5, 2, 9, 3, 1, 7, 4, 2, 6, 3, 1], list(range(3, 179, 4)), 5, 2, "fixed"),
+    ("many-row-40-queries-dynamic-beta", W.Geometry(1, 4, 2, 64, 256, 1000, "bf16"),
+     [1] * 20 + [2] * 20, [5 + (7 * i) % 90 for i in range(60)], 3, 2, None),
 ]
 
 
