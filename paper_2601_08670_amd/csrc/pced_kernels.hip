@@ -1424,134 +1424,151 @@ __global__ __launch_bounds__(256) void k_pack_x(const uint16_t* __restrict__ x, 
   if (lane == 0 && m < M) rho[m] = rms ? 1.0f / sqrtf(ss / (float)K + 1e-5f) : 1.0f;
 }
 
+// The many-row LM head's wait at the end of step s: vector loads retire in
+// order, and half step h (relative to 2s) issues W(2s + h + lead) and then, at
+// even h, x(s + h/2 + xl) (xb loads). Step s + 1 needs x(s + 1) and
+// W(2s + 2), W(2s + 3); the result is the number of loads issued after the
+// later of those two (w loads per half step), which may stay in flight.
+constexpr int lmhead_wide_wait(int lead, int xl, int xb, int w) {
+  const int hw = 3 - lead, hx = 2 - 2 * xl;  // half steps that issue W(2s + 3) and x(s + 1)
+  int n = 0, from = 0;
+  if (hw > hx) {
+    n = (hw % 2 == 0) ? xb : 0;  // the x issued after W in half step hw
+    from = hw + 1;
+  } else {
+    from = hx + 1;
+  }
+  for (int h = from; h <= 1; ++h) n += w + ((h % 2 == 0) ? xb : 0);
+  return n;
+}
+static_assert(lmhead_wide_wait(7, 3, 5, 2) == 20 && lmhead_wide_wait(3, 3, 5, 4) == 9, "wait counts");
+
 // LM head for 49..288 rows with W read once: logits[m][v] = rho_m sum_k x[m][k] W[v][k]
 // (x packed by k_pack_x, rho precomputed) on the matrix cores,
 // C^T[16 vocab x 16 rows] += W[16 x 32] X^T[32 x 16] (v_mfma_f32_16x16x32_bf16).
-// A block of 8 waves (two per SIMD) owns 256 vocabulary rows: wave w serves
-// vocab group w / 2 (64 rows, four 16-row tiles) for row half w % 2 (MTH
-// 16-row tiles), so each B operand read from LDS feeds four products (acc:
-// 4 x MTH x 4 registers). The hidden dimension is walked in 32-wide half steps;
-// per half step h every wave
-//   1. (even h) loads its share of x for the next 64-wide step (the packed x
-//      holds each (k step, row tile, half) B operand as one contiguous 1 KiB;
-//      the block's 2 MTP operands are shared by the 8 waves) into registers,
-//      then its four W operands of half step h + 2 into a 3-slot register ring;
-//   2. runs the MTH x 4 products of half step h, each tile's B operand read
-//      from LDS stage (h / 2) % 2 two tiles ahead of its products;
-//   3. (odd h) waits for its x only (vector loads retire in order and x was
-//      issued before the W still in flight), writes it to the other LDS stage
-//      and meets the other waves at a barrier.
-// Scheduling barriers pin this order (left alone, the compiler sinks the W
-// loads next to their use). The two waves of a vocab group load the same W
-// bytes with plain loads: the second is a cache hit. FUSED: Eq. 2 and the
-// slice argmax in the epilogue, in two halves of 128 columns through the
-// (then free) LDS buffers.
-template <int N>
-__device__ __forceinline__ void wait_lgkmcnt() {
-  static_assert(N >= 0 && N < 16, "lgkmcnt has 4 bits");
-  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (N << 8));
-}
-
+// A block of 8 waves (two per SIMD) owns 256 vocabulary rows; wave w computes
+// vocab rows 32w .. 32w + 31 of them (two 16-row tiles) for all MTP 16-row
+// tiles of x (acc: 2 x MTP x 4 registers), so every W byte is loaded by exactly
+// one wave. The products are cheap next to the weight stream, which they must
+// hide, so both operands are fetched far ahead. The hidden dimension is walked
+// in 32-wide half steps h:
+//   - W of half step h + 7 goes into slot (h + 7) % 8 of an 8-slot register
+//     ring (two tiles, 8 registers a slot);
+//   - at even h the packed x of 64-wide step h/2 + 3 goes from memory straight
+//     into LDS stage (h/2 + 3) % 4 (buffer loads with the LDS flag, no
+//     registers), the eight waves loading an eighth of its 1 KiB operands
+//     each; x is fetched as far ahead as W because vector loads retire in
+//     order, so waiting for an x issued after a W waits for that W too;
+//   - the 2 x MTP products of h read their B operands from LDS stage (h/2) % 4,
+//     three tiles ahead of their use, each feeding two products;
+//   - at odd h the wave waits until its loads of the next step's x and W have
+//     landed, leaving every later load in flight, and meets the other waves
+//     at a barrier, after which the next stage holds every wave's loads.
+// Scheduling barriers keep each half step's loads ahead of its products. Loads
+// past the end re-read the last step (in bounds, never used). FUSED: Eq. 2 and
+// the slice argmax in the epilogue, in two halves of 128 columns through the
+// (then free) LDS stages, with the row scales, beta, prior and query offsets
+// staged in LDS at the start.
 template <int MTH, bool FUSED>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_lmhead_wide_bf16(LmArgs a) {
   constexpr int MTP = 2 * MTH;           // 16-row tiles of the packed x
-  constexpr int XB = (2 * MTP + 7) / 8;  // x operand loads per wave and step
-  // two x stages (the ring) and two more: room for the fused epilogue's tile
-  __shared__ __align__(16) uint4 xsb[4][2 * MTP][64];
+  constexpr int XU = 2 * MTP;            // 1 KiB B operands of one x stage (tiles x 2 halves)
+  constexpr int XB = (XU + 7) / 8;       // of which each wave loads (the last one twice over if XU % 8 != 0)
+  constexpr int WR = 8, LEAD = WR - 1;   // W ring slots; half steps of W in flight
+  constexpr int XL = 3;                  // 64-wide steps of x in flight
+  constexpr int PF = 3;                  // B operands read from LDS ahead of their products
+  constexpr int WAITN = lmhead_wide_wait(LEAD, XL, XB, 2);
+  static_assert(WAITN < 64, "vmcnt has 6 bits");
+  // four separate stage arrays, so that the compiler can tell a stage being
+  // loaded into LDS from the one being read
+  __shared__ __align__(16) uint4 xs0[XU][64];
+  __shared__ __align__(16) uint4 xs1[XU][64];
+  __shared__ __align__(16) uint4 xs2[XU][64];
+  __shared__ __align__(16) uint4 xs3[XU][64];
   __shared__ WideEpi<FUSED> epi;
-  uint4(*xs0)[64] = xsb[0];
-  uint4(*xs1)[64] = xsb[1];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int grp = wave >> 1, rh = wave & 1;  // vocab group (64 rows) and row half of this wave
   const int col = lane & 15, quad = lane >> 4;
   const int K = a.K, KS = K / 64, H = 2 * KS;
+  const int M = a.M;
   const int nvb = (a.V + 15) / 16;
-  const int vb0 = blockIdx.x * 16 + 4 * grp;  // this wave's first 16-row vocab block (of 4)
-  // Buffer loads: a uniform descriptor per operand, one 32-bit vector offset per
-  // lane and the step's advance in a scalar offset (few registers per load).
+  const int vb0 = blockIdx.x * 16 + 2 * wave;  // this wave's first 16-row vocab block (of 2)
+  // buffer loads: a uniform descriptor per operand, one 32-bit vector offset per
+  // lane, the step's advance in a scalar offset
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc((void*)a.w, 0, 0x7FFFFFFF, 0x00020000);
-  uint32_t w_t[4];
+  uint32_t w_t[2];
 #pragma unroll
-  for (int vt = 0; vt < 4; ++vt) w_t[vt] = (uint32_t)min(vb0 + vt, nvb - 1) * (uint32_t)a.w_vb * 16u;
+  for (int vt = 0; vt < 2; ++vt) w_t[vt] = (uint32_t)min(vb0 + vt, nvb - 1) * (uint32_t)a.w_vb * 16u;
   const uint32_t w_ks = (uint32_t)a.w_ks * 16u;
   const uint32_t lane16 = 16u * lane;
   const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, 0x7FFFFFFF, 0x00020000);
-  const uint32_t x_ks = (uint32_t)MTP * 2048u;  // bytes of one k step of the packed x
-  uint32_t xoff[XB];
-  int xblk[XB];
-#pragma unroll
-  for (int i = 0; i < XB; ++i) {
-    int j = wave + 8 * i;
-    if (j >= 2 * MTP) j -= 2 * MTP;
-    xblk[i] = j;
-    xoff[i] = (uint32_t)j * 1024u + lane16;
-  }
-  u32x4 xr[XB];
-  auto load_x = [&](int ks) __attribute__((always_inline)) {
-    ks = min(ks, KS - 1);
-#pragma unroll
-    for (int i = 0; i < XB; ++i) xr[i] = __builtin_amdgcn_raw_buffer_load_b128(xrs, xoff[i], (uint32_t)ks * x_ks, 0);
-  };
-  auto store_x = [&](auto stage_c) __attribute__((always_inline)) {
-    uint4(*dst)[64] = decltype(stage_c)::value == 0 ? xs0 : xs1;
-#pragma unroll
-    for (int i = 0; i < XB; ++i) dst[xblk[i]][lane] = __builtin_bit_cast(uint4, xr[i]);
-  };
-  // W in half steps (32 of the hidden dimension): 4 vocab tiles each, a 3-slot
-  // ring loaded two half steps ahead. The two waves of a vocab group load the
-  // same bytes; plain loads, so that the second is a cache hit.
-  u32x4 wr[3][4];
+  constexpr uint32_t x_ks = XU * 1024u;  // bytes of one 64-wide step of the packed x
+  u32x4 wr[WR][2];
   auto load_w = [&](auto slot_c, int h) __attribute__((always_inline)) {
     constexpr int SL = decltype(slot_c)::value;
-    h = min(h, H - 1);  // past the end: the last half step again (cache hits)
+    h = min(h, H - 1);
     const uint32_t so = (uint32_t)(h >> 1) * w_ks + (uint32_t)(h & 1) * 1024u;
 #pragma unroll
-    for (int vt = 0; vt < 4; ++vt)
+    for (int vt = 0; vt < 2; ++vt)
       wr[SL][vt] = __builtin_amdgcn_raw_buffer_load_b128(wrs, lane16, so + w_t[vt], 0);
   };
-  f32x4 acc[4][MTH];
+  auto stage = [&](auto st_c) __attribute__((always_inline)) -> uint4(*)[64] {
+    constexpr int ST = decltype(st_c)::value;
+    return ST == 0 ? xs0 : ST == 1 ? xs1 : ST == 2 ? xs2 : xs3;
+  };
+  auto load_x = [&](auto st_c, int ks) __attribute__((always_inline)) {
+    uint4(*dst)[64] = stage(st_c);
+    ks = min(ks, KS - 1);
 #pragma unroll
-  for (int t = 0; t < MTH; ++t)
+    for (int i = 0; i < XB; ++i) {
+      const int j = min(wave + 8 * i, XU - 1);  // operand (tile j / 2, half j % 2) of the step
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xrs, (lds_void*)&dst[j][0], 16, lane16 + 1024u * j,
+                                               (uint32_t)ks * x_ks, 0, 0);
+    }
+  };
+  f32x4 acc[2][MTP];
 #pragma unroll
-    for (int vt = 0; vt < 4; ++vt) acc[vt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // half step h: W slot h % 3, LDS stage (h / 2) % 2, half h % 2 of the step's 64
-  auto half = [&](auto slot_c, auto stage_c, auto hf_c, int h) __attribute__((always_inline)) {
-    constexpr int SL = decltype(slot_c)::value, ST = decltype(stage_c)::value, HF = decltype(hf_c)::value;
-    if constexpr (HF == 0) load_x((h >> 1) + 1);
-    load_w(std::integral_constant<int, (SL + 2) % 3>{}, h + 2);
-    __builtin_amdgcn_sched_barrier(0);  // this step's loads are issued before its products
-    uint4(*src)[64] = ST == 0 ? xs0 : xs1;
-    const int r0 = 2 * rh * MTH + HF;  // B operand of tile t: src[r0 + 2 t]
-    bf16x8 b[3];
-    b[0] = as_bf16x8(src[r0][lane]);
-    if constexpr (MTH > 1) b[1] = as_bf16x8(src[r0 + 2][lane]);
+  for (int t = 0; t < MTP; ++t)
 #pragma unroll
-    for (int t = 0; t < MTH; ++t) {
-      if (t + 2 < MTH) b[(t + 2) % 3] = as_bf16x8(src[r0 + 2 * (t + 2)][lane]);  // two tiles ahead
+    for (int vt = 0; vt < 2; ++vt) acc[vt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto half = [&](auto slot_c, auto st_c, auto hf_c, int h) __attribute__((always_inline)) {
+    constexpr int SL = decltype(slot_c)::value, ST = decltype(st_c)::value, HF = decltype(hf_c)::value;
+    load_w(std::integral_constant<int, (SL + LEAD) % WR>{}, h + LEAD);
+    if constexpr (HF == 0) load_x(std::integral_constant<int, (ST + XL) % 4>{}, (h >> 1) + XL);
+    __builtin_amdgcn_sched_barrier(0);  // this half step's loads go out before its products
+    uint4(*src)[64] = stage(st_c);
+    bf16x8 b[PF + 1];
 #pragma unroll
-      for (int vt = 0; vt < 4; ++vt)
-        acc[vt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wr[SL][vt]), b[t % 3],
-                                                              acc[vt][t], 0, 0, 0);
+    for (int t = 0; t < PF; ++t) b[t] = as_bf16x8(src[2 * t + HF][lane]);
+#pragma unroll
+    for (int t = 0; t < MTP; ++t) {
+      if (t + PF < MTP) b[(t + PF) % (PF + 1)] = as_bf16x8(src[2 * (t + PF) + HF][lane]);
+#pragma unroll
+      for (int vt = 0; vt < 2; ++vt)
+        acc[vt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wr[SL][vt]),
+                                                              b[t % (PF + 1)], acc[vt][t], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
     if constexpr (HF == 1) {
-      wait_vmcnt<8>();  // this wave's x of the next step (the W of the next two half steps may stay in flight)
-      store_x(std::integral_constant<int, 1 - ST>{});
-      wait_lgkmcnt<0>();
-      __builtin_amdgcn_s_barrier();  // every wave's x of the next step is in LDS; stage ST is free
+      wait_vmcnt<WAITN>();           // this wave's x and W of the next step have landed
+      __builtin_amdgcn_s_barrier();  // and so have the other waves' x
     }
   };
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  using I4 = std::integral_constant<int, 4>;
+  using I5 = std::integral_constant<int, 5>;
+  using I6 = std::integral_constant<int, 6>;
+  using I7 = std::integral_constant<int, 7>;
   // the fused epilogue's row scales, beta, prior and query offsets: loaded first,
   // written to LDS once the prologue's loads are in flight
   float e_rho = 0.f, e_beta = 0.f, e_prior = 0.f;
   int e_qs = 0, e_qe = 0;
   if constexpr (FUSED) {
-    if (tid < a.M) e_rho = a.rho_in[tid];
-    if (tid < a.M - a.n_queries) {  // experts: every query has one amateur row
+    if (tid < M) e_rho = a.rho_in[tid];
+    if (tid < M - a.n_queries) {  // experts: every query has one amateur row
       e_beta = a.beta[tid];
       e_prior = a.prior[tid];
     }
@@ -1560,13 +1577,21 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       e_qe = a.query_exp0[tid];
     }
   }
-  // prologue: x of step 0 to LDS, W of half steps 0 and 1 in flight
-  load_x(0);
+  // prologue: the loads of half steps -7 .. -1 in the loop's order (half step h
+  // loads W(h + 7) and, at even h, x(h / 2 + 3))
   load_w(I0{}, 0);
   load_w(I1{}, 1);
+  load_x(I0{}, 0);
+  load_w(I2{}, 2);
+  load_w(I3{}, 3);
+  load_x(I1{}, 1);
+  load_w(I4{}, 4);
+  load_w(I5{}, 5);
+  load_x(I2{}, 2);
+  load_w(I6{}, 6);
   if constexpr (FUSED) {
-    if (tid < a.M) epi.rho[tid] = e_rho;
-    if (tid < a.M - a.n_queries) {  // experts: every query has one amateur row
+    if (tid < M) epi.rho[tid] = e_rho;
+    if (tid < M - a.n_queries) {
       epi.beta[tid] = e_beta;
       epi.prior[tid] = e_prior;
     }
@@ -1575,60 +1600,54 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       epi.qe[tid] = e_qe;
     }
   }
-  wait_vmcnt<8>();
-  store_x(I0{});
-  wait_lgkmcnt<0>();
+  wait_vmcnt<WAITN>();
   __builtin_amdgcn_s_barrier();
-  // W slot h % 3 and stage (h / 2) % 2 repeat every 12 half steps
-  int h = 0;
-  for (; h + 12 <= H; h += 12) {
+  // W slot h % 8 and x stage (h / 2) % 4 repeat every 8 half steps (H is a multiple of 8)
+  for (int h = 0; h < H; h += 8) {
     half(I0{}, I0{}, I0{}, h);
     half(I1{}, I0{}, I1{}, h + 1);
     half(I2{}, I1{}, I0{}, h + 2);
-    half(I0{}, I1{}, I1{}, h + 3);
-    half(I1{}, I0{}, I0{}, h + 4);
-    half(I2{}, I0{}, I1{}, h + 5);
-    half(I0{}, I1{}, I0{}, h + 6);
-    half(I1{}, I1{}, I1{}, h + 7);
-    half(I2{}, I0{}, I0{}, h + 8);
-    half(I0{}, I0{}, I1{}, h + 9);
-    half(I1{}, I1{}, I0{}, h + 10);
-    half(I2{}, I1{}, I1{}, h + 11);
+    half(I3{}, I1{}, I1{}, h + 3);
+    half(I4{}, I2{}, I0{}, h + 4);
+    half(I5{}, I2{}, I1{}, h + 5);
+    half(I6{}, I3{}, I0{}, h + 6);
+    half(I7{}, I3{}, I1{}, h + 7);
   }
-  // the remaining H % 12 half steps, whole steps (uniform branches)
-  if (h < H) { half(I0{}, I0{}, I0{}, h); half(I1{}, I0{}, I1{}, h + 1); }
-  if (h + 2 < H) { half(I2{}, I1{}, I0{}, h + 2); half(I0{}, I1{}, I1{}, h + 3); }
-  if (h + 4 < H) { half(I1{}, I0{}, I0{}, h + 4); half(I2{}, I0{}, I1{}, h + 5); }
-  if (h + 6 < H) { half(I0{}, I1{}, I0{}, h + 6); half(I1{}, I1{}, I1{}, h + 7); }
-  if (h + 8 < H) { half(I2{}, I0{}, I0{}, h + 8); half(I0{}, I0{}, I1{}, h + 9); }
-  wait_vmcnt<0>();  // the ring's loads past the end have landed
-  const int M = a.M;
+  wait_vmcnt<0>();  // the loads past the end (some into LDS) have landed
   if constexpr (FUSED) {
-    // two halves of 128 columns: waves 4h .. 4h + 3 (vocab groups 2h, 2h + 1) write
-    // their tiles (rows x 128 floats over the four stages, float4 groups
-    // XOR-swizzled by row against bank conflicts), then all waves fuse; one
+    // two halves of 128 columns: waves 4h .. 4h + 3 write their 32 columns each,
+    // column-major into stage (wave % 4) (column c of a stage at c * 16 MTP, rows
+    // XOR-swizzled by column against bank conflicts), then all waves fuse; one
     // query per group of tpq lanes (64 lanes per query up to 8 queries, 2 at 144)
-    constexpr int NC = 128;
-    static_assert(4 * 2 * MTP * 64 * 16 >= 16 * MTP * NC * 4, "the stages hold every tile row");
-    float* tile = (float*)&xsb[0][0][0];
-    auto at = [&](int m, int j) { return tile[m * NC + ((((j >> 2) ^ (m & 31)) << 2) | (j & 3))]; };
+    constexpr int NC = 128, RS = 16 * MTP;
+    static_assert(XU * 64 * 16 == 32 * RS * 4, "a stage holds 32 columns of every row");
+    auto col_base = [&](int j) -> float* {  // column j of the half
+      const int q = j >> 5;
+      float* base = q == 0 ? (float*)&xs0[0][0] : q == 1 ? (float*)&xs1[0][0] : q == 2 ? (float*)&xs2[0][0]
+                                                                                   : (float*)&xs3[0][0];
+      return base + (j & 31) * RS;
+    };
+    auto at = [&](int m, int j) { return col_base(j)[m ^ (j & 31)]; };
     int tpq = 64;
     while (tpq > 2 && (512 / tpq) < a.n_queries) tpq >>= 1;
     __syncthreads();  // every wave is done with the x stages
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       if ((wave >> 2) == h) {
+        float* colw = col_base(32 * (wave & 3));  // this wave's 32 columns
 #pragma unroll
-        for (int t = 0; t < MTH; ++t) {
-          const int m = 16 * (rh * MTH + t) + col;
+        for (int t = 0; t < MTP; ++t) {
+          const int m = 16 * t + col;
           if (m >= M) continue;
           const float rho = epi.rho[m];
-          float* row = tile + m * NC;
 #pragma unroll
-          for (int vt = 0; vt < 4; ++vt) {
+          for (int vt = 0; vt < 2; ++vt) {
             const f32x4 cc = acc[vt][t];
-            const int c4 = 16 * (grp & 1) + 4 * vt + quad;
-            *(float4*)(row + ((c4 ^ (m & 31)) << 2)) = make_float4(cc[0] * rho, cc[1] * rho, cc[2] * rho, cc[3] * rho);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int jl = 16 * vt + 4 * quad + r;  // column within the wave's 32
+              colw[jl * RS + (m ^ jl)] = cc[r] * rho;
+            }
           }
         }
       }
@@ -1640,12 +1659,12 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     return;
   }
 #pragma unroll
-  for (int t = 0; t < MTH; ++t) {
-    const int m = 16 * (rh * MTH + t) + col;
+  for (int t = 0; t < MTP; ++t) {
+    const int m = 16 * t + col;
     if (m >= M) continue;
     const float rho = a.rho_in[m];
 #pragma unroll
-    for (int vt = 0; vt < 4; ++vt) {
+    for (int vt = 0; vt < 2; ++vt) {
       if (vb0 + vt >= nvb) continue;
       const int v = 16 * (vb0 + vt) + 4 * quad;
       float* out = a.logits + (size_t)m * a.V + v;

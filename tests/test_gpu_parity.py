@@ -84,8 +84,9 @@ def test_bf16_llama_heads_fixed_beta_shuffled_pages():
 
 def test_lmhead_stage_bf16_and_tails():
     from paper_2601_08670_amd.session import PcedSession
-    # 1..48 rows: one pass; 49..288: W streamed once for all rows (tiles interleaved over
-    # two waves, 128-wide hidden stages); beyond: 48-row groups sharing W through L2
+    # 1..48 rows: one pass; 49..288: W streamed once for all rows (each wave two vocab
+    # tiles over every row tile, x staged in LDS by direct loads); beyond: 48-row
+    # groups sharing W through L2
     for (M, V, hidden) in [(1, 1000, 256), (33, 4104, 512), (50, 1003, 256), (101, 2048, 4096),
                            (272, 1000, 768), (288, 515, 256), (300, 515, 256), (17, 300, 768)]:
         hq = hidden // 64
