@@ -1503,6 +1503,9 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const uint32_t lane16 = 16u * lane;
   const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, 0x7FFFFFFF, 0x00020000);
   constexpr uint32_t x_ks = XU * 1024u;  // bytes of one 64-wide step of the packed x
+  // W is read once per launch: its loads carry the non-temporal hint (cache
+  // policy bit 1, "nt" on gfx950) so they stream through the caches
+  constexpr int kNt = 2;
   u32x4 wr[WR][2];
   auto load_w = [&](auto slot_c, int h) __attribute__((always_inline)) {
     constexpr int SL = decltype(slot_c)::value;
@@ -1510,7 +1513,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const uint32_t so = (uint32_t)(h >> 1) * w_ks + (uint32_t)(h & 1) * 1024u;
 #pragma unroll
     for (int vt = 0; vt < 2; ++vt)
-      wr[SL][vt] = __builtin_amdgcn_raw_buffer_load_b128(wrs, lane16, so + w_t[vt], 0);
+      wr[SL][vt] = __builtin_amdgcn_raw_buffer_load_b128(wrs, lane16, so + w_t[vt], kNt);
   };
   auto stage = [&](auto st_c) __attribute__((always_inline)) -> uint4(*)[64] {
     constexpr int ST = decltype(st_c)::value;
