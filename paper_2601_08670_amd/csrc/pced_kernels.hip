@@ -19,6 +19,7 @@
 
 #include <mutex>
 #include <type_traits>
+#include <utility>
 
 #include "pced_internal.h"
 
@@ -1424,6 +1425,16 @@ __global__ __launch_bounds__(256) void k_pack_x(const uint16_t* __restrict__ x, 
   if (lane == 0 && m < M) rho[m] = rms ? 1.0f / sqrtf(ss / (float)K + 1e-5f) : 1.0f;
 }
 
+// Compile-time loop: f(integral_constant<int, i>) for i = 0 .. N-1, in order.
+template <typename F, size_t... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::index_sequence<I...>) {
+  (f(std::integral_constant<int, (int)I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_index_sequence<N>{});
+}
+
 // The many-row LM head's wait at the end of step s: vector loads retire in
 // order, and half step h (relative to 2s) issues W(2s + h + lead) and then, at
 // even h, x(s + h/2 + xl) (xb loads). Step s + 1 needs x(s + 1) and
@@ -1441,7 +1452,9 @@ constexpr int lmhead_wide_wait(int lead, int xl, int xb, int w) {
   for (int h = from; h <= 1; ++h) n += w + ((h % 2 == 0) ? xb : 0);
   return n;
 }
-static_assert(lmhead_wide_wait(7, 3, 5, 2) == 20 && lmhead_wide_wait(3, 3, 5, 4) == 9, "wait counts");
+static_assert(lmhead_wide_wait(7, 3, 5, 2) == 20 && lmhead_wide_wait(3, 3, 5, 4) == 9 &&
+                  lmhead_wide_wait(15, 7, 2, 2) == 38,
+              "wait counts");
 
 // LM head for 49..288 rows with W read once: logits[m][v] = rho_m sum_k x[m][k] W[v][k]
 // (x packed by k_pack_x, rho precomputed) on the matrix cores,
@@ -1451,16 +1464,17 @@ static_assert(lmhead_wide_wait(7, 3, 5, 2) == 20 && lmhead_wide_wait(3, 3, 5, 4)
 // tiles of x (acc: 2 x MTP x 4 registers), so every W byte is loaded by exactly
 // one wave. The products are cheap next to the weight stream, which they must
 // hide, so both operands are fetched far ahead. The hidden dimension is walked
-// in 32-wide half steps h:
-//   - W of half step h + 7 goes into slot (h + 7) % 8 of an 8-slot register
+// in 32-wide half steps h, with NS = 4 LDS stages of x (8 when x has at most
+// 128 rows, its stages then being small) and a W ring of WR = 2 NS slots:
+//   - W of half step h + WR - 1 goes into slot (h + WR - 1) % WR of a register
 //     ring (two tiles, 8 registers a slot);
-//   - at even h the packed x of 64-wide step h/2 + 3 goes from memory straight
-//     into LDS stage (h/2 + 3) % 4 (buffer loads with the LDS flag, no
-//     registers), the eight waves loading an eighth of its 1 KiB operands
-//     each; x is fetched as far ahead as W because vector loads retire in
-//     order, so waiting for an x issued after a W waits for that W too;
-//   - the 2 x MTP products of h read their B operands from LDS stage (h/2) % 4,
-//     three tiles ahead of their use, each feeding two products;
+//   - at even h the packed x of 64-wide step h/2 + NS - 1 goes from memory
+//     straight into LDS stage (h/2 + NS - 1) % NS (buffer loads with the LDS
+//     flag, no registers), the eight waves loading an eighth of its 1 KiB
+//     operands each; x is fetched as far ahead as W because vector loads
+//     retire in order, so waiting for an x issued after a W waits for that W;
+//   - the 2 x MTP products of h read their B operands from LDS stage
+//     (h/2) % NS, three tiles ahead of their use, each feeding two products;
 //   - at odd h the wave waits until its loads of the next step's x and W have
 //     landed, leaving every later load in flight, and meets the other waves
 //     at a barrier, after which the next stage holds every wave's loads.
@@ -1469,22 +1483,29 @@ static_assert(lmhead_wide_wait(7, 3, 5, 2) == 20 && lmhead_wide_wait(3, 3, 5, 4)
 // the slice argmax in the epilogue, in two halves of 128 columns through the
 // (then free) LDS stages, with the row scales, beta, prior and query offsets
 // staged in LDS at the start.
-template <int MTH, bool FUSED>
+template <int MTH, int NS, bool FUSED>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_lmhead_wide_bf16(LmArgs a) {
+  static_assert(NS == 4 || NS == 8, "x stages");
   constexpr int MTP = 2 * MTH;           // 16-row tiles of the packed x
   constexpr int XU = 2 * MTP;            // 1 KiB B operands of one x stage (tiles x 2 halves)
   constexpr int XB = (XU + 7) / 8;       // of which each wave loads (the last one twice over if XU % 8 != 0)
-  constexpr int WR = 8, LEAD = WR - 1;   // W ring slots; half steps of W in flight
-  constexpr int XL = 3;                  // 64-wide steps of x in flight
+  constexpr int WR = 2 * NS, LEAD = WR - 1;  // W ring slots; half steps of W in flight
+  constexpr int XL = NS - 1;             // 64-wide steps of x in flight
   constexpr int PF = 3;                  // B operands read from LDS ahead of their products
+  constexpr int PERIOD = 2 * NS;         // half steps after which slots and stages repeat (H is a multiple)
   constexpr int WAITN = lmhead_wide_wait(LEAD, XL, XB, 2);
   static_assert(WAITN < 64, "vmcnt has 6 bits");
-  // four separate stage arrays, so that the compiler can tell a stage being
-  // loaded into LDS from the one being read
+  // separate stage arrays, so that the compiler can tell a stage being loaded
+  // into LDS from the one being read (stages 4 .. 7 only with NS = 8)
+  constexpr int XU8 = NS == 8 ? XU : 1;
   __shared__ __align__(16) uint4 xs0[XU][64];
   __shared__ __align__(16) uint4 xs1[XU][64];
   __shared__ __align__(16) uint4 xs2[XU][64];
   __shared__ __align__(16) uint4 xs3[XU][64];
+  __shared__ __align__(16) uint4 xs4[XU8][64];
+  __shared__ __align__(16) uint4 xs5[XU8][64];
+  __shared__ __align__(16) uint4 xs6[XU8][64];
+  __shared__ __align__(16) uint4 xs7[XU8][64];
   __shared__ WideEpi<FUSED> epi;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1517,7 +1538,11 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   };
   auto stage = [&](auto st_c) __attribute__((always_inline)) -> uint4(*)[64] {
     constexpr int ST = decltype(st_c)::value;
-    return ST == 0 ? xs0 : ST == 1 ? xs1 : ST == 2 ? xs2 : xs3;
+    if constexpr (ST < 4) {
+      return ST == 0 ? xs0 : ST == 1 ? xs1 : ST == 2 ? xs2 : xs3;
+    } else {
+      return ST == 4 ? xs4 : ST == 5 ? xs5 : ST == 6 ? xs6 : xs7;
+    }
   };
   auto load_x = [&](auto st_c, int ks) __attribute__((always_inline)) {
     uint4(*dst)[64] = stage(st_c);
@@ -1537,7 +1562,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   auto half = [&](auto slot_c, auto st_c, auto hf_c, int h) __attribute__((always_inline)) {
     constexpr int SL = decltype(slot_c)::value, ST = decltype(st_c)::value, HF = decltype(hf_c)::value;
     load_w(std::integral_constant<int, (SL + LEAD) % WR>{}, h + LEAD);
-    if constexpr (HF == 0) load_x(std::integral_constant<int, (ST + XL) % 4>{}, (h >> 1) + XL);
+    if constexpr (HF == 0) load_x(std::integral_constant<int, (ST + XL) % NS>{}, (h >> 1) + XL);
     __builtin_amdgcn_sched_barrier(0);  // this half step's loads go out before its products
     uint4(*src)[64] = stage(st_c);
     bf16x8 b[PF + 1];
@@ -1557,14 +1582,6 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       __builtin_amdgcn_s_barrier();  // and so have the other waves' x
     }
   };
-  using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  using I3 = std::integral_constant<int, 3>;
-  using I4 = std::integral_constant<int, 4>;
-  using I5 = std::integral_constant<int, 5>;
-  using I6 = std::integral_constant<int, 6>;
-  using I7 = std::integral_constant<int, 7>;
   // the fused epilogue's row scales, beta, prior and query offsets: loaded first,
   // written to LDS once the prologue's loads are in flight
   float e_rho = 0.f, e_beta = 0.f, e_prior = 0.f;
@@ -1580,18 +1597,15 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       e_qe = a.query_exp0[tid];
     }
   }
-  // prologue: the loads of half steps -7 .. -1 in the loop's order (half step h
-  // loads W(h + 7) and, at even h, x(h / 2 + 3))
-  load_w(I0{}, 0);
-  load_w(I1{}, 1);
-  load_x(I0{}, 0);
-  load_w(I2{}, 2);
-  load_w(I3{}, 3);
-  load_x(I1{}, 1);
-  load_w(I4{}, 4);
-  load_w(I5{}, 5);
-  load_x(I2{}, 2);
-  load_w(I6{}, 6);
+  // prologue: the loads of half steps -LEAD .. -1 in the loop's order (half step
+  // h loads W(h + LEAD) and, at even h, x(h / 2 + XL); LEAD = 2 XL + 1)
+  static_assert(LEAD == 2 * XL + 1, "W and x leads");
+  static_for<LEAD>([&](auto ic) __attribute__((always_inline)) {
+    constexpr int h = (int)decltype(ic)::value - LEAD;
+    if constexpr (h + LEAD >= 0) load_w(std::integral_constant<int, (h + LEAD) % WR>{}, h + LEAD);
+    if constexpr ((h & 1) == 0 && h / 2 + XL >= 0)
+      load_x(std::integral_constant<int, (h / 2 + XL) % NS>{}, h / 2 + XL);
+  });
   if constexpr (FUSED) {
     if (tid < M) epi.rho[tid] = e_rho;
     if (tid < M - a.n_queries) {
@@ -1605,16 +1619,13 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   }
   wait_vmcnt<WAITN>();
   __builtin_amdgcn_s_barrier();
-  // W slot h % 8 and x stage (h / 2) % 4 repeat every 8 half steps (H is a multiple of 8)
-  for (int h = 0; h < H; h += 8) {
-    half(I0{}, I0{}, I0{}, h);
-    half(I1{}, I0{}, I1{}, h + 1);
-    half(I2{}, I1{}, I0{}, h + 2);
-    half(I3{}, I1{}, I1{}, h + 3);
-    half(I4{}, I2{}, I0{}, h + 4);
-    half(I5{}, I2{}, I1{}, h + 5);
-    half(I6{}, I3{}, I0{}, h + 6);
-    half(I7{}, I3{}, I1{}, h + 7);
+  // W slot h % WR and x stage (h / 2) % NS repeat every PERIOD half steps
+  for (int h = 0; h < H; h += PERIOD) {
+    static_for<PERIOD>([&](auto jc) __attribute__((always_inline)) {
+      constexpr int j = decltype(jc)::value;
+      half(std::integral_constant<int, j % WR>{}, std::integral_constant<int, (j / 2) % NS>{},
+           std::integral_constant<int, j % 2>{}, h + j);
+    });
   }
   wait_vmcnt<0>();  // the loads past the end (some into LDS) have landed
   if constexpr (FUSED) {
@@ -2669,11 +2680,16 @@ hipError_t launch_lmhead(const LmArgs& a0, bool bf16, hipStream_t st, const Timi
       if (!a.rho_in) a.rho_in = a.rho_buf;
       a.x = a.x_packed;
       const dim3 g((nvb + 15) / 16), b(512);
-#define PCED_WIDE(MT)                                                                                        \
-  if (mtk == MT)                                                                                             \
-    return fused ? go(k_lmhead_wide_bf16<MT, true>, g, b, 0, st, nullptr, t1(tm), a)                         \
-                 : go(k_lmhead_wide_bf16<MT, false>, g, b, 0, st, nullptr, t1(tm), a);
-      PCED_WIDE(4) PCED_WIDE(6) PCED_WIDE(9)
+      // up to 128 rows the x stages are small enough for eight of them (and a
+      // 16-slot W ring), when the hidden size is a multiple of 8 steps
+      const bool deep = mtk == 4 && a.K % 512 == 0;
+#define PCED_WIDE(MT, NS)                                                                                    \
+  return fused ? go(k_lmhead_wide_bf16<MT, NS, true>, g, b, 0, st, nullptr, t1(tm), a)                       \
+               : go(k_lmhead_wide_bf16<MT, NS, false>, g, b, 0, st, nullptr, t1(tm), a);
+      if (deep) PCED_WIDE(4, 8)
+      if (mtk == 4) PCED_WIDE(4, 4)
+      if (mtk == 6) PCED_WIDE(6, 4)
+      if (mtk == 9) PCED_WIDE(9, 4)
 #undef PCED_WIDE
     }
     if (a.M > kLmRowsPad && a.M <= 32 * kLmRowsMTW) {  // many rows: W streamed once for all of them
