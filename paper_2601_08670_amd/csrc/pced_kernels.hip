@@ -1021,6 +1021,70 @@ __device__ void fuse_tile_groups(const LmArgs& a, int v0, int blk, At at, int tp
   }
 }
 
+// The same for at most NW / 2 queries, so that no wave idles: wq waves per
+// query (8, 4 or 2 for 1, 2 or up to 4 queries), one thread per column of the
+// NC = 128; with more threads than columns, es = wq / 2 adjacent lanes share a
+// column, lane s of them taking experts s + 1, s + 1 + es, ..., and they merge
+// (score, expert) keeping the lower expert on equal scores, which is what the
+// sequential scan over the experts keeps. A wave merges its columns with
+// shuffles, a query's waves merge through LDS. Every thread of the block calls
+// this (it has a block barrier).
+template <int NW, int NC, typename At>
+__device__ void fuse_tile_waves(const LmArgs& a, int v0, int blk, At at, int wq, const int* qs, const int* qe,
+                                const float* cb, const float* pr) {
+#pragma clang fp contract(off)
+  static_assert(NW == 8 && NC == 128, "two waves cover the columns");
+  __shared__ Top2 red[NW];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int es = wq / 2, b = wave / wq, wi = wave % wq;
+  const int s = lane % es, j = (64 * wi + lane) / es;
+  Top2 cand{kNegInf, 0x7FFFFFFF, 0, kNegInf, 0x7FFFFFFF};
+  if (b < a.n_queries) {  // wave-uniform
+    const int s0 = qs[b];
+    const int N = qs[b + 1] - s0 - 1;
+    const int e0 = qe[b];
+    const int v = v0 + j;
+    float best = kNegInf;
+    int bk = 0;
+    if (v < a.V) {
+      const float sa = at(s0, j);
+      for (int kb = 1 + s; kb <= N; kb += 8 * es) {
+        float x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = (kb + u * es <= N) ? at(s0 + kb + u * es, j) : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int k = kb + u * es;
+          if (k > N) continue;
+          const float beta = cb[e0 + k - 1];
+          const float coef = 1.0f + beta;
+          const float t1 = coef * x[u];
+          const float t2 = beta * sa;
+          const float val = (t1 - t2) + pr[e0 + k - 1];
+          if (val > best) { best = val; bk = k; }
+        }
+      }
+    }
+    for (int o = 1; o < es; o <<= 1) {
+      const float ob = __shfl_xor(best, o);
+      const int ok = __shfl_xor(bk, o);
+      if (ob > best || (ob == best && ok < bk)) { best = ob; bk = ok; }
+    }
+    if (s == 0 && v < a.V) cand = Top2{best, v, bk, kNegInf, 0x7FFFFFFF};
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) cand = merge(cand, shfl_top2(cand, o));
+  if (lane == 0) red[wave] = cand;
+  __syncthreads();
+  if (wi == 0 && lane == 0 && b < a.n_queries) {
+    Top2 r = red[wave];
+    for (int i = 1; i < wq; ++i) r = merge(r, red[wave + i]);
+    float* p = a.fuse_part + ((size_t)b * a.fuse_nblk + blk) * 5;
+    p[0] = r.v1; p[1] = __int_as_float(r.i1); p[2] = __int_as_float(r.k1);
+    p[3] = r.v2; p[4] = __int_as_float(r.i2);
+  }
+}
+
 // What the many-row LM head's fused epilogue reads besides its tile, staged in
 // LDS at the start of the launch (an empty struct without the epilogue).
 template <bool FUSED>
@@ -1642,8 +1706,11 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       return base + (j & 31) * RS;
     };
     auto at = [&](int m, int j) { return col_base(j)[m ^ (j & 31)]; };
+    // lanes per query (more than 4 queries), or waves per query (up to 4)
     int tpq = 64;
     while (tpq > 2 && (512 / tpq) < a.n_queries) tpq >>= 1;
+    int wq = 8;
+    while (wq > 2 && wq * a.n_queries > 8) wq >>= 1;
     __syncthreads();  // every wave is done with the x stages
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -1666,8 +1733,12 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         }
       }
       __syncthreads();
-      fuse_tile_groups<8, NC>(a, blockIdx.x * 256 + NC * h, 2 * blockIdx.x + h, at, tpq, epi.qs, epi.qe, epi.beta,
-                              epi.prior);
+      if (a.n_queries <= 4)
+        fuse_tile_waves<8, NC>(a, blockIdx.x * 256 + NC * h, 2 * blockIdx.x + h, at, wq, epi.qs, epi.qe, epi.beta,
+                               epi.prior);
+      else
+        fuse_tile_groups<8, NC>(a, blockIdx.x * 256 + NC * h, 2 * blockIdx.x + h, at, tpq, epi.qs, epi.qe,
+                                epi.beta, epi.prior);
       if (h == 0) __syncthreads();  // before the second half's tile overwrites the first
     }
     return;

@@ -352,6 +352,12 @@ FUSED = [
      [1, 5, 2, 9, 3, 1, 7, 4, 2, 6, 3, 1], list(range(3, 179, 4)), 5, 2, "fixed"),
     ("many-row-40-queries-dynamic-beta", W.Geometry(1, 4, 2, 64, 256, 1000, "bf16"),
      [1] * 20 + [2] * 20, [5 + (7 * i) % 90 for i in range(60)], 3, 2, None),
+    # at most 4 queries in the many-row kernel: several waves per query, lanes
+    # sharing a column split its experts (4 ways for one query, 2 for two)
+    ("many-row-1-query-dynamic-beta", W.Geometry(1, 8, 2, 64, 512, 1003, "bf16"), [61],
+     [3 + (11 * i) % 150 for i in range(61)], 9, 2, None),
+    ("many-row-2-queries-fixed-beta", W.Geometry(1, 4, 2, 64, 256, 1000, "bf16"), [27, 33],
+     [4 + (5 * i) % 70 for i in range(60)], 6, 2, "fixed"),
 ]
 
 
