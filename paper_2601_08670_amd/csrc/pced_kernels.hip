@@ -1965,16 +1965,46 @@ __device__ float block_reduce_sum(float v) {
   return r;
 }
 
-// Per (row, vocab chunk): chunk max M_c and sum exp(s - M_c).
+constexpr float kLog2E = 1.44269504088896341f;
+static_assert(kBetaChunk % 1024 == 0, "whole 16-byte loads per thread");
+
+// A thread's kBetaChunk / 256 values of a chunk [v0, v1) of a logits row, in
+// registers (16-byte loads when rows are 16-byte aligned); -inf past v1.
+__device__ __forceinline__ void beta_chunk_values(const float* row, int V, int v0, int v1,
+                                                  float (&x)[kBetaChunk / 256]) {
+  constexpr int PER = kBetaChunk / 256;
+  if ((V & 3) == 0) {
+#pragma unroll
+    for (int i = 0; i < PER / 4; ++i) {
+      const int v = v0 + 4 * (threadIdx.x + 256 * i);
+      float4 t = make_float4(kNegInf, kNegInf, kNegInf, kNegInf);
+      if (v < v1) t = *(const float4*)(row + v);
+      x[4 * i] = t.x; x[4 * i + 1] = t.y; x[4 * i + 2] = t.z; x[4 * i + 3] = t.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int v = v0 + threadIdx.x + 256 * i;
+      x[i] = v < v1 ? row[v] : kNegInf;
+    }
+  }
+}
+
+// Per (row, vocab chunk): chunk max M_c and sum 2^((s - M_c) log2 e), in one
+// pass (the block's values stay in registers between the two reductions).
 __global__ __launch_bounds__(256) void k_beta_lse(BetaArgs a) {
+  constexpr int PER = kBetaChunk / 256;
   const int s = blockIdx.y, ch = blockIdx.x;
-  const float* row = a.logits + (size_t)s * a.V;
   const int v0 = ch * kBetaChunk, v1 = min(a.V, v0 + kBetaChunk);
+  float x[PER];
+  beta_chunk_values(a.logits + (size_t)s * a.V, a.V, v0, v1, x);
   float m = kNegInf;
-  for (int v = v0 + threadIdx.x; v < v1; v += blockDim.x) m = fmaxf(m, row[v]);
+#pragma unroll
+  for (int i = 0; i < PER; ++i) m = fmaxf(m, x[i]);
   m = block_reduce_max(m);
   float sum = 0.f;
-  for (int v = v0 + threadIdx.x; v < v1; v += blockDim.x) sum += expf(row[v] - m);
+#pragma unroll
+  for (int i = 0; i < PER; ++i) sum += x[i] == kNegInf ? 0.f : __builtin_amdgcn_exp2f((x[i] - m) * kLog2E);
   sum = block_reduce_sum(sum);
   if (threadIdx.x == 0) {
     a.lse_part[((size_t)s * a.nchunk + ch) * 2] = m;
@@ -1982,46 +2012,71 @@ __global__ __launch_bounds__(256) void k_beta_lse(BetaArgs a) {
   }
 }
 
-__device__ __forceinline__ float row_lse(const BetaArgs& a, int s) {
+// Base-2 log-sum-exp of a row from its chunk partials, by one wave (lanes over
+// chunks, then shuffles); every lane returns it.
+__device__ __forceinline__ float wave_row_lse2(const BetaArgs& a, int s) {
   const float* p = a.lse_part + (size_t)s * a.nchunk * 2;
+  const int lane = threadIdx.x & 63;
   float m = kNegInf;
-  for (int c = 0; c < a.nchunk; ++c) m = fmaxf(m, p[2 * c]);
+  for (int c = lane; c < a.nchunk; c += 64) m = fmaxf(m, p[2 * c]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
   float sum = 0.f;
-  for (int c = 0; c < a.nchunk; ++c) sum += p[2 * c + 1] * expf(p[2 * c] - m);
-  return m + logf(sum);
+  for (int c = lane; c < a.nchunk; c += 64) sum += p[2 * c + 1] * __builtin_amdgcn_exp2f((p[2 * c] - m) * kLog2E);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+  return m * kLog2E + __builtin_amdgcn_logf(sum);
 }
 
 // beta_k = JSD(p_k || p_0) in bits (first step, dynamic mode; Section 3 reads
-// beta from AdaCAD's with-context vs no-context divergence). Per (expert, chunk)
-// partial sums of 1/2 p (ln p - ln m) + 1/2 q (ln q - ln m), m = (p + q) / 2,
-// with ln m = max(ln p, ln q) + log1p(exp(-|ln p - ln q|)) - ln 2.
+// beta from AdaCAD's with-context vs no-context divergence). Per (expert,
+// chunk) partial sums. With base-2 log-probabilities lp, lq, d = lp - lq,
+// hi = max(lp, lq), t = 2^-|d| and g = log2(1 + t), the mixture m = (p + q) / 2
+// has log2 m = hi + g - 1, so the larger probability 2^hi contributes
+// 2^hi (1 - g) / 2 and the smaller 2^hi t (1 - |d| - g) / 2: no difference of
+// two large logarithms is formed.
 __global__ __launch_bounds__(256) void k_beta_jsd(BetaArgs a) {
+  constexpr int PER = kBetaChunk / 256;
   const int e = blockIdx.y, ch = blockIdx.x;
   const int sk = a.exp_seq[e];
   const int s0 = a.query_seq0[a.exp_query[e]];
-  const float lk = row_lse(a, sk), l0 = row_lse(a, s0);
-  const float* rk = a.logits + (size_t)sk * a.V;
-  const float* r0 = a.logits + (size_t)s0 * a.V;
   const int v0 = ch * kBetaChunk, v1 = min(a.V, v0 + kBetaChunk);
-  const float ln2 = 0.69314718055994530942f;
+  float xk[PER], x0[PER];
+  beta_chunk_values(a.logits + (size_t)sk * a.V, a.V, v0, v1, xk);
+  beta_chunk_values(a.logits + (size_t)s0 * a.V, a.V, v0, v1, x0);
+  __shared__ float lse2[2];
+  if (threadIdx.x < 64) {
+    const float lk = wave_row_lse2(a, sk), l0 = wave_row_lse2(a, s0);
+    if (threadIdx.x == 0) {
+      lse2[0] = lk;
+      lse2[1] = l0;
+    }
+  }
+  __syncthreads();
+  const float lk = lse2[0], l0 = lse2[1];
   float acc = 0.f;
-  for (int v = v0 + threadIdx.x; v < v1; v += blockDim.x) {
-    const float lp = rk[v] - lk, lq = r0[v] - l0;
-    const float p = expf(lp), q = expf(lq);
-    const float lm = fmaxf(lp, lq) + log1pf(expf(-fabsf(lp - lq))) - ln2;
-    acc += 0.5f * (p * (lp - lm) + q * (lq - lm));
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    if (x0[i] == kNegInf) continue;  // past the chunk's end
+    const float lp = xk[i] * kLog2E - lk, lq = x0[i] * kLog2E - l0;
+    const float ad = fabsf(lp - lq), hi = fmaxf(lp, lq);
+    const float t = __builtin_amdgcn_exp2f(-ad);
+    const float g = __builtin_amdgcn_logf(1.0f + t);
+    acc += 0.5f * __builtin_amdgcn_exp2f(hi) * ((1.0f - g) + t * ((1.0f - ad) - g));
   }
   acc = block_reduce_sum(acc);
   if (threadIdx.x == 0) a.jsd_part[(size_t)e * a.nchunk + ch] = acc;
 }
 
-// beta_k = (sum of expert k's chunk partials, in chunk order) / ln 2.
-__global__ __launch_bounds__(256) void k_beta_final(BetaArgs a, int n_exp) {
-  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+// beta_k = sum of expert k's chunk partials (bits): one wave per expert.
+__global__ __launch_bounds__(64) void k_beta_final(BetaArgs a, int n_exp) {
+  const int e = blockIdx.x;
   if (e >= n_exp) return;
   float tot = 0.f;
-  for (int c = 0; c < a.nchunk; ++c) tot += a.jsd_part[(size_t)e * a.nchunk + c];
-  a.beta[e] = tot / 0.69314718055994530942f;
+  for (int c = threadIdx.x; c < a.nchunk; c += 64) tot += a.jsd_part[(size_t)e * a.nchunk + c];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) tot += __shfl_xor(tot, o);
+  if (threadIdx.x == 0) a.beta[e] = tot;
 }
 
 // Scalar beta (one per query): the mean of the query's per-expert divergences,
@@ -2794,7 +2849,7 @@ hipError_t launch_beta(const BetaArgs& a, int n_seqs, int n_exp, hipStream_t st,
   if (e != hipSuccess) return e;
   e = go(k_beta_jsd, dim3(a.nchunk, n_exp), dim3(256), 0, st, nullptr, nullptr, a);
   if (e != hipSuccess) return e;
-  return go(k_beta_final, dim3((n_exp + 255) / 256), dim3(256), 0, st, nullptr, t1(tm), a, n_exp);
+  return go(k_beta_final, dim3(n_exp), dim3(64), 0, st, nullptr, t1(tm), a, n_exp);
 }
 
 int fuse_slice(int V, int n_queries, int num_cus) {
