@@ -518,6 +518,7 @@ pced_status run_lmhead(pced_ctx* c, const void* x, int M, const void* w, float* 
     a.query_exp0 = c->at<int32_t>(c->lay.query_exp0);
     a.beta = c->at<float>(c->lay.beta);
     a.prior = c->at<float>(c->lay.prior);
+    a.exp_seq = c->at<int32_t>(c->lay.exp_seq);
     a.fuse_part = c->at<float>(c->lay.fuse_part);
     a.n_queries = c->B;
     a.fuse_nblk = fuse_nblk;

@@ -114,6 +114,7 @@ struct LmArgs {
   const int32_t* query_exp0;// [B+1]
   const float* beta;        // [sum N]
   const float* prior;       // [sum N]
+  const int32_t* exp_seq;   // [sum N] row of each expert (the many-row kernel stages beta and prior by row)
   float* fuse_part;
   int n_queries, fuse_nblk;
   const float* rho_in;      // optional [M] row scales used instead of rms (bf16 kernels)

@@ -902,12 +902,14 @@ __device__ Top2 block_top2(Top2 c) {
 // head's fused epilogue). The NC columns are vocabulary ids v0 .. v0+NC-1; row m
 // of column j is read through at(m, j). The block's NW waves form groups of NC
 // threads, one column per thread, and the groups take the queries in turn; the
-// experts' scores are read eight at a time so their LDS latencies overlap. The
+// experts' scores are read eight at a time so their LDS latencies overlap
+// (rows past the query's last are read too, clamped to the tile's last row
+// max_row, and not used: unconditional reads issue back to back). The
 // arithmetic is k_fuse's, in the same order and without contraction, so the
 // result is bit-identical to materialising the logits and fusing them
 // afterwards. Writes fuse_part[b][blk] for every query b.
 template <int NW, int NC, typename At>
-__device__ void fuse_tile(const LmArgs& a, int v0, int blk, At at) {
+__device__ void fuse_tile(const LmArgs& a, int v0, int blk, At at, int max_row) {
 #pragma clang fp contract(off)
   constexpr int NG = 64 * NW / NC;  // thread groups (queries in flight)
   constexpr int WG = NC / 64;       // waves per group
@@ -937,17 +939,17 @@ __device__ void fuse_tile(const LmArgs& a, int v0, int blk, At at) {
       for (int kb = 1; kb <= N; kb += 8) {
         float x[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) x[u] = (kb + u <= N) ? at(s0 + kb + u, j) : 0.f;
+        for (int u = 0; u < 8; ++u) x[u] = at(min(s0 + kb + u, max_row), j);
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-          const int k = kb + u;
-          if (k > N) continue;
-          const float beta = cb[e0 + k - 1];
+          // past the query's last expert: an in-bounds entry, the result unused
+          const int k = kb + u, ei = min(e0 + k - 1, 32 * kLmRowsMTW - 1);
+          const float beta = cb[ei];
           const float coef = 1.0f + beta;
           const float t1 = coef * x[u];
           const float t2 = beta * sa;
-          const float val = (t1 - t2) + pr[e0 + k - 1];
-          if (val > best) { best = val; bk = k; }
+          const float val = (t1 - t2) + pr[ei];
+          if (k <= N && val > best) { best = val; bk = k; }
         }
       }
       c.v1 = best; c.i1 = v; c.k1 = bk;
@@ -968,132 +970,45 @@ __device__ void fuse_tile(const LmArgs& a, int v0, int blk, At at) {
   }
 }
 
-// Eq. 2 and the best two tokens per query over a block's logits tile (the
-// many-row LM head's fused epilogue), with the queries' row and expert offsets
-// (qs, qe), beta (cb) and prior (pr) already in LDS: the block's threads form
-// groups of tpq lanes inside a wave (tpq a power of two, 2..64), one query per
-// group at a time; a lane takes every tpq-th of the NC columns (vocabulary ids
-// v0 + j, row m of column j read through at(m, j)) and keeps the best two
-// tokens over them, and the group merges its lanes with shuffles, so no block
-// barrier is needed per query. The arithmetic is k_fuse's, in the same order
-// and without contraction, so the result is bit-identical to materialising the
-// logits and fusing them afterwards. Writes fuse_part[b][blk] for every query b.
-template <int NW, int NC, typename At>
-__device__ void fuse_tile_groups(const LmArgs& a, int v0, int blk, At at, int tpq, const int* qs, const int* qe,
-                                 const float* cb, const float* pr) {
-#pragma clang fp contract(off)
-  const int groups = 64 * NW / tpq, g = threadIdx.x / tpq, c = threadIdx.x % tpq;
-  for (int b = g; b < a.n_queries; b += groups) {
-    const int s0 = qs[b];
-    const int N = qs[b + 1] - s0 - 1;
-    const int e0 = qe[b];
-    Top2 cand{kNegInf, 0x7FFFFFFF, 0, kNegInf, 0x7FFFFFFF};
-    for (int j = c; j < NC; j += tpq) {
-      const int v = v0 + j;
-      if (v >= a.V) break;
-      const float sa = at(s0, j);
-      float best = kNegInf;
-      int bk = 0;
-      for (int kb = 1; kb <= N; kb += 8) {
-        float x[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) x[u] = (kb + u <= N) ? at(s0 + kb + u, j) : 0.f;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int k = kb + u;
-          if (k > N) continue;
-          const float beta = cb[e0 + k - 1];
-          const float coef = 1.0f + beta;
-          const float t1 = coef * x[u];
-          const float t2 = beta * sa;
-          const float val = (t1 - t2) + pr[e0 + k - 1];
-          if (val > best) { best = val; bk = k; }
-        }
-      }
-      cand = merge(cand, Top2{best, v, bk, kNegInf, 0x7FFFFFFF});
-    }
-    for (int o = tpq >> 1; o >= 1; o >>= 1) cand = merge(cand, shfl_top2(cand, o));
-    if (c == 0) {
-      float* p = a.fuse_part + ((size_t)b * a.fuse_nblk + blk) * 5;
-      p[0] = cand.v1; p[1] = __int_as_float(cand.i1); p[2] = __int_as_float(cand.k1);
-      p[3] = cand.v2; p[4] = __int_as_float(cand.i2);
-    }
-  }
-}
-
-// The same for at most NW / 2 queries, so that no wave idles: wq waves per
-// query (8, 4 or 2 for 1, 2 or up to 4 queries), one thread per column of the
-// NC = 128; with more threads than columns, es = wq / 2 adjacent lanes share a
-// column, lane s of them taking experts s + 1, s + 1 + es, ..., and they merge
-// (score, expert) keeping the lower expert on equal scores, which is what the
-// sequential scan over the experts keeps. A wave merges its columns with
-// shuffles, a query's waves merge through LDS. Every thread of the block calls
-// this (it has a block barrier).
-template <int NW, int NC, typename At>
-__device__ void fuse_tile_waves(const LmArgs& a, int v0, int blk, At at, int wq, const int* qs, const int* qe,
-                                const float* cb, const float* pr) {
-#pragma clang fp contract(off)
-  static_assert(NW == 8 && NC == 128, "two waves cover the columns");
-  __shared__ Top2 red[NW];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int es = wq / 2, b = wave / wq, wi = wave % wq;
-  const int s = lane % es, j = (64 * wi + lane) / es;
-  Top2 cand{kNegInf, 0x7FFFFFFF, 0, kNegInf, 0x7FFFFFFF};
-  if (b < a.n_queries) {  // wave-uniform
-    const int s0 = qs[b];
-    const int N = qs[b + 1] - s0 - 1;
-    const int e0 = qe[b];
-    const int v = v0 + j;
-    float best = kNegInf;
-    int bk = 0;
-    if (v < a.V) {
-      const float sa = at(s0, j);
-      for (int kb = 1 + s; kb <= N; kb += 8 * es) {
-        float x[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) x[u] = (kb + u * es <= N) ? at(s0 + kb + u * es, j) : 0.f;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int k = kb + u * es;
-          if (k > N) continue;
-          const float beta = cb[e0 + k - 1];
-          const float coef = 1.0f + beta;
-          const float t1 = coef * x[u];
-          const float t2 = beta * sa;
-          const float val = (t1 - t2) + pr[e0 + k - 1];
-          if (val > best) { best = val; bk = k; }
-        }
-      }
-    }
-    for (int o = 1; o < es; o <<= 1) {
-      const float ob = __shfl_xor(best, o);
-      const int ok = __shfl_xor(bk, o);
-      if (ob > best || (ob == best && ok < bk)) { best = ob; bk = ok; }
-    }
-    if (s == 0 && v < a.V) cand = Top2{best, v, bk, kNegInf, 0x7FFFFFFF};
-  }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) cand = merge(cand, shfl_top2(cand, o));
-  if (lane == 0) red[wave] = cand;
-  __syncthreads();
-  if (wi == 0 && lane == 0 && b < a.n_queries) {
-    Top2 r = red[wave];
-    for (int i = 1; i < wq; ++i) r = merge(r, red[wave + i]);
-    float* p = a.fuse_part + ((size_t)b * a.fuse_nblk + blk) * 5;
-    p[0] = r.v1; p[1] = __int_as_float(r.i1); p[2] = __int_as_float(r.k1);
-    p[3] = r.v2; p[4] = __int_as_float(r.i2);
-  }
-}
+// Rows a block reads past a query's last one in the many-row LM head's fused
+// epilogue (whole 16-byte groups of 4 rows, two groups per step).
+constexpr int kWideOverRead = 40;
 
 // What the many-row LM head's fused epilogue reads besides its tile, staged in
-// LDS at the start of the launch (an empty struct without the epilogue).
+// LDS at the start of the launch (an empty struct without the epilogue): row
+// scales, beta and prior per row (each expert's at its row; amateur rows and
+// rows past M hold stale values that are never used) and the queries' first
+// rows.
 template <bool FUSED>
 struct WideEpi {
-  float rho[kLmWideMaxRows], beta[kLmWideMaxRows], prior[kLmWideMaxRows];
-  int qs[kLmWideMaxRows / 2 + 1], qe[kLmWideMaxRows / 2 + 1];
+  __align__(16) float beta_row[kLmWideMaxRows + kWideOverRead];
+  __align__(16) float prior_row[kLmWideMaxRows + kWideOverRead];
+  float rho[kLmWideMaxRows];
+  int qs[kLmWideMaxRows / 2 + 1];
 };
 template <>
 struct WideEpi<false> {};
+
+// Eq. 2 for the experts k0 .. k0 + 3 (scores x, beta b, prior p of their rows;
+// sa the amateur's score), keeping the best over those with 1 <= k <= N, the
+// lower k on equal scores. k_fuse's arithmetic in its order, no contraction.
+__device__ __forceinline__ void eq2_rows4(const float4 x, const float4 b, const float4 p, float sa, int k0, int N,
+                                          float& best, int& bk) {
+#pragma clang fp contract(off)
+  const float xv[4] = {x.x, x.y, x.z, x.w}, bv[4] = {b.x, b.y, b.z, b.w}, pv[4] = {p.x, p.y, p.z, p.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int k = k0 + q;
+    const float coef = 1.0f + bv[q];
+    const float t1 = coef * xv[q];
+    const float t2 = bv[q] * sa;
+    const float val = (t1 - t2) + pv[q];
+    if (k >= 1 && k <= N && val > best) {
+      best = val;
+      bk = k;
+    }
+  }
+}
 
 // ------------------------------------------------------------------- LM head
 
@@ -1247,7 +1162,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         }
       }
       __syncthreads();
-      fuse_tile<4, 64 * VT>(a, chunk * 256, chunk, [&](int m, int j) { return tile[m * LD + j]; });
+      fuse_tile<4, 64 * VT>(a, chunk * 256, chunk, [&](int m, int j) { return tile[m * LD + j]; }, 16 * NT - 1);
       return;  // fused: at most 16 NT rows, a single row group
     }
 #pragma unroll
@@ -1430,7 +1345,7 @@ __global__ __launch_bounds__(64 * WPB) __attribute__((amdgpu_waves_per_eu(2, 2))
       }
     }
     __syncthreads();
-    fuse_tile<WPB, NC>(a, blockIdx.x * NC, blockIdx.x, at);
+    fuse_tile<WPB, NC>(a, blockIdx.x * NC, blockIdx.x, at, 32 * MTW - 1);
     return;
   }
 #pragma unroll
@@ -1544,9 +1459,9 @@ static_assert(lmhead_wide_wait(7, 3, 5, 2) == 20 && lmhead_wide_wait(3, 3, 5, 4)
 //     at a barrier, after which the next stage holds every wave's loads.
 // Scheduling barriers keep each half step's loads ahead of its products. Loads
 // past the end re-read the last step (in bounds, never used). FUSED: Eq. 2 and
-// the slice argmax in the epilogue, in two halves of 128 columns through the
-// (then free) LDS stages, with the row scales, beta, prior and query offsets
-// staged in LDS at the start.
+// the slice argmax in the epilogue, in four passes of 64 columns through the
+// (then free) LDS stages, with the row scales, beta and prior by row and the
+// queries' first rows staged in LDS at the start.
 template <int MTH, int NS, bool FUSED>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_lmhead_wide_bf16(LmArgs a) {
   static_assert(NS == 4 || NS == 8, "x stages");
@@ -1649,17 +1564,15 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // the fused epilogue's row scales, beta, prior and query offsets: loaded first,
   // written to LDS once the prologue's loads are in flight
   float e_rho = 0.f, e_beta = 0.f, e_prior = 0.f;
-  int e_qs = 0, e_qe = 0;
+  int e_qs = 0, e_row = -1;
   if constexpr (FUSED) {
     if (tid < M) e_rho = a.rho_in[tid];
     if (tid < M - a.n_queries) {  // experts: every query has one amateur row
+      e_row = a.exp_seq[tid];
       e_beta = a.beta[tid];
       e_prior = a.prior[tid];
     }
-    if (tid <= a.n_queries) {
-      e_qs = a.query_seq0[tid];
-      e_qe = a.query_exp0[tid];
-    }
+    if (tid <= a.n_queries) e_qs = a.query_seq0[tid];
   }
   // prologue: the loads of half steps -LEAD .. -1 in the loop's order (half step
   // h loads W(h + LEAD) and, at even h, x(h / 2 + XL); LEAD = 2 XL + 1)
@@ -1672,14 +1585,11 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   });
   if constexpr (FUSED) {
     if (tid < M) epi.rho[tid] = e_rho;
-    if (tid < M - a.n_queries) {
-      epi.beta[tid] = e_beta;
-      epi.prior[tid] = e_prior;
+    if (e_row >= 0) {
+      epi.beta_row[e_row] = e_beta;
+      epi.prior_row[e_row] = e_prior;
     }
-    if (tid <= a.n_queries) {
-      epi.qs[tid] = e_qs;
-      epi.qe[tid] = e_qe;
-    }
+    if (tid <= a.n_queries) epi.qs[tid] = e_qs;
   }
   wait_vmcnt<WAITN>();
   __builtin_amdgcn_s_barrier();
@@ -1693,53 +1603,103 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   }
   wait_vmcnt<0>();  // the loads past the end (some into LDS) have landed
   if constexpr (FUSED) {
-    // two halves of 128 columns: waves 4h .. 4h + 3 write their 32 columns each,
-    // column-major into stage (wave % 4) (column c of a stage at c * 16 MTP, rows
-    // XOR-swizzled by column against bank conflicts), then all waves fuse; one
-    // query per group of tpq lanes (64 lanes per query up to 8 queries, 2 at 144)
-    constexpr int NC = 128, RS = 16 * MTP;
-    static_assert(XU * 64 * 16 == 32 * RS * 4, "a stage holds 32 columns of every row");
-    auto col_base = [&](int j) -> float* {  // column j of the half
-      const int q = j >> 5;
+    // Eq. 2 and the slice argmax in four passes of 64 columns through the (now
+    // free) x stages. Pass p takes accumulator element p of every lane of every
+    // wave: block column 32 w + 16 vt + 4 quad + p, staged as pass column
+    // c = 16 (w / 2) + 4 quad + 2 (w % 2) + vt at stage c / 16, offset
+    // (c % 16) RSP, rows in order. RSP = 4 (mod 32): a wave's stores hit each
+    // bank twice, and 16-byte reads of one row in eight consecutive columns
+    // fall in distinct banks; RSP >= M + kWideOverRead, so reads of whole 4-row
+    // groups past a query's last row stay in the column. Each query has T
+    // threads (a power of two); a thread takes 64 / T columns, or with T > 64
+    // es = T / 64 adjacent threads share a column and split its 4-row groups,
+    // merging (score, expert) with the lower expert on equal scores (the
+    // sequential scan's choice). After the last pass the query's threads merge
+    // their best two tokens (shuffles, then LDS across waves) into the block's
+    // first fuse_part slot; its second slot (if any) gets an empty candidate.
+    constexpr int NCP = 64;
+    static_assert(16 * (16 * MTP + kWideOverRead + 35) <= XU * 64 * 4, "16 padded columns per stage");
+    const int RSP = (((M + kWideOverRead + 27) >> 5) << 5) + 4;
+    auto colp = [&](int c) -> float* {
+      const int q = c >> 4;
       float* base = q == 0 ? (float*)&xs0[0][0] : q == 1 ? (float*)&xs1[0][0] : q == 2 ? (float*)&xs2[0][0]
                                                                                    : (float*)&xs3[0][0];
-      return base + (j & 31) * RS;
+      return base + (c & 15) * RSP;
     };
-    auto at = [&](int m, int j) { return col_base(j)[m ^ (j & 31)]; };
-    // lanes per query (more than 4 queries), or waves per query (up to 4)
-    int tpq = 64;
-    while (tpq > 2 && (512 / tpq) < a.n_queries) tpq >>= 1;
-    int wq = 8;
-    while (wq > 2 && wq * a.n_queries > 8) wq >>= 1;
+    int T = 512;
+    while (T > 2 && T * a.n_queries > 512) T >>= 1;
+    const int es = T > 64 ? T / 64 : 1, cpl = T < 64 ? 64 / T : 1;
+    const int qb = tid / T, ti = tid % T, sp = ti % es;
+    const bool active = qb < a.n_queries;
+    const int s0 = active ? epi.qs[qb] : 0;
+    const int N = active ? epi.qs[qb + 1] - s0 - 1 : 0;
+    const int rb = (s0 + 1) & ~3, nb = ((s0 + N) >> 2) - (rb >> 2) + 1;  // 4-row groups holding the experts
+    __shared__ Top2 red[8];
+    Top2 cand{kNegInf, 0x7FFFFFFF, 0, kNegInf, 0x7FFFFFFF};
     __syncthreads();  // every wave is done with the x stages
+#pragma unroll 1
+    for (int p = 0; p < 4; ++p) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      if ((wave >> 2) == h) {
-        float* colw = col_base(32 * (wave & 3));  // this wave's 32 columns
+      for (int t = 0; t < MTP; ++t) {
+        const int m = 16 * t + col;
+        if (m >= M) continue;
+        const float rho = epi.rho[m];
 #pragma unroll
-        for (int t = 0; t < MTP; ++t) {
-          const int m = 16 * t + col;
-          if (m >= M) continue;
-          const float rho = epi.rho[m];
-#pragma unroll
-          for (int vt = 0; vt < 2; ++vt) {
-            const f32x4 cc = acc[vt][t];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int jl = 16 * vt + 4 * quad + r;  // column within the wave's 32
-              colw[jl * RS + (m ^ jl)] = cc[r] * rho;
-            }
-          }
+        for (int vt = 0; vt < 2; ++vt) {
+          const f32x4 cc = acc[vt][t];
+          const float x = p == 0 ? cc[0] : p == 1 ? cc[1] : p == 2 ? cc[2] : cc[3];
+          colp(16 * (wave >> 1) + 4 * quad + 2 * (wave & 1) + vt)[m] = x * rho;
         }
       }
       __syncthreads();
-      if (a.n_queries <= 4)
-        fuse_tile_waves<8, NC>(a, blockIdx.x * 256 + NC * h, 2 * blockIdx.x + h, at, wq, epi.qs, epi.qe, epi.beta,
-                               epi.prior);
-      else
-        fuse_tile_groups<8, NC>(a, blockIdx.x * 256 + NC * h, 2 * blockIdx.x + h, at, tpq, epi.qs, epi.qe,
-                                epi.beta, epi.prior);
-      if (h == 0) __syncthreads();  // before the second half's tile overwrites the first
+      if (active) {
+        for (int i = 0; i < cpl; ++i) {
+          const int c = es > 1 ? ti / es : ti + T * i;
+          const int wc = 2 * (c >> 4) + ((c >> 1) & 1);
+          const int v = blockIdx.x * 256 + 32 * wc + 16 * (c & 1) + 4 * ((c >> 2) & 3) + p;
+          const float* cp = colp(c);
+          float best = kNegInf;
+          int bk = 0;
+          if (v < a.V) {
+            const float sa = cp[s0];
+            for (int ib = sp; ib < nb; ib += 2 * es) {
+              const int r1 = rb + 4 * ib, r2 = r1 + 4 * es;
+              const float4 x1 = *(const float4*)(cp + r1), x2 = *(const float4*)(cp + r2);
+              const float4 b1 = *(const float4*)(epi.beta_row + r1), b2 = *(const float4*)(epi.beta_row + r2);
+              const float4 p1 = *(const float4*)(epi.prior_row + r1), p2 = *(const float4*)(epi.prior_row + r2);
+              eq2_rows4(x1, b1, p1, sa, r1 - s0, N, best, bk);
+              eq2_rows4(x2, b2, p2, sa, r2 - s0, N, best, bk);
+            }
+          }
+          for (int o = 1; o < es; o <<= 1) {
+            const float ob = __shfl_xor(best, o);
+            const int ok = __shfl_xor(bk, o);
+            if (ob > best || (ob == best && ok < bk)) {
+              best = ob;
+              bk = ok;
+            }
+          }
+          if (sp == 0 && v < a.V) cand = merge(cand, Top2{best, v, bk, kNegInf, 0x7FFFFFFF});
+        }
+      }
+      __syncthreads();  // before the next pass writes the stages
+    }
+    // the query's best two tokens over the block's 256 columns
+    for (int o = min(T, 64) >> 1; o >= 1; o >>= 1) cand = merge(cand, shfl_top2(cand, o));
+    if (T > 64) {
+      if (lane == 0) red[wave] = cand;
+      __syncthreads();
+      if (ti == 0)
+        for (int w = 1; w < T / 64; ++w) cand = merge(cand, red[wave + w]);
+    }
+    if (ti == 0 && active) {
+      float* pp = a.fuse_part + ((size_t)qb * a.fuse_nblk + 2 * blockIdx.x) * 5;
+      pp[0] = cand.v1; pp[1] = __int_as_float(cand.i1); pp[2] = __int_as_float(cand.k1);
+      pp[3] = cand.v2; pp[4] = __int_as_float(cand.i2);
+      if (2 * (int)blockIdx.x + 1 < a.fuse_nblk) {  // (the last block's second slot may not exist)
+        pp[5] = kNegInf; pp[6] = __int_as_float(0x7FFFFFFF); pp[7] = __int_as_float(0);
+        pp[8] = kNegInf; pp[9] = __int_as_float(0x7FFFFFFF);
+      }
     }
     return;
   }
