@@ -374,6 +374,10 @@ pced_status pced_relevance(int32_t mode, int32_t n, const float* retrieval, cons
  *
  * Weights live in one caller-owned device buffer of pced_model_bytes(cfg),
  * filled once by pced_pack_model_layer (every layer) and pced_pack_model_globals.
+ * The buffer holds each layer's four matrices twice: in the matrix-core tile
+ * order that the decode kernels stream, and row-major for the library GEMMs
+ * (rocBLAS) that compute the projections of passes with more than 48 rows
+ * (the prefill's chunks).
  */
 
 /* Bytes of the packed decoder-stack weights (0 if cfg is invalid or ffn_dim == 0). */

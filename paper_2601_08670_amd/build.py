@@ -16,6 +16,8 @@ COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 SOURCES = ["pced_kernels.hip", "pced_api.cpp"]
+# rocBLAS: the many-row decoder projections' GEMMs
+LINK = ["-L/opt/rocm/lib", "-Wl,-rpath,/opt/rocm/lib", "-lrocblas"]
 
 
 def build(verbose: bool = False) -> str:
@@ -28,7 +30,7 @@ def build(verbose: bool = False) -> str:
         _run(cmd, verbose)
         objs.append(obj)
     tmp = LIB + ".tmp"
-    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp, *LINK], verbose)
     os.replace(tmp, LIB)
     for o in objs:
         os.remove(o)

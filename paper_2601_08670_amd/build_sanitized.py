@@ -8,7 +8,7 @@ from __future__ import annotations
 import os
 import subprocess
 
-from .build import COMMON, CSRC, HIPCC, _run
+from .build import COMMON, CSRC, HIPCC, LINK, _run
 
 # each host-only sanitizer flag follows its own -Xarch_host (device code is not instrumented)
 SANITIZE = ("-Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined "
@@ -26,7 +26,7 @@ def build(out_dir: str, verbose: bool = False) -> str:
         _run(cmd, verbose)
         objs.append(obj)
     lib = os.path.join(out_dir, "libpced_sanitized.so")
-    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", lib,
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", lib, *LINK,
           "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined", "-shared-libsan"], verbose)
     return lib
 

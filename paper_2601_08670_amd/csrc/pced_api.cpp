@@ -4,6 +4,7 @@
 #include "pced.h"
 
 #include <hip/hip_runtime.h>
+#include <rocblas/rocblas.h>
 
 #include <algorithm>
 #include <cmath>
@@ -210,6 +211,7 @@ struct pced_ctx {
   bool prof = false;
   std::vector<ProfRec> recs;
   std::vector<hipEvent_t> ev_free;
+  rocblas_handle blas = nullptr;  // created at the first many-row projection
   pced_profile totals{};
 
   template <class T> T* at(size_t off) { return reinterpret_cast<T*>(ws + off); }
@@ -569,9 +571,11 @@ pced_status check_room(const pced_ctx* c, int n_tokens) {
 // Byte offsets of the decoder-stack weights inside the packed model buffer:
 // per layer the two norm weights and the packed QKV (q, k, v tiles
 // concatenated), O, gate/up (gate and up tiles alternating) and down
-// matrices; then the embedding [V][hidden] and the final norm weight.
+// matrices, then the same four matrices row-major ([out][in], the same row
+// order: gate and up in alternating 16-row blocks) for the library GEMMs of
+// many-row passes; then the embedding [V][hidden] and the final norm weight.
 struct ModelLayout {
-  size_t attn_norm, mlp_norm, qkv, o, gu, down, layer_bytes;
+  size_t attn_norm, mlp_norm, qkv, o, gu, down, qkv_rm, o_rm, gu_rm, down_rm, layer_bytes;
   size_t embed, final_norm, total;
 };
 
@@ -587,6 +591,10 @@ ModelLayout model_layout(const pced_config& c) {
   m.o = take(H * qd * 2);
   m.gu = take(2 * F * H * 2);
   m.down = take(H * F * 2);
+  m.qkv_rm = take((qd + 2 * kd) * H * 2);
+  m.o_rm = take(H * qd * 2);
+  m.gu_rm = take(2 * F * H * 2);
+  m.down_rm = take(H * F * 2);
   m.layer_bytes = o;
   o = m.layer_bytes * c.n_layers;
   m.embed = take((size_t)c.vocab * H * 2);
@@ -630,11 +638,43 @@ struct FwdRows {
 
 AttnPlan plan_for_lengths(const pced_ctx* c, const std::vector<int>& lens);
 
+// One projection of a pass through the stack. Up to 48 rows: the split-K
+// kernel on the packed tiles, whose weight stream is the cost. More rows (the
+// prefill's chunks): the products are a dense contraction that the split-K
+// kernel would stream W for once per 48-row group, so rocBLAS computes them
+// (bf16 operands, fp32 accumulation and output) from the row-major copy as a
+// single K slice, and the epilogue kernel finishes the projection.
+pced_status project(pced_ctx* c, const GemmArgs& g, const char* w_rm, GemmEpi epi, hipStream_t st,
+                    const Timing* tm) {
+  if (g.M <= kLmRowsPad) {
+    HIP_OK(launch_gemm(g, epi, st, tm));
+    return PCED_OK;
+  }
+  if (!c->blas && rocblas_create_handle(&c->blas) != rocblas_status_success) {
+    c->blas = nullptr;
+    return fail(PCED_ERR_HIP, "rocblas_create_handle failed");
+  }
+  if (rocblas_set_stream(c->blas, st) != rocblas_status_success) return fail(PCED_ERR_HIP, "rocblas_set_stream failed");
+  const int N = 16 * g.n_tiles;
+  const float one = 1.0f, zero = 0.0f;
+  if (tm && tm->start) HIP_OK(hipEventRecord(tm->start, st));
+  // column-major view: part^T [N][M] = (W^T)^T [N][K] x^T [K][M]
+  const rocblas_status bs = rocblas_gemm_ex(
+      c->blas, rocblas_operation_transpose, rocblas_operation_none, N, g.M, g.K, &one, w_rm, rocblas_datatype_bf16_r,
+      g.K, g.x, rocblas_datatype_bf16_r, g.K, &zero, g.part, rocblas_datatype_f32_r, N, g.part, rocblas_datatype_f32_r,
+      N, rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+  if (bs != rocblas_status_success) return fail(PCED_ERR_HIP, "rocblas_gemm_ex: %s", rocblas_status_to_string(bs));
+  const Timing stop{nullptr, tm ? tm->stop : nullptr};
+  HIP_OK(launch_proj_epilogue(g, epi, st, tm ? &stop : nullptr));
+  return PCED_OK;
+}
+
 // Embedding plus every decoder layer for the rows (appending their K/V rows).
 // Leaves the residual stream in rows.h and bf16(h * g_final) in rows.a.
 pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, hipStream_t st) {
   const pced_config& cfg = c->cfg;
   const ModelLayout ml = model_layout(cfg);
+  pced_status r = PCED_OK;
   const int M = R.M, H = cfg.hidden, D = cfg.head_dim;
   const int qd = cfg.n_q_heads * D, kd = cfg.n_kv_heads * D;
   const AttnPlan plan = plan_for_lengths(c, R.lens);
@@ -785,7 +825,8 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
       ProfScope ps(c, PCED_PROF_QKV, (double)(qd + 2 * kd) * H * 2 + (double)M * (H * 2 + (qd + 2 * kd) * 2),
                    2.0 * M * (qd + 2 * kd) * H);
       if (!fits(q)) return fail(PCED_ERR_UNSUPPORTED, "QKV projection does not fit the partial buffer or LDS");
-      HIP_OK(launch_gemm(q, kEpiQkv, st, ps.timing()));
+      r = project(c, q, lw + ml.qkv_rm, kEpiQkv, st, ps.timing());
+      if (r != PCED_OK) return r;
     }
     at.layer = lq;
     at.kpool = kp;
@@ -809,7 +850,8 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
       o.g_next = (const uint16_t*)(lw + ml.mlp_norm);
       ProfScope ps(c, PCED_PROF_OPROJ, (double)H * qd * 2 + (double)M * (qd * 2 + H * 10), 2.0 * M * H * qd);
       if (!fits(o)) return fail(PCED_ERR_UNSUPPORTED, "O projection does not fit the partial buffer or LDS");
-      HIP_OK(launch_gemm(o, kEpiResid, st, ps.timing()));
+      r = project(c, o, lw + ml.o_rm, kEpiResid, st, ps.timing());
+      if (r != PCED_OK) return r;
     }
     if (trace_h(l, 1) != PCED_OK) return PCED_ERR_HIP;
     {  // norm + gate/up + SwiGLU
@@ -822,7 +864,8 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
       u.ss_in = R.ss;
       ProfScope ps(c, PCED_PROF_GATEUP, 2.0 * F * H * 2 + (double)M * (H * 2 + F * 2), 4.0 * M * F * H);
       if (!fits(u)) return fail(PCED_ERR_UNSUPPORTED, "gate/up projection does not fit the partial buffer or LDS");
-      HIP_OK(launch_gemm(u, kEpiSwiglu, st, ps.timing()));
+      r = project(c, u, lw + ml.gu_rm, kEpiSwiglu, st, ps.timing());
+      if (r != PCED_OK) return r;
     }
     if (R.act_trace)
       HIP_OK(hipMemcpyAsync(R.act_trace + (size_t)l * M * cfg.ffn_dim, R.act, (size_t)M * cfg.ffn_dim * 2,
@@ -837,7 +880,8 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
       d.g_next = g_next;
       ProfScope ps(c, PCED_PROF_DOWN, F * H * 2 + (double)M * (F * 2 + H * 10), 2.0 * M * H * F);
       if (!fits(d)) return fail(PCED_ERR_UNSUPPORTED, "down projection does not fit the partial buffer or LDS");
-      HIP_OK(launch_gemm(d, kEpiResid, st, ps.timing()));
+      r = project(c, d, lw + ml.down_rm, kEpiResid, st, ps.timing());
+      if (r != PCED_OK) return r;
     }
     if (l + 1 < cfg.n_layers && trace_h(l + 1, 0) != PCED_OK) return PCED_ERR_HIP;
   }
@@ -1119,6 +1163,7 @@ void pced_destroy(pced_ctx* ctx) {
   if (!ctx) return;
   for (auto& r : ctx->recs) { hipEventDestroy(r.a); hipEventDestroy(r.b); }
   for (auto e : ctx->ev_free) hipEventDestroy(e);
+  if (ctx->blas) rocblas_destroy_handle(ctx->blas);
   delete ctx;
 }
 
@@ -1393,6 +1438,16 @@ pced_status pced_pack_model_layer(const pced_config* cfg, int32_t layer, const v
   HIP_OK(launch_pack_tiles(tensors[6], lw + ml.gu, F, H, 2, 0, 2 * F / 16, st));
   HIP_OK(launch_pack_tiles(tensors[7], lw + ml.gu, F, H, 2, 1, 2 * F / 16, st));
   HIP_OK(launch_pack_tiles(tensors[8], lw + ml.down, H, F, 1, 0, H / 16, st));
+  // row-major copies: q, k, v rows in order; gate and up 16-row blocks alternating
+  const size_t row = (size_t)H * 2;
+  HIP_OK(hipMemcpyAsync(lw + ml.qkv_rm, tensors[1], qd * row, hipMemcpyDeviceToDevice, st));
+  HIP_OK(hipMemcpyAsync(lw + ml.qkv_rm + qd * row, tensors[2], kd * row, hipMemcpyDeviceToDevice, st));
+  HIP_OK(hipMemcpyAsync(lw + ml.qkv_rm + (qd + kd) * row, tensors[3], kd * row, hipMemcpyDeviceToDevice, st));
+  HIP_OK(hipMemcpyAsync(lw + ml.o_rm, tensors[4], (size_t)H * qd * 2, hipMemcpyDeviceToDevice, st));
+  for (int h = 0; h < 2; ++h)
+    HIP_OK(hipMemcpy2DAsync(lw + ml.gu_rm + h * 16 * row, 32 * row, tensors[6 + h], 16 * row, 16 * row, F / 16,
+                            hipMemcpyDeviceToDevice, st));
+  HIP_OK(hipMemcpyAsync(lw + ml.down_rm, tensors[8], (size_t)H * F * 2, hipMemcpyDeviceToDevice, st));
   return PCED_OK;
 }
 

@@ -291,6 +291,9 @@ hipError_t launch_stream_read(const void* src, size_t nbytes, uint32_t* xor_out,
 hipError_t launch_pack_tiles(const void* w, void* wp, int rows, int K, int stride, int offset, int n_tiles,
                              hipStream_t st);
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Timing* tm = nullptr);
+// The projection epilogue alone, over products already in a.part as one K
+// slice ([M][16 n_tiles] fp32, e.g. from a library GEMM).
+hipError_t launch_proj_epilogue(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Timing* tm = nullptr);
 int proj_tiles_per_wave(int n_tiles);                // 16-column tiles per wave of a projection block
 size_t proj_lds_bytes(int rows, int K, int ksplit);  // LDS of a projection block
 hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Timing* tm = nullptr);

@@ -2716,6 +2716,13 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Tim
   return launch_reduce(a, epi, st, t1(tm));
 }
 
+hipError_t launch_proj_epilogue(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Timing* tm) {
+  if (a.M < 1 || a.n_tiles < 1 || (epi == kEpiSwiglu && a.n_tiles % 2)) return hipErrorInvalidValue;
+  GemmArgs r = a;
+  r.ksplit = 1;
+  return launch_reduce(r, epi, st, t1(tm));
+}
+
 hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Timing* tm) {
   if (a.hidden % 256 != 0) return hipErrorInvalidValue;
   return go(k_embed, dim3(n_seqs), dim3(256), 0, st, t0(tm), t1(tm), a);

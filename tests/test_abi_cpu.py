@@ -220,8 +220,9 @@ def test_relevance_helper_errors():
 def test_decoder_stack_config_and_sizes():
     c = cfg(ffn_dim=512)
     H, qd, kd, F = 512, 512, 128, 512
-    per_layer = sum((-(-b // 256)) * 256 for b in (H * 2, H * 2, (qd + 2 * kd) * H * 2, H * qd * 2,
-                                                   2 * F * H * 2, H * F * 2))
+    mats = ((qd + 2 * kd) * H * 2, H * qd * 2, 2 * F * H * 2, H * F * 2)
+    # norms, the packed matrices, then the same matrices row-major (library GEMMs of many-row passes)
+    per_layer = sum((-(-b // 256)) * 256 for b in (H * 2, H * 2) + mats + mats)
     tail = sum((-(-b // 256)) * 256 for b in (1000 * H * 2, H * 2))
     assert _lib.pced_model_bytes(c) == 2 * per_layer + tail
     assert _lib.pced_workspace_bytes(c) > _lib.pced_workspace_bytes(cfg())   # decoder buffers
