@@ -405,7 +405,7 @@ pced_status pced_pack_model_globals(const pced_config* cfg, const void* embed, c
  * Query-suffix prefill (paper, Section 3: the query is processed into every
  * expert's cache): appends tokens[b][0 .. n_tokens-1] to every sequence of
  * query b. The tokens go through the stack in chunks of up to
- * max(256, max_seqs) / S tokens, all (sequence, token) rows of a chunk in one
+ * max(2304, max_seqs) / S tokens, all (sequence, token) rows of a chunk in one
  * pass; each token attends to the cache and to the suffix tokens before it
  * (causal). No logits.
  *   model   device, packed weights

@@ -164,7 +164,11 @@ Layout make_layout(const pced_config& c) {
   // (a multiple of 16 rows: the many-row projection path reads whole 16-row tiles)
   L.pf_rows = dec ? (int)ceil_div(std::max(c.max_seqs, kPrefillRows), 16) * 16 : 0;
   const size_t PR = L.pf_rows;
-  L.pf_proj_cols = L.part_cols;
+  // projection products of a chunk: one slice of up to max_cols columns for
+  // more than 48 rows (library GEMM), the split-K slices for up to 48
+  const size_t max_cols = std::max<size_t>({(size_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim,
+                                            (size_t)c.hidden, 2 * (size_t)c.ffn_dim});
+  L.pf_proj_cols = max_cols;
   L.pf_len0 = take(PR * 4);
   L.pf_pt = take(PR * c.max_pages_per_seq * 4);
   L.pf_tok = take(PR * 4);
@@ -177,7 +181,7 @@ Layout make_layout(const pced_config& c) {
   L.pf_x = take(PR * c.hidden * 2);
   L.pf_part_acc = take(PR * c.n_kv_heads * kPrefillParts * G * c.head_dim * 4);
   L.pf_part_ml = take(PR * c.n_kv_heads * kPrefillParts * G * 2 * 4);
-  L.pf_proj = take(PR * L.pf_proj_cols * 4);
+  L.pf_proj = take(std::max(PR * max_cols, (size_t)kLmRowsPad * L.part_cols) * 4);
   L.total = o;
   return L;
 }
@@ -787,14 +791,17 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
   // K slices per projection: about one block per compute unit, more where the
   // staged x slice would not fit in LDS
   const int stage_rows = std::min(M, M <= 16 ? 16 : M <= 32 ? 32 : 48);
+  // (more than 48 rows: one slice, the library GEMM's products)
   auto slices = [&](int n_tiles, int K) {
+    if (M > kLmRowsPad) return 1;
     const int groups = ceil_div(n_tiles, 8 * proj_tiles_per_wave(n_tiles));
     int ks = std::max(1, std::min({kProjMaxSplit, K / 64, c->num_cus / groups}));
     while (ks < std::min(kProjMaxSplit, K / 64) && proj_lds_bytes(stage_rows, K, ks) > kProjMaxLds) ++ks;
     return ks;
   };
   auto fits = [&](const GemmArgs& p) {
-    return proj_lds_bytes(stage_rows, p.K, p.ksplit) <= kProjMaxLds && (size_t)p.ksplit * 16 * p.n_tiles <= R.proj_cols;
+    return (M > kLmRowsPad || proj_lds_bytes(stage_rows, p.K, p.ksplit) <= kProjMaxLds) &&
+           (size_t)p.ksplit * 16 * p.n_tiles <= R.proj_cols;
   };
   const double F = cfg.ffn_dim;
   for (int l = 0; l < cfg.n_layers; ++l) {
@@ -964,7 +971,7 @@ pced_status run_prefill_chunk(pced_ctx* c, const char* model, const int32_t* tok
   R.part_ml = c->at<float>(c->lay.pf_part_ml);
   R.part_slots = (size_t)c->lay.pf_rows * cfg.n_kv_heads * kPrefillParts;
   R.proj_part = c->at<float>(c->lay.pf_proj);
-  R.proj_cols = c->lay.pf_proj_cols;
+  R.proj_cols = M > kLmRowsPad ? c->lay.pf_proj_cols : c->lay.part_cols;
   return run_model_forward(c, model, R, st);
 }
 

@@ -189,7 +189,7 @@ struct SynthArgs {
 enum GemmEpi { kEpiQkv = 0, kEpiResid = 1, kEpiSwiglu = 2 };
 constexpr int kProjMaxSplit = 16;  // K slices of a projection (partial buffer sized for this many)
 constexpr size_t kProjMaxLds = 150 * 1024;  // staged x slice of a projection block
-constexpr int kPrefillRows = 256;  // (sequence, suffix token) rows of one prefill chunk, at least
+constexpr int kPrefillRows = 2304;  // (sequence, suffix token) rows of one prefill chunk, at least
 constexpr int kPrefillParts = 8;   // attention partial states per prefill row and kv-head
 struct GemmArgs {
   const void* w;            // packed tiles of this projection

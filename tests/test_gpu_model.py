@@ -189,12 +189,21 @@ def test_model_prefill_then_steps_shuffled_pages():
 
 
 def test_model_many_rows_two_row_groups():
-    # 57 sequences: the projections loop over two groups of 48 rows; the prefill
-    # runs in chunks of 4 suffix tokens (228 rows: five row groups), then 2
+    # 57 sequences: more than 48 rows, so the decode steps' projections go to
+    # the library GEMM too; the prefill runs as one chunk of 570 rows
     geom = W.Geometry(1, 4, 1, 64, 256, 700, "bf16")
     wl = W.custom(geom, [30, 25], list(range(3, 58)), amateur_len=7, steps=2, seed=23)
     spec = ModelSpec(geom, ffn_dim=256, rope_theta=10000.0, seed=23)
     _run(wl, spec, steps=2, prefill=10)
+
+
+def test_model_prefill_in_two_chunks():
+    # 101 sequences: a prefill chunk holds 2304 // 101 = 22 suffix tokens, so 30
+    # tokens run as chunks of 22 and 8 (the second attends to the first's rows)
+    geom = W.Geometry(1, 4, 1, 64, 256, 700, "bf16")
+    wl = W.custom(geom, [50, 49], [3 + (7 * i) % 40 for i in range(99)], amateur_len=5, steps=1, seed=25)
+    spec = ModelSpec(geom, ffn_dim=256, rope_theta=10000.0, seed=25)
+    _run(wl, spec, steps=1, prefill=30)
 
 
 def test_model_llama3_8b_layer_shapes():
