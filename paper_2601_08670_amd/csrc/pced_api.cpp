@@ -80,7 +80,7 @@ struct Layout {
       load_items, src_k, src_v, meta_end;
   size_t chunk_info, seg, nparts, work_pages, prev_tok, beta, part_acc, part_ml, x, logits,
       rho, x_packed, fuse_part, lse_part, jsd_part, agg_lse, syn_q, syn_k, syn_v, dec_h, dec_a, dec_act, dec_ss, dec_rho, dec_part,
-      pf_len0, pf_pt, pf_tok, pf_nparts, pf_h, pf_a, pf_act, pf_ss, pf_q, pf_x, pf_part_acc, pf_part_ml, pf_proj,
+      pf_len0, pf_pt, pf_tok, pf_nparts, pf_glen0, pf_gpt, pf_gnparts, pf_h, pf_a, pf_act, pf_ss, pf_q, pf_x, pf_part_acc, pf_part_ml, pf_proj,
       total;
   int pf_rows;          // rows of one prefill chunk (sequences x suffix tokens)
   size_t pf_proj_cols;  // slices x columns per row of the prefill projection partials
@@ -173,6 +173,10 @@ Layout make_layout(const pced_config& c) {
   L.pf_pt = take(PR * c.max_pages_per_seq * 4);
   L.pf_tok = take(PR * 4);
   L.pf_nparts = take(PR * 4);
+  // the attention's token groups (at most one per row)
+  L.pf_glen0 = take(PR * 4);
+  L.pf_gpt = take(PR * c.max_pages_per_seq * 4);
+  L.pf_gnparts = take(PR * 4);
   L.pf_h = take(PR * c.hidden * 4);
   L.pf_a = take(PR * c.hidden * 2);
   L.pf_act = take(PR * c.ffn_dim * 2);
@@ -269,6 +273,7 @@ struct AttnPlan {
   int chunks = 0;     // C
   int max_seg = 0;    // most sequences met by one chunk
   int max_parts = 0;  // most chunks met by one sequence (partial slots per sequence)
+  int min_pages = 1;  // planned pages per sequence at least (padding pages are masked)
 };
 
 void plan_stats(const std::vector<long>& pre, long P, long C, AttnPlan* out) {
@@ -296,23 +301,34 @@ void plan_stats(const std::vector<long>& pre, long P, long C, AttnPlan* out) {
 // wave starts in the first round and streams the same number of pages), at
 // least P/64 (one page id per lane), raised when a chunk would meet more
 // sequences than a wave can stage q rows for.
-AttnPlan plan_for_lengths(const pced_ctx* c, const std::vector<int>& lens);
+AttnPlan plan_for_lengths(const pced_ctx* c, const std::vector<int>& lens, int group = 0, bool pad = false);
 
 AttnPlan plan_attention(const pced_ctx* c) {
   return plan_for_lengths(c, std::vector<int>(c->len.begin(), c->len.end()));
 }
 
-// The same plan for rows of the given lengths (before the step's append).
-AttnPlan plan_for_lengths(const pced_ctx* c, const std::vector<int>& lens) {
+// The same plan for rows of the given lengths (before the step's append);
+// group: query columns per kv-head of an item (0: the model's q-heads per kv-head).
+// pad: every item counts at least the chunk length of the unconstrained plan
+// (at most kMaxSplitPages / 2 pages), so that a run of short items does not
+// force small chunks when a wave can stage few segments.
+AttnPlan plan_for_lengths(const pced_ctx* c, const std::vector<int>& lens, int group, bool pad) {
   const int S = (int)lens.size();
-  std::vector<long> pre(S + 1, 0);
-  for (int s = 0; s < S; ++s) pre[s + 1] = pre[s] + ceil_div(lens[s] + 1, kPage);
-  const long P = pre[S];
   long cap = std::max<long>(1, (long)c->num_cus * c->attn_waves_per_cu / c->cfg.n_kv_heads);
   if (c->cfg.max_attn_chunks > 0) cap = std::min<long>(cap, c->cfg.max_attn_chunks);
-  long C = std::max<long>(std::min(cap, P), ceil_div(P, (long)kMaxSplitPages));
+  auto first_c = [&](long P) { return std::max<long>(std::min(cap, P), ceil_div(P, (long)kMaxSplitPages)); };
+  int min_pages = 1;
+  if (pad && S > 0) {
+    long P0 = 0;
+    for (int s = 0; s < S; ++s) P0 += ceil_div(lens[s] + 1, kPage);
+    min_pages = (int)std::min<long>(kMaxSplitPages / 2, ceil_div(P0, first_c(P0)));
+  }
+  std::vector<long> pre(S + 1, 0);
+  for (int s = 0; s < S; ++s) pre[s + 1] = pre[s] + std::max(min_pages, ceil_div(lens[s] + 1, kPage));
+  const long P = pre[S];
+  long C = first_c(P);
   // bf16: the later segments' q rows of a chunk are staged by its wave in LDS
-  const int per_seg_units = c->G * c->cfg.head_dim / 8;
+  const int per_seg_units = (group > 0 ? group : c->G) * c->cfg.head_dim / 8;
   const int seg_limit = c->bf16 ? std::min(kMaxSeg, 1 + 64 * kStageUnits / per_seg_units) : kMaxSeg;
   AttnPlan plan;
   for (;;) {
@@ -320,6 +336,7 @@ AttnPlan plan_for_lengths(const pced_ctx* c, const std::vector<int>& lens) {
     if (plan.max_seg <= seg_limit || C >= P) break;
     C = std::min(P, C + std::max<long>(1, C / 16));
   }
+  plan.min_pages = min_pages;
   return plan;
 }
 
@@ -611,6 +628,9 @@ ModelLayout model_layout(const pced_config& c) {
 // step has one row per sequence; a prefill chunk has one row per (sequence,
 // suffix token), each a virtual sequence that shares its base sequence's pages
 // and ends at its own token (so attention over it is causal by construction).
+// The prefill's attention runs on groups of consecutive suffix tokens of one
+// sequence instead (the att_* members): one plan item per group, ending at its
+// last token, whose tokens take their own query columns and causal ends.
 struct FwdRows {
   int M = 0;
   std::vector<int> lens;             // host: length of each row's sequence before its append
@@ -634,13 +654,22 @@ struct FwdRows {
   float* proj_part = nullptr;
   size_t proj_cols = 0;              // slices x columns per row of the projection partials
   float* attn_out = nullptr;
+  // The attention's items: the rows (att_tq = 1), or for the prefill groups of
+  // att_tq suffix tokens of one sequence (att_T tokens per sequence), each item
+  // ending at its last token; the kernels give a group's tokens their own
+  // query columns and causal ends.
+  int att_n = 0, att_tq = 1, att_T = 1;
+  std::vector<int> att_lens;
+  const int32_t* att_len0 = nullptr;
+  const int32_t* att_pt = nullptr;
+  int32_t* att_nparts = nullptr;
   // optional per-layer traces (decode rows only; see pced_step_out)
   float* resid_trace = nullptr;
   uint16_t* qkv_trace = nullptr;
   uint16_t* act_trace = nullptr;
 };
 
-AttnPlan plan_for_lengths(const pced_ctx* c, const std::vector<int>& lens);
+AttnPlan plan_for_lengths(const pced_ctx* c, const std::vector<int>& lens, int group, bool pad);
 
 // One projection of a pass through the stack. Up to 48 rows: the split-K
 // kernel on the packed tiles, whose weight stream is the cost. More rows (the
@@ -681,9 +710,11 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
   pced_status r = PCED_OK;
   const int M = R.M, H = cfg.hidden, D = cfg.head_dim;
   const int qd = cfg.n_q_heads * D, kd = cfg.n_kv_heads * D;
-  const AttnPlan plan = plan_for_lengths(c, R.lens);
+  const int AG = c->G * R.att_tq;  // query columns per kv-head of an attention item
+  const AttnPlan plan = plan_for_lengths(c, R.att_lens, AG, R.att_tq > 1);
   if (plan.chunks > c->lay.max_work) return fail(PCED_ERR_CAPACITY, "attention plan exceeds workspace");
-  if ((size_t)M * cfg.n_kv_heads * plan.max_parts > R.part_slots)
+  // (the partial buffers hold part_slots states of G columns)
+  if ((size_t)R.att_n * cfg.n_kv_heads * plan.max_parts * AG > R.part_slots * c->G)
     return fail(PCED_ERR_CAPACITY, "attention partial states exceed workspace");
   // per-layer pool offset when the queries are not laid out per layer (the
   // kernels then address layer 0 of the offset pools)
@@ -692,13 +723,13 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
   AppendArgs ap{};  // planning blocks only: K/V rows come from the QKV epilogue
   ap.kpool = c->kpool;
   ap.vpool = c->vpool;
-  ap.len0 = R.len0;
-  ap.page_table = R.page_table;
+  ap.len0 = R.att_len0;
+  ap.page_table = R.att_pt;
   ap.chunk_info = c->at<int2>(c->lay.chunk_info);
   ap.seg = c->at<int4>(c->lay.seg);
-  ap.nparts = R.nparts;
+  ap.nparts = R.att_nparts;
   ap.work_pages = c->at<int32_t>(c->lay.work_pages);
-  ap.n_seqs = M;
+  ap.n_seqs = R.att_n;
   ap.n_layers = cfg.n_layers;
   ap.n_kv_heads = cfg.n_kv_heads;
   ap.head_dim = D;
@@ -707,6 +738,7 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
   ap.t = c->t;
   ap.n_chunks = plan.chunks;
   ap.total_pages = (int)plan.pages;
+  ap.min_pages = plan.min_pages;
   {
     ProfScope ps(c, PCED_PROF_APPEND, 0, 0);
     HIP_OK(launch_append(ap, true, st, ps.timing()));
@@ -737,31 +769,34 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
 
   AttnArgs at{};
   at.q = R.q;
-  at.len0 = R.len0;
-  at.page_table = R.page_table;
+  at.len0 = R.att_len0;
+  at.page_table = R.att_pt;
   at.chunk_info = ap.chunk_info;
   at.seg = ap.seg;
-  at.nparts = R.nparts;
+  at.nparts = R.att_nparts;
   at.work_pages = ap.work_pages;
   at.part_acc = R.part_acc;
   at.part_ml = R.part_ml;
   at.x_out = R.x;
   at.attn_out = R.per_layer_q ? R.attn_out : nullptr;
   at.hidden_out = nullptr;
-  at.n_seqs = M;
+  at.n_seqs = R.att_n;
   at.n_layers = R.per_layer_q ? cfg.n_layers : 1;
-  at.kv_reread = R.per_layer_q ? 0 : 1;  // prefill: the virtual rows of a sequence share its pages
+  at.kv_reread = R.per_layer_q ? 0 : 1;  // prefill: the token groups of a sequence share its pages
   at.n_q_heads = cfg.n_q_heads;
   at.n_kv_heads = cfg.n_kv_heads;
-  at.group = c->G;
+  at.group = AG;
+  at.tq = R.att_tq;
+  at.tq_T = R.att_T;
   at.max_pages = cfg.max_pages;
   at.maxpps = cfg.max_pages_per_seq;
   at.t = c->t;
   at.split_stride = plan.max_parts;
   at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
-  double kv_tokens = 0;
+  double kv_tokens = 0, kv_item_tokens = 0;  // keys per query row; keys read per item
   for (int r = 0; r < M; ++r) kv_tokens += R.lens[r] + 1;
-  const double attn_bytes = kv_tokens * 2.0 * kd * 2 + 2.0 * M * qd * 2;
+  for (int v = 0; v < R.att_n; ++v) kv_item_tokens += R.att_lens[v] + 1;
+  const double attn_bytes = kv_item_tokens * 2.0 * kd * 2 + 2.0 * M * qd * 2;
   const double attn_flops = kv_tokens * 4.0 * qd;
 
   GemmArgs g{};
@@ -904,6 +939,11 @@ FwdRows decode_rows(pced_ctx* c, const int32_t* in_tok, const pced_step_out* ext
   R.len0 = c->at<int32_t>(c->lay.len0);
   R.page_table = c->at<int32_t>(c->lay.page_table);
   R.nparts = c->at<int32_t>(c->lay.nparts);
+  R.att_n = R.M;
+  R.att_lens = R.lens;
+  R.att_len0 = R.len0;
+  R.att_pt = R.page_table;
+  R.att_nparts = R.nparts;
   R.tok = in_tok;
   R.tok_map = c->at<int32_t>(c->lay.seq_query);
   R.tok_stride = 1;
@@ -947,6 +987,7 @@ pced_status run_prefill_chunk(pced_ctx* c, const char* model, const int32_t* tok
   pm.i0 = i0;
   pm.n_tokens = n_tokens;
   pm.maxpps = cfg.max_pages_per_seq;
+  pm.tq = 1;
   HIP_OK(launch_prefill_meta(pm, st));
   FwdRows R;
   R.M = M;
@@ -956,6 +997,33 @@ pced_status run_prefill_chunk(pced_ctx* c, const char* model, const int32_t* tok
   R.len0 = pm.len0_out;
   R.page_table = pm.page_table_out;
   R.nparts = c->at<int32_t>(c->lay.pf_nparts);
+  // attention items: groups of tq tokens of a sequence fill the matrix cores' 16
+  // query columns per kv-head (tq x q-heads per kv-head), so each group reads
+  // the sequence's pages once for all its tokens
+  // (fewer tokens per group where the partial states of the plan would not fit)
+  const size_t part_slots = (size_t)c->lay.pf_rows * cfg.n_kv_heads * kPrefillParts;
+  int tq = std::max(1, std::min(T, kMaxGroup / c->G)), ng = 0;
+  for (;; tq = (tq + 1) / 2) {
+    ng = ceil_div(T, tq);
+    R.att_lens.resize((size_t)S * ng);
+    for (int s = 0; s < S; ++s)
+      for (int j = 0; j < ng; ++j) R.att_lens[(size_t)s * ng + j] = c->len[s] + std::min(tq * j + tq, T) - 1;
+    if (tq == 1) break;
+    const AttnPlan p = plan_for_lengths(c, R.att_lens, c->G * tq, true);
+    if ((size_t)S * ng * cfg.n_kv_heads * p.max_parts * tq <= part_slots) break;
+  }
+  PrefillMetaArgs gm = pm;
+  gm.len0_out = c->at<int32_t>(c->lay.pf_glen0);
+  gm.page_table_out = c->at<int32_t>(c->lay.pf_gpt);
+  gm.tok_map = nullptr;
+  gm.tq = tq;
+  HIP_OK(launch_prefill_meta(gm, st));
+  R.att_n = S * ng;
+  R.att_tq = tq;
+  R.att_T = T;
+  R.att_len0 = gm.len0_out;
+  R.att_pt = gm.page_table_out;
+  R.att_nparts = c->at<int32_t>(c->lay.pf_gnparts);
   R.tok = tokens;
   R.tok_map = pm.tok_map;
   R.tok_stride = 1;
@@ -969,7 +1037,7 @@ pced_status run_prefill_chunk(pced_ctx* c, const char* model, const int32_t* tok
   R.x = c->at<void>(c->lay.pf_x);
   R.part_acc = c->at<float>(c->lay.pf_part_acc);
   R.part_ml = c->at<float>(c->lay.pf_part_ml);
-  R.part_slots = (size_t)c->lay.pf_rows * cfg.n_kv_heads * kPrefillParts;
+  R.part_slots = part_slots;
   R.proj_part = c->at<float>(c->lay.pf_proj);
   R.proj_cols = M > kLmRowsPad ? c->lay.pf_proj_cols : c->lay.part_cols;
   return run_model_forward(c, model, R, st);
@@ -1038,6 +1106,7 @@ pced_status run_step(pced_ctx* c, const void* q, const void* k_new, const void* 
   ap.t = c->t;
   ap.n_chunks = plan.chunks;
   ap.total_pages = (int)plan.pages;
+  ap.min_pages = plan.min_pages;
   {
     ProfScope ps(c, PCED_PROF_APPEND, 4.0 * c->S * cfg.n_layers * cfg.n_kv_heads * cfg.head_dim * es, 0);
     HIP_OK(launch_append(ap, c->bf16, st, ps.timing()));

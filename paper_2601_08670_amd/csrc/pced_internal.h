@@ -72,6 +72,10 @@ struct AttnArgs {
   int n_seqs, n_layers, layer, n_q_heads, n_kv_heads, group;
   int max_pages, maxpps, t, split_stride, is_last_layer;
   int kv_reread;            // pages are read by several rows of the launch (prefill): plain loads
+  // prefill only: each item of the plan is a group of tq suffix tokens of one
+  // sequence (tq_T tokens per sequence in the chunk, rows s * tq_T + i), and
+  // `group` counts its tq x (Hq / Hkv) query columns per kv-head
+  int tq, tq_T;
   float scale_log2;         // log2(e) / sqrt(D)
 };
 
@@ -88,6 +92,9 @@ struct AppendArgs {
   int32_t* work_pages;
   int n_seqs, n_layers, n_kv_heads, head_dim, max_pages, maxpps, t;
   int n_chunks, total_pages;  // C and P of the balanced plan (P = pages after the append)
+  // Planned pages per sequence are at least min_pages (0, 1: none): the pages
+  // past a sequence's own read its last page again and are masked.
+  int min_pages;
 };
 
 struct LoadArgs {
@@ -232,15 +239,18 @@ struct EmbedArgs {
   int hidden, vocab, tok_stride, ld_ss;
 };
 // Rows of one prefill chunk: row r = s*T + i is sequence s's suffix token i0 + i,
-// a virtual sequence over s's pages ending at position len_s + i.
+// a virtual sequence over s's pages ending at position len_s + i. With tq > 1
+// the rows are token groups instead: row r = s*ceil(T/tq) + j covers tokens
+// tq j .. min(tq j + tq, T) - 1 and ends at its last one.
 struct PrefillMetaArgs {
   const int32_t* len0;      // [S]
   const int32_t* page_table;// [S][maxpps]
   const int32_t* seq_query; // [S]
   int32_t* len0_out;        // [S*T] len0[s] + i
   int32_t* page_table_out;  // [S*T][maxpps] copy of s's row
-  int32_t* tok_map;         // [S*T] index of the row's token in tokens [B][n_tokens]
+  int32_t* tok_map;         // [S*T] index of the row's token in tokens [B][n_tokens] (optional)
   int n_seqs, T, i0, n_tokens, maxpps;
+  int tq;                   // >= 1: one output row per group of tq tokens (len0 of its last token)
 };
 // Copy of tokens [start, start + count) of one sequence and layer out of the pool.
 struct ReadCacheArgs {

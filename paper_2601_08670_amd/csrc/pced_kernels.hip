@@ -135,7 +135,7 @@ __global__ __launch_bounds__(128) void k_append(AppendArgs a) {
   if ((int)blockIdx.x >= n_app) {
     const int s = blockIdx.x - n_app;
     const long P = a.total_pages, C = a.n_chunks;
-    auto pages_of = [&](int r) { return (a.len0[r] + a.t + 1 + kPage - 1) / kPage; };
+    auto pages_of = [&](int r) { return max(a.min_pages, (a.len0[r] + a.t + 1 + kPage - 1) / kPage); };
     // first global page of this sequence: sum over earlier sequences; the page
     // counts of the kMaxSeg sequences just before s also go to LDS for the walk
     // back below (one round of loads instead of a chain of dependent ones)
@@ -152,7 +152,7 @@ __global__ __launch_bounds__(128) void k_append(AppendArgs a) {
     for (int o = 32; o >= 1; o >>= 1) part += __shfl_xor(part, o);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = part;
     const int len = a.len0[s] + a.t + 1;
-    const int ps = (len + kPage - 1) / kPage;
+    const int ps_own = (len + kPage - 1) / kPage, ps = max(a.min_pages, ps_own);
     __syncthreads();
     const long pre = red[0] + red[1];
     const int c0 = chunk_of(pre, P, C), c1 = chunk_of(pre + ps - 1, P, C);
@@ -176,7 +176,7 @@ __global__ __launch_bounds__(128) void k_append(AppendArgs a) {
       const int i0 = (int)(lo - lo_c), pa = (int)(lo - pre);
       if (k < kMaxSeg) {
         a.seg[((size_t)c * kMaxSeg + k) * 2] = make_int4(s, i0, pa - i0, min(len, (int)(hi - pre) * kPage));
-        a.seg[((size_t)c * kMaxSeg + k) * 2 + 1] = make_int4(c - c0, c1 - c0 + 1, 0, 0);
+        a.seg[((size_t)c * kMaxSeg + k) * 2 + 1] = make_int4(c - c0, c1 - c0 + 1, len, 0);
       }
       if (hi == hi_c) a.chunk_info[c] = make_int2(k + 1, (int)(hi_c - lo_c));  // last segment of chunk c
     }
@@ -184,7 +184,7 @@ __global__ __launch_bounds__(128) void k_append(AppendArgs a) {
     for (int p = threadIdx.x; p < ps; p += blockDim.x) {
       const long u = pre + p;
       const int c = chunk_of(u, P, C);
-      a.work_pages[(size_t)c * kMaxSplitPages + (u - chunk_lo(c, P, C))] = pt[p];
+      a.work_pages[(size_t)c * kMaxSplitPages + (u - chunk_lo(c, P, C))] = pt[min(p, ps_own - 1)];
     }
     return;
   }
@@ -258,11 +258,43 @@ __global__ __launch_bounds__(128) void k_append(AppendArgs a) {
 
 // ----------------------------------------------------------- decode attention
 
+// Prefill token groups (a.tq tokens per plan item): item v is token group
+// v % ng of sequence v / ng (ng = ceil(tq_T / tq)); of its a.group columns per
+// kv-head g, column c is token c / gk of the group and q-head g gk + c % gk
+// (gk = a.group / tq). Returns the physical row (s tq_T + token) and q-head,
+// the token clamped to the group's last, and whether the token exists.
+struct MqCol {
+  int row, head, valid;
+};
+__device__ __forceinline__ MqCol mq_col(const AttnArgs& a, int v, int g, int c) {
+  const int gk = a.group / a.tq, ng = (a.tq_T + a.tq - 1) / a.tq;
+  const int s = v / ng, j = v - s * ng;
+  const int last = min(a.tq, a.tq_T - a.tq * j) - 1;
+  const int u = c / gk;
+  return MqCol{s * a.tq_T + a.tq * j + min(u, last), g * gk + c % gk, u <= last};
+}
+// Tokens between column c's own token and the last token of group v: the
+// column's keys end that many positions before the group's.
+__device__ __forceinline__ int mq_end_off(const AttnArgs& a, int v, int c) {
+  const int gk = a.group / a.tq, ng = (a.tq_T + a.tq - 1) / a.tq;
+  const int j = v % ng;
+  const int last = min(a.tq, a.tq_T - a.tq * j) - 1;
+  return last - min(c / gk, last);
+}
+
 // Write 4 consecutive output dims of one q-head: fp32 debug copy, the layer
 // output in the storage type, and (last layer) the fp32 value of the stored x.
-template <bool BF16>
+// MQ: s is a prefill token group and head = kv-head x group + column (mq_col);
+// columns of tokens past the group's end are not written.
+template <bool BF16, bool MQ = false>
 __device__ __forceinline__ void write_o4(const AttnArgs& a, int s, int head, int d, int D, float4 o) {
   const int Hq = a.n_q_heads;
+  if constexpr (MQ) {
+    const MqCol m = mq_col(a, s, head / a.group, head % a.group);
+    if (!m.valid) return;
+    s = m.row;
+    head = m.head;
+  }
   const size_t xo = (size_t)s * Hq * D + (size_t)head * D + d;
   if (a.attn_out) {
     float4* p = (float4*)(a.attn_out + (((size_t)s * a.n_layers + a.layer) * Hq + head) * D + d);
@@ -355,7 +387,7 @@ __device__ __forceinline__ void merge_group(const MergeRegs<D>& R, int j0, int n
 
 // Sum over the lane groups and store: x_out (bf16), attn_out at `layer` and,
 // for the last layer, hidden_out (fp32 of the stored x).
-template <int D>
+template <int D, bool MQ = false>
 __device__ __forceinline__ void merge_store(const AttnArgs& a, int s, int head, int layer, bool last_layer,
                                             int lane, float den, float (&num)[8]) {
 #pragma clang fp contract(off)
@@ -376,6 +408,12 @@ __device__ __forceinline__ void merge_store(const AttnArgs& a, int s, int head, 
     b[e] = f2bf(o[e]);
   }
   const int d = 8 * lane;
+  if constexpr (MQ) {  // prefill token group: the column's own row and q-head
+    const MqCol m = mq_col(a, s, head / a.group, head % a.group);
+    if (!m.valid) return;
+    s = m.row;
+    head = m.head;
+  }
   const size_t row = (size_t)s * a.n_q_heads + head;
   *(uint4*)((uint16_t*)a.x_out + row * D + d) =
       make_uint4(b[0] | (b[1] << 16), b[2] | (b[3] << 16), b[4] | (b[5] << 16), b[6] | (b[7] << 16));
@@ -392,7 +430,7 @@ __device__ __forceinline__ void merge_store(const AttnArgs& a, int s, int head, 
 }
 
 // The whole merge of item `it` whose first group is already in R.
-template <int D>
+template <int D, bool MQ = false>
 __device__ __forceinline__ void merge_item(const AttnArgs& a, MergeRegs<D>& R, const uint16_t* acc,
                                            const float* ml, int s, int g, int h, int n, int layer,
                                            bool last_layer, int lane) {
@@ -404,11 +442,11 @@ __device__ __forceinline__ void merge_item(const AttnArgs& a, MergeRegs<D>& R, c
     if (j0 > 0) merge_load<D>(R, acc, ml, w0, a.split_stride, a.group, h, j0, lane);
     merge_group<D>(R, j0, n, lane, m_run, den, num);
   }
-  merge_store<D>(a, s, g * a.group + h, layer, last_layer, lane, den, num);
+  merge_store<D, MQ>(a, s, g * a.group + h, layer, last_layer, lane, den, num);
 }
 
 // The merge as a launch of its own: one wave per item.
-template <int D>
+template <int D, bool MQ>
 __global__ __launch_bounds__(64) void k_attn_combine_bf16(AttnArgs a) {
   const int lane = threadIdx.x;
   const int G = a.group, Hkv = a.n_kv_heads;
@@ -418,7 +456,7 @@ __global__ __launch_bounds__(64) void k_attn_combine_bf16(AttnArgs a) {
   const uint16_t* acc = (const uint16_t*)a.part_acc;
   MergeRegs<D> R;
   merge_load<D>(R, acc, a.part_ml, (size_t)(s * Hkv + g) * a.split_stride, a.split_stride, G, h, 0, lane);
-  merge_item<D>(a, R, acc, a.part_ml, s, g, h, n, a.layer, a.is_last_layer != 0, lane);
+  merge_item<D, MQ>(a, R, acc, a.part_ml, s, g, h, n, a.layer, a.is_last_layer != 0, lane);
 }
 
 // fp32: one block per (sequence, kv-head); each thread owns 4 output dims of
@@ -484,6 +522,8 @@ template <int D, int RING, bool STREAM>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 2 : 1, RING <= 4 ? 8 : 1))) void k_attn_bf16(AttnArgs a) {
   constexpr int NC = D / 32;
   constexpr int NJ = D / 16;
+  // the prefill launch (pages re-read: plain loads) runs on token groups (mq_col)
+  constexpr bool MQ = !STREAM;
   // q rows of the chunk's later segments, [segment - 1][G][D]
   __shared__ __align__(16) uint16_t q_lds[kStageUnits * 64 * 8];
   // finished segments' softmax states, [segment][G][D] accumulators and
@@ -521,6 +561,14 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
   const int4 d1 = sd[2 * min(lane, kMaxSeg - 1) + 1];
   const int4 e0 = sd[0], e1 = sd[1];  // segment 0, uniform loads
   int cur_s = e0.x, cur_poff = e0.z, cur_end = e0.w, cur_j = e1.x, cur_parts = e1.y;
+  // Token groups: this lane's column ends mq_end_off keys before the group's
+  // last token, so its keys in the segment end at min(segment end, keys of the
+  // sequence - offset); a column may have none in a later split of its sequence.
+  int col_end = cur_end;
+  if constexpr (MQ) col_end = min(cur_end, e1.z - mq_end_off(a, cur_s, min(col, G - 1)));
+  // (finite start in the grouped launch: a column without keys so far gives
+  // weights 2^(-inf - m0) = 0 rather than NaN)
+  constexpr float m0 = MQ ? -1e30f : kNegInf;
 
   const size_t q_layer = (size_t)a.layer * a.n_q_heads + (size_t)g * G;
   bf16x8 qop[NC];
@@ -528,8 +576,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
     // Columns past the group repeat its last head: their scores and outputs are
     // never stored, and the loads stay unconditional, so waiting for the page
     // ids below does not also wait for these.
-    const uint16_t* q = (const uint16_t*)a.q +
-        ((size_t)cur_s * a.n_layers * a.n_q_heads + q_layer + min(col, G - 1)) * D;
+    size_t qrow = (size_t)cur_s * a.n_layers * a.n_q_heads + q_layer + min(col, G - 1);
+    if constexpr (MQ) {
+      const MqCol m = mq_col(a, cur_s, g, min(col, G - 1));
+      qrow = (size_t)m.row * a.n_q_heads + m.head;
+    }
+    const uint16_t* q = (const uint16_t*)a.q + qrow * D;
 #pragma unroll
     for (int i = 0; i < NC; ++i) qop[i] = as_bf16x8(*(const uint4*)(q + 32 * i + 8 * quad));
   }
@@ -561,7 +613,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
   // m_ref per head, shared by the head's four lanes. m_ref (and the accumulators)
   // only move when some score of the page exceeds m_ref + 8, so weights stay
   // <= 2^8 and the common page needs neither cross-lane traffic nor a rescale.
-  float m_ref = kNegInf, l_part = 0.f;
+  float m_ref = m0, l_part = 0.f;
   int k = 0;
   int next_i0 = nseg > 1 ? sd[2].y : 0x7fffffff;
 
@@ -578,7 +630,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
         const float4 v = *(const float4*)(sa + col * D + 16 * j + 4 * quad);
-        write_o4<true>(a, s, g * G + col, 16 * j + 4 * quad, D, make_float4(v.x * inv, v.y * inv, v.z * inv, v.w * inv));
+        write_o4<true, MQ>(a, s, g * G + col, 16 * j + 4 * quad, D,
+                           make_float4(v.x * inv, v.y * inv, v.z * inv, v.w * inv));
       }
       return;
     }
@@ -587,7 +640,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
     const size_t w = (size_t)(s * Hkv + g) * a.split_stride + part;
     uint16_t* dst = (uint16_t*)a.part_acc + w * G * D;
     for (int e = 8 * lane; e < G * D; e += 512) {
-      const float inv = 1.0f / sm[2 * (e / D) + 1];
+      const float l = sm[2 * (e / D) + 1];
+      const float inv = l > 0.f ? 1.0f / l : 0.f;  // (a token-group column with no keys here: zeros)
       const float4 v0 = *(const float4*)(sa + e), v1 = *(const float4*)(sa + e + 4);
       uint4 pk;
       pk.x = f2bf(v0.x * inv) | (f2bf(v0.y * inv) << 16);
@@ -639,10 +693,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
       cur_j = __builtin_amdgcn_readlane(d1.x, k);
       cur_parts = __builtin_amdgcn_readlane(d1.y, k);
       next_i0 = k + 1 < nseg ? __builtin_amdgcn_readlane(d0.y, k + 1) : 0x7fffffff;
+      col_end = cur_end;
+      if constexpr (MQ)
+        col_end = min(cur_end, __builtin_amdgcn_readlane(d1.z, k) - mq_end_off(a, cur_s, min(col, G - 1)));
       const uint16_t* qs = q_lds + ((k - 1) * G + min(col, G - 1)) * D + 8 * quad;
 #pragma unroll
       for (int cc = 0; cc < NC; ++cc) qop[cc] = as_bf16x8(*(const uint4*)(qs + 32 * cc));
-      m_ref = kNegInf;
+      m_ref = m0;
       l_part = 0.f;
 #pragma unroll
       for (int j = 0; j < NJ; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -654,7 +711,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
     const int tb = (i + cur_poff) * kPage + 4 * quad;  // token of element r = 0 in the sequence
     float z[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) z[r] = (tb + r < cur_end) ? sc[r] * a.scale_log2 : kNegInf;
+    for (int r = 0; r < 4; ++r) z[r] = (tb + r < col_end) ? sc[r] * a.scale_log2 : kNegInf;
     const float zmax = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
     if (__builtin_amdgcn_ballot_w64(zmax > m_ref + 8.0f) != 0) {
       float mx = fmaxf(zmax, __shfl_xor(zmax, 16));
@@ -724,9 +781,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
     const bool valid = u < n_units;
     const int kk = min(1 + u / per_seg, kMaxSeg - 1), rem = valid ? u % per_seg : 0;
     const int sk = valid ? __shfl(d0.x, kk) : e0.x;
-    return *(const uint4*)((const uint16_t*)a.q +
-                           ((size_t)sk * a.n_layers * a.n_q_heads + q_layer + rem / (D / 8)) * D +
-                           8 * (rem % (D / 8)));
+    size_t qrow = (size_t)sk * a.n_layers * a.n_q_heads + q_layer + rem / (D / 8);
+    if constexpr (MQ) {
+      const MqCol m = mq_col(a, sk, g, rem / (D / 8));
+      qrow = (size_t)m.row * a.n_q_heads + m.head;
+    }
+    return *(const uint4*)((const uint16_t*)a.q + qrow * D + 8 * (rem % (D / 8)));
   };
   stg0 = stage(0);
   stg1 = stage(1);
@@ -734,7 +794,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
   stg3 = stage(3);
   for (int it = blockIdx.x; it < n_mrg; it += gridDim.x) {
     if (it != (int)blockIdx.x) mrg_item(it);
-    merge_item<D>(a, mr, a.mrg_acc, a.mrg_ml, m_s, m_g, m_h, m_n, a.mrg_layer, false, lane);
+    merge_item<D, MQ>(a, mr, a.mrg_acc, a.mrg_ml, m_s, m_g, m_h, m_n, a.mrg_layer, false, lane);
   }
   for (int i = 0; i < np; i += RING) {
 #pragma unroll
@@ -2470,10 +2530,12 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
 
 // Metadata of a prefill chunk's rows (see PrefillMetaArgs): one block per row.
 __global__ __launch_bounds__(64) void k_prefill_meta(PrefillMetaArgs a) {
-  const int r = blockIdx.x, s = r / a.T, i = r - s * a.T;
+  const int ng = (a.T + a.tq - 1) / a.tq;  // rows (token groups) per sequence
+  const int r = blockIdx.x, s = r / ng, j = r - s * ng;
+  const int i = min(a.tq * j + a.tq, a.T) - 1;  // the group's last token
   if (threadIdx.x == 0) {
     a.len0_out[r] = a.len0[s] + i;
-    a.tok_map[r] = a.seq_query[s] * a.n_tokens + a.i0 + i;
+    if (a.tok_map) a.tok_map[r] = a.seq_query[s] * a.n_tokens + a.i0 + i;
   }
   for (int p = threadIdx.x; p < a.maxpps; p += 64)
     a.page_table_out[(size_t)r * a.maxpps + p] = a.page_table[(size_t)s * a.maxpps + p];
@@ -2612,8 +2674,13 @@ hipError_t launch_attn_combine(const AttnArgs& a, int head_dim, int max_splits, 
   (void)max_splits;
   if (bf16) {
     const int items = blocks * a.group;
-    if (head_dim == 128) return go(k_attn_combine_bf16<128>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a);
-    if (head_dim == 64) return go(k_attn_combine_bf16<64>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a);
+    // (the prefill's token groups: kv_reread)
+    if (head_dim == 128)
+      return a.kv_reread ? go(k_attn_combine_bf16<128, true>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a)
+                         : go(k_attn_combine_bf16<128, false>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a);
+    if (head_dim == 64)
+      return a.kv_reread ? go(k_attn_combine_bf16<64, true>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a)
+                         : go(k_attn_combine_bf16<64, false>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a);
     return hipErrorInvalidValue;
   }
   return go(k_attn_combine_f32, dim3(blocks), dim3(128), 0, st, t0(tm), t1(tm), a, head_dim);
@@ -2729,7 +2796,8 @@ hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Ti
 }
 
 hipError_t launch_prefill_meta(const PrefillMetaArgs& a, hipStream_t st) {
-  return go(k_prefill_meta, dim3(a.n_seqs * a.T), dim3(64), 0, st, nullptr, nullptr, a);
+  if (a.tq < 1) return hipErrorInvalidValue;
+  return go(k_prefill_meta, dim3(a.n_seqs * ((a.T + a.tq - 1) / a.tq)), dim3(64), 0, st, nullptr, nullptr, a);
 }
 
 hipError_t launch_read_cache(const ReadCacheArgs& a, hipStream_t st) {

@@ -45,10 +45,10 @@ def _bf16(t):
     return decode_stored(_np(t).view(np.uint16), "bf16")
 
 
-def _setup(wl, spec, extra_tokens):
+def _setup(wl, spec, extra_tokens, max_attn_chunks=0):
     from paper_2601_08670_amd.session import session_for_workload
     sess = session_for_workload(wl, device=DEV, extra_tokens=extra_tokens, poison=True, ffn_dim=spec.ffn_dim,
-                                rope_theta=int(spec.rope_theta))
+                                rope_theta=int(spec.rope_theta), max_attn_chunks=max_attn_chunks)
     model = sess.pack_model(lambda l: [spec.device(n, l, DEV) for n in LAYER_TENSORS],
                             spec.device("embed", 0, DEV), spec.device("final_norm", 0, DEV))
     Wt = sess.pack_lm_head(wl.lm_head_device(DEV))
@@ -143,8 +143,8 @@ def _teach_prefill(sess, wl, orc, lens0, n_tok):
     return kv_rows
 
 
-def _run(wl, spec, steps, prefill=0, seed=1):
-    sess, model, Wt = _setup(wl, spec, extra_tokens=steps + prefill + 1)
+def _run(wl, spec, steps, prefill=0, seed=1, max_attn_chunks=0):
+    sess, model, Wt = _setup(wl, spec, extra_tokens=steps + prefill + 1, max_attn_chunks=max_attn_chunks)
     orc = _oracle(wl, spec)
     B, V = wl.n_queries, wl.geom.vocab
     lens0 = sess.lengths()
@@ -214,6 +214,27 @@ def test_model_llama3_8b_layer_shapes():
     wl = W.custom(geom, [8], rng.integers(100, 700, size=8).tolist(), amateur_len=64, steps=2, seed=24)
     spec = ModelSpec(geom, ffn_dim=14336, rope_theta=500000.0, seed=24)
     _run(wl, spec, steps=2, prefill=20)
+
+
+@pytest.mark.parametrize("case", [
+    # (name, q-heads, kv-heads, hidden, attention chunk cap)
+    ("4-per-kv-head-groups-of-4", 8, 2, 512, 0),
+    ("2-per-kv-head-groups-of-8-padded-items", 8, 4, 512, 5),
+    ("1-per-kv-head-groups-of-16-padded-items", 4, 4, 256, 6),
+    ("16-per-kv-head-token-rows", 16, 1, 1024, 0),
+], ids=lambda c: c[0])
+def test_model_prefill_token_groups(case):
+    """Two layers, so the second layer's K/V rows check the first layer's
+    prefill attention: the prefill's attention items are groups of suffix
+    tokens of one sequence (16 / (q-heads per kv-head) tokens; 21 tokens leave a
+    ragged last group), each token with its own causal end. A small chunk cap
+    pads the plan's short items to the chunk length and splits the long ones,
+    so later splits hold columns without keys and pages past the items' own."""
+    _, hq, hkv, hidden, cap = case
+    geom = W.Geometry(2, hq, hkv, 64, hidden, 1000, "bf16")
+    wl = W.custom(geom, [3, 2], [40, 300, 17, 5, 129], amateur_len=9, steps=1, seed=26)
+    spec = ModelSpec(geom, ffn_dim=2 * hidden, rope_theta=10000.0, seed=26)
+    _run(wl, spec, steps=1, prefill=21, max_attn_chunks=cap)
 
 
 def test_model_generate_equals_checked_steps():
