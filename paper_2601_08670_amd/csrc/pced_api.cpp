@@ -80,7 +80,7 @@ struct Layout {
       load_items, src_k, src_v, meta_end;
   size_t chunk_info, seg, nparts, work_pages, prev_tok, beta, part_acc, part_ml, x, logits,
       rho, x_packed, fuse_part, lse_part, jsd_part, agg_lse, syn_q, syn_k, syn_v, dec_h, dec_a, dec_act, dec_ss, dec_rho, dec_part,
-      pf_len0, pf_pt, pf_tok, pf_nparts, pf_glen0, pf_gpt, pf_gnparts, pf_h, pf_a, pf_act, pf_ss, pf_q, pf_x, pf_part_acc, pf_part_ml, pf_proj,
+      rope, pf_len0, pf_pt, pf_tok, pf_nparts, pf_glen0, pf_gpt, pf_gnparts, pf_rho, pf_h, pf_a, pf_act, pf_ss, pf_q, pf_x, pf_part_acc, pf_part_ml, pf_proj,
       total;
   int pf_rows;          // rows of one prefill chunk (sequences x suffix tokens)
   size_t pf_proj_cols;  // slices x columns per row of the prefill projection partials
@@ -155,6 +155,8 @@ Layout make_layout(const pced_config& c) {
   L.dec_act = take(dec * S * c.ffn_dim * 2);
   L.dec_ss = take(dec * (c.hidden / 16) * S * 4);
   L.dec_rho = take(dec * S * 4);
+  // RoPE (cos, sin) per position and pair, written by pced_load_caches
+  L.rope = take(dec * (size_t)c.max_pages_per_seq * kPage * (c.head_dim / 2) * 8);
   // K-slice partial sums of a projection: [slices][S][columns]
   L.part_cols = (size_t)kProjMaxSplit *
                 std::max<size_t>({(size_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim, (size_t)c.hidden,
@@ -177,6 +179,7 @@ Layout make_layout(const pced_config& c) {
   L.pf_glen0 = take(PR * 4);
   L.pf_gpt = take(PR * c.max_pages_per_seq * 4);
   L.pf_gnparts = take(PR * 4);
+  L.pf_rho = take(PR * 4);
   L.pf_h = take(PR * c.hidden * 4);
   L.pf_a = take(PR * c.hidden * 2);
   L.pf_act = take(PR * c.ffn_dim * 2);
@@ -654,6 +657,7 @@ struct FwdRows {
   float* proj_part = nullptr;
   size_t proj_cols = 0;              // slices x columns per row of the projection partials
   float* attn_out = nullptr;
+  float* rho_rows = nullptr;         // device [M]: the many-row epilogues' row scales
   // The attention's items: the rows (att_tq = 1), or for the prefill groups of
   // att_tq suffix tokens of one sequence (att_T tokens per sequence), each item
   // ending at its last token; the kernels give a group's tokens their own
@@ -821,8 +825,10 @@ pced_status run_model_forward(pced_ctx* c, const char* model, const FwdRows& R, 
   g.maxpps = cfg.max_pages_per_seq;
   g.t = c->t;
   g.log2_theta = std::log2((double)cfg.rope_theta);
+  g.rope = c->at<float2>(c->lay.rope);
   g.num_cus = c->num_cus;
   g.part = R.proj_part;
+  g.rho_rows = R.rho_rows;
   // K slices per projection: about one block per compute unit, more where the
   // staged x slice would not fit in LDS
   const int stage_rows = std::min(M, M <= 16 ? 16 : M <= 32 ? 32 : 48);
@@ -951,13 +957,14 @@ FwdRows decode_rows(pced_ctx* c, const int32_t* in_tok, const pced_step_out* ext
   R.a = c->at<uint16_t>(c->lay.dec_a);
   R.act = c->at<uint16_t>(c->lay.dec_act);
   R.ss = c->at<float>(c->lay.dec_ss);
-  R.ld_ss = cfg.max_seqs;
+  R.ld_ss = cfg.hidden / 16;
   R.q = c->at<uint16_t>(c->lay.syn_q);
   R.per_layer_q = true;
   R.x = c->at<void>(c->lay.x);
   R.part_acc = c->at<float>(c->lay.part_acc);
   R.part_ml = c->at<float>(c->lay.part_ml);
   R.part_slots = c->lay.part_slots;
+  R.rho_rows = c->at<float>(c->lay.dec_rho);  // (the final norm's scales are computed after the layers)
   R.proj_part = c->at<float>(c->lay.dec_part);
   R.proj_cols = c->lay.part_cols;
   if (extra) {
@@ -1031,13 +1038,14 @@ pced_status run_prefill_chunk(pced_ctx* c, const char* model, const int32_t* tok
   R.a = c->at<uint16_t>(c->lay.pf_a);
   R.act = c->at<uint16_t>(c->lay.pf_act);
   R.ss = c->at<float>(c->lay.pf_ss);
-  R.ld_ss = c->lay.pf_rows;
+  R.ld_ss = cfg.hidden / 16;
   R.q = c->at<uint16_t>(c->lay.pf_q);
   R.per_layer_q = false;
   R.x = c->at<void>(c->lay.pf_x);
   R.part_acc = c->at<float>(c->lay.pf_part_acc);
   R.part_ml = c->at<float>(c->lay.pf_part_ml);
   R.part_slots = part_slots;
+  R.rho_rows = c->at<float>(c->lay.pf_rho);
   R.proj_part = c->at<float>(c->lay.pf_proj);
   R.proj_cols = M > kLmRowsPad ? c->lay.pf_proj_cols : c->lay.part_cols;
   return run_model_forward(c, model, R, st);
@@ -1060,7 +1068,7 @@ pced_status run_model_step(pced_ctx* c, const void* model, const void* w, const 
   if (r != PCED_OK) return r;
   const pced_config& cfg = c->cfg;
   float* rho = c->at<float>(c->lay.dec_rho);
-  HIP_OK(launch_rho(c->at<float>(c->lay.dec_ss), cfg.hidden / 16, cfg.max_seqs, c->S, 1.0f / (float)cfg.hidden,
+  HIP_OK(launch_rho(c->at<float>(c->lay.dec_ss), cfg.hidden / 16, cfg.hidden / 16, c->S, 1.0f / (float)cfg.hidden,
                     1e-5f, rho, st));
   r = run_head(c, c->at<void>(c->lay.dec_a), rho, w, tokens_out, tok_stride, extra, st);
   if (r != PCED_OK) return r;
@@ -1386,6 +1394,9 @@ pced_status pced_load_caches(pced_ctx* c, int32_t n_queries, const int32_t* n_ex
   // per-batch device state
   HIP_OK(launch_fill_i32(c->at<int32_t>(L.prev_tok), -1, cfg.max_queries, st));
   HIP_OK(launch_zero_bytes(c->at<void>(L.x), (size_t)L.rows_pad * cfg.hidden * esize_of(cfg), st));
+  if (cfg.ffn_dim > 0)
+    HIP_OK(launch_rope_table(c->at<float2>(L.rope), cfg.max_pages_per_seq * kPage, cfg.head_dim,
+                             std::log2((double)cfg.rope_theta), st));
   HIP_OK(hipMemcpyAsync(c->at<float>(L.beta), c->at<float>(L.beta_fixed), (size_t)NE * 4,
                         hipMemcpyDeviceToDevice, st));
 

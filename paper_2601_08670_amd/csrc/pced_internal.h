@@ -205,14 +205,18 @@ struct GemmArgs {
   int ksplit;               // K slices (blocks per column group)
   float* part;              // [ksplit][M][16 n_tiles] fp32 partial sums
   // row scale rho_m = 1/sqrt(sum_p ss_in[p][m] * inv_norm_dim + eps), or 1 without ss_in
-  const float* ss_in;       // [ss_parts][ld_ss]
+  const float* ss_in;       // [M][ld_ss]: row m's per-16-column sums at m * ld_ss + p, p < ss_parts
+  // many-row epilogues (launch_proj_epilogue): [M] scratch that receives the row
+  // scales of ss_in once (k_rho), read as rho_in instead of a sum in every block
+  float* rho_rows;
+  const float* rho_in;
   int ss_parts, ld_ss;
   float inv_norm_dim, eps;
   // kEpiResid: h[m][n] += out; a_out = bf16(h * g_next); ss_out[n / 16][m] = sum of h^2 over the tile
   float* h;                 // [M][hidden]
   uint16_t* a_out;          // [M][hidden]
   const uint16_t* g_next;   // [hidden]
-  float* ss_out;            // [hidden/16][ld_ss]
+  float* ss_out;            // [rows][ld_ss], ld_ss >= hidden/16
   // kEpiSwiglu: tiles alternate gate / up; act[m][f] = bf16(silu(gate) * up)
   uint16_t* act;            // [M][F]
   int F;
@@ -226,6 +230,9 @@ struct GemmArgs {
   const int32_t* page_table;
   int layer, n_layers, n_q_heads, n_kv_heads, head_dim, max_pages, maxpps, t;
   double log2_theta;
+  // [maxpps * page][head_dim / 2]: (cos, sin) of RoPE angle pos * theta^(-2i/D)
+  // for each position and pair i (launch_rope_table)
+  const float2* rope;
   int num_cus;              // compute units of the device (choice of the many-row path)
 };
 struct EmbedArgs {
@@ -235,7 +242,7 @@ struct EmbedArgs {
   const int32_t* seq_query; // [S]
   float* h;                 // [S][hidden]
   uint16_t* a_out;          // [S][hidden] bf16(h * g)
-  float* ss_out;            // [hidden/16][ld_ss]
+  float* ss_out;            // [rows][ld_ss], ld_ss >= hidden/16
   int hidden, vocab, tok_stride, ld_ss;
 };
 // Rows of one prefill chunk: row r = s*T + i is sequence s's suffix token i0 + i,
@@ -316,5 +323,7 @@ constexpr size_t kNoAllocScratchBytes = (size_t)4 << 20;
 hipError_t noalloc_scratch(void** out);
 hipError_t launch_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps, float* rho,
                       hipStream_t st);
+// RoPE table of GemmArgs::rope for positions 0 .. positions - 1, in fp64 rounded to fp32
+hipError_t launch_rope_table(float2* out, int positions, int head_dim, double log2_theta, hipStream_t st);
 
 }  // namespace pced

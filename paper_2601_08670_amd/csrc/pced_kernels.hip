@@ -387,7 +387,7 @@ __device__ __forceinline__ void merge_group(const MergeRegs<D>& R, int j0, int n
 
 // Sum over the lane groups and store: x_out (bf16), attn_out at `layer` and,
 // for the last layer, hidden_out (fp32 of the stored x).
-template <int D, bool MQ = false>
+template <int D>
 __device__ __forceinline__ void merge_store(const AttnArgs& a, int s, int head, int layer, bool last_layer,
                                             int lane, float den, float (&num)[8]) {
 #pragma clang fp contract(off)
@@ -408,12 +408,6 @@ __device__ __forceinline__ void merge_store(const AttnArgs& a, int s, int head, 
     b[e] = f2bf(o[e]);
   }
   const int d = 8 * lane;
-  if constexpr (MQ) {  // prefill token group: the column's own row and q-head
-    const MqCol m = mq_col(a, s, head / a.group, head % a.group);
-    if (!m.valid) return;
-    s = m.row;
-    head = m.head;
-  }
   const size_t row = (size_t)s * a.n_q_heads + head;
   *(uint4*)((uint16_t*)a.x_out + row * D + d) =
       make_uint4(b[0] | (b[1] << 16), b[2] | (b[3] << 16), b[4] | (b[5] << 16), b[6] | (b[7] << 16));
@@ -430,7 +424,7 @@ __device__ __forceinline__ void merge_store(const AttnArgs& a, int s, int head, 
 }
 
 // The whole merge of item `it` whose first group is already in R.
-template <int D, bool MQ = false>
+template <int D>
 __device__ __forceinline__ void merge_item(const AttnArgs& a, MergeRegs<D>& R, const uint16_t* acc,
                                            const float* ml, int s, int g, int h, int n, int layer,
                                            bool last_layer, int lane) {
@@ -442,11 +436,11 @@ __device__ __forceinline__ void merge_item(const AttnArgs& a, MergeRegs<D>& R, c
     if (j0 > 0) merge_load<D>(R, acc, ml, w0, a.split_stride, a.group, h, j0, lane);
     merge_group<D>(R, j0, n, lane, m_run, den, num);
   }
-  merge_store<D, MQ>(a, s, g * a.group + h, layer, last_layer, lane, den, num);
+  merge_store<D>(a, s, g * a.group + h, layer, last_layer, lane, den, num);
 }
 
 // The merge as a launch of its own: one wave per item.
-template <int D, bool MQ>
+template <int D>
 __global__ __launch_bounds__(64) void k_attn_combine_bf16(AttnArgs a) {
   const int lane = threadIdx.x;
   const int G = a.group, Hkv = a.n_kv_heads;
@@ -456,7 +450,65 @@ __global__ __launch_bounds__(64) void k_attn_combine_bf16(AttnArgs a) {
   const uint16_t* acc = (const uint16_t*)a.part_acc;
   MergeRegs<D> R;
   merge_load<D>(R, acc, a.part_ml, (size_t)(s * Hkv + g) * a.split_stride, a.split_stride, G, h, 0, lane);
-  merge_item<D, MQ>(a, R, acc, a.part_ml, s, g, h, n, a.layer, a.is_last_layer != 0, lane);
+  merge_item<D>(a, R, acc, a.part_ml, s, g, h, n, a.layer, a.is_last_layer != 0, lane);
+}
+
+// The merge for the prefill's token groups, whose items are many and mostly
+// split in a few parts: one wave per (item, kv-head), each lane merging whole
+// 8-dim units (column h, dims d .. d+7) over the parts in order, with the same
+// formula as above (m* = max_j m_j, weights l_j 2^(m_j - m*) on the stored
+// normalised outputs) and no cross-lane traffic. Parts of a column without keys
+// hold l = 0 and zeros.
+template <int D>
+__global__ __launch_bounds__(256) void k_attn_combine_mq(AttnArgs a) {
+#pragma clang fp contract(off)
+  const int lane = threadIdx.x & 63;
+  const int G = a.group, Hkv = a.n_kv_heads;
+  const int wv = blockIdx.x * 4 + (int)(threadIdx.x >> 6);
+  if (wv >= a.n_seqs * Hkv) return;
+  const int s = wv / Hkv, g = wv - s * Hkv;
+  const int n = a.nparts[s];
+  if (n <= 1) return;  // written directly by the attention kernel
+  const size_t w0 = (size_t)wv * a.split_stride;
+  const uint16_t* acc = (const uint16_t*)a.part_acc;
+  for (int u = lane; u < G * (D / 8); u += 64) {
+    const int h = u / (D / 8), d = 8 * (u % (D / 8));
+    float mx = kNegInf;
+    for (int j = 0; j < n; ++j) mx = fmaxf(mx, a.part_ml[((w0 + j) * G + h) * 2]);
+    float den = 0.f, num[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < n; ++j) {
+      const float2 ml = *(const float2*)(a.part_ml + ((w0 + j) * G + h) * 2);
+      const uint4 v = *(const uint4*)(acc + ((w0 + j) * G + h) * D + d);
+      const float wt = ml.y * exp2f(ml.x - mx);
+      den += wt;
+      const uint32_t b[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) num[e] = fmaf(bf2f((b[e >> 1] >> (16 * (e & 1))) & 0xFFFFu), wt, num[e]);
+    }
+    const MqCol m = mq_col(a, s, g, h);
+    if (!m.valid) continue;
+    const float inv = 1.0f / den;
+    float o[8];
+    uint32_t bb[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      o[e] = num[e] * inv;
+      bb[e] = f2bf(o[e]);
+    }
+    const size_t row = (size_t)m.row * a.n_q_heads + m.head;
+    *(uint4*)((uint16_t*)a.x_out + row * D + d) = make_uint4(bb[0] | (bb[1] << 16), bb[2] | (bb[3] << 16),
+                                                            bb[4] | (bb[5] << 16), bb[6] | (bb[7] << 16));
+    if (a.attn_out) {
+      float* p = a.attn_out + (((size_t)m.row * a.n_layers + a.layer) * a.n_q_heads + m.head) * D + d;
+      *(float4*)p = make_float4(o[0], o[1], o[2], o[3]);
+      *(float4*)(p + 4) = make_float4(o[4], o[5], o[6], o[7]);
+    }
+    if (a.is_last_layer && a.hidden_out) {
+      float* p = a.hidden_out + row * D + d;
+      *(float4*)p = make_float4(bf2f(bb[0]), bf2f(bb[1]), bf2f(bb[2]), bf2f(bb[3]));
+      *(float4*)(p + 4) = make_float4(bf2f(bb[4]), bf2f(bb[5]), bf2f(bb[6]), bf2f(bb[7]));
+    }
+  }
 }
 
 // fp32: one block per (sequence, kv-head); each thread owns 4 output dims of
@@ -794,7 +846,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(RING <= 4 ? 
   stg3 = stage(3);
   for (int it = blockIdx.x; it < n_mrg; it += gridDim.x) {
     if (it != (int)blockIdx.x) mrg_item(it);
-    merge_item<D, MQ>(a, mr, a.mrg_acc, a.mrg_ml, m_s, m_g, m_h, m_n, a.mrg_layer, false, lane);
+    merge_item<D>(a, mr, a.mrg_acc, a.mrg_ml, m_s, m_g, m_h, m_n, a.mrg_layer, false, lane);
   }
   for (int i = 0; i < np; i += RING) {
 #pragma unroll
@@ -2242,17 +2294,6 @@ __global__ __launch_bounds__(256) void k_synth(SynthArgs a) {
 
 constexpr int kProjWaves = 8;  // waves per projection block
 
-// sum over the ss partials of row m, 8 lanes per row (lanes 8r .. 8r+7 of a
-// wave hold row r); every lane of the group returns the total
-__device__ __forceinline__ float row_ss8(const float* ss, int parts, int ld, int m, int j, bool valid) {
-  float t = 0.f;
-  if (valid)
-    for (int p = j; p < parts; p += 8) t += ss[(size_t)p * ld + m];
-  t += __shfl_xor(t, 1);
-  t += __shfl_xor(t, 2);
-  t += __shfl_xor(t, 4);
-  return t;
-}
 
 // Decoder projection for the rows of one decode step (M rows, in groups of up
 // to 16 NT): K-slice partial sums part[split][m][n] = sum_{k in slice}
@@ -2403,17 +2444,22 @@ __global__ __launch_bounds__(256) void k_proj_reduce(GemmArgs a) {
   float4 h_in = make_float4(0.f, 0.f, 0.f, 0.f);
   uint2 g_in = make_uint2(0u, 0u);
   int pos = 0, phys = 0;
+  float4 rope = make_float4(1.f, 0.f, 1.f, 0.f);
   if constexpr (EPI == kEpiResid) {
     h_in = *(const float4*)(a.h + (size_t)m * N + nc);  // residual row stride: hidden = N
     g_in = *(const uint2*)(a.g_next + nc);
   } else if constexpr (EPI == kEpiQkv) {
     pos = a.len0[m] + a.t;
     phys = a.page_table[(size_t)m * a.maxpps + pos / kPage];
+    // (cos, sin) of the pairs (nc % D) / 2 and + 1 (q and k sections start at multiples of D)
+    rope = *(const float4*)(a.rope + (size_t)pos * (a.head_dim / 2) + (nc % a.head_dim) / 2);
   }
   float rho = 1.0f;
-  if (EPI != kEpiResid && a.ss_in) {
+  if (EPI != kEpiResid && a.rho_in) {
+    rho = a.rho_in[m];
+  } else if (EPI != kEpiResid && a.ss_in) {
     float t = 0.f;
-    for (int p = threadIdx.x; p < a.ss_parts; p += 256) t += a.ss_in[(size_t)p * a.ld_ss + m];
+    for (int p = threadIdx.x; p < a.ss_parts; p += 256) t += a.ss_in[(size_t)m * a.ld_ss + p];
     rho = 1.0f / sqrtf(block_reduce_sum(t) * a.inv_norm_dim + a.eps);
   }
   if constexpr (EPI == kEpiSwiglu) {
@@ -2466,7 +2512,7 @@ __global__ __launch_bounds__(256) void k_proj_reduce(GemmArgs a) {
     }
     ss += __shfl_xor(ss, 1);
     ss += __shfl_xor(ss, 2);
-    if (valid && (c4 & 3) == 0) a.ss_out[(size_t)(n0 / 16) * a.ld_ss + m] = ss;
+    if (valid && (c4 & 3) == 0) a.ss_out[(size_t)m * a.ld_ss + n0 / 16] = ss;
   } else {  // kEpiQkv
     if (!valid) return;
     const int D = a.head_dim, qd = a.n_q_heads * D, kd = a.n_kv_heads * D;
@@ -2478,11 +2524,7 @@ __global__ __launch_bounds__(256) void k_proj_reduce(GemmArgs a) {
     if (sec < 2) {
 #pragma unroll
       for (int pr = 0; pr < 2; ++pr) {
-        const int i = d / 2 + pr;
-        const double ang = (double)pos * exp2(-(2.0 * i / D) * a.log2_theta);
-        double sn, cs;
-        sincos(ang, &sn, &cs);
-        const float c = (float)cs, s_ = (float)sn;
+        const float c = pr ? rope.z : rope.x, s_ = pr ? rope.w : rope.y;
         const float x0 = o[2 * pr], x1 = o[2 * pr + 1];
         o[2 * pr] = x0 * c - x1 * s_;
         o[2 * pr + 1] = x0 * s_ + x1 * c;
@@ -2524,7 +2566,7 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
     float ss = h0 * h0 + h1 * h1 + h2 * h2 + h3 * h3;
     ss += __shfl_xor(ss, 1);
     ss += __shfl_xor(ss, 2);
-    if ((j & 3) == 0) a.ss_out[(size_t)(j / 4) * a.ld_ss + s] = ss;
+    if ((j & 3) == 0) a.ss_out[(size_t)s * a.ld_ss + j / 4] = ss;
   }
 }
 
@@ -2585,13 +2627,29 @@ __global__ __launch_bounds__(256) void k_stream_read(const uint4* __restrict__ p
   if ((threadIdx.x & 63) == 0) atomicXor(out, x);
 }
 
-// rho[m] = 1/sqrt(sum_p ss[p][m] * inv_dim + eps), 8 lanes per row.
+// RoPE table: (cos, sin) of pos * theta^(-2i/D) in fp64, rounded to fp32.
+__global__ __launch_bounds__(256) void k_rope_table(float2* out, int P, int D, double log2_theta) {
+  const int half = D / 2;
+  for (size_t e = blockIdx.x * (size_t)256 + threadIdx.x; e < (size_t)P * half; e += (size_t)gridDim.x * 256) {
+    const int pos = (int)(e / half), i = (int)(e % half);
+    const double ang = (double)pos * exp2(-(2.0 * i / D) * log2_theta);
+    double sn, cs;
+    sincos(ang, &sn, &cs);
+    out[e] = make_float2((float)cs, (float)sn);
+  }
+}
+
+// rho[m] = 1/sqrt(sum_p ss[m][p] * inv_dim + eps) (row stride ld).
 __global__ __launch_bounds__(256) void k_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps,
                                              float* rho) {
-  const int t = blockIdx.x * 256 + threadIdx.x;
-  const int m = t >> 3;
-  const float tot = row_ss8(ss, parts, ld, m, t & 7, m < M);
-  if ((t & 7) == 0 && m < M) rho[m] = 1.0f / sqrtf(tot * inv_dim + eps);
+  // one wave per row: its partial sums are contiguous
+  const int m = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (m >= M) return;
+  float t = 0.f;
+  for (int p = lane; p < parts; p += 64) t += ss[(size_t)m * ld + p];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) t += __shfl_xor(t, o);
+  if (lane == 0) rho[m] = 1.0f / sqrtf(t * inv_dim + eps);
 }
 
 }  // namespace
@@ -2674,13 +2732,14 @@ hipError_t launch_attn_combine(const AttnArgs& a, int head_dim, int max_splits, 
   (void)max_splits;
   if (bf16) {
     const int items = blocks * a.group;
-    // (the prefill's token groups: kv_reread)
+    // the prefill's token groups (kv_reread): a wave per (item, kv-head)
+    const dim3 mq((blocks + 3) / 4);
     if (head_dim == 128)
-      return a.kv_reread ? go(k_attn_combine_bf16<128, true>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a)
-                         : go(k_attn_combine_bf16<128, false>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a);
+      return a.kv_reread ? go(k_attn_combine_mq<128>, mq, dim3(256), 0, st, t0(tm), t1(tm), a)
+                         : go(k_attn_combine_bf16<128>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a);
     if (head_dim == 64)
-      return a.kv_reread ? go(k_attn_combine_bf16<64, true>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a)
-                         : go(k_attn_combine_bf16<64, false>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a);
+      return a.kv_reread ? go(k_attn_combine_mq<64>, mq, dim3(256), 0, st, t0(tm), t1(tm), a)
+                         : go(k_attn_combine_bf16<64>, dim3(items), dim3(64), 0, st, t0(tm), t1(tm), a);
     return hipErrorInvalidValue;
   }
   return go(k_attn_combine_f32, dim3(blocks), dim3(128), 0, st, t0(tm), t1(tm), a, head_dim);
@@ -2787,7 +2846,19 @@ hipError_t launch_proj_epilogue(const GemmArgs& a, GemmEpi epi, hipStream_t st, 
   if (a.M < 1 || a.n_tiles < 1 || (epi == kEpiSwiglu && a.n_tiles % 2)) return hipErrorInvalidValue;
   GemmArgs r = a;
   r.ksplit = 1;
+  if (epi != kEpiResid && a.ss_in && a.rho_rows) {
+    const hipError_t e = launch_rho(a.ss_in, a.ss_parts, a.ld_ss, a.M, a.inv_norm_dim, a.eps, a.rho_rows, st);
+    if (e != hipSuccess) return e;
+    r.rho_in = a.rho_rows;
+  }
   return launch_reduce(r, epi, st, t1(tm));
+}
+
+hipError_t launch_rope_table(float2* out, int positions, int head_dim, double log2_theta, hipStream_t st) {
+  if (positions < 1 || head_dim < 4 || head_dim % 4) return hipErrorInvalidValue;
+  const size_t n = (size_t)positions * (head_dim / 2);
+  return go(k_rope_table, dim3((unsigned)std::min<size_t>((n + 255) / 256, 2048)), dim3(256), 0, st, nullptr, nullptr,
+            out, positions, head_dim, log2_theta);
 }
 
 hipError_t launch_embed(const EmbedArgs& a, int n_seqs, hipStream_t st, const Timing* tm) {
@@ -2806,7 +2877,7 @@ hipError_t launch_read_cache(const ReadCacheArgs& a, hipStream_t st) {
 
 hipError_t launch_rho(const float* ss, int parts, int ld, int M, float inv_dim, float eps, float* rho,
                       hipStream_t st) {
-  return go(k_rho, dim3((M * 8 + 255) / 256), dim3(256), 0, st, nullptr, nullptr, ss, parts, ld, M, inv_dim, eps,
+  return go(k_rho, dim3((M + 3) / 4), dim3(256), 0, st, nullptr, nullptr, ss, parts, ld, M, inv_dim, eps,
             rho);
 }
 
