@@ -55,7 +55,7 @@ struct AttnArgs {
   // in a single chunk.
   const int2* chunk_info;   // [C] (segments, pages) of each chunk
   const int4* seg;          // [C][kMaxSeg][2]: {s, first page in chunk, page offset in s - first page,
-                            //  token end}, {partial index in s, partials of s, 0, 0}
+                            //  token end in this chunk}, {partial index in s, partials of s, tokens of s, 0}
   const int32_t* nparts;    // [S] partial states of each sequence (chunks it meets)
   const int32_t* work_pages;// [C][kMaxSplitPages] physical pages of each chunk
   float* part_acc;          // [S*Hkv][split_stride][G][D] partial outputs (bf16 path: normalised, as bf16)

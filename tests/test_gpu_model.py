@@ -237,6 +237,19 @@ def test_model_prefill_token_groups(case):
     _run(wl, spec, steps=1, prefill=21, max_attn_chunks=cap)
 
 
+def test_model_prefill_token_groups_long_caches():
+    """Workload-3-like caches (32 documents of 512..2048 tokens and a 64-token
+    amateur, 4 q-heads per kv-head) with a 32-token suffix: 264 groups of 4
+    tokens, the amateur's short items padded to the chunk length in the plan,
+    the documents' items split over 2..6 chunks; the second layer's K/V rows
+    check the first layer's attention for every token."""
+    geom = W.Geometry(2, 8, 2, 128, 1024, 1000, "bf16")
+    rng = np.random.default_rng(27)
+    wl = W.custom(geom, [32], rng.integers(512, 2049, size=32).tolist(), amateur_len=64, steps=1, seed=27)
+    spec = ModelSpec(geom, ffn_dim=2048, rope_theta=500000.0, seed=27)
+    _run(wl, spec, steps=1, prefill=32)
+
+
 def test_model_generate_equals_checked_steps():
     """pced_model_generate (tokens fed back on the device) against a twin
     session stepping with pced_model_step on the tokens it chose itself, each
