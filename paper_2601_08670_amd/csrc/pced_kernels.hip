@@ -2295,8 +2295,8 @@ __global__ __launch_bounds__(256) void k_synth(SynthArgs a) {
 constexpr int kProjWaves = 8;  // waves per projection block
 
 
-// Decoder projection for the rows of one decode step (M rows, in groups of up
-// to 16 NT): K-slice partial sums part[split][m][n] = sum_{k in slice}
+// Decoder projection for the rows of one decode step (M <= 16 NT <= 48 rows,
+// in the matrix cores' N dimension): K-slice partial sums part[split][m][n] = sum_{k in slice}
 // x[m][k] W[n][k] on the matrix cores, C^T[16 columns x 16 rows] += W[16 x 32]
 // X^T[32 x 16] (v_mfma_f32_16x16x32_bf16); k_proj_reduce adds the slices in
 // order and applies the projection's epilogue.
@@ -2308,7 +2308,7 @@ constexpr int kProjWaves = 8;  // waves per projection block
 // and reads its x operands from LDS, so the whole register ring holds W bytes
 // in flight. The barrier after staging waits on LDS only; it does not drain the
 // ring.
-template <int NT, int TPW, bool STREAM>
+template <int NT, int TPW>
 __global__ __launch_bounds__(64 * kProjWaves) void k_proj(GemmArgs a) {
   constexpr int WPB = kProjWaves, CT = WPB * TPW, R = TPW == 1 ? 8 : 5;
   extern __shared__ __align__(16) uint16_t xs[];
@@ -2331,74 +2331,71 @@ __global__ __launch_bounds__(64 * kProjWaves) void k_proj(GemmArgs a) {
     wt[tt] = (const uint4*)a.w + ((size_t)min(grp * CT + wave * TPW + tt, a.n_tiles - 1) * t_vb + ks0 * t_ks) * 128 +
              lane;
 
-  for (int m0 = 0; m0 < a.M; m0 += 16 * NT) {
-    const int rows = min(16 * NT, a.M - m0);
-    f32x4 acc[TPW][NT];
+  const int m0 = 0, rows = a.M;  // one row group: M <= 16 NT
+  f32x4 acc[TPW][NT];
+#pragma unroll
+  for (int tt = 0; tt < TPW; ++tt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[tt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  struct Stage { uint4 w[TPW][2]; };
+  Stage st[R];
+  auto load = [&](Stage& S, int i) __attribute__((always_inline)) {
+    i = min(i, n - 1);  // past the end: the last step again (a cache hit), the ring stays branch-free
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      S.w[tt][0] = ld_w<true>(&wt[tt][(size_t)i * t_ks * 128]);
+      S.w[tt][1] = ld_w<true>(&wt[tt][(size_t)i * t_ks * 128 + 64]);
+    }
+  };
+  // x operand rows of this lane in LDS (rows past the group's end read the last row)
+  const uint16_t* xl[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) xl[nt] = xs + (size_t)min(16 * nt + col, rows - 1) * LDX + 16 * quad;
+  auto mma = [&](const Stage& S, int i) __attribute__((always_inline)) {
+    uint4 xv[NT][2];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      xv[nt][0] = *(const uint4*)(xl[nt] + 64 * i);
+      xv[nt][1] = *(const uint4*)(xl[nt] + 64 * i + 8);
+    }
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[tt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    struct Stage { uint4 w[TPW][2]; };
-    Stage st[R];
-    auto load = [&](Stage& S, int i) __attribute__((always_inline)) {
-      i = min(i, n - 1);  // past the end: the last step again (a cache hit), the ring stays branch-free
-#pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) {
-        S.w[tt][0] = ld_w<STREAM>(&wt[tt][(size_t)i * t_ks * 128]);
-        S.w[tt][1] = ld_w<STREAM>(&wt[tt][(size_t)i * t_ks * 128 + 64]);
+      for (int nt = 0; nt < NT; ++nt) {
+        acc[tt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[tt][0]), as_bf16x8(xv[nt][0]),
+                                                              acc[tt][nt], 0, 0, 0);
+        acc[tt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[tt][1]), as_bf16x8(xv[nt][1]),
+                                                              acc[tt][nt], 0, 0, 0);
       }
-    };
-    // x operand rows of this lane in LDS (rows past the group's end read the last row)
-    const uint16_t* xl[NT];
+  };
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) xl[nt] = xs + (size_t)min(16 * nt + col, rows - 1) * LDX + 16 * quad;
-    auto mma = [&](const Stage& S, int i) __attribute__((always_inline)) {
-      uint4 xv[NT][2];
+  for (int j = 0; j < R; ++j) load(st[j], j);
+  // stage the x slice: units of 8 elements, consecutive threads along a row
+  const int upr = 8 * n;  // units per row
+  for (int u = threadIdx.x; u < rows * upr; u += 64 * WPB) {
+    const int r = u / upr, c = u - r * upr;
+    *(uint4*)(xs + (size_t)r * LDX + 8 * c) = *(const uint4*)(a.x + (size_t)(m0 + r) * K + 64 * ks0 + 8 * c);
+  }
+  __syncthreads();
+  for (int i = 0; i < n; i += R) {
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      if (i + j < n) mma(st[j], i + j);
+      load(st[j], i + j + R);
+    }
+  }
+#pragma unroll
+  for (int tt = 0; tt < TPW; ++tt) {
+    const int tile = grp * CT + wave * TPW + tt;
+    if (tile < a.n_tiles) {
+      float* dst = a.part + (size_t)split * a.M * N + 16 * tile + 4 * quad;
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        xv[nt][0] = *(const uint4*)(xl[nt] + 64 * i);
-        xv[nt][1] = *(const uint4*)(xl[nt] + 64 * i + 8);
-      }
-#pragma unroll
-      for (int tt = 0; tt < TPW; ++tt)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          acc[tt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[tt][0]), as_bf16x8(xv[nt][0]),
-                                                                acc[tt][nt], 0, 0, 0);
-          acc[tt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(S.w[tt][1]), as_bf16x8(xv[nt][1]),
-                                                                acc[tt][nt], 0, 0, 0);
-        }
-    };
-#pragma unroll
-    for (int j = 0; j < R; ++j) load(st[j], j);
-    // stage the x slice: units of 8 elements, consecutive threads along a row
-    const int upr = 8 * n;  // units per row
-    for (int u = threadIdx.x; u < rows * upr; u += 64 * WPB) {
-      const int r = u / upr, c = u - r * upr;
-      *(uint4*)(xs + (size_t)r * LDX + 8 * c) = *(const uint4*)(a.x + (size_t)(m0 + r) * K + 64 * ks0 + 8 * c);
-    }
-    __syncthreads();
-    for (int i = 0; i < n; i += R) {
-#pragma unroll
-      for (int j = 0; j < R; ++j) {
-        if (i + j < n) mma(st[j], i + j);
-        load(st[j], i + j + R);
+        const int m = m0 + 16 * nt + col;
+        if (m < a.M)
+          *(float4*)(dst + (size_t)m * N) = make_float4(acc[tt][nt][0], acc[tt][nt][1], acc[tt][nt][2], acc[tt][nt][3]);
       }
     }
-#pragma unroll
-    for (int tt = 0; tt < TPW; ++tt) {
-      const int tile = grp * CT + wave * TPW + tt;
-      if (tile < a.n_tiles) {
-        float* dst = a.part + (size_t)split * a.M * N + 16 * tile + 4 * quad;
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int m = m0 + 16 * nt + col;
-          if (m < a.M)
-            *(float4*)(dst + (size_t)m * N) = make_float4(acc[tt][nt][0], acc[tt][nt][1], acc[tt][nt][2], acc[tt][nt][3]);
-        }
-      }
-    }
-    __syncthreads();  // the next row group restages xs
   }
 }
 
@@ -2793,51 +2790,26 @@ hipError_t launch_reduce(const GemmArgs& a, GemmEpi epi, hipStream_t st, hipEven
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t st, const Timing* tm) {
-  if (a.K % 64 != 0 || a.M < 1 || a.n_tiles < 1) return hipErrorInvalidValue;
+  // up to 48 rows (three 16-row groups in the matrix cores' N dimension); more
+  // rows are dense contractions for the library GEMM (launch_proj_epilogue)
+  if (a.K % 64 != 0 || a.M < 1 || a.M > kLmRowsPad || a.n_tiles < 1) return hipErrorInvalidValue;
   if (epi == kEpiSwiglu && a.n_tiles % 2) return hipErrorInvalidValue;
-  if (a.M > kLmRowsPad && a.M <= 32 * kLmRowsMTW && a.K % 256 == 0 && kProjKMajor == kLmKMajor &&
-      a.n_tiles / 8 >= a.num_cus / 2) {
-    // 49..288 rows (the prefill's chunks) of a wide projection (gate/up: a
-    // 128-column block for at least every other compute unit): the many-row
-    // LM-head kernel reads W once for all rows (the split-K kernel re-reads it
-    // per 48-row group) and writes the plain products as a single K slice; the
-    // reduce applies the epilogue (the norm's row scale included). Narrower
-    // projections would leave most compute units idle and keep split-K.
-    LmArgs l{};
-    l.x = a.x;
-    l.w = a.w;
-    l.logits = a.part;
-    l.M = a.M;
-    l.V = 16 * a.n_tiles;
-    l.K = a.K;
-    l.rms = 0;
-    l.row_groups = 1;
-    const Timing start{tm ? tm->start : nullptr, nullptr};
-    const hipError_t e = launch_lmhead(l, true, st, tm ? &start : nullptr);
-    if (e != hipSuccess) return e;
-    GemmArgs r = a;
-    r.ksplit = 1;
-    return launch_reduce(r, epi, st, t1(tm));
-  }
   if (a.ksplit < 1 || a.ksplit > a.K / 64) return hipErrorInvalidValue;
   const int NT = a.M <= 16 ? 1 : a.M <= 32 ? 2 : 3;
   const int tpw = proj_tiles_per_wave(a.n_tiles);
-  const size_t lds = proj_lds_bytes(min(a.M, 16 * NT), a.K, a.ksplit);
+  const size_t lds = proj_lds_bytes(a.M, a.K, a.ksplit);
   if (lds > kProjMaxLds) return hipErrorInvalidValue;
   const dim3 b(64 * kProjWaves);
   const dim3 g((a.n_tiles + kProjWaves * tpw - 1) / (kProjWaves * tpw) * a.ksplit);
   hipError_t e;
-  if (a.M > 16 * NT)  // several row groups: each re-reads the block's W tiles, plain loads
-    e = tpw == 1 ? go(k_proj<3, 1, false>, g, b, lds, st, t0(tm), nullptr, a)
-                 : go(k_proj<3, 2, false>, g, b, lds, st, t0(tm), nullptr, a);
-  else if (tpw == 1)
-    e = NT == 1 ? go(k_proj<1, 1, true>, g, b, lds, st, t0(tm), nullptr, a)
-        : NT == 2 ? go(k_proj<2, 1, true>, g, b, lds, st, t0(tm), nullptr, a)
-                  : go(k_proj<3, 1, true>, g, b, lds, st, t0(tm), nullptr, a);
+  if (tpw == 1)
+    e = NT == 1 ? go(k_proj<1, 1>, g, b, lds, st, t0(tm), nullptr, a)
+        : NT == 2 ? go(k_proj<2, 1>, g, b, lds, st, t0(tm), nullptr, a)
+                  : go(k_proj<3, 1>, g, b, lds, st, t0(tm), nullptr, a);
   else
-    e = NT == 1 ? go(k_proj<1, 2, true>, g, b, lds, st, t0(tm), nullptr, a)
-        : NT == 2 ? go(k_proj<2, 2, true>, g, b, lds, st, t0(tm), nullptr, a)
-                  : go(k_proj<3, 2, true>, g, b, lds, st, t0(tm), nullptr, a);
+    e = NT == 1 ? go(k_proj<1, 2>, g, b, lds, st, t0(tm), nullptr, a)
+        : NT == 2 ? go(k_proj<2, 2>, g, b, lds, st, t0(tm), nullptr, a)
+                  : go(k_proj<3, 2>, g, b, lds, st, t0(tm), nullptr, a);
   if (e != hipSuccess) return e;
   return launch_reduce(a, epi, st, t1(tm));
 }
