@@ -410,7 +410,8 @@ pced_status pced_pack_model_globals(const pced_config* cfg, const void* embed, c
  * (causal). No logits.
  *   model   device, packed weights
  *   tokens  device int32 [B][n_tokens]; ids outside [0, V) are clamped
- * Errors: STATE (nothing loaded), CAPACITY (pages), INVALID_ARG, HIP.
+ * Errors: STATE (nothing loaded), CAPACITY (pages, or an attention plan whose
+ * chunks or partial states exceed the workspace), INVALID_ARG, HIP.
  */
 pced_status pced_model_prefill(pced_ctx* ctx, const void* model, int32_t n_tokens, const int32_t* tokens,
                                hipStream_t stream);
