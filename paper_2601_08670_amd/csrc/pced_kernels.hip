@@ -2368,13 +2368,34 @@ __global__ __launch_bounds__(64 * kProjWaves) void k_proj(GemmArgs a) {
                                                               acc[tt][nt], 0, 0, 0);
       }
   };
+  // Stage the x slice: units of 8 elements, consecutive threads along a row, SB
+  // units per thread in flight at once (indices past the end repeat the last
+  // unit: same value, same place). The first batch is issued before the W ring,
+  // so its wait leaves the ring in flight; a load-then-store loop paid one
+  // memory round trip per unit with the ring stalled.
+  constexpr int SB = 8;
+  const int upr = 8 * n, units = rows * upr;  // units per row, in all
+  uint4 xv[SB];
+  int xo[SB];  // LDS element offsets of the batch's units
+#pragma unroll
+  for (int j = 0; j < SB; ++j) {
+    const int u = min((int)threadIdx.x + j * 64 * WPB, units - 1), r = u / upr, c = u - r * upr;
+    xv[j] = *(const uint4*)(a.x + (size_t)(m0 + r) * K + 64 * ks0 + 8 * c);
+    xo[j] = r * LDX + 8 * c;
+  }
 #pragma unroll
   for (int j = 0; j < R; ++j) load(st[j], j);
-  // stage the x slice: units of 8 elements, consecutive threads along a row
-  const int upr = 8 * n;  // units per row
-  for (int u = threadIdx.x; u < rows * upr; u += 64 * WPB) {
-    const int r = u / upr, c = u - r * upr;
-    *(uint4*)(xs + (size_t)r * LDX + 8 * c) = *(const uint4*)(a.x + (size_t)(m0 + r) * K + 64 * ks0 + 8 * c);
+#pragma unroll
+  for (int j = 0; j < SB; ++j) *(uint4*)(xs + xo[j]) = xv[j];
+  for (int u0 = threadIdx.x + SB * 64 * WPB; u0 < units; u0 += SB * 64 * WPB) {
+#pragma unroll
+    for (int j = 0; j < SB; ++j) {
+      const int u = min(u0 + j * 64 * WPB, units - 1), r = u / upr, c = u - r * upr;
+      xv[j] = *(const uint4*)(a.x + (size_t)(m0 + r) * K + 64 * ks0 + 8 * c);
+      xo[j] = r * LDX + 8 * c;
+    }
+#pragma unroll
+    for (int j = 0; j < SB; ++j) *(uint4*)(xs + xo[j]) = xv[j];
   }
   __syncthreads();
   for (int i = 0; i < n; i += R) {
