@@ -80,7 +80,7 @@ struct Layout {
       load_items, src_k, src_v, meta_end;
   size_t chunk_info, seg, nparts, work_pages, prev_tok, beta, part_acc, part_ml, x, logits,
       rho, x_packed, fuse_part, lse_part, jsd_part, agg_lse, syn_q, syn_k, syn_v, dec_h, dec_a, dec_act, dec_ss, dec_rho, dec_part,
-      rope, pf_len0, pf_pt, pf_tok, pf_nparts, pf_glen0, pf_gpt, pf_gnparts, pf_rho, pf_h, pf_a, pf_act, pf_ss, pf_q, pf_x, pf_part_acc, pf_part_ml, pf_proj,
+      rope, pf_len0, pf_pt, pf_tok, pf_glen0, pf_gpt, pf_nparts, pf_rho, pf_h, pf_a, pf_act, pf_ss, pf_q, pf_x, pf_part_acc, pf_part_ml, pf_proj,
       total;
   int pf_rows;          // rows of one prefill chunk (sequences x suffix tokens)
   size_t pf_proj_cols;  // slices x columns per row of the prefill projection partials
@@ -174,11 +174,10 @@ Layout make_layout(const pced_config& c) {
   L.pf_len0 = take(PR * 4);
   L.pf_pt = take(PR * c.max_pages_per_seq * 4);
   L.pf_tok = take(PR * 4);
-  L.pf_nparts = take(PR * 4);
   // the attention's token groups (at most one per row)
   L.pf_glen0 = take(PR * 4);
   L.pf_gpt = take(PR * c.max_pages_per_seq * 4);
-  L.pf_gnparts = take(PR * 4);
+  L.pf_nparts = take(PR * 4);
   L.pf_rho = take(PR * 4);
   L.pf_h = take(PR * c.hidden * 4);
   L.pf_a = take(PR * c.hidden * 2);
@@ -639,7 +638,6 @@ struct FwdRows {
   std::vector<int> lens;             // host: length of each row's sequence before its append
   const int32_t* len0 = nullptr;     // device [M]: the row's length minus the step counter t
   const int32_t* page_table = nullptr;  // device [M][max_pages_per_seq]
-  int32_t* nparts = nullptr;         // device [M]
   const int32_t* tok = nullptr;      // embedding token of row r: tok[tok_map[r] * tok_stride]
   const int32_t* tok_map = nullptr;
   int tok_stride = 1;
@@ -653,7 +651,7 @@ struct FwdRows {
   void* x = nullptr;                 // attention output [M][hidden]
   float* part_acc = nullptr;
   float* part_ml = nullptr;
-  size_t part_slots = 0;             // (row, kv-head, partial) slots of the attention partials
+  size_t part_slots = 0;             // (item, kv-head, partial) slots of G columns in the attention partials
   float* proj_part = nullptr;
   size_t proj_cols = 0;              // slices x columns per row of the projection partials
   float* attn_out = nullptr;
@@ -666,7 +664,7 @@ struct FwdRows {
   std::vector<int> att_lens;
   const int32_t* att_len0 = nullptr;
   const int32_t* att_pt = nullptr;
-  int32_t* att_nparts = nullptr;
+  int32_t* att_nparts = nullptr;     // device [att_n]: partial states of each item (the planner's output)
   // optional per-layer traces (decode rows only; see pced_step_out)
   float* resid_trace = nullptr;
   uint16_t* qkv_trace = nullptr;
@@ -944,12 +942,11 @@ FwdRows decode_rows(pced_ctx* c, const int32_t* in_tok, const pced_step_out* ext
   R.lens.assign(c->len.begin(), c->len.end());
   R.len0 = c->at<int32_t>(c->lay.len0);
   R.page_table = c->at<int32_t>(c->lay.page_table);
-  R.nparts = c->at<int32_t>(c->lay.nparts);
   R.att_n = R.M;
   R.att_lens = R.lens;
   R.att_len0 = R.len0;
   R.att_pt = R.page_table;
-  R.att_nparts = R.nparts;
+  R.att_nparts = c->at<int32_t>(c->lay.nparts);
   R.tok = in_tok;
   R.tok_map = c->at<int32_t>(c->lay.seq_query);
   R.tok_stride = 1;
@@ -1003,7 +1000,6 @@ pced_status run_prefill_chunk(pced_ctx* c, const char* model, const int32_t* tok
     for (int i = 0; i < T; ++i) R.lens[(size_t)s * T + i] = c->len[s] + i;
   R.len0 = pm.len0_out;
   R.page_table = pm.page_table_out;
-  R.nparts = c->at<int32_t>(c->lay.pf_nparts);
   // attention items: groups of tq tokens of a sequence fill the matrix cores' 16
   // query columns per kv-head (tq x q-heads per kv-head), so each group reads
   // the sequence's pages once for all its tokens
@@ -1030,7 +1026,7 @@ pced_status run_prefill_chunk(pced_ctx* c, const char* model, const int32_t* tok
   R.att_T = T;
   R.att_len0 = gm.len0_out;
   R.att_pt = gm.page_table_out;
-  R.att_nparts = c->at<int32_t>(c->lay.pf_gnparts);
+  R.att_nparts = c->at<int32_t>(c->lay.pf_nparts);
   R.tok = tokens;
   R.tok_map = pm.tok_map;
   R.tok_stride = 1;
