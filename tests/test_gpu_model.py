@@ -181,6 +181,16 @@ def test_model_steps_two_layers_two_queries():
     assert _run(wl, spec, steps=3) <= 1
 
 
+def test_model_steps_two_row_tiles():
+    # 2 queries of 10 and 8 documents: 20 rows, so the projections run with two
+    # 16-row tiles in the matrix cores' N dimension (17..32 rows)
+    geom = W.Geometry(2, 8, 2, 64, 512, 1200, "bf16")
+    rng = np.random.default_rng(28)
+    wl = W.custom(geom, [10, 8], rng.integers(5, 400, size=18).tolist(), amateur_len=12, steps=2, seed=28)
+    spec = ModelSpec(geom, ffn_dim=1536, rope_theta=10000.0, seed=28)
+    assert _run(wl, spec, steps=2, prefill=5) <= 1
+
+
 def test_model_prefill_then_steps_shuffled_pages():
     geom = W.Geometry(1, 8, 2, 64, 512, 2000, "bf16")
     wl = W.custom(geom, [2], [20, 33], amateur_len=5, steps=2, seed=22, shuffle_pages=True)
