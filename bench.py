@@ -349,9 +349,35 @@ def model_timing(wl, K, Wm, dev) -> dict:
 
     ms_plain, _ = timed(False)
     log(f"[bench] model: {K} steps {ms_plain / K:.3f} ms/step")
+    ref = toks[:, :K].clone()
     ms_ev, prof = timed(True)
     log(f"[bench] model with per-launch events: {ms_ev / K:.3f} ms/step")
     kernels = kernel_table(prof, ms_ev)
+
+    # the same K steps captured into a HIP graph from the same state and
+    # replayed (caches reloaded before each replay); tokens must equal the direct run's
+    load_workload(sess, wl, src=src)
+    torch.cuda.synchronize()
+    gtoks = torch.empty_like(toks)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        sess.ctx.pced_model_generate(model, Wt, K, first, gtoks)
+    torch.cuda.synchronize()
+    replays, match = [], True
+    for _ in range(2):
+        load_workload(sess, wl, src=src)
+        gtoks.fill_(-1)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(torch.cuda.current_stream())
+        graph.replay()
+        b.record(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        replays.append(a.elapsed_time(b))
+        match = match and bool(torch.equal(gtoks[:, :K], ref))
+    del graph
+    ms_graph = min(replays)
+    log(f"[bench] model graph replay: {ms_graph / K:.3f} ms/step (tokens match: {match})")
 
     # query-suffix prefill: `suffix` tokens into every cache, chunked token-parallel
     from pced_inputs.model import suffix_tokens
@@ -373,6 +399,7 @@ def model_timing(wl, K, Wm, dev) -> dict:
     return {"metric": "PCED decode steps/sec at N docs, through the decoder stack", "value": K / (ms_plain * 1e-3),
             "unit": "steps/s", "ms_per_step": ms_plain / K, "ms_per_step_with_launch_events": ms_ev / K,
             "steps": K, "warmup": Wm,
+            "graph_replay": {"steps_per_s": K / (ms_graph * 1e-3), "ms": replays, "tokens_match_direct": match},
             "prefill": {"suffix_tokens": suffix, "sequences": int(wl.n_seqs), "ms": prefill_ms[-1],
                         "tokens_per_s": suffix * wl.n_seqs / (prefill_ms[-1] * 1e-3)},
             "model": {"layers": g.n_layers, "hidden": g.hidden, "ffn_dim": spec.ffn_dim, "q_heads": g.n_q_heads,
