@@ -244,6 +244,12 @@ struct ProfScope {
     rec.flops = flops;
     rec.a = take();
     rec.b = take();
+    if (!rec.a || !rec.b) {  // no events to be had: this launch goes untimed
+      if (rec.a) c->ev_free.push_back(rec.a);
+      if (rec.b) c->ev_free.push_back(rec.b);
+      on = false;
+      return;
+    }
     tm.start = rec.a;
     tm.stop = rec.b;
   }
@@ -251,7 +257,10 @@ struct ProfScope {
   hipEvent_t take() {
     if (!c->ev_free.empty()) { hipEvent_t e = c->ev_free.back(); c->ev_free.pop_back(); return e; }
     hipEvent_t e = nullptr;
-    hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
     return e;
   }
   ~ProfScope() {
@@ -1241,8 +1250,11 @@ pced_status pced_create(const pced_config* cfg, void* d_workspace, size_t ws_byt
 
 void pced_destroy(pced_ctx* ctx) {
   if (!ctx) return;
-  for (auto& r : ctx->recs) { hipEventDestroy(r.a); hipEventDestroy(r.b); }
-  for (auto e : ctx->ev_free) hipEventDestroy(e);
+  for (auto& r : ctx->recs) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (auto e : ctx->ev_free) (void)hipEventDestroy(e);
   if (ctx->blas) rocblas_destroy_handle(ctx->blas);
   delete ctx;
 }

@@ -901,7 +901,7 @@ __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a, int D) {
       const float v0 = has0 ? vp[base + lane] : 0.f, v1 = has1 ? vp[base + lane + 64] : 0.f;
 #pragma unroll
       for (int h = 0; h < kMaxGroup; ++h) {
-        if (h >= G) break;
+        if (h >= G) continue;  // (G is uniform: the rest are skipped too)
         const float z = wave_sum(qv[h][0] * k0 + qv[h][1] * k1) * a.scale_log2;
         const float mn = fmaxf(m[h], z);
         const float al = exp2f(m[h] - mn), pz = exp2f(z - mn);
@@ -914,7 +914,7 @@ __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a, int D) {
     if (d1.y == 1) {  // the sequence lies in this chunk alone: final output
 #pragma unroll
       for (int h = 0; h < kMaxGroup; ++h) {
-        if (h >= G) break;
+        if (h >= G) continue;  // (G is uniform: the rest are skipped too)
         const float inv = 1.0f / l[h];
         const int head = g * G + h;
         const size_t xo = (size_t)s * a.n_q_heads * D + (size_t)head * D;
@@ -933,7 +933,7 @@ __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a, int D) {
     const size_t w = (size_t)(s * Hkv + g) * a.split_stride + d1.x;
 #pragma unroll
     for (int h = 0; h < kMaxGroup; ++h) {
-      if (h >= G) break;
+      if (h >= G) continue;
       if (has0) a.part_acc[(w * G + h) * D + lane] = acc[h][0];
       if (has1) a.part_acc[(w * G + h) * D + lane + 64] = acc[h][1];
       if (lane == 0) {
@@ -2572,19 +2572,36 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
   const int s = blockIdx.x;
   const int tok = min(max(a.tokens[(size_t)a.seq_query[s] * a.tok_stride], 0), a.vocab - 1);
   const uint16_t* e = a.embed + (size_t)tok * a.hidden;
-  for (int j = threadIdx.x; j < a.hidden / 4; j += 256) {
-    const uint2 ev = *(const uint2*)(e + 4 * j);
-    const uint2 g = *(const uint2*)(a.g + 4 * j);
-    const float h0 = bf2f(ev.x & 0xFFFFu), h1 = bf2f(ev.x >> 16), h2 = bf2f(ev.y & 0xFFFFu), h3 = bf2f(ev.y >> 16);
-    *(float4*)(a.h + (size_t)s * a.hidden + 4 * j) = make_float4(h0, h1, h2, h3);
-    uint2 pk;
-    pk.x = f2bf(h0 * bf2f(g.x & 0xFFFFu)) | (f2bf(h1 * bf2f(g.x >> 16)) << 16);
-    pk.y = f2bf(h2 * bf2f(g.y & 0xFFFFu)) | (f2bf(h3 * bf2f(g.y >> 16)) << 16);
-    *(uint2*)(a.a_out + (size_t)s * a.hidden + 4 * j) = pk;
-    float ss = h0 * h0 + h1 * h1 + h2 * h2 + h3 * h3;
-    ss += __shfl_xor(ss, 1);
-    ss += __shfl_xor(ss, 2);
-    if ((j & 3) == 0) a.ss_out[(size_t)s * a.ld_ss + j / 4] = ss;
+  const int n4 = a.hidden / 4;  // a multiple of 64: a wave's groups are all in range or all out
+  // the loads of up to U 4-element groups per thread go out before any store
+  // (the stores could alias the inputs as far as the compiler knows)
+  constexpr int U = 4;
+  for (int j0 = threadIdx.x; j0 < n4; j0 += U * 256) {
+    uint2 evs[U], gs[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = min(j0 + u * 256, n4 - 1);
+      evs[u] = *(const uint2*)(e + 4 * j);
+      gs[u] = *(const uint2*)(a.g + 4 * j);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u * 256;
+      if (j < n4) {
+        const uint2 ev = evs[u], g = gs[u];
+        const float h0 = bf2f(ev.x & 0xFFFFu), h1 = bf2f(ev.x >> 16), h2 = bf2f(ev.y & 0xFFFFu),
+                    h3 = bf2f(ev.y >> 16);
+        *(float4*)(a.h + (size_t)s * a.hidden + 4 * j) = make_float4(h0, h1, h2, h3);
+        uint2 pk;
+        pk.x = f2bf(h0 * bf2f(g.x & 0xFFFFu)) | (f2bf(h1 * bf2f(g.x >> 16)) << 16);
+        pk.y = f2bf(h2 * bf2f(g.y & 0xFFFFu)) | (f2bf(h3 * bf2f(g.y >> 16)) << 16);
+        *(uint2*)(a.a_out + (size_t)s * a.hidden + 4 * j) = pk;
+        float ss = h0 * h0 + h1 * h1 + h2 * h2 + h3 * h3;
+        ss += __shfl_xor(ss, 1);
+        ss += __shfl_xor(ss, 2);
+        if ((j & 3) == 0) a.ss_out[(size_t)s * a.ld_ss + j / 4] = ss;
+      }
+    }
   }
 }
 
