@@ -191,6 +191,18 @@ def test_model_steps_two_row_tiles():
     assert _run(wl, spec, steps=2, prefill=5) <= 1
 
 
+@pytest.mark.parametrize("experts", [[15], [16], [15, 15], [23, 23]], ids=lambda e: f"{sum(e) + len(e)}-rows")
+def test_model_steps_row_tile_edges(experts):
+    # 16, 17, 32 and 48 rows: the edges of one, two and three 16-row tiles in the
+    # projections' N dimension (48 is the most the split-K kernel takes)
+    geom = W.Geometry(2, 4, 2, 64, 256, 800, "bf16")
+    rng = np.random.default_rng(29 + sum(experts))
+    wl = W.custom(geom, experts, rng.integers(3, 200, size=sum(experts)).tolist(), amateur_len=8, steps=1,
+                  seed=29 + sum(experts))
+    spec = ModelSpec(geom, ffn_dim=512, rope_theta=10000.0, seed=29)
+    assert _run(wl, spec, steps=1) <= 1
+
+
 def test_model_prefill_then_steps_shuffled_pages():
     geom = W.Geometry(1, 8, 2, 64, 512, 2000, "bf16")
     wl = W.custom(geom, [2], [20, 33], amateur_len=5, steps=2, seed=22, shuffle_pages=True)
