@@ -244,6 +244,7 @@ def test_model_llama3_8b_layer_shapes():
     ("2-per-kv-head-groups-of-8-padded-items", 8, 4, 512, 5),
     ("1-per-kv-head-groups-of-16-padded-items", 4, 4, 256, 6),
     ("16-per-kv-head-token-rows", 16, 1, 1024, 0),
+    ("8-per-kv-head-groups-of-2-padded-items", 16, 2, 1024, 4),
 ], ids=lambda c: c[0])
 def test_model_prefill_token_groups(case):
     """Two layers, so the second layer's K/V rows check the first layer's
