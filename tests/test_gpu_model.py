@@ -260,6 +260,16 @@ def test_model_prefill_token_groups(case):
     _run(wl, spec, steps=1, prefill=21, max_attn_chunks=cap)
 
 
+@pytest.mark.parametrize("n_tok", [1, 4, 16])
+def test_model_prefill_short_suffixes(n_tok):
+    """Two layers, 4 q-heads per kv-head: a one-token suffix (one token per
+    group), one full group, and four full groups that fill a page."""
+    geom = W.Geometry(2, 8, 2, 64, 512, 900, "bf16")
+    wl = W.custom(geom, [3], [16, 47, 130], amateur_len=31, steps=1, seed=30 + n_tok)
+    spec = ModelSpec(geom, ffn_dim=1024, rope_theta=10000.0, seed=30)
+    _run(wl, spec, steps=1, prefill=n_tok)
+
+
 def test_model_prefill_token_groups_long_caches():
     """Workload-3-like caches (32 documents of 512..2048 tokens and a 64-token
     amateur, 4 q-heads per kv-head) with a 32-token suffix: 264 groups of 4
